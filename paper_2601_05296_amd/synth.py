@@ -1,0 +1,175 @@
+"""Seeded synthetic inputs for one MoE layer (forward + backward).
+
+This module only draws random numbers and rounds them to the storage format.
+It holds none of the layer's arithmetic: routing, dispatch, the expert FFN and
+the combine live in the HIP library (product path) and in ``oracle/`` (test
+infrastructure), and both receive the arrays made here.
+
+Workloads follow the paper's setting (a single MoE layer, token-choice top-k
+routing, SwiGLU experts; Sections 2 and 5.1); the paper trains on synthetic
+shapes, so no dataset is involved. Shapes and distributions:
+
+* ``x ~ N(0, 1)``            ``[T, d]``
+* ``w_gate ~ N(0, 0.02)``    ``[E, d]``   (router, Section 2.1)
+* ``w1, w3 ~ N(0, 1/sqrt(d))`` ``[E, d, f]`` (SiLU branch, linear branch)
+* ``w2 ~ N(0, 1/sqrt(f))``   ``[E, f, d]`` (down projection)
+* ``dy ~ N(0, 1)``           ``[T, d]``   (upstream gradient)
+
+The second argument of N is the standard deviation. Independent streams are
+spawned from one ``SeedSequence`` in the fixed order x, w_gate, w1, w3, w2, dy,
+bias, perm, so that changing one tensor's size never changes another's values.
+
+For the skewed many-small-experts workload a per-expert bias is added to the
+router logits before the softmax. Expert ``e`` has popularity rank ``r(e)``
+(a seeded permutation) and bias ``-s * c * log(r(e))`` with ``s = 1.2`` and
+``c = sigma * sqrt(6) / pi``, where ``sigma = 0.02 * sqrt(d)`` is the standard
+deviation of one router logit. With Gumbel noise of that scale, top-k selection
+would be Plackett-Luce sampling with weights ``r**-s`` (Zipf(s)); the Gaussian
+router noise makes the shares Zipf-like rather than exact. The popular head is
+capped at T tokens per expert by top-k itself.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+
+DTYPES = ("f32", "bf16")
+
+
+@dataclass(frozen=True)
+class MoEConfig:
+    name: str
+    T: int
+    d: int
+    f: int
+    E: int
+    k: int
+    dtype: str = "bf16"
+    renorm: bool = False
+    zipf_s: float = 0.0          # > 0: per-expert Zipf-shaped router bias
+    n_dead: int = 0              # experts whose bias is -inf (never chosen)
+    seed: int = 0
+
+    @property
+    def S(self) -> int:
+        return self.T * self.k
+
+    def with_(self, **kw) -> "MoEConfig":
+        d = dict(self.__dict__)
+        d.update(kw)
+        return MoEConfig(**d)
+
+
+# The five layer workloads this library is measured on.
+CONFIGS = {
+    "tiny_f32": MoEConfig("tiny_f32", T=1024, d=256, f=512, E=8, k=2, dtype="f32"),
+    "mid_e64k6": MoEConfig("mid_e64k6", T=16384, d=2048, f=1408, E=64, k=6,
+                           dtype="bf16", renorm=True),
+    "few_large_e8k2": MoEConfig("few_large_e8k2", T=32768, d=4096, f=14336, E=8,
+                                k=2, dtype="bf16"),
+    "many_small_zipf": MoEConfig("many_small_zipf", T=65536, d=2048, f=768, E=128,
+                                 k=8, dtype="bf16", zipf_s=1.2),
+    "mem_sweep_e64k8": MoEConfig("mem_sweep_e64k8", T=16384, d=4096, f=2048, E=64,
+                                 k=8, dtype="bf16"),
+}
+
+
+def bf16_round(a: np.ndarray) -> np.ndarray:
+    """Round float32 values to the nearest bfloat16 (ties to even); returns the
+    16-bit patterns as uint16."""
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+    bias = ((u >> 16) & 1) + np.uint32(0x7FFF)
+    return ((u + bias) >> 16).astype(np.uint16)
+
+
+def bf16_to_f32(b: np.ndarray) -> np.ndarray:
+    """Widen bfloat16 bit patterns (uint16) to float32 exactly."""
+    return (b.astype(np.uint32) << 16).view(np.float32)
+
+
+@dataclass
+class LayerInputs:
+    """Host copies of one layer's inputs.
+
+    ``vals`` holds float32 arrays of exactly the values the device sees (for
+    bf16 workloads: the bf16-rounded values, widened). ``store`` holds what is
+    uploaded: uint16 bf16 patterns, or float32 for the f32 workload. ``bias``
+    stays float32 in both.
+    """
+    cfg: MoEConfig
+    vals: dict = field(default_factory=dict)
+    store: dict = field(default_factory=dict)
+
+
+def _normal(rng: np.random.Generator, shape, std: float) -> np.ndarray:
+    out = rng.standard_normal(size=shape, dtype=np.float32)
+    if std != 1.0:
+        out *= np.float32(std)
+    return out
+
+
+def zipf_bias(cfg: MoEConfig, rng_bias: np.random.Generator, rng_perm: np.random.Generator):
+    """Per-expert router bias (float32 [E]) or None; see the module docstring."""
+    if cfg.zipf_s <= 0.0 and cfg.n_dead == 0:
+        return None
+    E = cfg.E
+    bias = np.zeros(E, dtype=np.float64)
+    if cfg.zipf_s > 0.0:
+        sigma = 0.02 * math.sqrt(cfg.d)
+        c = sigma * math.sqrt(6.0) / math.pi
+        rank = rng_perm.permutation(E) + 1          # rank 1 = most popular
+        bias = -cfg.zipf_s * c * np.log(rank.astype(np.float64))
+    if cfg.n_dead > 0:
+        dead = rng_bias.choice(E, size=cfg.n_dead, replace=False)
+        bias[dead] = -np.inf
+    return bias.astype(np.float32)
+
+
+def make_inputs(cfg: MoEConfig, T: int | None = None, with_dy: bool = True) -> LayerInputs:
+    """Draw one layer's inputs. ``T`` overrides the token count (the first T
+    rows of x and dy are the same for every T, because each row is drawn from
+    the same stream in order)."""
+    T = cfg.T if T is None else T
+    ss = np.random.SeedSequence(cfg.seed)
+    s_x, s_g, s_w1, s_w3, s_w2, s_dy, s_bias, s_perm = ss.spawn(8)
+    rng = lambda s: np.random.Generator(np.random.PCG64(s))
+    d, f, E = cfg.d, cfg.f, cfg.E
+    raw = {
+        "x": _normal(rng(s_x), (T, d), 1.0),
+        "w_gate": _normal(rng(s_g), (E, d), 0.02),
+        "w1": _normal(rng(s_w1), (E, d, f), 1.0 / math.sqrt(d)),
+        "w3": _normal(rng(s_w3), (E, d, f), 1.0 / math.sqrt(d)),
+        "w2": _normal(rng(s_w2), (E, f, d), 1.0 / math.sqrt(f)),
+    }
+    if with_dy:
+        raw["dy"] = _normal(rng(s_dy), (T, d), 1.0)
+    out = LayerInputs(cfg.with_(T=T))
+    for name, a in raw.items():
+        if cfg.dtype == "bf16":
+            b = bf16_round(a)
+            out.store[name] = b
+            out.vals[name] = bf16_to_f32(b)
+        else:
+            out.store[name] = a
+            out.vals[name] = a
+    bias = zipf_bias(cfg, rng(s_bias), rng(s_perm))
+    out.vals["bias"] = bias
+    out.store["bias"] = bias
+    return out
+
+
+def random_ids(T: int, E: int, k: int, seed: int = 0, popularity=None) -> np.ndarray:
+    """Random top-k expert choices [T, k] int32 with distinct ids per row.
+    ``popularity`` (length E, nonnegative) skews the draw (Plackett-Luce)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    if popularity is None:
+        keys = rng.random((T, E))
+    else:
+        w = np.asarray(popularity, dtype=np.float64)
+        g = rng.gumbel(size=(T, E))
+        with np.errstate(divide="ignore"):
+            keys = np.log(w)[None, :] + g
+    ids = np.argsort(-keys, axis=1, kind="stable")[:, :k]
+    return np.ascontiguousarray(ids.astype(np.int32))
