@@ -1,0 +1,186 @@
+/*
+ * moeblaze.h -- C ABI of the MI355X (gfx950) MoEBlaze MoE-layer library.
+ *
+ * One MoE block, forward and backward, on one GPU, as described in the
+ * MoEBlaze paper (arXiv 2601.05296): top-k softmax gating (Section 2.1),
+ * buffer-free dispatch through index maps (Sections 3.1 and 4), SwiGLU expert
+ * FFNs computed as grouped GEMMs that gather token rows on load, with SiLU
+ * recomputed instead of stored (Section 5, Algorithm 1), and the gate-weighted
+ * combine (Section 2.3).
+ *
+ * Conventions shared by every call:
+ *  - All tensor arguments are DEVICE pointers owned by the caller. The library
+ *    never allocates or frees device memory and never synchronises with the
+ *    host: each call validates its arguments, enqueues kernels on `stream`
+ *    and returns. Results are ready when the stream reaches that point.
+ *  - Validation happens before any launch. On a non-zero return nothing has
+ *    been enqueued and no output has been written (except MOE_ERR_HIP, which
+ *    reports a failed launch).
+ *  - Layouts are row-major and dense. Row-vector convention: x[1,d] W[d,f].
+ *      x        [T, d]         token activations
+ *      w_gate   [E, d]         router weights
+ *      w1, w3   [E, d, f]      expert first layer: SiLU branch, linear branch
+ *      w2       [E, f, d]      expert down projection
+ *    Element type of x, w_gate, w1, w3, w2, dy, A, B, O, dX_slot and the
+ *    y / dx outputs: bfloat16 (MOE_BF16, the default) or float32 (MOE_F32,
+ *    a debug mode). Gates, logits, gate gradients and weight gradients are
+ *    float32 in both modes; index arrays are int32.
+ *  - A slot is one (token, chosen expert) pair; there are S = T*k slots,
+ *    grouped by expert and, inside an expert, by ascending token id.
+ *  - Limits: 1 <= k <= min(E, 16), 1 <= E <= 256, d and f multiples of 128,
+ *    T*k < 2^31. T == 0 is a no-op returning MOE_OK. All pointers must be
+ *    16-byte aligned.
+ *  - Calls that share output or workspace buffers must be ordered on one
+ *    stream; concurrent calls on different streams must use disjoint buffers.
+ */
+#ifndef MOEBLAZE_H
+#define MOEBLAZE_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* status codes */
+#define MOE_OK               0
+#define MOE_ERR_INVALID_ARG  (-1)  /* null pointer, bad size, k > E, ... */
+#define MOE_ERR_UNSUPPORTED  (-2)  /* valid but outside the limits above */
+#define MOE_ERR_WORKSPACE    (-3)  /* workspace null or smaller than queried */
+#define MOE_ERR_HIP          (-4)  /* a kernel launch failed */
+
+/* flags (bitwise or) */
+#define MOE_BF16        0u   /* bfloat16 activations and weights (default) */
+#define MOE_F32         1u   /* float32 activations and weights (debug mode) */
+#define MOE_RENORM      2u   /* moe_route / moe_route_bwd: renormalise the k gates */
+#define MOE_ACCUMULATE  4u   /* moe_combine / moe_route_bwd: add into the output */
+
+/* Human-readable name of a status code (static storage). */
+const char* moe_strerror(int status);
+
+/* Detail of the last non-OK status returned on the calling thread. */
+const char* moe_last_error(void);
+
+/*
+ * moe_route -- top-k softmax gating (Section 2.1: TopK(softmax(W_g x))).
+ *   logits[t,e] = x[t] . w_gate[e] (+ bias[e]),  p = softmax over e,
+ *   topk_ids[t, 0..k-1] = the k experts with the largest logits, in
+ *   decreasing order (equal logits: lower id first),
+ *   gates[t,j] = p[t, topk_ids[t,j]]  (MOE_RENORM: divided by the sum of the
+ *   k selected probabilities).
+ * In:  x [T,d], w_gate [E,d] (element type per flags), bias [E] float32 or
+ *      NULL (added before the softmax; -INFINITY excludes an expert).
+ * Out: topk_ids [T,k] int32, gates [T,k] float32, logits [T,E] float32
+ *      (may be NULL; moe_route_bwd needs it).
+ * Logits accumulate in float32; selection is made on the float32 logits.
+ */
+int moe_route(const void* x, const void* w_gate, const float* bias,
+              int64_t T, int d, int E, int k, unsigned flags,
+              int32_t* topk_ids, float* gates, float* logits, hipStream_t stream);
+
+/*
+ * moe_build_index -- dispatch index maps (Section 4.1 definitions, built
+ * without global atomics as in Section 4.2: per-tile expert counts, one
+ * prefix sum, then a stable in-tile rank and scatter).
+ * In:  topk_ids [T,k] int32, each row k distinct ids in [0,E) (not checked).
+ * Out: counts [E]                        tokens routed to each expert
+ *      offsets [E+1]                     exclusive prefix sum of counts
+ *                                        (expert_token_offsets)
+ *      expert_token_indices [T*k]        token ids grouped by expert,
+ *                                        ascending inside an expert
+ *      token_index_map [T,k]             slot of (t,j):
+ *                                        expert_token_indices[token_index_map[t,j]] == t
+ *      slot_src [T*k]                    t*k + j of each slot (inverse map)
+ * workspace: moe_build_index_workspace_size(T,E,k) bytes of device memory.
+ * Deterministic: identical inputs give bit-identical outputs.
+ */
+size_t moe_build_index_workspace_size(int64_t T, int E, int k);
+int moe_build_index(const int32_t* topk_ids, int64_t T, int E, int k,
+                    int32_t* counts, int32_t* offsets, int32_t* expert_token_indices,
+                    int32_t* token_index_map, int32_t* slot_src,
+                    void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * moe_ffn_fwd -- expert forward without a routed-token buffer (Section 3.1,
+ * Algorithm 1 forward). For each slot s of expert e with token
+ * t = expert_token_indices[s] (x rows are gathered while loading):
+ *   A[s] = x[t] w1[e],   B[s] = x[t] w3[e]           (saved for backward)
+ *   O[s] = (SiLU(A[s]) * B[s]) w2[e]                 (SiLU(A)*B recomputed
+ *                                                     on load, never stored)
+ * In:  x, w1, w3, w2, offsets [E+1], expert_token_indices [T*k] (from
+ *      moe_build_index).
+ * Out: A, B [T*k, f], O [T*k, d] (element type per flags).
+ */
+int moe_ffn_fwd(const void* x, const void* w1, const void* w3, const void* w2,
+                const int32_t* offsets, const int32_t* expert_token_indices,
+                int64_t T, int d, int f, int E, int k, unsigned flags,
+                void* A, void* B, void* O, hipStream_t stream);
+
+/*
+ * moe_combine -- gate-weighted aggregation (Section 2.3) through the
+ * per-token slot list (Section 3.1), and, with weights == NULL, the token
+ * gradient accumulation of the backward pass (Section 3.2, step 3):
+ *   out[t] = sum_{j<k} weights[t,j] * src[token_index_map[t,j]]
+ * The k terms are added in order j = 0..k-1 in float32.
+ * MOE_ACCUMULATE: out[t] += (the sum) instead of overwriting.
+ * In:  src [T*k, d], weights [T,k] float32 or NULL (all ones),
+ *      token_index_map [T,k].
+ * Out: out [T, d] (element type per flags).
+ */
+int moe_combine(const void* src, const float* weights, const int32_t* token_index_map,
+                int64_t T, int d, int k, unsigned flags, void* out, hipStream_t stream);
+
+/*
+ * moe_ffn_bwd -- expert backward (Section 3.2, Algorithm 1 backward).
+ * Per slot s of expert e, token t, gate g = gates[slot_src[s]]; dY rows are
+ * gathered and scaled by g on load (expert-summation backward, never
+ * materialised); h = SiLU(A) * B is recomputed from the saved A, B:
+ *   dw2[e]         = sum_s h[s]^T (g dY[t])
+ *   u              = dY[t] w2[e]^T
+ *   d_gates[t,j]   = sum_f u * h           (= <dY[t], O[s]>)
+ *   dA = g u * B * SiLU'(A),   dB = g u * SiLU(A)      (written over A, B)
+ *   dw1[e] = sum_s x[t]^T dA[s],   dw3[e] = sum_s x[t]^T dB[s]
+ *   dX_slot[s] = dA[s] w1[e]^T + dB[s] w3[e]^T
+ * The token gradient is then moe_combine(dX_slot, NULL, token_index_map).
+ * In:  dy [T,d], x, w1, w3, w2, gates [T,k], offsets, expert_token_indices,
+ *      slot_src; A, B [T*k,f] as written by moe_ffn_fwd.
+ * Out: A, B overwritten with dA, dB; dw1, dw3 [E,d,f], dw2 [E,f,d] float32
+ *      (overwritten, zero for experts with no tokens); d_gates [T,k] float32;
+ *      dX_slot [T*k, d].
+ * workspace: moe_ffn_bwd_workspace_size(T,d,f,E,k,flags) bytes.
+ */
+size_t moe_ffn_bwd_workspace_size(int64_t T, int d, int f, int E, int k, unsigned flags);
+int moe_ffn_bwd(const void* dy, const void* x, const void* w1, const void* w3, const void* w2,
+                const float* gates, const int32_t* offsets,
+                const int32_t* expert_token_indices, const int32_t* slot_src,
+                void* A, void* B, int64_t T, int d, int f, int E, int k, unsigned flags,
+                float* dw1, float* dw3, float* dw2, float* d_gates, void* dX_slot,
+                void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * moe_route_bwd -- router backward. The paper does not state it; this is the
+ * closed form of the gating Jacobian for the forward of moe_route:
+ *   without MOE_RENORM: dl = p * (dp - <p, dp>), dp[e] = d_gates[t,j] where
+ *                       topk_ids[t,j] == e, else 0 (p = softmax(logits));
+ *   with MOE_RENORM:    dl[topk_ids[t,j]] = g_j (d_gates[t,j] - sum_j' g_j'
+ *                       d_gates[t,j']), zero for unselected experts.
+ *   dw_gate = dl^T x   (float32 [E,d], overwritten),
+ *   dx      = dl w_gate (written, or added with MOE_ACCUMULATE).
+ * The bias receives no gradient.
+ * In:  d_gates [T,k], logits [T,E], topk_ids [T,k], gates [T,k] (from
+ *      moe_route), x [T,d], w_gate [E,d].
+ * workspace: moe_route_bwd_workspace_size(T,d,E,k,flags) bytes.
+ */
+size_t moe_route_bwd_workspace_size(int64_t T, int d, int E, int k, unsigned flags);
+int moe_route_bwd(const float* d_gates, const float* logits, const int32_t* topk_ids,
+                  const float* gates, const void* x, const void* w_gate,
+                  int64_t T, int d, int E, int k, unsigned flags,
+                  float* dw_gate, void* dx, void* workspace, size_t workspace_bytes,
+                  hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MOEBLAZE_H */

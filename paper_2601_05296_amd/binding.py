@@ -1,0 +1,164 @@
+"""ctypes binding of libmoeblaze.so: one Python function per C entry point,
+same names, argument marshalling only.
+
+Tensors are torch tensors on the GPU (PyTorch supplies device memory and
+streams); every computation runs in the library's HIP kernels. If the library
+is not built, or no GPU is present when a call is made, the call raises: there
+is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+from .build import LIB
+
+MOE_OK = 0
+MOE_ERR_INVALID_ARG = -1
+MOE_ERR_UNSUPPORTED = -2
+MOE_ERR_WORKSPACE = -3
+MOE_ERR_HIP = -4
+
+MOE_BF16 = 0
+MOE_F32 = 1
+MOE_RENORM = 2
+MOE_ACCUMULATE = 4
+
+# Every symbol declared in include/moeblaze.h.
+EXPORTS = ("moe_strerror", "moe_last_error", "moe_route", "moe_build_index_workspace_size",
+           "moe_build_index", "moe_ffn_fwd", "moe_combine", "moe_ffn_bwd_workspace_size",
+           "moe_ffn_bwd", "moe_route_bwd_workspace_size", "moe_route_bwd")
+
+
+class MoEError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        super().__init__("%s: %s" % (_status_name(status), detail))
+        self.status = status
+
+
+_lib = None
+
+
+def _status_name(s: int) -> str:
+    return {0: "MOE_OK", -1: "MOE_ERR_INVALID_ARG", -2: "MOE_ERR_UNSUPPORTED",
+            -3: "MOE_ERR_WORKSPACE", -4: "MOE_ERR_HIP"}.get(s, "status %d" % s)
+
+
+def load_library(path: str = LIB):
+    """Load libmoeblaze.so and declare the C signatures. Raises if absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise ImportError("libmoeblaze.so is not built (%s); run "
+                          "`python -m paper_2601_05296_amd.build`" % path)
+    lib = ctypes.CDLL(path)
+    P, I64, I, U, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_uint, ctypes.c_size_t
+    sig = {
+        "moe_strerror": (ctypes.c_char_p, [I]),
+        "moe_last_error": (ctypes.c_char_p, []),
+        "moe_route": (I, [P, P, P, I64, I, I, I, U, P, P, P, P]),
+        "moe_build_index_workspace_size": (SZ, [I64, I, I]),
+        "moe_build_index": (I, [P, I64, I, I, P, P, P, P, P, P, SZ, P]),
+        "moe_ffn_fwd": (I, [P, P, P, P, P, P, I64, I, I, I, I, U, P, P, P, P]),
+        "moe_combine": (I, [P, P, P, I64, I, I, U, P, P]),
+        "moe_ffn_bwd_workspace_size": (SZ, [I64, I, I, I, I, U]),
+        "moe_ffn_bwd": (I, [P] * 11 + [I64, I, I, I, I, U] + [P] * 6 + [SZ, P]),
+        "moe_route_bwd_workspace_size": (SZ, [I64, I, I, I, U]),
+        "moe_route_bwd": (I, [P] * 6 + [I64, I, I, I, U, P, P, P, SZ, P]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if not t.is_cuda:
+        raise ValueError("tensor must be on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
+
+
+def _check(status: int):
+    if status != MOE_OK:
+        raise MoEError(status, load_library().moe_last_error().decode())
+
+
+def dtype_flag(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return MOE_BF16
+    if t.dtype == torch.float32:
+        return MOE_F32
+    raise ValueError("unsupported dtype %s" % t.dtype)
+
+
+def moe_route(x, w_gate, bias, T, d, E, k, flags, topk_ids, gates, logits, stream=None):
+    _check(load_library().moe_route(_ptr(x), _ptr(w_gate), _ptr(bias), T, d, E, k, flags,
+                                    _ptr(topk_ids), _ptr(gates), _ptr(logits), _stream(stream)))
+
+
+def moe_build_index_workspace_size(T, E, k) -> int:
+    return load_library().moe_build_index_workspace_size(T, E, k)
+
+
+def moe_build_index(topk_ids, T, E, k, counts, offsets, expert_token_indices, token_index_map,
+                    slot_src, workspace, workspace_bytes, stream=None):
+    _check(load_library().moe_build_index(_ptr(topk_ids), T, E, k, _ptr(counts), _ptr(offsets),
+                                          _ptr(expert_token_indices), _ptr(token_index_map),
+                                          _ptr(slot_src), _ptr(workspace), workspace_bytes,
+                                          _stream(stream)))
+
+
+def moe_ffn_fwd(x, w1, w3, w2, offsets, expert_token_indices, T, d, f, E, k, flags, A, B, O,
+                stream=None):
+    _check(load_library().moe_ffn_fwd(_ptr(x), _ptr(w1), _ptr(w3), _ptr(w2), _ptr(offsets),
+                                      _ptr(expert_token_indices), T, d, f, E, k, flags, _ptr(A),
+                                      _ptr(B), _ptr(O), _stream(stream)))
+
+
+def moe_combine(src, weights, token_index_map, T, d, k, flags, out, stream=None):
+    _check(load_library().moe_combine(_ptr(src), _ptr(weights), _ptr(token_index_map), T, d, k,
+                                      flags, _ptr(out), _stream(stream)))
+
+
+def moe_ffn_bwd_workspace_size(T, d, f, E, k, flags) -> int:
+    return load_library().moe_ffn_bwd_workspace_size(T, d, f, E, k, flags)
+
+
+def moe_ffn_bwd(dy, x, w1, w3, w2, gates, offsets, expert_token_indices, slot_src, A, B, T, d,
+                f, E, k, flags, dw1, dw3, dw2, d_gates, dX_slot, workspace, workspace_bytes,
+                stream=None):
+    _check(load_library().moe_ffn_bwd(_ptr(dy), _ptr(x), _ptr(w1), _ptr(w3), _ptr(w2),
+                                      _ptr(gates), _ptr(offsets), _ptr(expert_token_indices),
+                                      _ptr(slot_src), _ptr(A), _ptr(B), T, d, f, E, k, flags,
+                                      _ptr(dw1), _ptr(dw3), _ptr(dw2), _ptr(d_gates),
+                                      _ptr(dX_slot), _ptr(workspace), workspace_bytes,
+                                      _stream(stream)))
+
+
+def moe_route_bwd_workspace_size(T, d, E, k, flags) -> int:
+    return load_library().moe_route_bwd_workspace_size(T, d, E, k, flags)
+
+
+def moe_route_bwd(d_gates, logits, topk_ids, gates, x, w_gate, T, d, E, k, flags, dw_gate, dx,
+                  workspace, workspace_bytes, stream=None):
+    _check(load_library().moe_route_bwd(_ptr(d_gates), _ptr(logits), _ptr(topk_ids),
+                                        _ptr(gates), _ptr(x), _ptr(w_gate), T, d, E, k, flags,
+                                        _ptr(dw_gate), _ptr(dx), _ptr(workspace),
+                                        workspace_bytes, _stream(stream)))

@@ -1,0 +1,93 @@
+// common.hpp -- device helpers shared by the gfx950 kernels of the MoE layer.
+//
+// bfloat16 values travel as raw 16-bit patterns (uint16_t in memory, 8 of
+// them per 16-byte vector). Matrix-core work uses the gfx950 instruction
+// v_mfma_f32_16x16x32_bf16 with float32 accumulation.
+//
+// MFMA 16x16x32 operand layout (wave64), verified on gfx950: for D = P * Q,
+// lane L supplies P[L%16][8*(L/16) + 0..7] and Q[8*(L/16) + 0..7][L%16], and
+// receives D[4*(L/16) + r][L%16] for r = 0..3. The GEMM kernels call it with
+// P = a tile of the right operand (rows = output columns n) and Q = a tile of
+// the left operand (columns = output rows m), so that lane L ends up holding
+// output row m = L%16 at the four consecutive columns n = 4*(L/16) + r.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace moe {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef uint16_t bf16_t;  // storage pattern
+
+constexpr int WAVE = 64;
+
+// ---- bfloat16 <-> float32 ---------------------------------------------------
+__device__ __forceinline__ float bf2f(uint32_t bits16) {
+    return __uint_as_float(bits16 << 16);
+}
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// round to nearest even; NaN stays NaN
+__device__ __forceinline__ uint32_t f2bf(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0u;
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+__device__ __forceinline__ uint32_t pack_bf2(float lo, float hi) {
+    return f2bf(lo) | (f2bf(hi) << 16);
+}
+
+// unpack 8 bf16 (one 16-byte vector) to float
+__device__ __forceinline__ void unpack8(const uint4& v, float (&o)[8]) {
+    o[0] = bf_lo(v.x); o[1] = bf_hi(v.x); o[2] = bf_lo(v.y); o[3] = bf_hi(v.y);
+    o[4] = bf_lo(v.z); o[5] = bf_hi(v.z); o[6] = bf_lo(v.w); o[7] = bf_hi(v.w);
+}
+__device__ __forceinline__ uint4 pack8(const float (&o)[8]) {
+    uint4 v;
+    v.x = pack_bf2(o[0], o[1]); v.y = pack_bf2(o[2], o[3]);
+    v.z = pack_bf2(o[4], o[5]); v.w = pack_bf2(o[6], o[7]);
+    return v;
+}
+
+// ---- activation -------------------------------------------------------------
+__device__ __forceinline__ float sigmoidf_(float u) { return 1.0f / (1.0f + __expf(-u)); }
+
+// ---- memory helpers -----------------------------------------------------------
+__device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+__device__ __forceinline__ void st16(void* p, const uint4& v) { *reinterpret_cast<uint4*>(p) = v; }
+__device__ __forceinline__ uint4 zero16() { return make_uint4(0u, 0u, 0u, 0u); }
+
+// ---- MFMA ---------------------------------------------------------------------
+__device__ __forceinline__ f32x4 mfma16x16x32(const bf16x8& p, const bf16x8& q, const f32x4& c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(p, q, c, 0, 0, 0);
+}
+
+// ---- XCD-aware block order ------------------------------------------------------
+// Consecutive hardware workgroup ids are dealt round-robin to the 8 XCDs (each
+// with its own L2). Renumber so that every XCD works on one contiguous range of
+// logical tiles, which keeps neighbouring tiles (sharing operand panels) in the
+// same L2. Bijective for any grid size.
+__device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
+    const int q = nblocks >> 3, r = nblocks & 7;
+    const int x = bid & 7, i = bid >> 3;
+    return x * q + (x < r ? x : r) + i;
+}
+
+// ---- wave reductions ------------------------------------------------------------
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, WAVE);
+    return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, WAVE));
+    return v;
+}
+
+}  // namespace moe

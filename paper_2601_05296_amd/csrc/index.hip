@@ -1,0 +1,173 @@
+// index.hip -- dispatch index maps without global atomics.
+//
+// Builds the data structures of the MoEBlaze paper, Section 4.1
+// (expert_token_indices, expert_token_offsets, token_index_map, plus the
+// per-expert lengths and the inverse slot map), following the three-step,
+// atomic-free construction of Section 4.2, re-shaped for gfx950:
+//
+//   1. tile_hist:   each workgroup counts the expert choices of one tile of
+//                   tokens with LDS counters and writes them expert-major to
+//                   cnt[e][tile] (the expert lengths, split by tile). No dense
+//                   [T, E] map is materialised: the per-tile counts carry the
+//                   same information.
+//   2. tile_scan:   one workgroup takes the exclusive prefix sum of cnt in
+//                   expert-major order. Entry (e, tile) then holds
+//                   offsets[e] + (tokens of e in earlier tiles), i.e. the first
+//                   slot of that tile's run inside expert e's segment.
+//   3. tile_rank:   each workgroup revisits its tile in chunks of 64 tokens per
+//                   wave. A lane sets its bit in an LDS 64-bit mask per chosen
+//                   expert; the token's rank among the expert's tokens is the
+//                   popcount of the lower lanes' bits plus the counts of
+//                   earlier waves and chunks. Slots are therefore assigned in
+//                   ascending token order inside every expert, as in the
+//                   paper's worked example, and the result is deterministic.
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace moe {
+namespace {
+
+constexpr int IDX_THREADS = 256;
+constexpr int MAX_TILES = 1024;
+
+// tokens per tile: a multiple of 256 keeping the number of tiles <= MAX_TILES
+inline int64_t tile_tokens(int64_t T) {
+    int64_t tb = (T + MAX_TILES - 1) / MAX_TILES;
+    tb = ((tb + IDX_THREADS - 1) / IDX_THREADS) * IDX_THREADS;
+    return tb < IDX_THREADS ? IDX_THREADS : tb;
+}
+
+__global__ void __launch_bounds__(IDX_THREADS)
+tile_hist(const int32_t* __restrict__ ids, int64_t T, int E, int k, int64_t tb, int ntiles,
+          int32_t* __restrict__ cnt) {
+    __shared__ int32_t c[256];
+    const int tid = threadIdx.x;
+    const int b = blockIdx.x;
+    for (int e = tid; e < E; e += IDX_THREADS) c[e] = 0;
+    __syncthreads();
+    const int64_t lo = (int64_t)b * tb * k;
+    int64_t hi = lo + tb * k;
+    if (hi > T * k) hi = T * k;
+    for (int64_t i = lo + tid; i < hi; i += IDX_THREADS) atomicAdd(&c[ids[i]], 1);
+    __syncthreads();
+    for (int e = tid; e < E; e += IDX_THREADS) cnt[(int64_t)e * ntiles + b] = c[e];
+}
+
+constexpr int SCAN_THREADS = 1024;
+
+__global__ void __launch_bounds__(SCAN_THREADS)
+tile_scan(int32_t* __restrict__ cnt, int E, int ntiles, int32_t* __restrict__ counts,
+          int32_t* __restrict__ offsets) {
+    __shared__ int32_t part[SCAN_THREADS];
+    const int tid = threadIdx.x;
+    const int n = E * ntiles;
+    const int per = (n + SCAN_THREADS - 1) / SCAN_THREADS;
+    const int lo = tid * per;
+    const int hi = min(lo + per, n);
+    int s = 0;
+    for (int i = lo; i < hi; ++i) s += cnt[i];
+    part[tid] = s;
+    __syncthreads();
+    // Hillis-Steele inclusive scan of the per-thread sums
+    for (int o = 1; o < SCAN_THREADS; o <<= 1) {
+        int v = tid >= o ? part[tid - o] : 0;
+        __syncthreads();
+        part[tid] += v;
+        __syncthreads();
+    }
+    int run = tid ? part[tid - 1] : 0;
+    for (int i = lo; i < hi; ++i) {
+        const int c = cnt[i];
+        cnt[i] = run;
+        run += c;
+    }
+    __syncthreads();
+    const int total = part[SCAN_THREADS - 1];
+    for (int e = tid; e <= E; e += SCAN_THREADS) {
+        const int oe = e < E ? cnt[e * ntiles] : total;
+        offsets[e] = oe;
+    }
+    __syncthreads();
+    for (int e = tid; e < E; e += SCAN_THREADS) {
+        const int nxt = e + 1 < E ? cnt[(e + 1) * ntiles] : total;
+        counts[e] = nxt - cnt[e * ntiles];
+    }
+}
+
+__global__ void __launch_bounds__(IDX_THREADS)
+tile_rank(const int32_t* __restrict__ ids, int64_t T, int E, int k, int64_t tb, int ntiles,
+          const int32_t* __restrict__ base, int32_t* __restrict__ eti,
+          int32_t* __restrict__ tim, int32_t* __restrict__ slot_src) {
+    __shared__ int32_t run[256];
+    __shared__ unsigned long long mask[IDX_THREADS / WAVE][256];
+    __shared__ int32_t chunk_ids[IDX_THREADS * 16];
+    __shared__ int32_t chunk_tim[IDX_THREADS * 16];
+    const int tid = threadIdx.x;
+    const int lane = tid & (WAVE - 1);
+    const int wv = tid / WAVE;
+    const int b = blockIdx.x;
+    for (int e = tid; e < E; e += IDX_THREADS) run[e] = base[(int64_t)e * ntiles + b];
+    const int64_t t_lo = (int64_t)b * tb;
+    int64_t t_hi = t_lo + tb;
+    if (t_hi > T) t_hi = T;
+    const unsigned long long below = (1ull << lane) - 1ull;
+    for (int64_t c0 = t_lo; c0 < t_hi; c0 += IDX_THREADS) {
+        const int nt = (int)min((int64_t)IDX_THREADS, t_hi - c0);
+        for (int e = tid; e < E; e += IDX_THREADS)
+#pragma unroll
+            for (int w = 0; w < IDX_THREADS / WAVE; ++w) mask[w][e] = 0ull;
+        for (int i = tid; i < nt * k; i += IDX_THREADS) chunk_ids[i] = ids[c0 * k + i];
+        __syncthreads();
+        const bool valid = tid < nt;
+        if (valid)
+            for (int j = 0; j < k; ++j)
+                atomicOr(&mask[wv][chunk_ids[tid * k + j]], 1ull << lane);
+        __syncthreads();
+        if (valid) {
+            const int64_t t = c0 + tid;
+            for (int j = 0; j < k; ++j) {
+                const int e = chunk_ids[tid * k + j];
+                int r = run[e] + __popcll(mask[wv][e] & below);
+                for (int w = 0; w < wv; ++w) r += __popcll(mask[w][e]);
+                eti[r] = (int32_t)t;
+                slot_src[r] = (int32_t)(t * k + j);
+                chunk_tim[tid * k + j] = r;
+            }
+        }
+        __syncthreads();
+        for (int e = tid; e < E; e += IDX_THREADS) {
+            int add = 0;
+#pragma unroll
+            for (int w = 0; w < IDX_THREADS / WAVE; ++w) add += __popcll(mask[w][e]);
+            run[e] += add;
+        }
+        for (int i = tid; i < nt * k; i += IDX_THREADS) tim[c0 * k + i] = chunk_tim[i];
+        __syncthreads();
+    }
+}
+
+}  // namespace
+
+size_t build_index_workspace(int64_t T, int E, int k) {
+    (void)k;
+    const int64_t tb = tile_tokens(T);
+    const int64_t ntiles = (T + tb - 1) / tb;
+    return (size_t)(E * ntiles * (int64_t)sizeof(int32_t));
+}
+
+hipError_t build_index(const int32_t* ids, int64_t T, int E, int k, int32_t* counts,
+                       int32_t* offsets, int32_t* eti, int32_t* tim, int32_t* slot_src,
+                       void* ws, hipStream_t st) {
+    const int64_t tb = tile_tokens(T);
+    const int ntiles = (int)((T + tb - 1) / tb);
+    int32_t* cnt = static_cast<int32_t*>(ws);
+    hipLaunchKernelGGL(tile_hist, dim3(ntiles), dim3(IDX_THREADS), 0, st, ids, T, E, k, tb,
+                       ntiles, cnt);
+    hipLaunchKernelGGL(tile_scan, dim3(1), dim3(SCAN_THREADS), 0, st, cnt, E, ntiles, counts,
+                       offsets);
+    hipLaunchKernelGGL(tile_rank, dim3(ntiles), dim3(IDX_THREADS), 0, st, ids, T, E, k, tb,
+                       ntiles, cnt, eti, tim, slot_src);
+    return hipGetLastError();
+}
+
+}  // namespace moe

@@ -1,0 +1,45 @@
+// launch.hpp -- internal launchers behind the C ABI (arguments already
+// validated by api.hip). Each returns hipSuccess or the launch error.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace moe {
+
+// ---- dispatch index build ----
+size_t build_index_workspace(int64_t T, int E, int k);
+hipError_t build_index(const int32_t* ids, int64_t T, int E, int k, int32_t* counts,
+                       int32_t* offsets, int32_t* eti, int32_t* tim, int32_t* slot_src,
+                       void* ws, hipStream_t st);
+
+// ---- routing ----
+hipError_t route(const void* x, const void* wg, const float* bias, int64_t T, int d, int E,
+                 int k, bool f32, bool renorm, int32_t* ids, float* gates, float* logits,
+                 hipStream_t st);
+size_t route_bwd_workspace(int64_t T, int d, int E, int k, bool f32);
+hipError_t route_bwd(const float* dgates, const float* logits, const int32_t* ids,
+                     const float* gates, const void* x, const void* wg, int64_t T, int d,
+                     int E, int k, bool f32, bool renorm, bool accumulate, float* dwg,
+                     void* dx, void* ws, hipStream_t st);
+
+// ---- combine ----
+hipError_t combine(const void* src, const float* w, const int32_t* tim, int64_t T, int d,
+                   int k, bool f32, bool accumulate, void* out, hipStream_t st);
+
+// ---- expert FFN ----
+struct FfnArgs {
+    const void* x; const void* w1; const void* w3; const void* w2;
+    const int32_t* offsets; const int32_t* eti; const int32_t* slot_src;
+    const float* gates; const void* dy;
+    void* A; void* B; void* O; void* dX;
+    float* dw1; float* dw3; float* dw2; float* dgates;
+    int64_t T; int d, f, E, k;
+    void* ws;
+};
+hipError_t ffn_fwd(const FfnArgs& a, bool f32, hipStream_t st);
+size_t ffn_bwd_workspace(int64_t T, int d, int f, int E, int k, bool f32);
+hipError_t ffn_bwd(const FfnArgs& a, bool f32, hipStream_t st);
+
+}  // namespace moe

@@ -1,0 +1,132 @@
+"""One MoE layer, forward and backward, driven through the C ABI.
+
+This module only allocates device buffers with torch and calls the library's
+entry points in order; every arithmetic step runs in the HIP kernels.
+
+Forward (MoEBlaze paper, Sections 2-5):
+  moe_route -> moe_build_index -> moe_ffn_fwd -> moe_combine
+Backward (Section 3.2):
+  moe_ffn_bwd -> moe_combine (unit weights: token gradient accumulation)
+  -> moe_route_bwd (router gradient, added into dx)
+
+What the forward keeps for the backward (the "saved activations"): the first
+layer outputs A and B [S, f], the routing decision (ids, gates, logits) and the
+dispatch maps (offsets, expert_token_indices, token_index_map, slot_src). No
+permuted copy of x, no SiLU(A), no h and no expert output O is kept.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import torch
+
+from . import binding as B
+
+ELEM = {torch.bfloat16: 2, torch.float32: 4}
+
+
+@dataclass
+class Saved:
+    T: int
+    d: int
+    f: int
+    E: int
+    k: int
+    flags: int
+    renorm: bool
+    ids: torch.Tensor
+    gates: torch.Tensor
+    logits: torch.Tensor
+    counts: torch.Tensor
+    offsets: torch.Tensor
+    eti: torch.Tensor
+    tim: torch.Tensor
+    slot_src: torch.Tensor
+    A: torch.Tensor
+    B: torch.Tensor
+
+    def tensors(self):
+        return [self.ids, self.gates, self.logits, self.counts, self.offsets, self.eti,
+                self.tim, self.slot_src, self.A, self.B]
+
+    def nbytes(self) -> int:
+        return sum(t.numel() * t.element_size() for t in self.tensors())
+
+
+def saved_bytes_per_token(d: int, f: int, E: int, k: int, elem: int, T: int) -> float:
+    """Closed form of Saved.nbytes() / T: A and B (2 k f elem), ids, gates,
+    token_index_map, expert_token_indices and slot_src (5 x 4k), logits (4E),
+    counts and offsets (4(2E+1) per layer)."""
+    return 2.0 * k * f * elem + 20.0 * k + 4.0 * E + 4.0 * (2 * E + 1) / T
+
+
+def forward(x, w_gate, bias, w1, w3, w2, k: int, renorm: bool, stream=None, keep_O=False):
+    """Returns (y, saved[, O])."""
+    T, d = x.shape
+    E, _, f = w1.shape
+    dev = x.device
+    flags = B.dtype_flag(x)
+    S = T * k
+    i32 = dict(dtype=torch.int32, device=dev)
+    f32 = dict(dtype=torch.float32, device=dev)
+    ids = torch.empty((T, k), **i32)
+    gates = torch.empty((T, k), **f32)
+    logits = torch.empty((T, E), **f32)
+    B.moe_route(x, w_gate, bias, T, d, E, k, flags | (B.MOE_RENORM if renorm else 0), ids, gates,
+                logits, stream)
+    counts = torch.empty(E, **i32)
+    offsets = torch.empty(E + 1, **i32)
+    eti = torch.empty(S, **i32)
+    tim = torch.empty((T, k), **i32)
+    slot_src = torch.empty(S, **i32)
+    wsb = B.moe_build_index_workspace_size(T, E, k)
+    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
+    B.moe_build_index(ids, T, E, k, counts, offsets, eti, tim, slot_src, ws, wsb, stream)
+    del ws
+    A = torch.empty((S, f), dtype=x.dtype, device=dev)
+    Bm = torch.empty((S, f), dtype=x.dtype, device=dev)
+    O = torch.empty((S, d), dtype=x.dtype, device=dev)
+    B.moe_ffn_fwd(x, w1, w3, w2, offsets, eti, T, d, f, E, k, flags, A, Bm, O, stream)
+    y = torch.empty((T, d), dtype=x.dtype, device=dev)
+    B.moe_combine(O, gates, tim, T, d, k, flags, y, stream)
+    saved = Saved(T, d, f, E, k, flags, renorm, ids, gates, logits, counts, offsets, eti, tim,
+                  slot_src, A, Bm)
+    if keep_O:
+        return y, saved, O
+    del O
+    return y, saved
+
+
+def backward(saved: Saved, dy, x, w_gate, w1, w3, w2, stream=None, keep=False):
+    """Returns dict(dx, dw_gate, dw1, dw3, dw2, d_gates[, dX_slot]). Overwrites
+    saved.A / saved.B with dA / dB."""
+    s = saved
+    T, d, f, E, k = s.T, s.d, s.f, s.E, s.k
+    dev = dy.device
+    f32 = dict(dtype=torch.float32, device=dev)
+    dw1 = torch.empty((E, d, f), **f32)
+    dw3 = torch.empty((E, d, f), **f32)
+    dw2 = torch.empty((E, f, d), **f32)
+    d_gates = torch.empty((T, k), **f32)
+    dX = torch.empty((T * k, d), dtype=dy.dtype, device=dev)
+    wsb = B.moe_ffn_bwd_workspace_size(T, d, f, E, k, s.flags)
+    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
+    B.moe_ffn_bwd(dy, x, w1, w3, w2, s.gates, s.offsets, s.eti, s.slot_src, s.A, s.B, T, d, f,
+                  E, k, s.flags, dw1, dw3, dw2, d_gates, dX, ws, wsb, stream)
+    del ws
+    dx = torch.empty((T, d), dtype=dy.dtype, device=dev)
+    B.moe_combine(dX, None, s.tim, T, d, k, s.flags, dx, stream)
+    out = dict(dw1=dw1, dw3=dw3, dw2=dw2, d_gates=d_gates)
+    if keep:
+        out["dX_slot"] = dX
+        out["dx_ffn"] = dx.clone()
+    del dX
+    dwg = torch.empty((E, d), **f32)
+    rflags = s.flags | B.MOE_ACCUMULATE | (B.MOE_RENORM if s.renorm else 0)
+    wsb = B.moe_route_bwd_workspace_size(T, d, E, k, rflags)
+    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
+    B.moe_route_bwd(d_gates, s.logits, s.ids, s.gates, x, w_gate, T, d, E, k, rflags, dwg, dx, ws,
+                    wsb, stream)
+    del ws
+    out.update(dx=dx, dw_gate=dwg)
+    return out

@@ -1,0 +1,80 @@
+"""CPU checks of the C ABI: the built library exports every function the
+header declares, and argument validation rejects bad calls before touching
+the GPU (no kernel is launched in these tests)."""
+import os
+import re
+
+import pytest
+
+from paper_2601_05296_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "moeblaze.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(moe_[a-z_]+)\s*\(", src)))
+
+
+def test_header_and_binding_agree():
+    assert sorted(B.EXPORTS) == _declared()
+
+
+def test_library_exports_every_declared_symbol():
+    lib = B.load_library()
+    for name in _declared():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings():
+    lib = B.load_library()
+    for code, name in ((0, b"MOE_OK"), (-1, b"MOE_ERR_INVALID_ARG"), (-2, b"MOE_ERR_UNSUPPORTED"),
+                       (-3, b"MOE_ERR_WORKSPACE"), (-4, b"MOE_ERR_HIP")):
+        assert lib.moe_strerror(code) == name
+
+
+FAKE = 1 << 20  # an aligned non-null address that is never dereferenced
+
+
+@pytest.mark.parametrize("args,status", [
+    (dict(T=10, d=128, E=8, k=9), B.MOE_ERR_INVALID_ARG),    # k > E
+    (dict(T=10, d=128, E=8, k=0), B.MOE_ERR_INVALID_ARG),
+    (dict(T=-1, d=128, E=8, k=2), B.MOE_ERR_INVALID_ARG),
+    (dict(T=10, d=100, E=8, k=2), B.MOE_ERR_UNSUPPORTED),    # d % 128
+    (dict(T=10, d=128, E=300, k=2), B.MOE_ERR_UNSUPPORTED),  # E > 256
+    (dict(T=10, d=128, E=64, k=17), B.MOE_ERR_UNSUPPORTED),  # k > 16
+    (dict(T=1 << 30, d=128, E=64, k=8), B.MOE_ERR_UNSUPPORTED),  # T*k >= 2^31
+])
+def test_route_validation(args, status):
+    lib = B.load_library()
+    r = lib.moe_route(FAKE, FAKE, None, args["T"], args["d"], args["E"], args["k"], 0, FAKE, FAKE,
+                      None, None)
+    assert r == status, lib.moe_last_error()
+
+
+def test_null_and_misaligned_pointers():
+    lib = B.load_library()
+    assert lib.moe_route(None, FAKE, None, 10, 128, 8, 2, 0, FAKE, FAKE, None, None) == B.MOE_ERR_INVALID_ARG
+    assert b"x is NULL" in lib.moe_last_error()
+    assert lib.moe_route(FAKE + 2, FAKE, None, 10, 128, 8, 2, 0, FAKE, FAKE, None, None) == B.MOE_ERR_INVALID_ARG
+    assert b"aligned" in lib.moe_last_error()
+    assert lib.moe_combine(FAKE, None, FAKE, 10, 128, 2, B.MOE_RENORM, FAKE, None) == B.MOE_ERR_INVALID_ARG
+    assert lib.moe_route(FAKE, FAKE, None, 10, 128, 8, 2, 0x80, FAKE, FAKE, None, None) == B.MOE_ERR_INVALID_ARG
+
+
+def test_workspace_checks_and_zero_tokens():
+    lib = B.load_library()
+    need = lib.moe_build_index_workspace_size(1000, 8, 2)
+    assert need > 0
+    r = lib.moe_build_index(FAKE, 1000, 8, 2, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, need - 1, None)
+    assert r == B.MOE_ERR_WORKSPACE
+    r = lib.moe_ffn_bwd(*([FAKE] * 11), 1000, 128, 128, 8, 2, 0, *([FAKE] * 6), 0, None)
+    assert r == B.MOE_ERR_WORKSPACE
+    need = lib.moe_route_bwd_workspace_size(1000, 128, 8, 2, 0)
+    r = lib.moe_route_bwd(*([FAKE] * 6), 1000, 128, 8, 2, 0, FAKE, FAKE, FAKE, need - 16, None)
+    assert r == B.MOE_ERR_WORKSPACE
+    # T == 0: no-op success, pointers not even inspected
+    assert lib.moe_ffn_fwd(*([None] * 6), 0, 128, 128, 8, 2, 0, None, None, None, None) == B.MOE_OK
+    assert lib.moe_build_index_workspace_size(0, 8, 2) == 0

@@ -1,0 +1,303 @@
+"""GPU parity: every C-ABI entry point against the CPU oracle on the same
+seeded inputs, at sizes the oracle finishes in seconds (several tiles per
+expert plus ragged tails), and the edge cases of the method."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle
+from paper_2601_05296_amd import binding as B
+from paper_2601_05296_amd import layer, synth
+from tests.parity import TOL, assert_close, dev, host, near_tie_ok, rel_err
+
+pytestmark = pytest.mark.gpu
+
+
+def _ids_case(T, E, k, pattern, seed=0):
+    pop = None
+    if pattern == "zipf":
+        pop = np.arange(1, E + 1, dtype=np.float64) ** -1.2
+    elif pattern == "dead":
+        pop = np.ones(E)
+        pop[::2] = 0.0
+    elif pattern == "one":
+        pop = np.full(E, 1e-9)
+        pop[: k] = 1.0
+    return synth.random_ids(T, E, k, seed=seed, popularity=pop)
+
+
+def _gpu_index(ids, E):
+    T, k = ids.shape
+    S = T * k
+    i32 = dict(dtype=torch.int32, device="cuda")
+    out = dict(counts=torch.empty(E, **i32), offsets=torch.empty(E + 1, **i32),
+               eti=torch.empty(S, **i32), tim=torch.empty((T, k), **i32),
+               slot_src=torch.empty(S, **i32))
+    wsb = B.moe_build_index_workspace_size(T, E, k)
+    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+    B.moe_build_index(dev(ids), T, E, k, out["counts"], out["offsets"], out["eti"], out["tim"],
+                      out["slot_src"], ws, wsb)
+    torch.cuda.synchronize()
+    return {n: t.cpu().numpy() for n, t in out.items()}
+
+
+# ---------------------------------------------------------------------------
+# moe_build_index: bit-exact
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("T,E,k,pattern", [
+    (5, 4, 2, "worked"), (1, 4, 1, None), (1000, 8, 2, None), (4097, 64, 6, None),
+    (3000, 128, 8, "zipf"), (2000, 32, 4, "dead"), (777, 256, 16, None), (513, 16, 4, "one"),
+    (300000, 64, 8, None), (65536, 128, 8, "zipf")])
+def test_build_index_bit_exact(T, E, k, pattern):
+    if pattern == "worked":
+        ids = np.array([[2, 3], [0, 1], [0, 3], [1, 2], [0, 3]], np.int32)
+    else:
+        ids = _ids_case(T, E, k, pattern, seed=T)
+    ref = oracle.build_index(ids, E)
+    got = _gpu_index(ids, E)
+    assert np.array_equal(got["counts"], ref.counts)
+    assert np.array_equal(got["offsets"], ref.offsets)
+    assert np.array_equal(got["eti"], ref.eti)
+    assert np.array_equal(got["tim"], ref.tim)
+    assert np.array_equal(got["slot_src"], ref.slot_src)
+
+
+def test_build_index_deterministic():
+    ids = _ids_case(50000, 64, 6, "zipf", seed=1)
+    a = _gpu_index(ids, 64)
+    b = _gpu_index(ids, 64)
+    for n in a:
+        assert np.array_equal(a[n], b[n])
+
+
+# ---------------------------------------------------------------------------
+# moe_route
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype,T,d,E,k,renorm,bias", [
+    ("bf16", 1000, 256, 8, 2, False, None), ("bf16", 1000, 512, 64, 6, True, None),
+    ("bf16", 777, 256, 128, 8, False, "zipf"), ("bf16", 300, 384, 200, 16, False, "dead"),
+    ("f32", 1000, 256, 8, 2, False, None), ("f32", 500, 256, 64, 6, True, "dead")])
+def test_route_parity(dtype, T, d, E, k, renorm, bias):
+    cfg = synth.MoEConfig("r", T=T, d=d, f=128, E=E, k=k, dtype=dtype, renorm=renorm,
+                          zipf_s=1.2 if bias == "zipf" else 0.0,
+                          n_dead=E // 4 if bias == "dead" else 0)
+    inp = synth.make_inputs(cfg, with_dy=False)
+    v = inp.vals
+    ids_r, gates_r, logits_r, _ = oracle.route(v["x"], v["w_gate"], v["bias"], k, renorm)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    x, wg = dev(inp.store["x"]), dev(inp.store["w_gate"])
+    bias_t = dev(v["bias"]) if v["bias"] is not None else None
+    ids = torch.empty((T, k), dtype=torch.int32, device="cuda")
+    gates = torch.empty((T, k), dtype=torch.float32, device="cuda")
+    logits = torch.empty((T, E), dtype=torch.float32, device="cuda")
+    flags = B.dtype_flag(x) | (B.MOE_RENORM if renorm else 0)
+    B.moe_route(x, wg, bias_t, T, d, E, k, flags, ids, gates, logits)
+    torch.cuda.synchronize()
+    assert x.dtype == tdt
+    ids_g = ids.cpu().numpy()
+    lg = host(logits)
+    fin = np.isfinite(logits_r)
+    assert np.array_equal(np.isfinite(lg), fin)
+    assert_close("logits", lg[fin], logits_r[fin], "f32")
+    nflip = near_tie_ok(ids_g, ids_r, logits_r)
+    assert nflip <= max(1, T // 200)
+    same = np.all(ids_g == ids_r, axis=1)
+    assert_close("gates", host(gates)[same], gates_r[same], "f32" if dtype == "f32" else "bf16")
+    # ids are distinct per row and in range
+    assert np.all(np.sort(ids_g, axis=1)[:, 1:] != np.sort(ids_g, axis=1)[:, :-1])
+    assert ids_g.min() >= 0 and ids_g.max() < E
+
+
+# ---------------------------------------------------------------------------
+# moe_combine
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype,T,d,k,weighted,accumulate", [
+    ("bf16", 1000, 256, 2, True, False), ("bf16", 333, 2048, 6, True, True),
+    ("bf16", 257, 512, 8, False, False), ("f32", 1000, 256, 2, True, False),
+    ("f32", 100, 128, 16, False, True)])
+def test_combine_parity(dtype, T, d, k, weighted, accumulate):
+    rng = np.random.default_rng(T + d + k)
+    E = max(k, 8)
+    ids = _ids_case(T, E, k, None, seed=3)
+    ix = oracle.build_index(ids, E)
+    src = rng.standard_normal((T * k, d)).astype(np.float32)
+    base = rng.standard_normal((T, d)).astype(np.float32)
+    w = rng.random((T, k)).astype(np.float32) if weighted else None
+    if dtype == "bf16":
+        src_s, base_s = synth.bf16_round(src), synth.bf16_round(base)
+        src, base = synth.bf16_to_f32(src_s), synth.bf16_to_f32(base_s)
+    else:
+        src_s, base_s = src, base
+    out = dev(base_s)
+    flags = (B.MOE_F32 if dtype == "f32" else 0) | (B.MOE_ACCUMULATE if accumulate else 0)
+    B.moe_combine(dev(src_s), dev(w), dev(ix.tim), T, d, k, flags, out)
+    torch.cuda.synchronize()
+    ref = oracle.combine(src, w, ix.tim) + (base if accumulate else 0.0)
+    assert_close("combine", host(out), ref, dtype)
+
+
+# ---------------------------------------------------------------------------
+# moe_ffn_fwd / moe_ffn_bwd / moe_route_bwd on one layer
+# ---------------------------------------------------------------------------
+
+FFN_CASES = [
+    # dtype, T, d, f, E, k, renorm, ids pattern
+    ("bf16", 300, 256, 384, 8, 2, False, None),
+    ("bf16", 700, 256, 256, 16, 4, True, "zipf"),
+    ("bf16", 500, 384, 128, 12, 3, False, "dead"),
+    ("f32", 300, 256, 384, 8, 2, False, None),
+    ("f32", 257, 128, 256, 16, 4, True, "dead"),
+]
+
+
+def _layer_case(dtype, T, d, f, E, k, renorm, pattern, seed=0):
+    cfg = synth.MoEConfig("l", T=T, d=d, f=f, E=E, k=k, dtype=dtype, renorm=renorm, seed=seed)
+    inp = synth.make_inputs(cfg)
+    ids = _ids_case(T, E, k, pattern, seed=seed + 11)
+    rng = np.random.default_rng(seed + 5)
+    g = rng.random((T, k)).astype(np.float32)
+    return inp, ids, g
+
+
+@pytest.mark.parametrize("dtype,T,d,f,E,k,renorm,pattern", FFN_CASES)
+def test_ffn_fwd_bwd_parity(dtype, T, d, f, E, k, renorm, pattern):
+    inp, ids, g = _layer_case(dtype, T, d, f, E, k, renorm, pattern)
+    v, st = inp.vals, inp.store
+    S = T * k
+    # oracle
+    ix = oracle.build_index(ids, E)
+    A_r, B_r, O_r = oracle.ffn_fwd(v["x"], v["w1"], v["w3"], v["w2"], ix, k)
+    y_r = oracle.combine(O_r, g, ix.tim)
+    bw = oracle.ffn_bwd(v["dy"], v["x"], v["w1"], v["w3"], v["w2"], g, ix, A_r, B_r)
+    dx_r = oracle.combine(bw["dX_slot"], None, ix.tim)
+    # device
+    gi = _gpu_index(ids, E)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    x, w1, w3, w2, dy = (dev(st[n]) for n in ("x", "w1", "w3", "w2", "dy"))
+    offsets, eti, tim, ss = (dev(gi[n]) for n in ("offsets", "eti", "tim", "slot_src"))
+    gates = dev(g)
+    flags = B.dtype_flag(x)
+    A = torch.empty((S, f), dtype=tdt, device="cuda")
+    Bm = torch.empty((S, f), dtype=tdt, device="cuda")
+    O = torch.empty((S, d), dtype=tdt, device="cuda")
+    B.moe_ffn_fwd(x, w1, w3, w2, offsets, eti, T, d, f, E, k, flags, A, Bm, O)
+    y = torch.empty((T, d), dtype=tdt, device="cuda")
+    B.moe_combine(O, gates, tim, T, d, k, flags, y)
+    torch.cuda.synchronize()
+    assert_close("A", host(A), A_r, dtype)
+    assert_close("B", host(Bm), B_r, dtype)
+    assert_close("O", host(O), O_r, dtype)
+    assert_close("y", host(y), y_r, dtype)
+    f32 = dict(dtype=torch.float32, device="cuda")
+    dw1 = torch.full((E, d, f), float("nan"), **f32)
+    dw3 = torch.full((E, d, f), float("nan"), **f32)
+    dw2 = torch.full((E, f, d), float("nan"), **f32)
+    dg = torch.full((T, k), float("nan"), **f32)
+    dX = torch.empty((S, d), dtype=tdt, device="cuda")
+    wsb = B.moe_ffn_bwd_workspace_size(T, d, f, E, k, flags)
+    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+    B.moe_ffn_bwd(dy, x, w1, w3, w2, gates, offsets, eti, ss, A, Bm, T, d, f, E, k, flags,
+                  dw1, dw3, dw2, dg, dX, ws, wsb)
+    dx = torch.empty((T, d), dtype=tdt, device="cuda")
+    B.moe_combine(dX, None, tim, T, d, k, flags, dx)
+    torch.cuda.synchronize()
+    assert_close("dA", host(A), bw["dA"], dtype)
+    assert_close("dB", host(Bm), bw["dB"], dtype)
+    assert_close("dw2", host(dw2), bw["dw2"], dtype)
+    assert_close("dw1", host(dw1), bw["dw1"], dtype)
+    assert_close("dw3", host(dw3), bw["dw3"], dtype)
+    assert_close("d_gates", host(dg), bw["d_gates"], dtype)
+    assert_close("dX_slot", host(dX), bw["dX_slot"], dtype)
+    assert_close("dx_ffn", host(dx), dx_r, dtype)
+    if pattern == "dead":  # experts without tokens get exact zero gradients
+        empty = np.nonzero(gi["counts"] == 0)[0]
+        assert empty.size > 0
+        assert np.all(host(dw1)[empty] == 0) and np.all(host(dw2)[empty] == 0)
+
+
+@pytest.mark.parametrize("dtype,T,d,E,k,renorm,accumulate", [
+    ("bf16", 1000, 256, 8, 2, False, False), ("bf16", 2500, 512, 64, 6, True, True),
+    ("bf16", 1500, 256, 128, 8, False, True), ("f32", 1000, 256, 8, 2, False, False),
+    ("f32", 700, 128, 32, 4, True, True)])
+def test_route_bwd_parity(dtype, T, d, E, k, renorm, accumulate):
+    cfg = synth.MoEConfig("rb", T=T, d=d, f=128, E=E, k=k, dtype=dtype, renorm=renorm)
+    inp = synth.make_inputs(cfg)
+    v = inp.vals
+    ids, gates, logits, _ = oracle.route(v["x"], v["w_gate"], None, k, renorm)
+    rng = np.random.default_rng(7)
+    dgates = rng.standard_normal((T, k))
+    dl, dwg_r, dxr_r = oracle.route_bwd(dgates, logits, ids, v["x"], v["w_gate"], renorm)
+    base = synth.bf16_to_f32(synth.bf16_round(v["dy"])) if dtype == "bf16" else v["dy"]
+    base_store = synth.bf16_round(v["dy"]) if dtype == "bf16" else v["dy"]
+    x, wg = dev(inp.store["x"]), dev(inp.store["w_gate"])
+    flags = B.dtype_flag(x) | (B.MOE_RENORM if renorm else 0) | (B.MOE_ACCUMULATE if accumulate else 0)
+    dwg = torch.empty((E, d), dtype=torch.float32, device="cuda")
+    dx = dev(base_store)
+    wsb = B.moe_route_bwd_workspace_size(T, d, E, k, flags)
+    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+    B.moe_route_bwd(dev(dgates.astype(np.float32)), dev(logits.astype(np.float32)), dev(ids),
+                    dev(gates.astype(np.float32)), x, wg, T, d, E, k, flags, dwg, dx, ws, wsb)
+    torch.cuda.synchronize()
+    assert_close("dw_gate", host(dwg), dwg_r, "f32" if dtype == "f32" else "bf16")
+    ref_dx = dxr_r + (base if accumulate else 0.0)
+    got = host(dx)
+    if accumulate:  # compare the router part, which is small next to the base
+        got = got - base
+        ref_dx = dxr_r
+    tol = "f32" if dtype == "f32" else "bf16"
+    e = rel_err(got, ref_dx)
+    lim = TOL[tol] if not (accumulate and dtype == "bf16") else 2e-2 * np.abs(base).max() / np.abs(dxr_r).max()
+    assert e <= max(lim, TOL[tol]), e
+
+
+# ---------------------------------------------------------------------------
+# whole layer (routing included) on the tiny float32 workload
+# ---------------------------------------------------------------------------
+
+def test_layer_end_to_end_tiny_f32():
+    cfg = synth.CONFIGS["tiny_f32"]
+    inp = synth.make_inputs(cfg)
+    v, st = inp.vals, inp.store
+    fw_r = oracle.layer_forward(v["x"], v["w_gate"], None, v["w1"], v["w3"], v["w2"], cfg.k, cfg.renorm)
+    bw_r = oracle.layer_backward(fw_r, v["dy"], v["x"], v["w_gate"], v["w1"], v["w3"], v["w2"], cfg.renorm)
+    x, wg, w1, w3, w2, dy = (dev(st[n]) for n in ("x", "w_gate", "w1", "w3", "w2", "dy"))
+    y, saved = layer.forward(x, wg, None, w1, w3, w2, cfg.k, cfg.renorm)
+    ids_g = saved.ids.cpu().numpy()
+    assert near_tie_ok(ids_g, fw_r["ids"], fw_r["logits"]) == 0
+    assert saved.nbytes() == pytest.approx(
+        layer.saved_bytes_per_token(cfg.d, cfg.f, cfg.E, cfg.k, 4, cfg.T) * cfg.T)
+    g = layer.backward(saved, dy, x, wg, w1, w3, w2)
+    torch.cuda.synchronize()
+    assert_close("y", host(y), fw_r["y"], "f32")
+    for n in ("dw1", "dw3", "dw2", "dw_gate", "dx", "d_gates"):
+        assert_close(n, host(g[n]), bw_r[n], "f32")
+
+
+def test_layer_deterministic_bf16():
+    cfg = synth.MoEConfig("det", T=2000, d=256, f=256, E=16, k=4, dtype="bf16", renorm=True)
+    inp = synth.make_inputs(cfg)
+    st = inp.store
+    x, wg, w1, w3, w2, dy = (dev(st[n]) for n in ("x", "w_gate", "w1", "w3", "w2", "dy"))
+    outs = []
+    for _ in range(2):
+        y, saved = layer.forward(x, wg, None, w1, w3, w2, cfg.k, cfg.renorm)
+        g = layer.backward(saved, dy, x, wg, w1, w3, w2)
+        torch.cuda.synchronize()
+        outs.append([y.cpu()] + [g[n].cpu() for n in ("dx", "dw1", "dw3", "dw2", "dw_gate")])
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+
+
+def test_error_codes_launch_nothing():
+    x = torch.zeros((4, 128), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(B.MoEError) as ei:
+        B.moe_route(x, x, None, 4, 128, 2, 3, 0, x, x, None)
+    assert ei.value.status == B.MOE_ERR_INVALID_ARG
+    with pytest.raises(B.MoEError) as ei:
+        B.moe_build_index(x, 4, 8, 2, x, x, x, x, x, x, 0)
+    assert ei.value.status == B.MOE_ERR_WORKSPACE
+    # T == 0 is a no-op
+    B.moe_combine(x, None, x, 0, 128, 2, 0, x)
