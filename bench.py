@@ -1,0 +1,252 @@
+"""Benchmark: one MoE layer, forward + backward, on one MI355X.
+
+A step is the whole hot path on one batch: route, dispatch index build,
+expert FFN forward (two grouped GEMMs), combine, expert FFN backward (four
+grouped GEMMs + gate-gradient reduction), token-gradient combine and router
+backward. Inputs and weights are resident in HBM before the timed region.
+
+Prints one JSON line: tokens/s (whole job), per-kernel times from HIP events
+recorded on the launch stream inside the timed region, the roofline of the
+dominant kernel, saved and peak activation bytes per token next to a
+materialised-permutation PyTorch baseline, and the CPU oracle timed on a
+bounded token sample of the same workload.
+
+python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload mid_e64k6]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="mid_e64k6")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="approximate CPU time budget of the oracle baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-baseline-memory", action="store_true")
+    return ap.parse_args()
+
+
+def kernel_model(name, cfg, elem):
+    """Algorithmic work of one launch: (amount, unit, bound)."""
+    T, d, f, E, k = cfg.T, cfg.d, cfg.f, cfg.E, cfg.k
+    S = T * k
+    g = 2.0 * S * d * f  # flops of one [S x d] x [d x f] product
+    flops = {"g1_kernel": 2 * g, "g2_kernel": g, "g3_kernel": g, "g4_kernel": g,
+             "g5_kernel": 2 * g, "g6_kernel": 2 * g}
+    if name in flops:
+        return flops[name], "TFLOP/s", "mfma"
+    nparts = (f // 128) * 2
+    byts = {
+        "route_bf16": T * d * elem + E * d * elem + T * E * 4 + T * k * 8,
+        "tile_hist": S * 4,
+        "tile_scan": 0,
+        "tile_rank": S * 4 + 3 * S * 4,
+        "combine": S * d * elem + T * d * elem + T * k * 8,
+        "dgate_reduce": S * nparts * 4 + S * 8,
+        "rb_dlogits": T * E * 4 * 2 + T * k * 12,
+        "rb_dx": T * E * 4 + E * d * elem + 2 * T * d * elem,
+        "rb_dwg_partial": T * E * 4 + T * d * elem,
+        "rb_dwg_reduce": 0,
+    }
+    return float(byts.get(name, 0)), "GB/s", "hbm"
+
+
+def materialised_saved_bytes(x, w_gate, bias, w1, w3, w2, k, renorm):
+    """Saved-for-backward bytes of a conventional MoE layer that materialises
+    the permuted tokens and every SwiGLU intermediate (plain PyTorch autograd,
+    forward only; weights are parameters and not counted)."""
+    import torch
+    params = {t.data_ptr() for t in (w_gate, w1, w3, w2)}
+    seen = {}
+
+    def pack(t):
+        if t.data_ptr() not in params:
+            seen[(t.data_ptr(), t.dtype, tuple(t.shape))] = t.numel() * t.element_size()
+        return t
+
+    T, d = x.shape
+    E = w1.shape[0]
+    xs = x.detach().requires_grad_(True)
+    wg = w_gate.detach().requires_grad_(True)
+    W1, W3, W2 = (w.detach().requires_grad_(True) for w in (w1, w3, w2))
+    with torch.autograd.graph.saved_tensors_hooks(pack, lambda t: t):
+        logits = xs.float() @ wg.float().t()
+        if bias is not None:
+            logits = logits + bias
+        p = torch.softmax(logits, dim=1)
+        g, ids = torch.topk(p, k, dim=1)
+        if renorm:
+            g = g / g.sum(dim=1, keepdim=True)
+        flat = ids.reshape(-1)
+        order = torch.argsort(flat, stable=True)
+        tok = order // k
+        x_perm = xs.index_select(0, tok)               # routed-token buffer
+        counts = torch.bincount(flat, minlength=E).tolist()
+        outs = []
+        o0 = 0
+        for e in range(E):
+            xe = x_perm[o0:o0 + counts[e]]
+            a = xe @ W1[e]
+            b = xe @ W3[e]
+            h = torch.nn.functional.silu(a) * b
+            outs.append(h @ W2[e])
+            o0 += counts[e]
+        O = torch.cat(outs, 0)
+        gw = g.reshape(-1)[order].to(O.dtype)
+        y = torch.zeros_like(xs).index_add_(0, tok, O * gw[:, None])
+    del y
+    return sum(seen.values())
+
+
+def cpu_oracle_baseline(inp, cfg, budget_s):
+    """Time the CPU oracle (fwd + bwd of the whole layer) on the first tokens
+    of the same workload; the sample grows until about budget_s of work."""
+    from oracle import oracle
+    v = {n: (None if a is None else a.astype(np.float64)) for n, a in inp.vals.items()}
+
+    def run(n):
+        t0 = time.perf_counter()
+        fw = oracle.layer_forward(v["x"][:n], v["w_gate"], v["bias"], v["w1"], v["w3"], v["w2"],
+                                  cfg.k, cfg.renorm)
+        oracle.layer_backward(fw, v["dy"][:n], v["x"][:n], v["w_gate"], v["w1"], v["w3"],
+                              v["w2"], cfg.renorm)
+        return time.perf_counter() - t0
+
+    n0 = 8
+    t_small = run(n0)
+    n = int(min(cfg.T, max(n0, n0 * budget_s / max(t_small, 1e-3))))
+    t = run(n)
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": n / t, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": "first %d of %d tokens of %s, whole-layer fwd+bwd in fp64 "
+                      "(%.1f s; calibration run of %d tokens %.1f s not counted)"
+                      % (n, cfg.T, cfg.name, t, n0, t_small)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(see the sharding note in DESIGN.md); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2601_05296_amd import binding as B
+    from paper_2601_05296_amd import layer, synth
+
+    cfg = synth.CONFIGS[args.workload]
+    assert cfg.dtype == "bf16", "the benchmark workloads are bf16"
+    elem = 2
+    dev = torch.device("cuda:0")
+    inp = synth.make_inputs(cfg)
+
+    def up(a):
+        if a is None:
+            return None
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    x, wg, w1, w3, w2, dy = (up(inp.store[n]) for n in ("x", "w_gate", "w1", "w3", "w2", "dy"))
+    bias = up(inp.store["bias"])
+    T, d, f, E, k = cfg.T, cfg.d, cfg.f, cfg.E, cfg.k
+
+    def step():
+        y, saved = layer.forward(x, wg, bias, w1, w3, w2, k, cfg.renorm)
+        g = layer.backward(saved, dy, x, wg, w1, w3, w2)
+        return y, saved, g
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # peak activation bytes of one step (weights, inputs and weight gradients excluded)
+    torch.cuda.reset_peak_memory_stats(dev)
+    base = torch.cuda.memory_allocated(dev)
+    y, saved, g = step()
+    torch.cuda.synchronize()
+    peak = torch.cuda.max_memory_allocated(dev) - base
+    grad_bytes = sum(g[n].numel() * 4 for n in ("dw1", "dw3", "dw2", "dw_gate"))
+    saved_bytes = saved.nbytes()
+    formula = layer.saved_bytes_per_token(d, f, E, k, elem, T) * T
+    assert abs(saved_bytes - formula) < 1, (saved_bytes, formula)
+    del y, saved, g
+
+    # timed region: K whole steps, per-kernel events recorded on the stream
+    per_step_records = 32
+    B.moe_probe_enable(per_step_records * args.steps + 64)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    recs = [B.moe_probe_get(i) for i in range(B.moe_probe_count())]
+    B.moe_probe_disable()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    tokens_per_s = T * args.steps / (t1 - t0)
+
+    kern = {}
+    for name, ms in recs:
+        kern.setdefault(name, []).append(ms)
+    kernels = {}
+    for name, lst in kern.items():
+        avg = float(np.mean(lst))
+        amount, unit, bound = kernel_model(name, cfg, elem)
+        rate = amount / (avg * 1e-3) / (1e12 if unit == "TFLOP/s" else 1e9) if amount else None
+        peak_ = PEAK_BF16_TFLOPS if unit == "TFLOP/s" else PEAK_HBM_GBS
+        kernels[name] = {"avg_ms": round(avg, 4), "launches_per_step": len(lst) / args.steps,
+                         "ms_per_step": round(avg * len(lst) / args.steps, 4),
+                         "bound": bound, "achieved": None if rate is None else round(rate, 1),
+                         "unit": unit, "frac": None if rate is None else round(rate / peak_, 4)}
+    dom = max(kernels, key=lambda n: kernels[n]["ms_per_step"])
+    kd = kernels[dom]
+    amount, unit, bound = kernel_model(dom, cfg, elem)
+    roofline = {"bound": bound, "achieved": kd["achieved"], "unit": unit,
+                "peak": PEAK_BF16_TFLOPS if unit == "TFLOP/s" else PEAK_HBM_GBS,
+                "frac": kd["frac"], "traffic": None, "kernel": dom,
+                "per_launch": amount, "avg_ms": kd["avg_ms"]}
+    gemm_ms = sum(kernels[n]["ms_per_step"] for n in kernels if n.startswith("g") and n[1].isdigit())
+    gemm_flops = 18.0 * T * k * d * f
+    out = {
+        "metric": "MoE layer fwd+bwd tokens/sec + peak activation bytes/token, 1 MI355X",
+        "value": round(tokens_per_s, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": cfg.name, "T": T, "d": d, "f": f, "E": E, "k": k,
+                   "renorm": cfg.renorm, "zipf_s": cfg.zipf_s, "parallelism": "none"},
+        "peak_activation_bytes_per_token": round((peak - grad_bytes) / T, 1),
+        "saved_activation_bytes_per_token": round(saved_bytes / T, 1),
+        "roofline": roofline,
+        "gemm": {"ms_per_step": round(gemm_ms, 4),
+                 "tflops": round(gemm_flops / (gemm_ms * 1e-3) / 1e12, 1),
+                 "frac": round(gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)},
+        "kernels": kernels,
+    }
+    if not args.no_baseline_memory:
+        mb = materialised_saved_bytes(x, wg, bias, w1, w3, w2, k, cfg.renorm)
+        out["materialised_baseline_saved_bytes_per_token"] = round(mb / T, 1)
+        torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_oracle_baseline(inp, cfg, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

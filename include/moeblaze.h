@@ -107,16 +107,22 @@ int moe_build_index(const int32_t* topk_ids, int64_t T, int E, int k,
  * Algorithm 1 forward). For each slot s of expert e with token
  * t = expert_token_indices[s] (x rows are gathered while loading):
  *   A[s] = x[t] w1[e],   B[s] = x[t] w3[e]           (saved for backward)
- *   O[s] = (SiLU(A[s]) * B[s]) w2[e]                 (SiLU(A)*B recomputed
- *                                                     on load, never stored)
+ *   h[s] = SiLU(A[s]) * B[s]                         (formed in the epilogue of
+ *                                                     the first GEMM from the
+ *                                                     stored A, B; transient)
+ *   O[s] = h[s] w2[e]
  * In:  x, w1, w3, w2, offsets [E+1], expert_token_indices [T*k] (from
  *      moe_build_index).
  * Out: A, B [T*k, f], O [T*k, d] (element type per flags).
+ * workspace: moe_ffn_fwd_workspace_size(T,d,f,E,k,flags) bytes (holds h
+ *      between the two GEMMs; 0 in MOE_F32 mode, where NULL is accepted).
  */
+size_t moe_ffn_fwd_workspace_size(int64_t T, int d, int f, int E, int k, unsigned flags);
 int moe_ffn_fwd(const void* x, const void* w1, const void* w3, const void* w2,
                 const int32_t* offsets, const int32_t* expert_token_indices,
                 int64_t T, int d, int f, int E, int k, unsigned flags,
-                void* A, void* B, void* O, hipStream_t stream);
+                void* A, void* B, void* O, void* workspace, size_t workspace_bytes,
+                hipStream_t stream);
 
 /*
  * moe_combine -- gate-weighted aggregation (Section 2.3) through the
@@ -135,8 +141,9 @@ int moe_combine(const void* src, const float* weights, const int32_t* token_inde
 /*
  * moe_ffn_bwd -- expert backward (Section 3.2, Algorithm 1 backward).
  * Per slot s of expert e, token t, gate g = gates[slot_src[s]]; dY rows are
- * gathered and scaled by g on load (expert-summation backward, never
- * materialised); h = SiLU(A) * B is recomputed from the saved A, B:
+ * gathered on load (the expert-summation backward never materialises g*dY:
+ * g is applied in the epilogue of u and carried in g*h); h = SiLU(A) * B is
+ * recomputed from the saved A, B in the epilogue of the u GEMM:
  *   dw2[e]         = sum_s h[s]^T (g dY[t])
  *   u              = dY[t] w2[e]^T
  *   d_gates[t,j]   = sum_f u * h           (= <dY[t], O[s]>)
@@ -149,7 +156,8 @@ int moe_combine(const void* src, const float* weights, const int32_t* token_inde
  * Out: A, B overwritten with dA, dB; dw1, dw3 [E,d,f], dw2 [E,f,d] float32
  *      (overwritten, zero for experts with no tokens); d_gates [T,k] float32;
  *      dX_slot [T*k, d].
- * workspace: moe_ffn_bwd_workspace_size(T,d,f,E,k,flags) bytes.
+ * workspace: moe_ffn_bwd_workspace_size(T,d,f,E,k,flags) bytes (gate-gradient
+ *      partial sums and g*h for the dw2 GEMM; 0 in MOE_F32 mode).
  */
 size_t moe_ffn_bwd_workspace_size(int64_t T, int d, int f, int E, int k, unsigned flags);
 int moe_ffn_bwd(const void* dy, const void* x, const void* w1, const void* w3, const void* w2,
@@ -179,6 +187,22 @@ int moe_route_bwd(const float* d_gates, const float* logits, const int32_t* topk
                   int64_t T, int d, int E, int k, unsigned flags,
                   float* dw_gate, void* dx, void* workspace, size_t workspace_bytes,
                   hipStream_t stream);
+
+/*
+ * Kernel timing probe (diagnostics; not needed for computing anything).
+ * moe_probe_enable(capacity) creates `capacity` HIP events and starts
+ * recording: each entry point then records an event on its stream before its
+ * first kernel and one after every kernel it launches. Record i (0-based,
+ * counting kernel records only) is the time between the kernel's preceding
+ * event and its own, i.e. that kernel's duration on the stream. Recording
+ * stops silently when the events run out. moe_probe_get waits for record i
+ * and returns the kernel's name (static storage) and its duration in ms.
+ * moe_probe_disable destroys the events. Not thread-safe; single stream.
+ */
+int moe_probe_enable(int capacity);
+void moe_probe_disable(void);
+int moe_probe_count(void);
+int moe_probe_get(int index, const char** kernel_name, float* ms);
 
 #ifdef __cplusplus
 }

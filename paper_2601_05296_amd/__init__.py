@@ -9,4 +9,5 @@ layer's forward and backward; `synth` draws the seeded synthetic inputs.
 from .binding import (EXPORTS, MOE_ACCUMULATE, MOE_BF16, MOE_F32, MOE_RENORM, MoEError,  # noqa: F401
                       load_library, moe_build_index, moe_build_index_workspace_size,
                       moe_combine, moe_ffn_bwd, moe_ffn_bwd_workspace_size, moe_ffn_fwd,
+                      moe_ffn_fwd_workspace_size,
                       moe_route, moe_route_bwd, moe_route_bwd_workspace_size)

@@ -28,8 +28,9 @@ MOE_ACCUMULATE = 4
 
 # Every symbol declared in include/moeblaze.h.
 EXPORTS = ("moe_strerror", "moe_last_error", "moe_route", "moe_build_index_workspace_size",
-           "moe_build_index", "moe_ffn_fwd", "moe_combine", "moe_ffn_bwd_workspace_size",
-           "moe_ffn_bwd", "moe_route_bwd_workspace_size", "moe_route_bwd")
+           "moe_build_index", "moe_ffn_fwd_workspace_size", "moe_ffn_fwd", "moe_combine", "moe_ffn_bwd_workspace_size",
+           "moe_ffn_bwd", "moe_route_bwd_workspace_size", "moe_route_bwd", "moe_probe_enable",
+           "moe_probe_disable", "moe_probe_count", "moe_probe_get")
 
 
 class MoEError(RuntimeError):
@@ -62,12 +63,17 @@ def load_library(path: str = LIB):
         "moe_route": (I, [P, P, P, I64, I, I, I, U, P, P, P, P]),
         "moe_build_index_workspace_size": (SZ, [I64, I, I]),
         "moe_build_index": (I, [P, I64, I, I, P, P, P, P, P, P, SZ, P]),
-        "moe_ffn_fwd": (I, [P, P, P, P, P, P, I64, I, I, I, I, U, P, P, P, P]),
+        "moe_ffn_fwd_workspace_size": (SZ, [I64, I, I, I, I, U]),
+        "moe_ffn_fwd": (I, [P, P, P, P, P, P, I64, I, I, I, I, U, P, P, P, P, SZ, P]),
         "moe_combine": (I, [P, P, P, I64, I, I, U, P, P]),
         "moe_ffn_bwd_workspace_size": (SZ, [I64, I, I, I, I, U]),
         "moe_ffn_bwd": (I, [P] * 11 + [I64, I, I, I, I, U] + [P] * 6 + [SZ, P]),
         "moe_route_bwd_workspace_size": (SZ, [I64, I, I, I, U]),
         "moe_route_bwd": (I, [P] * 6 + [I64, I, I, I, U, P, P, P, SZ, P]),
+        "moe_probe_enable": (I, [I]),
+        "moe_probe_disable": (None, []),
+        "moe_probe_count": (I, []),
+        "moe_probe_get": (I, [I, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_float)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -125,11 +131,16 @@ def moe_build_index(topk_ids, T, E, k, counts, offsets, expert_token_indices, to
                                           _stream(stream)))
 
 
+def moe_ffn_fwd_workspace_size(T, d, f, E, k, flags) -> int:
+    return load_library().moe_ffn_fwd_workspace_size(T, d, f, E, k, flags)
+
+
 def moe_ffn_fwd(x, w1, w3, w2, offsets, expert_token_indices, T, d, f, E, k, flags, A, B, O,
-                stream=None):
+                workspace, workspace_bytes, stream=None):
     _check(load_library().moe_ffn_fwd(_ptr(x), _ptr(w1), _ptr(w3), _ptr(w2), _ptr(offsets),
                                       _ptr(expert_token_indices), T, d, f, E, k, flags, _ptr(A),
-                                      _ptr(B), _ptr(O), _stream(stream)))
+                                      _ptr(B), _ptr(O), _ptr(workspace), workspace_bytes,
+                                      _stream(stream)))
 
 
 def moe_combine(src, weights, token_index_map, T, d, k, flags, out, stream=None):
@@ -162,3 +173,23 @@ def moe_route_bwd(d_gates, logits, topk_ids, gates, x, w_gate, T, d, E, k, flags
                                         _ptr(gates), _ptr(x), _ptr(w_gate), T, d, E, k, flags,
                                         _ptr(dw_gate), _ptr(dx), _ptr(workspace),
                                         workspace_bytes, _stream(stream)))
+
+
+def moe_probe_enable(capacity: int):
+    _check(load_library().moe_probe_enable(capacity))
+
+
+def moe_probe_disable():
+    load_library().moe_probe_disable()
+
+
+def moe_probe_count() -> int:
+    return load_library().moe_probe_count()
+
+
+def moe_probe_get(index: int):
+    """Returns (kernel name, milliseconds) of kernel record `index`."""
+    name = ctypes.c_char_p()
+    ms = ctypes.c_float()
+    _check(load_library().moe_probe_get(index, ctypes.byref(name), ctypes.byref(ms)))
+    return name.value.decode(), ms.value

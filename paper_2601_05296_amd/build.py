@@ -16,7 +16,8 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmoeblaze.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["index.hip", "route.hip", "combine.hip", "ffn.hip", "route_bwd.hip", "api.cpp"]
+SOURCES = ["index.hip", "route.hip", "combine.hip", "ffn.hip", "route_bwd.hip", "api.cpp",
+           "probe.cpp"]
 
 # Packed-FP32 instructions are kept out of every code object.
 DEVICE_FLAGS = ["--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17",

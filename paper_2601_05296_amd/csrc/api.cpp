@@ -5,6 +5,7 @@
 
 #include "../../include/moeblaze.h"
 #include "launch.hpp"
+#include "probe.hpp"
 
 namespace {
 
@@ -75,6 +76,24 @@ const char* moe_strerror(int status) {
 
 const char* moe_last_error(void) { return g_err; }
 
+int moe_probe_enable(int capacity) {
+    if (capacity < 1) return fail(MOE_ERR_INVALID_ARG, "moe_probe_enable: capacity %d < 1", capacity);
+    if (moe::probe::enable(capacity) != 0)
+        return fail(MOE_ERR_HIP, "moe_probe_enable: hipEventCreate failed");
+    return MOE_OK;
+}
+
+void moe_probe_disable(void) { moe::probe::disable(); }
+
+int moe_probe_count(void) { return moe::probe::count(); }
+
+int moe_probe_get(int index, const char** kernel_name, float* ms) {
+    if (!kernel_name || !ms) return fail(MOE_ERR_INVALID_ARG, "moe_probe_get: NULL output");
+    if (moe::probe::get(index, kernel_name, ms) != 0)
+        return fail(MOE_ERR_INVALID_ARG, "moe_probe_get: no record %d", index);
+    return MOE_OK;
+}
+
 int moe_route(const void* x, const void* w_gate, const float* bias, int64_t T, int d, int E,
               int k, unsigned flags, int32_t* topk_ids, float* gates, float* logits,
               hipStream_t stream) {
@@ -85,6 +104,7 @@ int moe_route(const void* x, const void* w_gate, const float* bias, int64_t T, i
     if (T == 0) return MOE_OK;
     REQUIRE_PTR(x); REQUIRE_PTR(w_gate); OPT_PTR(bias); REQUIRE_PTR(topk_ids); REQUIRE_PTR(gates);
     OPT_PTR(logits);
+    moe::probe::begin(stream);
     return hip_status(fn, moe::route(x, w_gate, bias, T, d, E, k, flags & MOE_F32,
                                      flags & MOE_RENORM, topk_ids, gates, logits, stream));
 }
@@ -108,14 +128,20 @@ int moe_build_index(const int32_t* topk_ids, int64_t T, int E, int k, int32_t* c
     if (!workspace || workspace_bytes < need)
         return fail(MOE_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, workspace_bytes, need);
     REQUIRE_PTR(workspace);
+    moe::probe::begin(stream);
     return hip_status(fn, moe::build_index(topk_ids, T, E, k, counts, offsets, expert_token_indices,
                                            token_index_map, slot_src, workspace, stream));
 }
 
+size_t moe_ffn_fwd_workspace_size(int64_t T, int d, int f, int E, int k, unsigned flags) {
+    if (T <= 0 || d < 1 || f < 1 || E < 1 || k < 1) return 0;
+    return moe::ffn_fwd_workspace(T, d, f, E, k, flags & MOE_F32);
+}
+
 int moe_ffn_fwd(const void* x, const void* w1, const void* w3, const void* w2,
                 const int32_t* offsets, const int32_t* expert_token_indices, int64_t T, int d,
-                int f, int E, int k, unsigned flags, void* A, void* B, void* O,
-                hipStream_t stream) {
+                int f, int E, int k, unsigned flags, void* A, void* B, void* O, void* workspace,
+                size_t workspace_bytes, hipStream_t stream) {
     const char* fn = "moe_ffn_fwd";
     int r;
     if ((r = check_common(fn, T, E, k, flags)) || (r = check_dim(fn, "d", d)) ||
@@ -126,9 +152,14 @@ int moe_ffn_fwd(const void* x, const void* w1, const void* w3, const void* w2,
     if (T == 0) return MOE_OK;
     REQUIRE_PTR(x); REQUIRE_PTR(w1); REQUIRE_PTR(w3); REQUIRE_PTR(w2); REQUIRE_PTR(offsets);
     REQUIRE_PTR(expert_token_indices); REQUIRE_PTR(A); REQUIRE_PTR(B); REQUIRE_PTR(O);
+    const size_t need = moe::ffn_fwd_workspace(T, d, f, E, k, flags & MOE_F32);
+    if (need && (!workspace || workspace_bytes < need))
+        return fail(MOE_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, workspace_bytes, need);
+    OPT_PTR(workspace);
     moe::FfnArgs a{};
     a.x = x; a.w1 = w1; a.w3 = w3; a.w2 = w2; a.offsets = offsets; a.eti = expert_token_indices;
-    a.A = A; a.B = B; a.O = O; a.T = T; a.d = d; a.f = f; a.E = E; a.k = k;
+    a.A = A; a.B = B; a.O = O; a.T = T; a.d = d; a.f = f; a.E = E; a.k = k; a.ws = workspace;
+    moe::probe::begin(stream);
     return hip_status(fn, moe::ffn_fwd(a, flags & MOE_F32, stream));
 }
 
@@ -140,6 +171,7 @@ int moe_combine(const void* src, const float* weights, const int32_t* token_inde
     if (flags & MOE_RENORM) return fail(MOE_ERR_INVALID_ARG, "%s: MOE_RENORM not valid here", fn);
     if (T == 0) return MOE_OK;
     REQUIRE_PTR(src); OPT_PTR(weights); REQUIRE_PTR(token_index_map); REQUIRE_PTR(out);
+    moe::probe::begin(stream);
     return hip_status(fn, moe::combine(src, weights, token_index_map, T, d, k, flags & MOE_F32,
                                        flags & MOE_ACCUMULATE, out, stream));
 }
@@ -175,6 +207,7 @@ int moe_ffn_bwd(const void* dy, const void* x, const void* w1, const void* w3, c
     a.slot_src = slot_src; a.gates = gates; a.dy = dy; a.A = A; a.B = B; a.dX = dX_slot;
     a.dw1 = dw1; a.dw3 = dw3; a.dw2 = dw2; a.dgates = d_gates; a.T = T; a.d = d; a.f = f;
     a.E = E; a.k = k; a.ws = workspace;
+    moe::probe::begin(stream);
     return hip_status(fn, moe::ffn_bwd(a, flags & MOE_F32, stream));
 }
 
@@ -197,6 +230,7 @@ int moe_route_bwd(const float* d_gates, const float* logits, const int32_t* topk
     if (!workspace || workspace_bytes < need)
         return fail(MOE_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, workspace_bytes, need);
     REQUIRE_PTR(workspace);
+    moe::probe::begin(stream);
     return hip_status(fn, moe::route_bwd(d_gates, logits, topk_ids, gates, x, w_gate, T, d, E, k,
                                          flags & MOE_F32, flags & MOE_RENORM,
                                          flags & MOE_ACCUMULATE, dw_gate, dx, workspace, stream));

@@ -11,6 +11,7 @@
 // which adds the k terms in order j = 0..k-1.
 #include "common.hpp"
 #include "launch.hpp"
+#include "probe.hpp"
 
 namespace moe {
 namespace {
@@ -91,12 +92,15 @@ combine_kernel(const void* __restrict__ src_, const float* __restrict__ w,
 hipError_t combine(const void* src, const float* w, const int32_t* tim, int64_t T, int d,
                    int k, bool f32, bool accumulate, void* out, hipStream_t st) {
     const dim3 grid((unsigned)((T + CMB_TOK - 1) / CMB_TOK));
-    if (f32)
+    if (f32) {
         hipLaunchKernelGGL(combine_kernel<true>, grid, dim3(CMB_THREADS), 0, st, src, w, tim,
                            T, d, k, (int)accumulate, out);
-    else
+        probe::mark("combine_f32", st);
+    } else {
         hipLaunchKernelGGL(combine_kernel<false>, grid, dim3(CMB_THREADS), 0, st, src, w, tim,
                            T, d, k, (int)accumulate, out);
+        probe::mark("combine", st);
+    }
     return hipGetLastError();
 }
 

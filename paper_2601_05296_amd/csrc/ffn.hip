@@ -28,306 +28,208 @@
 #include "common.hpp"
 #include "gemm.hpp"
 #include "launch.hpp"
+#include "probe.hpp"
 
 namespace moe {
 namespace {
 
-using C1 = GemmCfg<128, 128, 2, 2, 2>;  // G1, G5 (two right operands)
-using CS = GemmCfg<128, 128, 2, 2, 1>;  // G2, G3, G4, G6
+// Tile configurations: <BM, BN, WM, WN, NB>. 256-row tiles, 2x4 waves.
+// Single right operand: each wave owns 128 x 64 outputs. Two right operands
+// (G1: W1 and W3; G5: dA and dB): 128 x 32 of each.
+using CD = GemmCfg<256, 128, 2, 4, 2>;  // G1, G5
+using CS = GemmCfg<256, 256, 2, 4, 1>;  // G2, G3, G4, G6
 
 // ============================ operand loaders ===================================
+// Each loader issues its 1 KB global->LDS copies for one K slice (see
+// gemm.hpp). Rows or columns at or beyond the operand's extent are clamped to
+// valid memory; the epilogues never store the outputs that depend on them.
 
-// KC rows gathered through an index list: row r -> base[idx[r]] (rows beyond
-// `rows` read row 0; their results are discarded).
 template <class C, int R>
-struct GatherKC {
+struct KCBase {
     static constexpr bool MC = false;
-    using Map = KCMap<R, C::THREADS>;
-    const bf16_t* p[Map::NCH];
-    uint4 reg[Map::NCH];
+    static constexpr int NQ = R * GBK * 2 / 1024 / C::NW;  // copies per wave per slice
+    __device__ static int q(int i) { return (threadIdx.x >> 6) + i * C::NW; }
+};
+
+// KC rows gathered through an index list: row r -> base[idx[r]] (rows at or
+// beyond `rows` read row 0).
+template <class C, int R>
+struct GatherKC : KCBase<C, R> {
+    using KCBase<C, R>::NQ;
+    const bf16_t* p[NQ];
     __device__ void init(const bf16_t* base, int ld, const int32_t* idx, int rows) {
+        const int lane = threadIdx.x & 63;
 #pragma unroll
-        for (int i = 0; i < Map::NCH; ++i) {
-            int r = Map::row(threadIdx.x, i);
+        for (int i = 0; i < NQ; ++i) {
+            const int q = this->q(i);
+            int r = KCDma::row(q, lane);
             r = r < rows ? r : 0;
-            p[i] = base + (int64_t)idx[r] * ld + Map::kcol(threadIdx.x);
+            p[i] = base + (int64_t)idx[r] * ld + KCDma::kcol(q, lane);
         }
     }
-    __device__ void fetch(int kt) {
+    __device__ void issue(int kt, char* t) {
 #pragma unroll
-        for (int i = 0; i < Map::NCH; ++i) reg[i] = ld16(p[i] + kt * GBK);
-    }
-    __device__ void stage(char* t) {
-#pragma unroll
-        for (int i = 0; i < Map::NCH; ++i) st16(t + Map::off(threadIdx.x, i), reg[i]);
+        for (int i = 0; i < NQ; ++i) dma16(p[i] + kt * GBK, t + this->q(i) * 1024);
     }
 };
 
-// KC rows of a dense row-major matrix, K split over two sources:
-// k < ksplit from src0, k >= ksplit from src1 (same row, same ld).
+// KC rows row0 + r (r < rows, else row0) of a dense row-major matrix, K split
+// over two sources: k < ksplit from src0, k >= ksplit from src1 (same ld).
 template <class C, int R>
-struct DenseKC2 {
-    static constexpr bool MC = false;
-    using Map = KCMap<R, C::THREADS>;
-    const bf16_t* p0[Map::NCH];
-    const bf16_t* p1[Map::NCH];
+struct DenseKC2 : KCBase<C, R> {
+    using KCBase<C, R>::NQ;
+    const bf16_t* p0[NQ];
+    const bf16_t* p1[NQ];
     int kst;  // K slices served by src0
-    uint4 reg[Map::NCH];
     __device__ void init(const bf16_t* src0, const bf16_t* src1, int ld, int64_t row0, int rows,
                          int ksplit) {
+        const int lane = threadIdx.x & 63;
         kst = ksplit / GBK;
 #pragma unroll
-        for (int i = 0; i < Map::NCH; ++i) {
-            int r = Map::row(threadIdx.x, i);
+        for (int i = 0; i < NQ; ++i) {
+            const int q = this->q(i);
+            int r = KCDma::row(q, lane);
             r = r < rows ? r : 0;
-            const int64_t o = (row0 + r) * (int64_t)ld + Map::kcol(threadIdx.x);
+            const int64_t o = (row0 + r) * (int64_t)ld + KCDma::kcol(q, lane);
             p0[i] = src0 + o;
             p1[i] = src1 + o - (int64_t)ksplit;
         }
     }
-    __device__ void fetch(int kt) {
+    __device__ void issue(int kt, char* t) {
         const bool first = kt < kst;
 #pragma unroll
-        for (int i = 0; i < Map::NCH; ++i) reg[i] = ld16((first ? p0[i] : p1[i]) + kt * GBK);
-    }
-    __device__ void stage(char* t) {
-#pragma unroll
-        for (int i = 0; i < Map::NCH; ++i) st16(t + Map::off(threadIdx.x, i), reg[i]);
+        for (int i = 0; i < NQ; ++i)
+            dma16((first ? p0[i] : p1[i]) + kt * GBK, t + this->q(i) * 1024);
     }
 };
 
-// KC rows of h = SiLU(A) * B, computed from the saved A, B (rows = slots).
 template <class C, int R>
-struct SwigluKC {
-    static constexpr bool MC = false;
-    using Map = KCMap<R, C::THREADS>;
-    const bf16_t* pa[Map::NCH];
-    const bf16_t* pb[Map::NCH];
-    uint4 ra[Map::NCH], rb[Map::NCH];
-    __device__ void init(const bf16_t* A, const bf16_t* B, int ld, int64_t row0, int rows) {
-#pragma unroll
-        for (int i = 0; i < Map::NCH; ++i) {
-            int r = Map::row(threadIdx.x, i);
-            r = r < rows ? r : 0;
-            const int64_t o = (row0 + r) * (int64_t)ld + Map::kcol(threadIdx.x);
-            pa[i] = A + o;
-            pb[i] = B + o;
-        }
-    }
-    __device__ void fetch(int kt) {
-#pragma unroll
-        for (int i = 0; i < Map::NCH; ++i) {
-            ra[i] = ld16(pa[i] + kt * GBK);
-            rb[i] = ld16(pb[i] + kt * GBK);
-        }
-    }
-    __device__ void stage(char* t) {
-#pragma unroll
-        for (int i = 0; i < Map::NCH; ++i) {
-            float a[8], b[8], h[8];
-            unpack8(ra[i], a);
-            unpack8(rb[i], b);
-#pragma unroll
-            for (int j = 0; j < 8; ++j) h[j] = a[j] * sigmoidf_(a[j]) * b[j];
-            st16(t + Map::off(threadIdx.x, i), pack8(h));
-        }
-    }
-};
-
-// MC tile of a dense row-major [K][N] matrix (K rows k0.., columns col0..).
-template <class C, int R>
-struct DenseMC {
+struct MCBase {
     static constexpr bool MC = true;
-    using Map = MCMap<R, C::THREADS>;
-    const bf16_t* p[Map::NCH];
+    using D = MCDma<R>;
+    static constexpr int NQ = GBK * R * 2 / 1024 / C::NW;
+    __device__ static int q(int i) { return (threadIdx.x >> 6) + i * C::NW; }
+    // column of copy i for this lane, clamped into [0, ncols)
+    __device__ static int colc(int i, int col0, int ncols) {
+        const int c = col0 + D::col(q(i), threadIdx.x & 63);
+        return c < ncols ? c : ncols - 8;
+    }
+    __device__ static int krow(int i) { return D::krow(q(i), threadIdx.x & 63); }
+};
+
+// MC tile of a dense row-major [K][ncols] matrix, columns col0..
+template <class C, int R>
+struct DenseMC : MCBase<C, R> {
+    using MCBase<C, R>::NQ;
+    const bf16_t* p[NQ];
     int64_t step;
-    uint4 reg[Map::NCH];
-    __device__ void init(const bf16_t* W, int ld, int col0) {
+    __device__ void init(const bf16_t* W, int ld, int col0, int ncols) {
         step = (int64_t)GBK * ld;
 #pragma unroll
-        for (int i = 0; i < Map::NCH; ++i)
-            p[i] = W + (int64_t)Map::krow(threadIdx.x, i) * ld + col0 + Map::col(threadIdx.x);
+        for (int i = 0; i < NQ; ++i)
+            p[i] = W + (int64_t)this->krow(i) * ld + this->colc(i, col0, ncols);
     }
-    __device__ void fetch(int kt) {
+    __device__ void issue(int kt, char* t) {
 #pragma unroll
-        for (int i = 0; i < Map::NCH; ++i) reg[i] = ld16(p[i] + kt * step);
-    }
-    __device__ void stage(char* t) {
-#pragma unroll
-        for (int i = 0; i < Map::NCH; ++i) st16(t + Map::off(threadIdx.x, i), reg[i]);
+        for (int i = 0; i < NQ; ++i) dma16(p[i] + kt * step, t + this->q(i) * 1024);
     }
 };
 
 // ---- loaders whose K is the slot dimension of one expert (weight gradients) ----
-// K row kr (0 <= kr < cnt) is slot off + kr. Rows at or past cnt are either
-// zero (ZERO = true; used for the left operand so the tail adds nothing) or a
-// copy of a valid row (right operand; multiplied by the zero rows).
+// K row kr (0 <= kr < cnt) is slot off + kr; rows at or past cnt are clamped to
+// row cnt - 1 (the main loop zeroes them in the left operand).
 
 // MC rows gathered through eti: row kr -> base[eti[off + kr]] (x or dY).
-// Indices are fetched one slice ahead of the data.
-template <class C, int R, bool ZERO>
-struct GatherMC {
-    static constexpr bool MC = true;
-    using Map = MCMap<R, C::THREADS>;
-    const bf16_t* base;
+// Indices are read one slice ahead of the copies that use them.
+template <class C, int R>
+struct GatherMC : MCBase<C, R> {
+    using MCBase<C, R>::NQ;
+    const bf16_t* base[NQ];
     const int32_t* idx;  // eti + off
     int ld, cnt;
-    int nidx[Map::NCH];
-    uint4 reg[Map::NCH];
+    int nidx[NQ];
     __device__ int load_idx(int kt, int i) const {
-        int kr = kt * GBK + Map::krow(threadIdx.x, i);
+        int kr = kt * GBK + this->krow(i);
         kr = kr < cnt ? kr : cnt - 1;
         return idx[kr];
     }
-    __device__ void init(const bf16_t* b, int ld_, int col0, const int32_t* ix, int cnt_) {
-        base = b + col0 + Map::col(threadIdx.x);
+    __device__ void init(const bf16_t* b, int ld_, int col0, int ncols, const int32_t* ix,
+                         int cnt_) {
         ld = ld_;
         idx = ix;
         cnt = cnt_;
 #pragma unroll
-        for (int i = 0; i < Map::NCH; ++i) nidx[i] = load_idx(0, i);
+        for (int i = 0; i < NQ; ++i) {
+            base[i] = b + this->colc(i, col0, ncols);
+            nidx[i] = load_idx(0, i);
+        }
     }
-    __device__ void fetch(int kt) {
+    __device__ void issue(int kt, char* t) {
 #pragma unroll
-        for (int i = 0; i < Map::NCH; ++i) {
-            const int kr = kt * GBK + Map::krow(threadIdx.x, i);
-            uint4 v = ld16(base + (int64_t)nidx[i] * ld);
-            if (ZERO && kr >= cnt) v = zero16();
-            reg[i] = v;
+        for (int i = 0; i < NQ; ++i) {
+            dma16(base[i] + (int64_t)nidx[i] * ld, t + this->q(i) * 1024);
             nidx[i] = load_idx(kt + 1, i);
         }
     }
-    __device__ void stage(char* t) {
-#pragma unroll
-        for (int i = 0; i < Map::NCH; ++i) st16(t + Map::off(threadIdx.x, i), reg[i]);
-    }
 };
 
-// MC rows of a slot-ordered matrix (dA or dB): row kr -> src[off + kr].
+// MC rows of a slot-ordered matrix (g*h, dA or dB): row kr -> src[off + kr].
 template <class C, int R>
-struct SlotMC {
-    static constexpr bool MC = true;
-    using Map = MCMap<R, C::THREADS>;
-    const bf16_t* base;
+struct SlotMC : MCBase<C, R> {
+    using MCBase<C, R>::NQ;
+    const bf16_t* base[NQ];
     int ld, cnt;
-    uint4 reg[Map::NCH];
-    __device__ void init(const bf16_t* src, int ld_, int64_t off, int col0, int cnt_) {
-        base = src + off * ld_ + col0 + Map::col(threadIdx.x);
-        ld = ld_;
-        cnt = cnt_;
-    }
-    __device__ void fetch(int kt) {
-#pragma unroll
-        for (int i = 0; i < Map::NCH; ++i) {
-            int kr = kt * GBK + Map::krow(threadIdx.x, i);
-            kr = kr < cnt ? kr : cnt - 1;
-            reg[i] = ld16(base + (int64_t)kr * ld);
-        }
-    }
-    __device__ void stage(char* t) {
-#pragma unroll
-        for (int i = 0; i < Map::NCH; ++i) st16(t + Map::off(threadIdx.x, i), reg[i]);
-    }
-};
-
-// MC rows of g * SiLU(A) * B (h scaled by the slot's gate), zero past cnt.
-template <class C, int R>
-struct SwigluGateMC {
-    static constexpr bool MC = true;
-    using Map = MCMap<R, C::THREADS>;
-    const bf16_t* pa;
-    const bf16_t* pb;
-    const float* gates;
-    const int32_t* src;  // slot_src + off
-    int ld, cnt;
-    float ng[Map::NCH];
-    uint4 ra[Map::NCH], rb[Map::NCH];
-    float rg[Map::NCH];
-    __device__ float load_g(int kt, int i) const {
-        int kr = kt * GBK + Map::krow(threadIdx.x, i);
-        if (kr >= cnt) return 0.0f;
-        return gates[src[kr]];
-    }
-    __device__ void init(const bf16_t* A, const bf16_t* B, const float* g, const int32_t* ss,
-                         int ld_, int64_t off, int col0, int cnt_) {
-        const int64_t o = off * ld_ + col0 + Map::col(threadIdx.x);
-        pa = A + o;
-        pb = B + o;
-        gates = g;
-        src = ss;
+    __device__ void init(const bf16_t* src, int ld_, int64_t off, int col0, int ncols, int cnt_) {
         ld = ld_;
         cnt = cnt_;
 #pragma unroll
-        for (int i = 0; i < Map::NCH; ++i) ng[i] = load_g(0, i);
+        for (int i = 0; i < NQ; ++i) base[i] = src + off * ld_ + this->colc(i, col0, ncols);
     }
-    __device__ void fetch(int kt) {
+    __device__ void issue(int kt, char* t) {
 #pragma unroll
-        for (int i = 0; i < Map::NCH; ++i) {
-            int kr = kt * GBK + Map::krow(threadIdx.x, i);
+        for (int i = 0; i < NQ; ++i) {
+            int kr = kt * GBK + this->krow(i);
             kr = kr < cnt ? kr : cnt - 1;
-            ra[i] = ld16(pa + (int64_t)kr * ld);
-            rb[i] = ld16(pb + (int64_t)kr * ld);
-            rg[i] = ng[i];
-            ng[i] = load_g(kt + 1, i);
-        }
-    }
-    __device__ void stage(char* t) {
-#pragma unroll
-        for (int i = 0; i < Map::NCH; ++i) {
-            float a[8], b[8], h[8];
-            unpack8(ra[i], a);
-            unpack8(rb[i], b);
-#pragma unroll
-            for (int j = 0; j < 8; ++j) h[j] = rg[i] * (a[j] * sigmoidf_(a[j]) * b[j]);
-            st16(t + Map::off(threadIdx.x, i), pack8(h));
+            dma16(base[i] + (int64_t)kr * ld, t + this->q(i) * 1024);
         }
     }
 };
+
+// k rows of the last slice at or beyond the expert's token count
+__device__ __forceinline__ int tail_from(int cnt) {
+    const int r = cnt % GBK;
+    return r == 0 ? GBK : r;
+}
 
 // ============================ epilogue helpers ===================================
 
-// Store acc (one 16x16 fragment row-slice: 4 consecutive columns) as bf16.
-__device__ __forceinline__ void store4_bf16(bf16_t* p, const f32x4& v) {
-    uint2 w;
-    w.x = pack_bf2(v[0], v[1]);
-    w.y = pack_bf2(v[2], v[3]);
-    *reinterpret_cast<uint2*>(p) = w;
+__device__ __forceinline__ void store4_bf16(bf16_t* p, float a, float b, float c, float d) {
+    *reinterpret_cast<uint2*>(p) = make_uint2(pack_bf2(a, b), pack_bf2(c, d));
 }
-
-template <class C>
-struct WaveCoord {
-    int lane, wm, wn;
-    __device__ WaveCoord() {
-        lane = threadIdx.x & 63;
-        const int wv = threadIdx.x >> 6;
-        wm = wv / C::WN;
-        wn = wv % C::WN;
-    }
-    __device__ int row(int fm) const { return wm * C::WTM + fm * 16 + (lane & 15); }
-    __device__ int col(int fn) const { return wn * C::WTN + fn * 16 + (lane >> 4) * 4; }
-};
+__device__ __forceinline__ float silu_bf(float a) { return a * sigmoidf_(a); }
 
 // ============================ kernels ==============================================
 
-// G1: A = x[eti] W1[e], B = x[eti] W3[e]
-__global__ void __launch_bounds__(C1::THREADS)
+// G1: A = x[eti] W1[e], B = x[eti] W3[e]; also H = SiLU(A) * B (from the
+// bf16-rounded A and B, exactly as the backward recomputes it).
+__global__ void __launch_bounds__(CD::THREADS)
 g1_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w1,
           const bf16_t* __restrict__ w3, const int32_t* __restrict__ offsets,
           const int32_t* __restrict__ eti, int d, int f, int E, bf16_t* __restrict__ A,
-          bf16_t* __restrict__ B) {
+          bf16_t* __restrict__ B, bf16_t* __restrict__ H) {
     extern __shared__ __align__(16) char lds[];
-    using C = C1;
+    using C = CD;
     SlotTile t;
-    const int NT = f / C::BN;
+    const int NT = (f + C::BN - 1) / C::BN;
     if (!find_slot_tile<C::THREADS>(offsets, E, C::BM, NT, xcd_remap(blockIdx.x, gridDim.x), C::BN, t))
         return;
     GatherKC<C, C::BM> la;
     la.init(x, d, eti + t.off + t.m0, t.mrows);
     DenseMC<C, C::BN> lb0, lb1;
-    lb0.init(w1 + (int64_t)t.e * d * f, f, t.n0);
-    lb1.init(w3 + (int64_t)t.e * d * f, f, t.n0);
-    f32x4 acc[C::NB][C::FM][C::FN];
-    gemm_mainloop<C>(la, lb0, lb1, d / GBK, lds, acc);
+    lb0.init(w1 + (int64_t)t.e * d * f, f, t.n0, f);
+    lb1.init(w3 + (int64_t)t.e * d * f, f, t.n0, f);
+    Acc<C> acc;
+    gemm_mainloop<C>(la, lb0, lb1, d / GBK, GBK, lds, acc);
     WaveCoord<C> wc;
 #pragma unroll
     for (int i = 0; i < C::FM; ++i) {
@@ -335,32 +237,42 @@ g1_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w1,
         if (m >= t.mrows) continue;
         const int64_t s = (int64_t)t.off + t.m0 + m;
 #pragma unroll
-        for (int j = 0; j < C::FN; ++j) {
-            const int n = t.n0 + wc.col(j);
-            store4_bf16(A + s * f + n, acc[0][i][j]);
-            store4_bf16(B + s * f + n, acc[1][i][j]);
-        }
+        for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int n = t.n0 + wc.col(j, q);
+                if (n >= f) continue;
+                float a[4], b[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    a[r] = bf2f(f2bf(acc[0][i][j][4 * q + r]));
+                    b[r] = bf2f(f2bf(acc[1][i][j][4 * q + r]));
+                }
+                store4_bf16(A + s * f + n, a[0], a[1], a[2], a[3]);
+                store4_bf16(B + s * f + n, b[0], b[1], b[2], b[3]);
+                store4_bf16(H + s * f + n, silu_bf(a[0]) * b[0], silu_bf(a[1]) * b[1],
+                            silu_bf(a[2]) * b[2], silu_bf(a[3]) * b[3]);
+            }
     }
 }
 
-// G2: O = (SiLU(A) * B) W2[e]
+// G2: O = H W2[e]
 __global__ void __launch_bounds__(CS::THREADS)
-g2_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B,
-          const bf16_t* __restrict__ w2, const int32_t* __restrict__ offsets, int d, int f,
-          int E, bf16_t* __restrict__ O) {
+g2_kernel(const bf16_t* __restrict__ H, const bf16_t* __restrict__ w2,
+          const int32_t* __restrict__ offsets, int d, int f, int E, bf16_t* __restrict__ O) {
     extern __shared__ __align__(16) char lds[];
     using C = CS;
     SlotTile t;
-    const int NT = d / C::BN;
+    const int NT = (d + C::BN - 1) / C::BN;
     if (!find_slot_tile<C::THREADS>(offsets, E, C::BM, NT, xcd_remap(blockIdx.x, gridDim.x), C::BN, t))
         return;
-    SwigluKC<C, C::BM> la;
-    la.init(A, B, f, (int64_t)t.off + t.m0, t.mrows);
+    DenseKC2<C, C::BM> la;
+    la.init(H, H, f, (int64_t)t.off + t.m0, t.mrows, f);
     DenseMC<C, C::BN> lb;
-    lb.init(w2 + (int64_t)t.e * f * d, d, t.n0);
+    lb.init(w2 + (int64_t)t.e * f * d, d, t.n0, d);
     NoLoader nl;
-    f32x4 acc[C::NB][C::FM][C::FN];
-    gemm_mainloop<C>(la, lb, nl, f / GBK, lds, acc);
+    Acc<C> acc;
+    gemm_mainloop<C>(la, lb, nl, f / GBK, GBK, lds, acc);
     WaveCoord<C> wc;
 #pragma unroll
     for (int i = 0; i < C::FM; ++i) {
@@ -368,66 +280,39 @@ g2_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B,
         if (m >= t.mrows) continue;
         const int64_t s = (int64_t)t.off + t.m0 + m;
 #pragma unroll
-        for (int j = 0; j < C::FN; ++j) store4_bf16(O + s * d + t.n0 + wc.col(j), acc[0][i][j]);
-    }
-}
-
-// G3: dW2[e] = sum_s (g_s h_s)^T dY[eti[s]]   (M = f, N = d, K = slots of e)
-__global__ void __launch_bounds__(CS::THREADS)
-g3_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B,
-          const bf16_t* __restrict__ dy, const float* __restrict__ gates,
-          const int32_t* __restrict__ offsets, const int32_t* __restrict__ eti,
-          const int32_t* __restrict__ slot_src, int d, int f, float* __restrict__ dw2) {
-    extern __shared__ __align__(16) char lds[];
-    using C = CS;
-    const int MT = f / C::BM, NT = d / C::BN;
-    const int bid = blockIdx.x;
-    const int e = bid / (MT * NT);
-    const int rem = bid % (MT * NT);
-    const int m0 = (rem % MT) * C::BM;
-    const int n0 = (rem / MT) * C::BN;
-    const int off = offsets[e];
-    const int cnt = offsets[e + 1] - off;
-    SwigluGateMC<C, C::BM> la;
-    GatherMC<C, C::BN, false> lb;
-    NoLoader nl;
-    if (cnt > 0) {
-        la.init(A, B, gates, slot_src + off, f, off, m0, cnt);
-        lb.init(dy, d, n0, eti + off, cnt);
-    }
-    f32x4 acc[C::NB][C::FM][C::FN];
-    gemm_mainloop<C>(la, lb, nl, (cnt + GBK - 1) / GBK, lds, acc);
-    WaveCoord<C> wc;
-    float* out = dw2 + (int64_t)e * f * d;
-#pragma unroll
-    for (int i = 0; i < C::FM; ++i) {
-        const int m = m0 + wc.row(i);
-#pragma unroll
         for (int j = 0; j < C::FN; ++j)
-            *reinterpret_cast<f32x4*>(out + (int64_t)m * d + n0 + wc.col(j)) = acc[0][i][j];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int n = t.n0 + wc.col(j, q);
+                if (n >= d) continue;
+                const f32x16& v = acc[0][i][j];
+                store4_bf16(O + s * d + n, v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+            }
     }
 }
 
-// G4: u = dY[eti] W2[e]^T; epilogue: d_gate partials, dA/dB over A/B.
+// G4: u = dY[eti] W2[e]^T; epilogue: d_gate partials sum(u*h), dA/dB over
+// A/B, and HG = g * h (h recomputed from A, B) for G3.
 __global__ void __launch_bounds__(CS::THREADS)
 g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
           const float* __restrict__ gates, const int32_t* __restrict__ offsets,
           const int32_t* __restrict__ eti, const int32_t* __restrict__ slot_src, int d, int f,
-          int E, bf16_t* __restrict__ A, bf16_t* __restrict__ B, float* __restrict__ part) {
+          int E, bf16_t* __restrict__ A, bf16_t* __restrict__ B, bf16_t* __restrict__ HG,
+          float* __restrict__ part) {
     extern __shared__ __align__(16) char lds[];
     using C = CS;
     SlotTile t;
-    const int NT = f / C::BN;
+    const int NT = (f + C::BN - 1) / C::BN;
     if (!find_slot_tile<C::THREADS>(offsets, E, C::BM, NT, xcd_remap(blockIdx.x, gridDim.x), C::BN, t))
         return;
     GatherKC<C, C::BM> la;
     la.init(dy, d, eti + t.off + t.m0, t.mrows);
     DenseKC2<C, C::BN> lb;  // rows c of W2[e] ([f][d]), K = d
     const bf16_t* W2e = w2 + (int64_t)t.e * f * d;
-    lb.init(W2e, W2e, d, t.n0, C::BN, d);
+    lb.init(W2e, W2e, d, t.n0, min(C::BN, f - t.n0), d);
     NoLoader nl;
-    f32x4 acc[C::NB][C::FM][C::FN];
-    gemm_mainloop<C>(la, lb, nl, d / GBK, lds, acc);
+    Acc<C> acc;
+    gemm_mainloop<C>(la, lb, nl, d / GBK, GBK, lds, acc);
     WaveCoord<C> wc;
     const int nparts = NT * C::WN;
     const int pidx = (t.n0 / C::BN) * C::WN + wc.wn;
@@ -437,47 +322,57 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
         const bool valid = m < t.mrows;
         const int64_t s = (int64_t)t.off + t.m0 + (valid ? m : 0);
         const float g = gates[slot_src[s]];
+        // all A/B loads of this row block first (they alias the stores below)
+        uint2 av[C::FN][4], bv[C::FN][4];
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                int n = t.n0 + wc.col(j, q);
+                n = n < f ? n : f - 4;
+                av[j][q] = *reinterpret_cast<const uint2*>(A + s * f + n);
+                bv[j][q] = *reinterpret_cast<const uint2*>(B + s * f + n);
+            }
         float dg = 0.f;
 #pragma unroll
-        for (int j = 0; j < C::FN; ++j) {
-            const int n = t.n0 + wc.col(j);
-            bf16_t* pa = A + s * f + n;
-            bf16_t* pb = B + s * f + n;
-            const uint2 av = *reinterpret_cast<const uint2*>(pa);
-            const uint2 bv = *reinterpret_cast<const uint2*>(pb);
-            const float a[4] = {bf_lo(av.x), bf_hi(av.x), bf_lo(av.y), bf_hi(av.y)};
-            const float b[4] = {bf_lo(bv.x), bf_hi(bv.x), bf_lo(bv.y), bf_hi(bv.y)};
-            float da[4], db[4];
+        for (int j = 0; j < C::FN; ++j)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const float u = acc[0][i][j][r];
-                const float sg = sigmoidf_(a[r]);
-                const float sl = a[r] * sg;
-                dg += u * sl * b[r];
-                const float dh = g * u;
-                da[r] = dh * b[r] * sg * (1.0f + a[r] * (1.0f - sg));
-                db[r] = dh * sl;
+            for (int q = 0; q < 4; ++q) {
+                const int n = t.n0 + wc.col(j, q);
+                const float a[4] = {bf_lo(av[j][q].x), bf_hi(av[j][q].x), bf_lo(av[j][q].y), bf_hi(av[j][q].y)};
+                const float b[4] = {bf_lo(bv[j][q].x), bf_hi(bv[j][q].x), bf_lo(bv[j][q].y), bf_hi(bv[j][q].y)};
+                float da[4], db[4], hg[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const float u = acc[0][i][j][4 * q + r];
+                    const float sg = sigmoidf_(a[r]);
+                    const float sl = a[r] * sg;
+                    const float h = sl * b[r];
+                    dg += n < f ? u * h : 0.f;
+                    hg[r] = g * h;
+                    const float dh = g * u;
+                    da[r] = dh * b[r] * sg * (1.0f + a[r] * (1.0f - sg));
+                    db[r] = dh * sl;
+                }
+                if (valid && n < f) {
+                    store4_bf16(A + s * f + n, da[0], da[1], da[2], da[3]);
+                    store4_bf16(B + s * f + n, db[0], db[1], db[2], db[3]);
+                    store4_bf16(HG + s * f + n, hg[0], hg[1], hg[2], hg[3]);
+                }
             }
-            if (valid) {
-                *reinterpret_cast<uint2*>(pa) = make_uint2(pack_bf2(da[0], da[1]), pack_bf2(da[2], da[3]));
-                *reinterpret_cast<uint2*>(pb) = make_uint2(pack_bf2(db[0], db[1]), pack_bf2(db[2], db[3]));
-            }
-        }
-        dg += __shfl_xor(dg, 16, 64);
         dg += __shfl_xor(dg, 32, 64);
-        if (valid && (wc.lane >> 4) == 0) part[s * nparts + pidx] = dg;
+        if (valid && wc.lane < 32) part[s * nparts + pidx] = dg;
     }
 }
 
-// G5: dW1[e] = x[eti]^T dA, dW3[e] = x[eti]^T dB   (M = d, N = f, K = slots of e)
-__global__ void __launch_bounds__(C1::THREADS)
-g5_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ dA,
-          const bf16_t* __restrict__ dB, const int32_t* __restrict__ offsets,
-          const int32_t* __restrict__ eti, int d, int f, float* __restrict__ dw1,
-          float* __restrict__ dw3) {
+// G3: dW2[e] = sum_s HG[s]^T dY[eti[s]]   (M = f, N = d, K = slots of e)
+__global__ void __launch_bounds__(CS::THREADS)
+g3_kernel(const bf16_t* __restrict__ HG, const bf16_t* __restrict__ dy,
+          const int32_t* __restrict__ offsets, const int32_t* __restrict__ eti, int d, int f,
+          float* __restrict__ dw2) {
     extern __shared__ __align__(16) char lds[];
-    using C = C1;
-    const int MT = d / C::BM, NT = f / C::BN;
+    using C = CS;
+    const int MT = (f + C::BM - 1) / C::BM, NT = (d + C::BN - 1) / C::BN;
     const int bid = blockIdx.x;
     const int e = bid / (MT * NT);
     const int rem = bid % (MT * NT);
@@ -485,27 +380,78 @@ g5_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ dA,
     const int n0 = (rem / MT) * C::BN;
     const int off = offsets[e];
     const int cnt = offsets[e + 1] - off;
-    GatherMC<C, C::BM, true> la;
+    SlotMC<C, C::BM> la;
+    GatherMC<C, C::BN> lb;
+    NoLoader nl;
+    if (cnt > 0) {
+        la.init(HG, f, off, m0, f, cnt);
+        lb.init(dy, d, n0, d, eti + off, cnt);
+    }
+    Acc<C> acc;
+    gemm_mainloop<C>(la, lb, nl, (cnt + GBK - 1) / GBK, tail_from(cnt), lds, acc);
+    WaveCoord<C> wc;
+    float* out = dw2 + (int64_t)e * f * d;
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i) {
+        const int m = m0 + wc.row(i);
+        if (m >= f) continue;
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int n = n0 + wc.col(j, q);
+                if (n >= d) continue;
+                const f32x16& v = acc[0][i][j];
+                *reinterpret_cast<f32x4*>(out + (int64_t)m * d + n) =
+                    f32x4{v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
+            }
+    }
+}
+
+// G5: dW1[e] = x[eti]^T dA, dW3[e] = x[eti]^T dB   (M = d, N = f, K = slots of e)
+__global__ void __launch_bounds__(CD::THREADS)
+g5_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ dA,
+          const bf16_t* __restrict__ dB, const int32_t* __restrict__ offsets,
+          const int32_t* __restrict__ eti, int d, int f, float* __restrict__ dw1,
+          float* __restrict__ dw3) {
+    extern __shared__ __align__(16) char lds[];
+    using C = CD;
+    const int MT = (d + C::BM - 1) / C::BM, NT = (f + C::BN - 1) / C::BN;
+    const int bid = blockIdx.x;
+    const int e = bid / (MT * NT);
+    const int rem = bid % (MT * NT);
+    const int m0 = (rem % MT) * C::BM;
+    const int n0 = (rem / MT) * C::BN;
+    const int off = offsets[e];
+    const int cnt = offsets[e + 1] - off;
+    GatherMC<C, C::BM> la;
     SlotMC<C, C::BN> lb0, lb1;
     if (cnt > 0) {
-        la.init(x, d, m0, eti + off, cnt);
-        lb0.init(dA, f, off, n0, cnt);
-        lb1.init(dB, f, off, n0, cnt);
+        la.init(x, d, m0, d, eti + off, cnt);
+        lb0.init(dA, f, off, n0, f, cnt);
+        lb1.init(dB, f, off, n0, f, cnt);
     }
-    f32x4 acc[C::NB][C::FM][C::FN];
-    gemm_mainloop<C>(la, lb0, lb1, (cnt + GBK - 1) / GBK, lds, acc);
+    Acc<C> acc;
+    gemm_mainloop<C>(la, lb0, lb1, (cnt + GBK - 1) / GBK, tail_from(cnt), lds, acc);
     WaveCoord<C> wc;
     float* o1 = dw1 + (int64_t)e * d * f;
     float* o3 = dw3 + (int64_t)e * d * f;
 #pragma unroll
     for (int i = 0; i < C::FM; ++i) {
         const int m = m0 + wc.row(i);
+        if (m >= d) continue;
 #pragma unroll
-        for (int j = 0; j < C::FN; ++j) {
-            const int64_t o = (int64_t)m * f + n0 + wc.col(j);
-            *reinterpret_cast<f32x4*>(o1 + o) = acc[0][i][j];
-            *reinterpret_cast<f32x4*>(o3 + o) = acc[1][i][j];
-        }
+        for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int n = n0 + wc.col(j, q);
+                if (n >= f) continue;
+                const int64_t o = (int64_t)m * f + n;
+                const f32x16& v1 = acc[0][i][j];
+                const f32x16& v3 = acc[1][i][j];
+                *reinterpret_cast<f32x4*>(o1 + o) = f32x4{v1[4 * q], v1[4 * q + 1], v1[4 * q + 2], v1[4 * q + 3]};
+                *reinterpret_cast<f32x4*>(o3 + o) = f32x4{v3[4 * q], v3[4 * q + 1], v3[4 * q + 2], v3[4 * q + 3]};
+            }
     }
 }
 
@@ -517,16 +463,16 @@ g6_kernel(const bf16_t* __restrict__ dA, const bf16_t* __restrict__ dB,
     extern __shared__ __align__(16) char lds[];
     using C = CS;
     SlotTile t;
-    const int NT = d / C::BN;
+    const int NT = (d + C::BN - 1) / C::BN;
     if (!find_slot_tile<C::THREADS>(offsets, E, C::BM, NT, xcd_remap(blockIdx.x, gridDim.x), C::BN, t))
         return;
     DenseKC2<C, C::BM> la;
     la.init(dA, dB, f, (int64_t)t.off + t.m0, t.mrows, f);
     DenseKC2<C, C::BN> lb;  // rows i of W1[e] / W3[e] ([d][f]), K = f then f
-    lb.init(w1 + (int64_t)t.e * d * f, w3 + (int64_t)t.e * d * f, f, t.n0, C::BN, f);
+    lb.init(w1 + (int64_t)t.e * d * f, w3 + (int64_t)t.e * d * f, f, t.n0, min(C::BN, d - t.n0), f);
     NoLoader nl;
-    f32x4 acc[C::NB][C::FM][C::FN];
-    gemm_mainloop<C>(la, lb, nl, 2 * f / GBK, lds, acc);
+    Acc<C> acc;
+    gemm_mainloop<C>(la, lb, nl, 2 * f / GBK, GBK, lds, acc);
     WaveCoord<C> wc;
 #pragma unroll
     for (int i = 0; i < C::FM; ++i) {
@@ -534,7 +480,14 @@ g6_kernel(const bf16_t* __restrict__ dA, const bf16_t* __restrict__ dB,
         if (m >= t.mrows) continue;
         const int64_t s = (int64_t)t.off + t.m0 + m;
 #pragma unroll
-        for (int j = 0; j < C::FN; ++j) store4_bf16(dX + s * d + t.n0 + wc.col(j), acc[0][i][j]);
+        for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int n = t.n0 + wc.col(j, q);
+                if (n >= d) continue;
+                const f32x16& v = acc[0][i][j];
+                store4_bf16(dX + s * d + n, v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+            }
     }
 }
 
@@ -666,6 +619,12 @@ __global__ void f32_g6(const float* dA, const float* dB, const float* w1, const 
 
 inline dim3 grid1d(int64_t n, int bs) { return dim3((unsigned)((n + bs - 1) / bs)); }
 
+// number of workgroups for a row-wise grouped GEMM (upper bound on tiles)
+inline unsigned slot_grid(int64_t S, int E, int BM, int NT) {
+    return (unsigned)(((S + BM - 1) / BM + E) * NT);
+}
+inline int cdiv(int a, int b) { return (a + b - 1) / b; }
+
 // Raise the dynamic LDS limit of the GEMM kernels once per process.
 hipError_t set_lds_limits() {
     static hipError_t status = [] {
@@ -674,23 +633,27 @@ hipError_t set_lds_limits() {
             if (e == hipSuccess)
                 e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
         };
-        set(reinterpret_cast<const void*>(g1_kernel), C1::LDS);
+        set(reinterpret_cast<const void*>(g1_kernel), CD::LDS);
         set(reinterpret_cast<const void*>(g2_kernel), CS::LDS);
         set(reinterpret_cast<const void*>(g3_kernel), CS::LDS);
         set(reinterpret_cast<const void*>(g4_kernel), CS::LDS);
-        set(reinterpret_cast<const void*>(g5_kernel), C1::LDS);
+        set(reinterpret_cast<const void*>(g5_kernel), CD::LDS);
         set(reinterpret_cast<const void*>(g6_kernel), CS::LDS);
         return e;
     }();
     return status;
 }
 
-// number of workgroups for a row-wise grouped GEMM (upper bound on tiles)
-inline unsigned slot_grid(int64_t S, int E, int BM, int NT) {
-    return (unsigned)(((S + BM - 1) / BM + E) * NT);
-}
+inline size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+inline int g4_nparts(int f) { return cdiv(f, CS::BN) * CS::WN; }
 
 }  // namespace
+
+size_t ffn_fwd_workspace(int64_t T, int d, int f, int E, int k, bool f32) {
+    (void)d; (void)E;
+    if (f32) return 0;
+    return align256((size_t)T * k * f * sizeof(bf16_t));  // H
+}
 
 hipError_t ffn_fwd(const FfnArgs& a, bool f32, hipStream_t st) {
     const int64_t S = a.T * a.k;
@@ -698,18 +661,24 @@ hipError_t ffn_fwd(const FfnArgs& a, bool f32, hipStream_t st) {
         hipLaunchKernelGGL(f32_g1, grid1d(S * a.f, 256), dim3(256), 0, st,
                            (const float*)a.x, (const float*)a.w1, (const float*)a.w3, a.offsets,
                            a.eti, S, a.d, a.f, a.E, (float*)a.A, (float*)a.B);
+        probe::mark("f32_g1", st);
         hipLaunchKernelGGL(f32_g2, grid1d(S * a.d, 256), dim3(256), 0, st,
                            (const float*)a.A, (const float*)a.B, (const float*)a.w2, a.offsets, S,
                            a.d, a.f, a.E, (float*)a.O);
+        probe::mark("f32_g2", st);
         return hipGetLastError();
     }
     if (hipError_t e = set_lds_limits(); e != hipSuccess) return e;
-    hipLaunchKernelGGL(g1_kernel, dim3(slot_grid(S, a.E, C1::BM, a.f / C1::BN)), dim3(C1::THREADS),
-                       C1::LDS, st, (const bf16_t*)a.x, (const bf16_t*)a.w1, (const bf16_t*)a.w3,
-                       a.offsets, a.eti, a.d, a.f, a.E, (bf16_t*)a.A, (bf16_t*)a.B);
-    hipLaunchKernelGGL(g2_kernel, dim3(slot_grid(S, a.E, CS::BM, a.d / CS::BN)), dim3(CS::THREADS),
-                       CS::LDS, st, (const bf16_t*)a.A, (const bf16_t*)a.B, (const bf16_t*)a.w2,
+    bf16_t* H = static_cast<bf16_t*>(a.ws);
+    hipLaunchKernelGGL(g1_kernel, dim3(slot_grid(S, a.E, CD::BM, cdiv(a.f, CD::BN))),
+                       dim3(CD::THREADS), CD::LDS, st, (const bf16_t*)a.x, (const bf16_t*)a.w1,
+                       (const bf16_t*)a.w3, a.offsets, a.eti, a.d, a.f, a.E, (bf16_t*)a.A,
+                       (bf16_t*)a.B, H);
+    probe::mark("g1_kernel", st);
+    hipLaunchKernelGGL(g2_kernel, dim3(slot_grid(S, a.E, CS::BM, cdiv(a.d, CS::BN))),
+                       dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)H, (const bf16_t*)a.w2,
                        a.offsets, a.d, a.f, a.E, (bf16_t*)a.O);
+    probe::mark("g2_kernel", st);
     return hipGetLastError();
 }
 
@@ -717,8 +686,7 @@ size_t ffn_bwd_workspace(int64_t T, int d, int f, int E, int k, bool f32) {
     (void)d; (void)E;
     if (f32) return 0;
     const int64_t S = T * k;
-    const int nparts = (f / CS::BN) * CS::WN;
-    return (size_t)(S * nparts * (int64_t)sizeof(float));
+    return align256((size_t)S * g4_nparts(f) * sizeof(float)) + align256((size_t)S * f * sizeof(bf16_t));
 }
 
 hipError_t ffn_bwd(const FfnArgs& a, bool f32, hipStream_t st) {
@@ -727,34 +695,47 @@ hipError_t ffn_bwd(const FfnArgs& a, bool f32, hipStream_t st) {
         hipLaunchKernelGGL(f32_g3, grid1d((int64_t)a.E * a.f * a.d, 256), dim3(256), 0, st,
                            (const float*)a.A, (const float*)a.B, (const float*)a.dy, a.gates,
                            a.offsets, a.eti, a.slot_src, a.d, a.f, a.E, a.dw2);
+        probe::mark("f32_g3", st);
         hipLaunchKernelGGL(f32_g4, grid1d(S, 64), dim3(64), 0, st, (const float*)a.dy,
                            (const float*)a.w2, a.gates, a.offsets, a.eti, a.slot_src, S, a.d, a.f,
                            a.E, (float*)a.A, (float*)a.B, a.dgates);
+        probe::mark("f32_g4", st);
         hipLaunchKernelGGL(f32_g5, grid1d((int64_t)a.E * a.d * a.f, 256), dim3(256), 0, st,
                            (const float*)a.x, (const float*)a.A, (const float*)a.B, a.offsets,
                            a.eti, a.d, a.f, a.E, a.dw1, a.dw3);
+        probe::mark("f32_g5", st);
         hipLaunchKernelGGL(f32_g6, grid1d(S * a.d, 256), dim3(256), 0, st, (const float*)a.A,
                            (const float*)a.B, (const float*)a.w1, (const float*)a.w3, a.offsets,
                            S, a.d, a.f, a.E, (float*)a.dX);
+        probe::mark("f32_g6", st);
         return hipGetLastError();
     }
     if (hipError_t e = set_lds_limits(); e != hipSuccess) return e;
+    const int nparts = g4_nparts(a.f);
     float* part = static_cast<float*>(a.ws);
-    const int nparts = (a.f / CS::BN) * CS::WN;
-    hipLaunchKernelGGL(g3_kernel, dim3(a.E * (a.f / CS::BM) * (a.d / CS::BN)), dim3(CS::THREADS),
-                       CS::LDS, st, (const bf16_t*)a.A, (const bf16_t*)a.B, (const bf16_t*)a.dy,
-                       a.gates, a.offsets, a.eti, a.slot_src, a.d, a.f, a.dw2);
-    hipLaunchKernelGGL(g4_kernel, dim3(slot_grid(S, a.E, CS::BM, a.f / CS::BN)), dim3(CS::THREADS),
-                       CS::LDS, st, (const bf16_t*)a.dy, (const bf16_t*)a.w2, a.gates, a.offsets,
-                       a.eti, a.slot_src, a.d, a.f, a.E, (bf16_t*)a.A, (bf16_t*)a.B, part);
+    bf16_t* HG = reinterpret_cast<bf16_t*>(static_cast<char*>(a.ws) +
+                                           align256((size_t)S * nparts * sizeof(float)));
+    hipLaunchKernelGGL(g4_kernel, dim3(slot_grid(S, a.E, CS::BM, cdiv(a.f, CS::BN))),
+                       dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)a.dy, (const bf16_t*)a.w2,
+                       a.gates, a.offsets, a.eti, a.slot_src, a.d, a.f, a.E, (bf16_t*)a.A,
+                       (bf16_t*)a.B, HG, part);
+    probe::mark("g4_kernel", st);
     hipLaunchKernelGGL(dgate_reduce, grid1d(S, 256), dim3(256), 0, st, part, nparts, a.slot_src,
                        S, a.dgates);
-    hipLaunchKernelGGL(g5_kernel, dim3(a.E * (a.d / C1::BM) * (a.f / C1::BN)), dim3(C1::THREADS),
-                       C1::LDS, st, (const bf16_t*)a.x, (const bf16_t*)a.A, (const bf16_t*)a.B,
-                       a.offsets, a.eti, a.d, a.f, a.dw1, a.dw3);
-    hipLaunchKernelGGL(g6_kernel, dim3(slot_grid(S, a.E, CS::BM, a.d / CS::BN)), dim3(CS::THREADS),
-                       CS::LDS, st, (const bf16_t*)a.A, (const bf16_t*)a.B, (const bf16_t*)a.w1,
-                       (const bf16_t*)a.w3, a.offsets, a.d, a.f, a.E, (bf16_t*)a.dX);
+    probe::mark("dgate_reduce", st);
+    hipLaunchKernelGGL(g3_kernel, dim3(a.E * cdiv(a.f, CS::BM) * cdiv(a.d, CS::BN)),
+                       dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)HG, (const bf16_t*)a.dy,
+                       a.offsets, a.eti, a.d, a.f, a.dw2);
+    probe::mark("g3_kernel", st);
+    hipLaunchKernelGGL(g5_kernel, dim3(a.E * cdiv(a.d, CD::BM) * cdiv(a.f, CD::BN)),
+                       dim3(CD::THREADS), CD::LDS, st, (const bf16_t*)a.x, (const bf16_t*)a.A,
+                       (const bf16_t*)a.B, a.offsets, a.eti, a.d, a.f, a.dw1, a.dw3);
+    probe::mark("g5_kernel", st);
+    hipLaunchKernelGGL(g6_kernel, dim3(slot_grid(S, a.E, CS::BM, cdiv(a.d, CS::BN))),
+                       dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)a.A, (const bf16_t*)a.B,
+                       (const bf16_t*)a.w1, (const bf16_t*)a.w3, a.offsets, a.d, a.f, a.E,
+                       (bf16_t*)a.dX);
+    probe::mark("g6_kernel", st);
     return hipGetLastError();
 }
 

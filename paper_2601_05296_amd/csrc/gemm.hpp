@@ -1,92 +1,133 @@
 // gemm.hpp -- grouped bf16 MFMA GEMM core for the expert FFN (gfx950).
 //
 // One workgroup computes a BM x BN output tile with WM x WN waves; every wave
-// owns a (BM/WM) x (BN/WN) sub-tile made of 16x16 MFMA fragments. K advances
-// in slices of 64. Operand tiles are staged in LDS, double-buffered: global
-// loads of slice kt+1 are issued before the MFMAs of slice kt, written to the
-// other LDS buffer after them, and a single barrier per slice separates the
-// two.
+// owns a (BM/WM) x (BN/WN) sub-tile made of 32x32 fragments computed with
+// v_mfma_f32_32x32x16_bf16 (float32 accumulation). K advances in slices of
+// BK = 32.
 //
-// Two LDS tile layouts, chosen per operand by its global layout:
-//  * KC ("K contiguous"): [R rows][64 k] bf16, used when K is the contiguous
-//    dimension in memory (activations with K = d, weights read transposed).
-//    The 16-byte chunk index inside a 128-byte row is XOR-ed with (row & 7).
-//    Fragments are single ds_read_b128 loads.
-//  * MC ("rows contiguous"): [64 k][R] bf16, used when K is the outer
-//    dimension (weights [K][N], and every operand of the weight-gradient
+// Data movement: operand tiles go straight from global memory into LDS with
+// gfx950's global_load_lds_dwordx4 (no register staging). One instruction
+// moves 64 lanes x 16 bytes into 1 KB of contiguous LDS, lane l writing bytes
+// 16l..16l+15; each lane therefore fetches whichever global 16-byte chunk the
+// swizzled LDS layout wants at that position (this is also how rows are
+// gathered through the dispatch index maps). LDS holds a ring of NST slices:
+// while the MFMAs consume slice kt, the loads for slices kt+1 .. kt+NST-1 are
+// in flight. The hardware counts outstanding loads per wave (vmcnt); a wave
+// waits until the loads of slice kt+1 have landed and a workgroup barrier
+// publishes them to the other waves. The waits are explicit because a
+// compiler-generated __syncthreads() would drain every outstanding load.
+//
+// MFMA 32x32x16 operand layout (wave64), verified on gfx950: for D = P * Q,
+// lane L supplies P[L%32][8*(L/32) + 0..7] and Q[8*(L/32) + 0..7][L%32] and
+// receives D[8*(j/4) + 4*(L/32) + j%4][L%32] in accumulator register j. The
+// kernels pass P = right-operand tile (rows = output columns n) and
+// Q = left-operand tile (rows = output rows m), so lane L ends up holding
+// output row m = L%32 at columns n = 8*(j/4) + 4*(L/32) + (j%4): four runs of
+// four consecutive columns.
+//
+// Two LDS tile layouts, chosen per operand by its layout in memory:
+//  * KC ("K contiguous"): [R rows][32 k] bf16 (64-byte rows), for operands
+//    whose K is the contiguous dimension. The 16-byte chunk index c of row r
+//    is stored at c ^ ((r >> 1) & 3), so the 8 rows read by 8 consecutive
+//    lanes of a ds_read_b128 fall in distinct banks.
+//  * MC ("rows contiguous"): [32 k][R] bf16, for operands whose K is the
+//    outer dimension (weights [K][N], and every operand of the weight-gradient
 //    GEMMs, whose K is the token dimension). The 32-byte chunk index inside a
-//    row is XOR-ed with (k & 3). Fragments are read with gfx950's transposing
-//    LDS load ds_read_b64_tr_b16: within each 16-lane group, lane l receives
-//    element l%4 of the 4-element pieces supplied by lanes 4q + l/4, q = 0..3,
-//    so 16 lanes that each point at 4 consecutive columns of 4 consecutive k
-//    rows receive, per lane, one column's 4 k values.
-//
-// The operand loaders (fetch: global -> registers, stage: registers -> LDS,
-// possibly computing on the way) are supplied per GEMM stage.
+//    k row is XOR-ed with (k & 3). Fragments are read with gfx950's
+//    transposing LDS load ds_read_b64_tr_b16: within each 16-lane group, lane
+//    l receives element l%4 of the 4-element pieces supplied by lanes
+//    4q + l/4 (q = 0..3), so when lane 4q + c points at columns 4c..4c+3 of k
+//    row q, lane l receives column l of k rows 0..3.
 #pragma once
 
 #include "common.hpp"
 
 namespace moe {
 
-constexpr int GBK = 64;  // K slice
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+constexpr int GBK = 32;  // K slice
+constexpr int NST = 3;   // LDS ring depth (slices)
+
+__device__ __forceinline__ f32x16 mfma32x32x16(const bf16x8& p, const bf16x8& q, const f32x16& c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(p, q, c, 0, 0, 0);
+}
+
+// Wait until at most N vector-memory operations of this wave are outstanding.
+// Inline assembly with a memory clobber, so that the compiler moves no memory
+// access across it.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Workgroup barrier without the implicit drain of outstanding loads that
+// __syncthreads() adds; also a compiler memory barrier.
+__device__ __forceinline__ void barrier_only() { asm volatile("s_barrier" ::: "memory"); }
+
+// 16-byte global -> LDS copy by one lane; `lds` must be wave-uniform: lane l
+// writes lds + 16*l.
+__device__ __forceinline__ void dma16(const void* g, char* lds) {
+    __builtin_amdgcn_global_load_lds(g, (lds_void_t*)lds, 16, 0, 0);
+}
 
 template <int BM_, int BN_, int WM_, int WN_, int NB_>
 struct GemmCfg {
     static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, NB = NB_;
-    static constexpr int THREADS = WM * WN * WAVE;
-    static constexpr int WTM = BM / WM, WTN = BN / WN;
-    static constexpr int FM = WTM / 16, FN = WTN / 16;
+    static constexpr int NW = WM * WN;
+    static constexpr int THREADS = NW * WAVE;
+    static constexpr int WTM = BM / WM, WTN = BN / WN;   // wave tile
+    static constexpr int FM = WTM / 32, FN = WTN / 32;   // 32x32 fragments per wave
     static constexpr int A_BYTES = BM * GBK * 2;
     static constexpr int B_BYTES = BN * GBK * 2;
     static constexpr int STAGE = A_BYTES + NB * B_BYTES;
-    static constexpr int LDS = 2 * STAGE;
+    static constexpr int LDS = NST * STAGE;
     static_assert(FM >= 1 && FN >= 1, "wave tile too small");
+    static_assert(LDS <= 160 * 1024, "LDS budget");
+    static_assert(A_BYTES % (1024 * NW) == 0 && B_BYTES % (1024 * NW) == 0,
+                  "every wave issues the same number of 1 KB copies");
 };
 
-// ---- per-thread chunk maps ---------------------------------------------------
-// KC tile of R rows: chunk c = tid + i*THREADS -> row c/8, 16-byte chunk c%8.
-template <int R, int THREADS>
-struct KCMap {
-    static constexpr int NCH = R * 8 / THREADS;
-    static_assert(NCH >= 1 && R * 8 % THREADS == 0, "KC tile / thread count mismatch");
-    __device__ static int row(int tid, int i) { return (tid >> 3) + i * (THREADS / 8); }
-    __device__ static int kcol(int tid) { return (tid & 7) * 8; }  // element offset in slice
-    __device__ static int off(int tid, int i) {
-        const int r = row(tid, i);
-        return r * 128 + (((tid & 7) ^ (r & 7)) << 4);
+// ---- LDS layouts -------------------------------------------------------------------
+__device__ __forceinline__ int kc_swz(int r, int c) { return c ^ ((r >> 1) & 3); }
+
+// KC tile of R rows, copy q (1 KB = 16 rows): lane l -> row 16q + l/4, physical
+// chunk l%4, i.e. logical chunk kc_swz(row, l%4).
+struct KCDma {
+    __device__ static int row(int q, int lane) { return q * 16 + (lane >> 2); }
+    __device__ static int kcol(int q, int lane) { return kc_swz(row(q, lane), lane & 3) * 8; }
+};
+
+// MC tile of R columns, copy q (1 KB = 1024/(2R) k rows): lane l -> k row
+// q*KPK + l/(R/8), physical 16-byte chunk p = l%(R/8), logical column
+// ((p/2) ^ (k&3))*16 + (p&1)*8.
+template <int R>
+struct MCDma {
+    static constexpr int CPR = R / 8, KPK = 1024 / (2 * R);
+    static_assert(KPK >= 1 && R >= 64, "MC tile width");
+    __device__ static int krow(int q, int lane) { return q * KPK + lane / CPR; }
+    __device__ static int col(int q, int lane) {
+        const int k = krow(q, lane);
+        const int p = lane % CPR;
+        return (((p >> 1) ^ (k & 3)) << 4) + ((p & 1) << 3);
     }
 };
 
-// MC tile of R columns: chunk c = tid + i*THREADS -> k row c/(R/8), column chunk c%(R/8).
-template <int R, int THREADS>
-struct MCMap {
-    static constexpr int CPR = R / 8;
-    static constexpr int NCH = GBK * CPR / THREADS;
-    static_assert(NCH >= 1 && GBK * CPR % THREADS == 0, "MC tile / thread count mismatch");
-    static_assert(R >= 64, "MC tile needs at least 64 columns for the swizzle");
-    __device__ static int krow(int tid, int i) { return tid / CPR + i * (THREADS / CPR); }
-    __device__ static int col(int tid) { return (tid % CPR) * 8; }
-    __device__ static int off(int tid, int i) {
-        const int k = krow(tid, i);
-        const int c = tid % CPR;
-        return k * (R * 2) + ((((c >> 1) ^ (k & 3)) << 5) | ((c & 1) << 4));
-    }
-};
-
-// ---- fragment reads ------------------------------------------------------------
-// 8 consecutive k (k-octet L/16 of MFMA step kk) of tile row rbase + L%16.
+// ---- fragment reads (32 rows x 16 k of MFMA step kk in the 32-wide slice) -----
 __device__ __forceinline__ bf16x8 frag_kc(const char* tile, int rbase, int kk, int lane) {
-    const int r = rbase + (lane & 15);
-    const int c = kk * 4 + (lane >> 4);
-    return *reinterpret_cast<const bf16x8*>(tile + r * 128 + ((c ^ (r & 7)) << 4));
+    const int r = rbase + (lane & 31);
+    const int c = kk * 2 + (lane >> 5);
+    return *reinterpret_cast<const bf16x8*>(tile + r * 64 + (kc_swz(r, c) << 4));
 }
 
 template <int R>
 __device__ __forceinline__ bf16x8 frag_mc(const char* tile, int rbase, int kk, int lane) {
+    const int g = lane >> 4;          // 16-lane group: column half (g&1), k octet (g>>1)
     const int p = lane & 15;
-    const int k = kk * 32 + (lane >> 4) * 8 + (p >> 2);
-    const int cc = rbase >> 4;
+    const int k = kk * 16 + (g >> 1) * 8 + (p >> 2);
+    const int cc = (rbase >> 4) + (g & 1);
     const int cb = (p & 3) * 8;
     typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
     const char* a0 = tile + k * (R * 2) + (((cc ^ (k & 3)) << 5) | cb);
@@ -104,77 +145,121 @@ __device__ __forceinline__ bf16x8 frag(const char* tile, int rbase, int kk, int 
     else return frag_kc(tile, rbase, kk, lane);
 }
 
+template <class C>
+using Acc = f32x16[C::NB][C::FM][C::FN];
+
+// Zero k rows [from, GBK) of an MC tile of R columns (all threads take part).
+template <class C, int R>
+__device__ __forceinline__ void zero_mc_rows(char* tile, int from) {
+    const int nbytes = (GBK - from) * R * 2;
+    char* base = tile + from * R * 2;
+    for (int o = threadIdx.x * 16; o < nbytes; o += C::THREADS * 16) st16(base + o, zero16());
+}
+
 // ---- main loop -------------------------------------------------------------------
 // LA: left-operand loader (rows = output rows m), LB0/LB1: right-operand
-// loaders (rows = output columns n). Each loader has a static bool MC, and
-// members fetch(int kt) and stage(char* tile). acc[b][fm][fn] receives
-// sum_k A[m][k] B_b[k][n] for m = wm*WTM + fm*16 + L%16,
-// n = wn*WTN + fn*16 + 4*(L/16) + r.
+// loaders (rows = output columns n, same layout). A loader has a static bool
+// MC, a static int NQ (1 KB copies per wave per slice) and issue(kt, tile),
+// which is called once per slice in increasing kt. If zero_from < GBK, k rows
+// zero_from.. of the left operand's last slice are cleared after they land
+// (the left operand is then MC; used for the weight gradients' token tails).
+// On return acc[b][i][j] holds sum_k A[m][k] B_b[k][n] for the fragment at
+// rows wm*WTM + 32i, columns wn*WTN + 32j.
 template <class C, class LA, class LB0, class LB1>
-__device__ __forceinline__ void gemm_mainloop(LA& la, LB0& lb0, LB1& lb1, int nk, char* lds,
-                                              f32x4 (&acc)[C::NB][C::FM][C::FN]) {
+__device__ __forceinline__ void gemm_mainloop(LA& la, LB0& lb0, LB1& lb1, int nk, int zero_from,
+                                              char* lds, Acc<C>& acc) {
 #pragma unroll
     for (int b = 0; b < C::NB; ++b)
 #pragma unroll
         for (int i = 0; i < C::FM; ++i)
 #pragma unroll
-            for (int j = 0; j < C::FN; ++j) acc[b][i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[b][i][j][r] = 0.f;
     if (nk <= 0) return;
     const int lane = threadIdx.x & 63;
     const int wv = threadIdx.x >> 6;
     const int wm = wv / C::WN, wn = wv % C::WN;
+    constexpr int PER = LA::NQ + LB0::NQ + (C::NB == 2 ? LB1::NQ : 0);  // copies per slice
 
-    la.fetch(0);
-    lb0.fetch(0);
-    if constexpr (C::NB == 2) lb1.fetch(0);
-    la.stage(lds);
-    lb0.stage(lds + C::A_BYTES);
-    if constexpr (C::NB == 2) lb1.stage(lds + C::A_BYTES + C::B_BYTES);
-    __syncthreads();
+    auto issue = [&](int kt) {
+        char* t = lds + (kt % NST) * C::STAGE;
+        la.issue(kt, t);
+        lb0.issue(kt, t + C::A_BYTES);
+        if constexpr (C::NB == 2) lb1.issue(kt, t + C::A_BYTES + C::B_BYTES);
+    };
+    auto fix_tail = [&](int kt) {  // called once slice kt is visible to all waves
+        if (kt == nk - 1 && zero_from < GBK) {
+            zero_mc_rows<C, C::BM>(lds + (kt % NST) * C::STAGE, zero_from);
+            __syncthreads();
+        }
+    };
+
+    // prologue: slices 0 .. NST-2
+#pragma unroll
+    for (int s = 0; s < NST - 1; ++s)
+        if (s < nk) issue(s);
+    if (nk >= NST - 1) wait_vmcnt<PER * (NST - 2)>();
+    else wait_vmcnt<0>();
+    barrier_only();
+    fix_tail(0);
 
     for (int kt = 0; kt < nk; ++kt) {
-        char* cur = lds + (kt & 1) * C::STAGE;
-        char* nxt = lds + ((kt + 1) & 1) * C::STAGE;
-        const bool more = kt + 1 < nk;
-        if (more) {
-            la.fetch(kt + 1);
-            lb0.fetch(kt + 1);
-            if constexpr (C::NB == 2) lb1.fetch(kt + 1);
-        }
+        if (kt + NST - 1 < nk) issue(kt + NST - 1);
+        const char* cur = lds + (kt % NST) * C::STAGE;
 #pragma unroll
-        for (int kk = 0; kk < GBK / 32; ++kk) {
+        for (int kk = 0; kk < GBK / 16; ++kk) {
             bf16x8 fa[C::FM];
 #pragma unroll
             for (int i = 0; i < C::FM; ++i)
-                fa[i] = frag<LA::MC, C::BM>(cur, wm * C::WTM + i * 16, kk, lane);
+                fa[i] = frag<LA::MC, C::BM>(cur, wm * C::WTM + i * 32, kk, lane);
 #pragma unroll
             for (int b = 0; b < C::NB; ++b) {
                 const char* bt = cur + C::A_BYTES + b * C::B_BYTES;
                 bf16x8 fb[C::FN];
 #pragma unroll
                 for (int j = 0; j < C::FN; ++j)
-                    fb[j] = frag<LB0::MC, C::BN>(bt, wn * C::WTN + j * 16, kk, lane);
+                    fb[j] = frag<LB0::MC, C::BN>(bt, wn * C::WTN + j * 32, kk, lane);
 #pragma unroll
                 for (int i = 0; i < C::FM; ++i)
 #pragma unroll
                     for (int j = 0; j < C::FN; ++j)
-                        acc[b][i][j] = mfma16x16x32(fb[j], fa[i], acc[b][i][j]);
+                        acc[b][i][j] = mfma32x32x16(fb[j], fa[i], acc[b][i][j]);
             }
         }
-        if (more) {
-            la.stage(nxt);
-            lb0.stage(nxt + C::A_BYTES);
-            if constexpr (C::NB == 2) lb1.stage(nxt + C::A_BYTES + C::B_BYTES);
+        if (kt + 1 < nk) {
+            // slice kt+1 has landed once only the copies of later slices remain
+            if (kt + NST - 1 < nk) wait_vmcnt<PER * (NST - 2)>();
+            else wait_vmcnt<0>();
+            barrier_only();
+            fix_tail(kt + 1);
         }
-        __syncthreads();
     }
+    // every wave is done reading LDS before an epilogue reuses it
+    __syncthreads();
 }
 
 // Placeholder loader for single-B GEMMs.
 struct NoLoader {
     static constexpr bool MC = false;
-    __device__ void fetch(int) {}
-    __device__ void stage(char*) {}
+    static constexpr int NQ = 0;
+    __device__ void issue(int, char*) {}
+};
+
+// ---- output coordinates of a lane ------------------------------------------------
+template <class C>
+struct WaveCoord {
+    int lane, wm, wn;
+    __device__ WaveCoord() {
+        lane = threadIdx.x & 63;
+        const int wv = threadIdx.x >> 6;
+        wm = wv / C::WN;
+        wn = wv % C::WN;
+    }
+    // tile-local output row of fragment row-block i
+    __device__ int row(int i) const { return wm * C::WTM + i * 32 + (lane & 31); }
+    // tile-local first column of run q (0..3) of fragment column-block j
+    __device__ int col(int j, int q) const { return wn * C::WTN + j * 32 + q * 8 + (lane >> 5) * 4; }
 };
 
 // ---- grouped tile lookup ------------------------------------------------------------
@@ -192,6 +277,7 @@ struct SlotTile {
 template <int THREADS>
 __device__ bool find_slot_tile(const int32_t* __restrict__ offsets, int E, int BM, int NT,
                                int bid, int BN, SlotTile& t) {
+    static_assert(THREADS >= 256, "one thread per expert");
     __shared__ int s_scan[THREADS];
     __shared__ int s_res[2];
     const int tid = threadIdx.x;
@@ -218,17 +304,13 @@ __device__ bool find_slot_tile(const int32_t* __restrict__ offsets, int E, int B
     const int e = s_res[0];
     if (e < 0) return false;
     const int local = s_res[1];
-    const int mtiles = tiles;  // unused by other threads
-    (void)mtiles;
     const int cnt = offsets[e + 1] - offsets[e];
     const int nmt = (cnt + BM - 1) / BM;
-    const int mt = local % nmt;
-    const int nt = local / nmt;
     t.e = e;
     t.off = offsets[e];
-    t.m0 = mt * BM;
+    t.m0 = (local % nmt) * BM;
     t.mrows = min(BM, cnt - t.m0);
-    t.n0 = nt * BN;
+    t.n0 = (local / nmt) * BN;
     return true;
 }
 

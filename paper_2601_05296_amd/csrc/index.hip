@@ -23,6 +23,7 @@
 //                   paper's worked example, and the result is deterministic.
 #include "common.hpp"
 #include "launch.hpp"
+#include "probe.hpp"
 
 namespace moe {
 namespace {
@@ -163,10 +164,13 @@ hipError_t build_index(const int32_t* ids, int64_t T, int E, int k, int32_t* cou
     int32_t* cnt = static_cast<int32_t*>(ws);
     hipLaunchKernelGGL(tile_hist, dim3(ntiles), dim3(IDX_THREADS), 0, st, ids, T, E, k, tb,
                        ntiles, cnt);
+    probe::mark("tile_hist", st);
     hipLaunchKernelGGL(tile_scan, dim3(1), dim3(SCAN_THREADS), 0, st, cnt, E, ntiles, counts,
                        offsets);
+    probe::mark("tile_scan", st);
     hipLaunchKernelGGL(tile_rank, dim3(ntiles), dim3(IDX_THREADS), 0, st, ids, T, E, k, tb,
                        ntiles, cnt, eti, tim, slot_src);
+    probe::mark("tile_rank", st);
     return hipGetLastError();
 }
 

@@ -38,6 +38,7 @@ struct FfnArgs {
     int64_t T; int d, f, E, k;
     void* ws;
 };
+size_t ffn_fwd_workspace(int64_t T, int d, int f, int E, int k, bool f32);
 hipError_t ffn_fwd(const FfnArgs& a, bool f32, hipStream_t st);
 size_t ffn_bwd_workspace(int64_t T, int d, int f, int E, int k, bool f32);
 hipError_t ffn_bwd(const FfnArgs& a, bool f32, hipStream_t st);

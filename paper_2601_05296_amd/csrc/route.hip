@@ -14,6 +14,7 @@
 // f32 path (debug mode): one thread per token, float32 FMA.
 #include "common.hpp"
 #include "launch.hpp"
+#include "probe.hpp"
 
 namespace moe {
 namespace {
@@ -183,6 +184,7 @@ hipError_t launch_route_bf16(const void* x, const void* wg, const float* bias, i
     hipLaunchKernelGGL(route_bf16<NE>, grid, dim3(RT_THREADS), lds, st,
                        static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(wg), bias, T,
                        d, E, k, (int)renorm, ids, gates, logits);
+    probe::mark("route_bf16", st);
     return hipGetLastError();
 }
 
@@ -196,6 +198,7 @@ hipError_t route(const void* x, const void* wg, const float* bias, int64_t T, in
         hipLaunchKernelGGL(route_f32, grid, dim3(128), 0, st, static_cast<const float*>(x),
                            static_cast<const float*>(wg), bias, T, d, E, k, (int)renorm, ids,
                            gates, logits);
+        probe::mark("route_f32", st);
         return hipGetLastError();
     }
     if (E <= 16) return launch_route_bf16<1>(x, wg, bias, T, d, E, k, renorm, ids, gates, logits, st);

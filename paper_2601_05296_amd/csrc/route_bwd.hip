@@ -12,6 +12,7 @@
 // (4) a fixed-order sum of the chunk partials. Float32 FMA throughout.
 #include "common.hpp"
 #include "launch.hpp"
+#include "probe.hpp"
 
 namespace moe {
 namespace {
@@ -160,18 +161,24 @@ hipError_t route_bwd(const float* dgates, const float* logits, const int32_t* id
     float* part = reinterpret_cast<float*>(static_cast<char*>(ws) + dl_bytes);
     hipLaunchKernelGGL(rb_dlogits, dim3((unsigned)((T + 3) / 4)), dim3(256), 0, st, dgates,
                        logits, ids, gates, T, E, k, (int)renorm, dl);
+    probe::mark("rb_dlogits", st);
     const dim3 gdx((unsigned)((T + RB_TOK - 1) / RB_TOK));
     const int ns = nsplits(T);
     const dim3 gdw((unsigned)((d + 255) / 256), (unsigned)((E + RB_EB - 1) / RB_EB), (unsigned)ns);
     if (f32) {
         hipLaunchKernelGGL(rb_dx<true>, gdx, dim3(256), 0, st, dl, wg, T, d, E, (int)accumulate, dx);
+        probe::mark("rb_dx", st);
         hipLaunchKernelGGL(rb_dwg_partial<true>, gdw, dim3(256), 0, st, dl, x, T, d, E, part);
+        probe::mark("rb_dwg_partial", st);
     } else {
         hipLaunchKernelGGL(rb_dx<false>, gdx, dim3(256), 0, st, dl, wg, T, d, E, (int)accumulate, dx);
+        probe::mark("rb_dx", st);
         hipLaunchKernelGGL(rb_dwg_partial<false>, gdw, dim3(256), 0, st, dl, x, T, d, E, part);
+        probe::mark("rb_dwg_partial", st);
     }
     hipLaunchKernelGGL(rb_dwg_reduce, dim3((unsigned)(((int64_t)E * d + 255) / 256)), dim3(256), 0,
                        st, part, ns, E, d, dwg);
+    probe::mark("rb_dwg_reduce", st);
     return hipGetLastError();
 }
 

@@ -86,7 +86,10 @@ def forward(x, w_gate, bias, w1, w3, w2, k: int, renorm: bool, stream=None, keep
     A = torch.empty((S, f), dtype=x.dtype, device=dev)
     Bm = torch.empty((S, f), dtype=x.dtype, device=dev)
     O = torch.empty((S, d), dtype=x.dtype, device=dev)
-    B.moe_ffn_fwd(x, w1, w3, w2, offsets, eti, T, d, f, E, k, flags, A, Bm, O, stream)
+    wsb = B.moe_ffn_fwd_workspace_size(T, d, f, E, k, flags)
+    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
+    B.moe_ffn_fwd(x, w1, w3, w2, offsets, eti, T, d, f, E, k, flags, A, Bm, O, ws, wsb, stream)
+    del ws
     y = torch.empty((T, d), dtype=x.dtype, device=dev)
     B.moe_combine(O, gates, tim, T, d, k, flags, y, stream)
     saved = Saved(T, d, f, E, k, flags, renorm, ids, gates, logits, counts, offsets, eti, tim,

@@ -76,5 +76,9 @@ def test_workspace_checks_and_zero_tokens():
     r = lib.moe_route_bwd(*([FAKE] * 6), 1000, 128, 8, 2, 0, FAKE, FAKE, FAKE, need - 16, None)
     assert r == B.MOE_ERR_WORKSPACE
     # T == 0: no-op success, pointers not even inspected
-    assert lib.moe_ffn_fwd(*([None] * 6), 0, 128, 128, 8, 2, 0, None, None, None, None) == B.MOE_OK
+    assert lib.moe_ffn_fwd(*([None] * 6), 0, 128, 128, 8, 2, 0, None, None, None, None, 0,
+                           None) == B.MOE_OK
+    need = lib.moe_ffn_fwd_workspace_size(1000, 128, 128, 8, 2, 0)
+    r = lib.moe_ffn_fwd(*([FAKE] * 6), 1000, 128, 128, 8, 2, 0, FAKE, FAKE, FAKE, FAKE, need - 1, None)
+    assert r == B.MOE_ERR_WORKSPACE
     assert lib.moe_build_index_workspace_size(0, 8, 2) == 0

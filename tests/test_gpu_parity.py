@@ -183,7 +183,9 @@ def test_ffn_fwd_bwd_parity(dtype, T, d, f, E, k, renorm, pattern):
     A = torch.empty((S, f), dtype=tdt, device="cuda")
     Bm = torch.empty((S, f), dtype=tdt, device="cuda")
     O = torch.empty((S, d), dtype=tdt, device="cuda")
-    B.moe_ffn_fwd(x, w1, w3, w2, offsets, eti, T, d, f, E, k, flags, A, Bm, O)
+    wsf = B.moe_ffn_fwd_workspace_size(T, d, f, E, k, flags)
+    wsf_t = torch.empty(max(wsf, 16), dtype=torch.uint8, device="cuda")
+    B.moe_ffn_fwd(x, w1, w3, w2, offsets, eti, T, d, f, E, k, flags, A, Bm, O, wsf_t, wsf)
     y = torch.empty((T, d), dtype=tdt, device="cuda")
     B.moe_combine(O, gates, tim, T, d, k, flags, y)
     torch.cuda.synchronize()
