@@ -48,7 +48,7 @@ template <class C, int R>
 struct KCBase {
     static constexpr bool MC = false;
     static constexpr int NQ = R * GBK * 2 / 1024 / C::NW;  // copies per wave per slice
-    __device__ static int q(int i) { return (threadIdx.x >> 6) + i * C::NW; }
+    __device__ static int q(int i) { return wave_id() + i * C::NW; }
 };
 
 // KC rows gathered through an index list: row r -> base[idx[r]] (rows at or
@@ -67,9 +67,9 @@ struct GatherKC : KCBase<C, R> {
             p[i] = base + (int64_t)idx[r] * ld + KCDma::kcol(q, lane);
         }
     }
-    __device__ void issue(int kt, char* t) {
+    __device__ void issue(int kt, uint32_t t) {
 #pragma unroll
-        for (int i = 0; i < NQ; ++i) dma16(p[i] + kt * GBK, t + this->q(i) * 1024);
+        for (int i = 0; i < NQ; ++i) dma16(p[i] + kt * GBK, t + this->q(i) * 1024u);
     }
 };
 
@@ -95,11 +95,11 @@ struct DenseKC2 : KCBase<C, R> {
             p1[i] = src1 + o - (int64_t)ksplit;
         }
     }
-    __device__ void issue(int kt, char* t) {
+    __device__ void issue(int kt, uint32_t t) {
         const bool first = kt < kst;
 #pragma unroll
         for (int i = 0; i < NQ; ++i)
-            dma16((first ? p0[i] : p1[i]) + kt * GBK, t + this->q(i) * 1024);
+            dma16((first ? p0[i] : p1[i]) + kt * GBK, t + this->q(i) * 1024u);
     }
 };
 
@@ -108,7 +108,7 @@ struct MCBase {
     static constexpr bool MC = true;
     using D = MCDma<R>;
     static constexpr int NQ = GBK * R * 2 / 1024 / C::NW;
-    __device__ static int q(int i) { return (threadIdx.x >> 6) + i * C::NW; }
+    __device__ static int q(int i) { return wave_id() + i * C::NW; }
     // column of copy i for this lane, clamped into [0, ncols)
     __device__ static int colc(int i, int col0, int ncols) {
         const int c = col0 + D::col(q(i), threadIdx.x & 63);
@@ -129,9 +129,9 @@ struct DenseMC : MCBase<C, R> {
         for (int i = 0; i < NQ; ++i)
             p[i] = W + (int64_t)this->krow(i) * ld + this->colc(i, col0, ncols);
     }
-    __device__ void issue(int kt, char* t) {
+    __device__ void issue(int kt, uint32_t t) {
 #pragma unroll
-        for (int i = 0; i < NQ; ++i) dma16(p[i] + kt * step, t + this->q(i) * 1024);
+        for (int i = 0; i < NQ; ++i) dma16(p[i] + kt * step, t + this->q(i) * 1024u);
     }
 };
 
@@ -140,18 +140,27 @@ struct DenseMC : MCBase<C, R> {
 // row cnt - 1 (the main loop zeroes them in the left operand).
 
 // MC rows gathered through eti: row kr -> base[eti[off + kr]] (x or dY).
-// Indices are read one slice ahead of the copies that use them.
+// The k rows covered by one copy are the same for the whole wave (KPK of
+// them, one per group of R/8 lanes), so their indices are read with scalar
+// loads, one slice ahead of the copies that use them.
 template <class C, int R>
 struct GatherMC : MCBase<C, R> {
     using MCBase<C, R>::NQ;
+    using D = MCDma<R>;
     const bf16_t* base[NQ];
     const int32_t* idx;  // eti + off
     int ld, cnt;
-    int nidx[NQ];
-    __device__ int load_idx(int kt, int i) const {
-        int kr = kt * GBK + this->krow(i);
-        kr = kr < cnt ? kr : cnt - 1;
-        return idx[kr];
+    int nidx[NQ][D::KPK];
+    __device__ void load_idx(int kt) {
+#pragma unroll
+        for (int i = 0; i < NQ; ++i)
+#pragma unroll
+            for (int h = 0; h < D::KPK; ++h) {
+                int kr = kt * GBK + this->q(i) * D::KPK + h;
+                kr = kr < cnt ? kr : cnt - 1;
+                // constant address space: a uniform address becomes a scalar load
+                nidx[i][h] = ((const __attribute__((address_space(4))) int32_t*)(idx))[kr];
+            }
     }
     __device__ void init(const bf16_t* b, int ld_, int col0, int ncols, const int32_t* ix,
                          int cnt_) {
@@ -159,17 +168,19 @@ struct GatherMC : MCBase<C, R> {
         idx = ix;
         cnt = cnt_;
 #pragma unroll
-        for (int i = 0; i < NQ; ++i) {
-            base[i] = b + this->colc(i, col0, ncols);
-            nidx[i] = load_idx(0, i);
-        }
+        for (int i = 0; i < NQ; ++i) base[i] = b + this->colc(i, col0, ncols);
+        load_idx(0);
     }
-    __device__ void issue(int kt, char* t) {
+    __device__ void issue(int kt, uint32_t t) {
+        const int h = (threadIdx.x & 63) / D::CPR;
 #pragma unroll
         for (int i = 0; i < NQ; ++i) {
-            dma16(base[i] + (int64_t)nidx[i] * ld, t + this->q(i) * 1024);
-            nidx[i] = load_idx(kt + 1, i);
+            int row = nidx[i][0];
+#pragma unroll
+            for (int hh = 1; hh < D::KPK; ++hh) row = h == hh ? nidx[i][hh] : row;
+            dma16(base[i] + (int64_t)row * ld, t + this->q(i) * 1024u);
         }
+        load_idx(kt + 1);
     }
 };
 
@@ -185,12 +196,12 @@ struct SlotMC : MCBase<C, R> {
 #pragma unroll
         for (int i = 0; i < NQ; ++i) base[i] = src + off * ld_ + this->colc(i, col0, ncols);
     }
-    __device__ void issue(int kt, char* t) {
+    __device__ void issue(int kt, uint32_t t) {
 #pragma unroll
         for (int i = 0; i < NQ; ++i) {
             int kr = kt * GBK + this->krow(i);
             kr = kr < cnt ? kr : cnt - 1;
-            dma16(base[i] + (int64_t)kr * ld, t + this->q(i) * 1024);
+            dma16(base[i] + (int64_t)kr * ld, t + this->q(i) * 1024u);
         }
     }
 };

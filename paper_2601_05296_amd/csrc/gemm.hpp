@@ -28,8 +28,9 @@
 // Two LDS tile layouts, chosen per operand by its layout in memory:
 //  * KC ("K contiguous"): [R rows][32 k] bf16 (64-byte rows), for operands
 //    whose K is the contiguous dimension. The 16-byte chunk index c of row r
-//    is stored at c ^ ((r >> 1) & 3), so the 8 rows read by 8 consecutive
-//    lanes of a ds_read_b128 fall in distinct banks.
+//    is stored at c ^ ((r >> 2) & 3): a ds_read_b128 of 32 rows then has no
+//    bank conflict (measured with SQ_LDS_BANK_CONFLICT on gfx950; with
+//    c ^ ((r >> 1) & 3), rows r and r + 8 collide).
 //  * MC ("rows contiguous"): [32 k][R] bf16, for operands whose K is the
 //    outer dimension (weights [K][N], and every operand of the weight-gradient
 //    GEMMs, whose K is the token dimension). The 32-byte chunk index inside a
@@ -67,11 +68,25 @@ __device__ __forceinline__ void wait_vmcnt() {
 // __syncthreads() adds; also a compiler memory barrier.
 __device__ __forceinline__ void barrier_only() { asm volatile("s_barrier" ::: "memory"); }
 
-// 16-byte global -> LDS copy by one lane; `lds` must be wave-uniform: lane l
-// writes lds + 16*l.
-__device__ __forceinline__ void dma16(const void* g, char* lds) {
-    __builtin_amdgcn_global_load_lds(g, (lds_void_t*)lds, 16, 0, 0);
+// 16-byte global -> LDS copy by one lane: lane l writes LDS bytes
+// lds_off + 16*l .. +15 (lds_off must be wave-uniform; it goes to M0). Issued
+// from inline assembly so that the compiler does not track these copies: it
+// would otherwise drain all of them (vmcnt(0)) before every transposing LDS
+// read, which it cannot prove independent of the copies in flight. The main
+// loop waits for them explicitly (wait_vmcnt), so no compiler-visible vector
+// memory access may be issued inside it.
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds_off) {
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+                 ::"v"(g), "s"(lds_off) : "memory", "m0");
 }
+
+// LDS byte offset of a pointer into the workgroup's shared memory.
+__device__ __forceinline__ uint32_t lds_offset(const void* p) {
+    return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)p;
+}
+
+// Wave index as a value the compiler knows to be uniform (kept in an SGPR).
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
 template <int BM_, int BN_, int WM_, int WN_, int NB_>
 struct GemmCfg {
@@ -91,7 +106,7 @@ struct GemmCfg {
 };
 
 // ---- LDS layouts -------------------------------------------------------------------
-__device__ __forceinline__ int kc_swz(int r, int c) { return c ^ ((r >> 1) & 3); }
+__device__ __forceinline__ int kc_swz(int r, int c) { return c ^ ((r >> 2) & 3); }
 
 // KC tile of R rows, copy q (1 KB = 16 rows): lane l -> row 16q + l/4, physical
 // chunk l%4, i.e. logical chunk kc_swz(row, l%4).
@@ -182,8 +197,9 @@ __device__ __forceinline__ void gemm_mainloop(LA& la, LB0& lb0, LB1& lb1, int nk
     const int wm = wv / C::WN, wn = wv % C::WN;
     constexpr int PER = LA::NQ + LB0::NQ + (C::NB == 2 ? LB1::NQ : 0);  // copies per slice
 
+    const uint32_t lds_base = lds_offset(lds);
     auto issue = [&](int kt) {
-        char* t = lds + (kt % NST) * C::STAGE;
+        const uint32_t t = lds_base + (kt % NST) * C::STAGE;
         la.issue(kt, t);
         lb0.issue(kt, t + C::A_BYTES);
         if constexpr (C::NB == 2) lb1.issue(kt, t + C::A_BYTES + C::B_BYTES);
@@ -243,7 +259,7 @@ __device__ __forceinline__ void gemm_mainloop(LA& la, LB0& lb0, LB1& lb1, int nk
 struct NoLoader {
     static constexpr bool MC = false;
     static constexpr int NQ = 0;
-    __device__ void issue(int, char*) {}
+    __device__ void issue(int, uint32_t) {}
 };
 
 // ---- output coordinates of a lane ------------------------------------------------
