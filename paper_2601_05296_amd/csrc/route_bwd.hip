@@ -5,13 +5,20 @@
 //   renorm:    g_j = p[id_j]/sum p[id]  dl[id_j] = g_j (dg_j - sum_j' g_j' dg_j')
 // followed by dW_g = dl^T x and dx += dl W_g.
 //
-// Kernels: (1) one wave per token computes dl [T,E] into the workspace;
-// (2) dx: each workgroup keeps the dl rows of 32 tokens in LDS and streams
-// W_g column blocks (W_g is read once per 32 tokens); (3) dW_g: split over
-// token chunks, each workgroup accumulating 32 experts x 256 columns, then
-// (4) a fixed-order sum of the chunk partials. Float32 FMA throughout.
+// bf16 path: one wave per token computes dl and stores it as two bf16 terms
+// dl = hi + lo (hi = bf16(dl), lo = bf16(dl - hi); relative error about
+// 2^-16), laid out [T][2Ep] with Ep = E rounded up to 32 (zero padding). Both
+// products then run on the matrix cores with the grouped GEMM core:
+//   dx  += [hi|lo] [W_g; W_g]       (K = 2Ep)
+//   dW_g = hi^T x + lo^T x          (K = tokens, split into chunks; the
+//                                    chunk partials and the two halves are
+//                                    summed in a fixed order)
+// f32 debug path: dl in float32, dx from LDS-staged dl rows, dW_g from
+// token-chunk partials, float32 FMA throughout.
 #include "common.hpp"
+#include "gemm.hpp"
 #include "launch.hpp"
+#include "loaders.hpp"
 #include "probe.hpp"
 
 namespace moe {
@@ -141,43 +148,208 @@ __global__ void rb_dwg_reduce(const float* __restrict__ part, int nsplit, int E,
     dwg[i] = acc;
 }
 
+using CR = GemmCfg<256, 256, 2, 4, 1>;
+constexpr int RB_MCH = 512;  // tokens per split of the MFMA dW_g kernel
+
+inline int epad(int E) { return (E + 31) / 32 * 32; }
+
+// dl of token t as bf16 hi/lo pairs: hl[t][e] = hi, hl[t][Ep + e] = lo
+__global__ void __launch_bounds__(256)
+rb_dlogits_hilo(const float* __restrict__ dg, const float* __restrict__ logits,
+                const int32_t* __restrict__ ids, const float* __restrict__ gates, int64_t T,
+                int E, int Ep, int k, int renorm, bf16_t* __restrict__ hl) {
+    const int lane = threadIdx.x & 63;
+    const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (t >= T) return;
+    float gdg = 0.f;
+    for (int j = 0; j < k; ++j) gdg += gates[t * k + j] * dg[t * k + j];
+    const float* lt = logits + t * E;
+    float mx = -INFINITY, z = 0.f;
+    if (!renorm) {
+        for (int e = lane; e < E; e += 64) mx = fmaxf(mx, lt[e]);
+        mx = wave_max(mx);
+        for (int e = lane; e < E; e += 64) z += __expf(lt[e] - mx);
+        z = wave_sum(z);
+    }
+    bf16_t* out = hl + t * 2 * Ep;
+    for (int e = lane; e < Ep; e += 64) {
+        float v = 0.f;
+        if (e < E) {
+            float dp = 0.f, gsel = 0.f;
+            bool sel = false;
+            for (int j = 0; j < k; ++j)
+                if (ids[t * k + j] == e) { dp = dg[t * k + j]; gsel = gates[t * k + j]; sel = true; }
+            if (renorm) v = sel ? gsel * (dp - gdg) : 0.f;
+            else v = (__expf(lt[e] - mx) / z) * (dp - gdg);
+        }
+        const uint32_t hi = f2bf(v);
+        const uint32_t lo = f2bf(v - bf2f(hi));
+        out[e] = (bf16_t)hi;
+        out[Ep + e] = (bf16_t)lo;
+    }
+}
+
+// dx[t] (+)= sum_k hl[t][k] * W_g[k mod Ep]   (tile: 256 tokens x 256 columns)
+__global__ void __launch_bounds__(CR::THREADS)
+rb_dx_mfma(const bf16_t* __restrict__ hl, const bf16_t* __restrict__ wg, int64_t T, int d,
+           int E, int Ep, int accumulate, bf16_t* __restrict__ dx) {
+    extern __shared__ __align__(16) char lds[];
+    using C = CR;
+    const int64_t m0 = (int64_t)blockIdx.x * C::BM;
+    const int n0 = blockIdx.y * C::BN;
+    const int rows = (int)min((int64_t)C::BM, T - m0);
+    DenseKC2<C, C::BM> la;
+    la.init(hl, hl, 2 * Ep, m0, rows, 2 * Ep);
+    SplitRowsMC<C, C::BN> lb;
+    lb.init(wg, d, n0, d, Ep, E);
+    NoLoader nl;
+    Acc<C> acc;
+    gemm_mainloop<C>(la, lb, nl, 2 * Ep / GBK, GBK, lds, acc);
+    WaveCoord<C> wc;
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i) {
+        const int m = wc.row(i);
+        if (m >= rows) continue;
+        bf16_t* row = dx + (m0 + m) * d;
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int n = n0 + wc.col(j, q);
+                if (n >= d) continue;
+                float v[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) v[r] = acc[0][i][j][4 * q + r];
+                if (accumulate) {
+                    const uint2 o = *reinterpret_cast<const uint2*>(row + n);
+                    v[0] += bf_lo(o.x); v[1] += bf_hi(o.x); v[2] += bf_lo(o.y); v[3] += bf_hi(o.y);
+                }
+                *reinterpret_cast<uint2*>(row + n) = make_uint2(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]));
+            }
+    }
+}
+
+// part[split][m][n] = sum over the split's tokens of hl[t][m] * x[t][n], m < 2Ep
+__global__ void __launch_bounds__(CR::THREADS)
+rb_dwg_mfma(const bf16_t* __restrict__ hl, const bf16_t* __restrict__ x, int64_t T, int d,
+            int Ep, float* __restrict__ part) {
+    extern __shared__ __align__(16) char lds[];
+    using C = CR;
+    const int n0 = blockIdx.x * C::BN;
+    const int m0 = blockIdx.y * C::BM;
+    const int split = blockIdx.z;
+    const int64_t t0 = (int64_t)split * RB_MCH;
+    const int cnt = (int)min((int64_t)RB_MCH, T - t0);
+    const int M = 2 * Ep;
+    SlotMC<C, C::BM> la;
+    la.init(hl, M, t0, m0, M, cnt);
+    SlotMC<C, C::BN> lb;
+    lb.init(x, d, t0, n0, d, cnt);
+    NoLoader nl;
+    Acc<C> acc;
+    gemm_mainloop<C>(la, lb, nl, (cnt + GBK - 1) / GBK, tail_from(cnt), lds, acc);
+    WaveCoord<C> wc;
+    float* out = part + (int64_t)split * M * d;
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i) {
+        const int m = m0 + wc.row(i);
+        if (m >= M) continue;
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int n = n0 + wc.col(j, q);
+                if (n >= d) continue;
+                const f32x16& v = acc[0][i][j];
+                *reinterpret_cast<f32x4*>(out + (int64_t)m * d + n) =
+                    f32x4{v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
+            }
+    }
+}
+
+// dw_gate[e][i] = sum_split (part[split][e][i] + part[split][Ep + e][i])
+__global__ void rb_dwg_reduce_hilo(const float* __restrict__ part, int nsplit, int E, int Ep,
+                                   int d, float* __restrict__ dwg) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= (int64_t)E * d) return;
+    const int64_t per = (int64_t)2 * Ep * d;
+    const int64_t lo_off = (int64_t)Ep * d;
+    float acc = 0.f;
+    for (int s = 0; s < nsplit; ++s) acc += part[s * per + i] + part[s * per + lo_off + i];
+    dwg[i] = acc;
+}
+
 inline int nsplits(int64_t T) { return (int)((T + RB_CHUNK - 1) / RB_CHUNK); }
+inline int msplits(int64_t T) { return (int)((T + RB_MCH - 1) / RB_MCH); }
+inline size_t al256(size_t b) { return (b + 255) / 256 * 256; }
+
+hipError_t set_rb_lds_limits() {
+    static hipError_t status = [] {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(rb_dx_mfma),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, CR::LDS);
+        if (e == hipSuccess)
+            e = hipFuncSetAttribute(reinterpret_cast<const void*>(rb_dwg_mfma),
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, CR::LDS);
+        return e;
+    }();
+    return status;
+}
 
 }  // namespace
 
 size_t route_bwd_workspace(int64_t T, int d, int E, int k, bool f32) {
-    (void)k; (void)f32;
-    const size_t dl = (size_t)T * E * sizeof(float);
-    const size_t part = (size_t)nsplits(T) * E * d * sizeof(float);
-    return ((dl + 255) / 256) * 256 + part;
+    (void)k;
+    if (f32) {
+        const size_t dl = (size_t)T * E * sizeof(float);
+        const size_t part = (size_t)nsplits(T) * E * d * sizeof(float);
+        return al256(dl) + part;
+    }
+    const int Ep = epad(E);
+    return al256((size_t)T * 2 * Ep * sizeof(bf16_t)) + (size_t)msplits(T) * 2 * Ep * d * sizeof(float);
 }
 
 hipError_t route_bwd(const float* dgates, const float* logits, const int32_t* ids,
                      const float* gates, const void* x, const void* wg, int64_t T, int d,
                      int E, int k, bool f32, bool renorm, bool accumulate, float* dwg,
                      void* dx, void* ws, hipStream_t st) {
-    float* dl = static_cast<float*>(ws);
-    const size_t dl_bytes = (((size_t)T * E * sizeof(float) + 255) / 256) * 256;
-    float* part = reinterpret_cast<float*>(static_cast<char*>(ws) + dl_bytes);
-    hipLaunchKernelGGL(rb_dlogits, dim3((unsigned)((T + 3) / 4)), dim3(256), 0, st, dgates,
-                       logits, ids, gates, T, E, k, (int)renorm, dl);
-    probe::mark("rb_dlogits", st);
-    const dim3 gdx((unsigned)((T + RB_TOK - 1) / RB_TOK));
-    const int ns = nsplits(T);
-    const dim3 gdw((unsigned)((d + 255) / 256), (unsigned)((E + RB_EB - 1) / RB_EB), (unsigned)ns);
     if (f32) {
-        hipLaunchKernelGGL(rb_dx<true>, gdx, dim3(256), 0, st, dl, wg, T, d, E, (int)accumulate, dx);
+        float* dl = static_cast<float*>(ws);
+        float* part = reinterpret_cast<float*>(static_cast<char*>(ws) + al256((size_t)T * E * sizeof(float)));
+        hipLaunchKernelGGL(rb_dlogits, dim3((unsigned)((T + 3) / 4)), dim3(256), 0, st, dgates,
+                           logits, ids, gates, T, E, k, (int)renorm, dl);
+        probe::mark("rb_dlogits", st);
+        hipLaunchKernelGGL(rb_dx<true>, dim3((unsigned)((T + RB_TOK - 1) / RB_TOK)), dim3(256), 0,
+                           st, dl, wg, T, d, E, (int)accumulate, dx);
         probe::mark("rb_dx", st);
-        hipLaunchKernelGGL(rb_dwg_partial<true>, gdw, dim3(256), 0, st, dl, x, T, d, E, part);
+        const int ns = nsplits(T);
+        hipLaunchKernelGGL(rb_dwg_partial<true>,
+                           dim3((unsigned)((d + 255) / 256), (unsigned)((E + RB_EB - 1) / RB_EB), (unsigned)ns),
+                           dim3(256), 0, st, dl, x, T, d, E, part);
         probe::mark("rb_dwg_partial", st);
-    } else {
-        hipLaunchKernelGGL(rb_dx<false>, gdx, dim3(256), 0, st, dl, wg, T, d, E, (int)accumulate, dx);
-        probe::mark("rb_dx", st);
-        hipLaunchKernelGGL(rb_dwg_partial<false>, gdw, dim3(256), 0, st, dl, x, T, d, E, part);
-        probe::mark("rb_dwg_partial", st);
+        hipLaunchKernelGGL(rb_dwg_reduce, dim3((unsigned)(((int64_t)E * d + 255) / 256)), dim3(256), 0,
+                           st, part, ns, E, d, dwg);
+        probe::mark("rb_dwg_reduce", st);
+        return hipGetLastError();
     }
-    hipLaunchKernelGGL(rb_dwg_reduce, dim3((unsigned)(((int64_t)E * d + 255) / 256)), dim3(256), 0,
-                       st, part, ns, E, d, dwg);
+    if (hipError_t e = set_rb_lds_limits(); e != hipSuccess) return e;
+    const int Ep = epad(E);
+    bf16_t* hl = static_cast<bf16_t*>(ws);
+    float* part = reinterpret_cast<float*>(static_cast<char*>(ws) +
+                                           al256((size_t)T * 2 * Ep * sizeof(bf16_t)));
+    hipLaunchKernelGGL(rb_dlogits_hilo, dim3((unsigned)((T + 3) / 4)), dim3(256), 0, st, dgates,
+                       logits, ids, gates, T, E, Ep, k, (int)renorm, hl);
+    probe::mark("rb_dlogits", st);
+    hipLaunchKernelGGL(rb_dx_mfma, dim3((unsigned)((T + CR::BM - 1) / CR::BM), (unsigned)((d + CR::BN - 1) / CR::BN)),
+                       dim3(CR::THREADS), CR::LDS, st, (const bf16_t*)hl, (const bf16_t*)wg, T, d, E,
+                       Ep, (int)accumulate, (bf16_t*)dx);
+    probe::mark("rb_dx", st);
+    const int ms = msplits(T);
+    hipLaunchKernelGGL(rb_dwg_mfma, dim3((unsigned)((d + CR::BN - 1) / CR::BN), (unsigned)((2 * Ep + CR::BM - 1) / CR::BM), (unsigned)ms),
+                       dim3(CR::THREADS), CR::LDS, st, (const bf16_t*)hl, (const bf16_t*)x, T, d, Ep,
+                       part);
+    probe::mark("rb_dwg_partial", st);
+    hipLaunchKernelGGL(rb_dwg_reduce_hilo, dim3((unsigned)(((int64_t)E * d + 255) / 256)), dim3(256), 0,
+                       st, part, ms, E, Ep, d, dwg);
     probe::mark("rb_dwg_reduce", st);
     return hipGetLastError();
 }

@@ -222,7 +222,8 @@ def test_ffn_fwd_bwd_parity(dtype, T, d, f, E, k, renorm, pattern):
 
 @pytest.mark.parametrize("dtype,T,d,E,k,renorm,accumulate", [
     ("bf16", 1000, 256, 8, 2, False, False), ("bf16", 2500, 512, 64, 6, True, True),
-    ("bf16", 1500, 256, 128, 8, False, True), ("f32", 1000, 256, 8, 2, False, False),
+    ("bf16", 1500, 256, 128, 8, False, True), ("bf16", 777, 384, 200, 16, True, False),
+    ("f32", 1000, 256, 8, 2, False, False),
     ("f32", 700, 128, 32, 4, True, True)])
 def test_route_bwd_parity(dtype, T, d, E, k, renorm, accumulate):
     cfg = synth.MoEConfig("rb", T=T, d=d, f=128, E=E, k=k, dtype=dtype, renorm=renorm)
