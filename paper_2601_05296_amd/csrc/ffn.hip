@@ -38,7 +38,11 @@ namespace {
 // Single right operand: each wave owns 128 x 64 outputs. Two right operands
 // (G1: W1 and W3; G5: dA and dB): 128 x 32 of each.
 using CD = GemmCfg<256, 128, 2, 4, 2>;  // G1, G5
-using CS = GemmCfg<256, 256, 2, 4, 1>;  // G2, G3, G4, G6
+using CS = GemmCfg<256, 256, 2, 4, 1>;  // G2, G3, G6
+// G4 has a heavy epilogue (it reads A, B and writes dA, dB, g*h): 4-wave
+// workgroups with 72 KB of LDS, so that two share a CU and one's epilogue
+// overlaps the other's main loop.
+using C4 = GemmCfg<128, 256, 2, 2, 1>;
 
 // ============================ epilogue helpers ===================================
 
@@ -132,14 +136,14 @@ g2_kernel(const bf16_t* __restrict__ H, const bf16_t* __restrict__ w2,
 
 // G4: u = dY[eti] W2[e]^T; epilogue: d_gate partials sum(u*h), dA/dB over
 // A/B, and HG = g * h (h recomputed from A, B) for G3.
-__global__ void __launch_bounds__(CS::THREADS)
+__global__ void __launch_bounds__(C4::THREADS, 2)
 g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
           const float* __restrict__ gates, const int32_t* __restrict__ offsets,
           const int32_t* __restrict__ eti, const int32_t* __restrict__ slot_src, int d, int f,
           int E, bf16_t* __restrict__ A, bf16_t* __restrict__ B, bf16_t* __restrict__ HG,
           float* __restrict__ part) {
     extern __shared__ __align__(16) char lds[];
-    using C = CS;
+    using C = C4;
     SlotTile t;
     const int NT = (f + C::BN - 1) / C::BN;
     if (!find_slot_tile<C::THREADS>(offsets, E, C::BM, NT, xcd_remap(blockIdx.x, gridDim.x), C::BN, t))
@@ -475,7 +479,7 @@ hipError_t set_lds_limits() {
         set(reinterpret_cast<const void*>(g1_kernel), CD::LDS);
         set(reinterpret_cast<const void*>(g2_kernel), CS::LDS);
         set(reinterpret_cast<const void*>(g3_kernel), CS::LDS);
-        set(reinterpret_cast<const void*>(g4_kernel), CS::LDS);
+        set(reinterpret_cast<const void*>(g4_kernel), C4::LDS);
         set(reinterpret_cast<const void*>(g5_kernel), CD::LDS);
         set(reinterpret_cast<const void*>(g6_kernel), CS::LDS);
         return e;
@@ -484,7 +488,7 @@ hipError_t set_lds_limits() {
 }
 
 inline size_t align256(size_t b) { return (b + 255) / 256 * 256; }
-inline int g4_nparts(int f) { return cdiv(f, CS::BN) * CS::WN; }
+inline int g4_nparts(int f) { return cdiv(f, C4::BN) * C4::WN; }
 
 }  // namespace
 
@@ -554,8 +558,8 @@ hipError_t ffn_bwd(const FfnArgs& a, bool f32, hipStream_t st) {
     float* part = static_cast<float*>(a.ws);
     bf16_t* HG = reinterpret_cast<bf16_t*>(static_cast<char*>(a.ws) +
                                            align256((size_t)S * nparts * sizeof(float)));
-    hipLaunchKernelGGL(g4_kernel, dim3(slot_grid(S, a.E, CS::BM, cdiv(a.f, CS::BN))),
-                       dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)a.dy, (const bf16_t*)a.w2,
+    hipLaunchKernelGGL(g4_kernel, dim3(slot_grid(S, a.E, C4::BM, cdiv(a.f, C4::BN))),
+                       dim3(C4::THREADS), C4::LDS, st, (const bf16_t*)a.dy, (const bf16_t*)a.w2,
                        a.gates, a.offsets, a.eti, a.slot_src, a.d, a.f, a.E, (bf16_t*)a.A,
                        (bf16_t*)a.B, HG, part);
     probe::mark("g4_kernel", st);

@@ -1,0 +1,154 @@
+"""GPU parity at the full sizes of the benchmarked workloads, in the launch
+configuration bench.py times (layer.forward / layer.backward).
+
+The oracle cannot run a whole layer of these sizes, so the checks are:
+  * routing for every token (oracle route is cheap): ids equal up to
+    near-ties, logits and gates within tolerance;
+  * the index build, fed the oracle's ids, bit-exact for every token;
+  * y, dx, d_gates, A, B, dA, dB at sampled tokens, from an oracle run on
+    just those tokens (each of these depends on its own token only);
+  * dw1, dw3, dw2 at sampled hidden columns of one expert, from an oracle run
+    on a sub-problem holding that expert's tokens and those columns of its
+    weights (SwiGLU columns are independent);
+  * the router backward at full size on the oracle's logits and seeded gate
+    gradients, against the oracle's router backward for every token.
+No oracle input is taken from the device.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle
+from paper_2601_05296_amd import binding as B
+from paper_2601_05296_amd import layer, synth
+from tests.parity import assert_close, dev, host, near_tie_ok
+
+pytestmark = pytest.mark.gpu
+
+CASES = ["mid_e64k6", "few_large_e8k2", "many_small_zipf", "mem_sweep_e64k8", "zipf_empty"]
+NTOK = 12      # sampled tokens
+NCOL = 8       # sampled hidden columns
+
+
+def _cfg(name):
+    if name == "zipf_empty":
+        return synth.CONFIGS["many_small_zipf"].with_(name="zipf_empty", n_dead=16)
+    return synth.CONFIGS[name]
+
+
+def _f64(a):
+    return None if a is None else a.astype(np.float64)
+
+
+@pytest.mark.parametrize("name", CASES)
+def test_full_size_layer(name):
+    cfg = _cfg(name)
+    T, d, f, E, k = cfg.T, cfg.d, cfg.f, cfg.E, cfg.k
+    print("full-size case %s: T=%d d=%d f=%d E=%d k=%d" % (name, T, d, f, E, k), flush=True)
+    inp = synth.make_inputs(cfg)
+    v = {n: _f64(a) for n, a in inp.vals.items()}
+    st = inp.store
+    x, wg, w1, w3, w2, dy = (dev(st[n]) for n in ("x", "w_gate", "w1", "w3", "w2", "dy"))
+    bias = dev(st["bias"]) if st["bias"] is not None else None
+
+    # ---- device: the benchmarked forward + backward --------------------------
+    y, saved = layer.forward(x, wg, bias, w1, w3, w2, k, cfg.renorm)
+    A_fwd = saved.A.clone()
+    B_fwd = saved.B.clone()
+    g = layer.backward(saved, dy, x, wg, w1, w3, w2)
+    torch.cuda.synchronize()
+    ids_g = saved.ids.cpu().numpy()
+
+    # ---- routing, every token --------------------------------------------------
+    ids_r, gates_r, logits_r, _ = oracle.route(v["x"], v["w_gate"], v["bias"], k, cfg.renorm)
+    nflip = near_tie_ok(ids_g, ids_r, logits_r)
+    assert nflip <= max(2, T // 5000), nflip
+    same_tok = np.all(ids_g == ids_r, axis=1)
+    fin = np.isfinite(logits_r)
+    assert_close("logits", host(saved.logits)[fin], logits_r[fin], "f32")
+    assert_close("gates", host(saved.gates)[same_tok], gates_r[same_tok], "bf16")
+    if cfg.n_dead:
+        dead = np.nonzero(~np.isfinite(v["bias"]))[0]
+        assert np.all(saved.counts.cpu().numpy()[dead] == 0)
+
+    # ---- index build on the oracle's ids, bit-exact ------------------------------
+    ix_r = oracle.build_index(ids_r, E)
+    S = T * k
+    i32 = dict(dtype=torch.int32, device="cuda")
+    o = [torch.empty(E, **i32), torch.empty(E + 1, **i32), torch.empty(S, **i32),
+         torch.empty((T, k), **i32), torch.empty(S, **i32)]
+    wsb = B.moe_build_index_workspace_size(T, E, k)
+    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+    B.moe_build_index(dev(ids_r), T, E, k, *o, ws, wsb)
+    torch.cuda.synchronize()
+    for got, ref in zip(o, (ix_r.counts, ix_r.offsets, ix_r.eti, ix_r.tim, ix_r.slot_src)):
+        assert np.array_equal(got.cpu().numpy(), ref)
+
+    # ---- sampled tokens: forward and backward rows -------------------------------
+    rng = np.random.default_rng(1234)
+    cand = np.nonzero(same_tok)[0]
+    toks = np.sort(rng.choice(cand, size=min(NTOK, cand.size), replace=False))
+    sub = lambda a: None if a is None else a[toks]
+    fw = oracle.layer_forward(v["x"][toks], v["w_gate"], v["bias"], v["w1"], v["w3"], v["w2"], k,
+                              cfg.renorm)
+    assert np.array_equal(fw["ids"], ids_g[toks])
+    bw = oracle.layer_backward(fw, v["dy"][toks], v["x"][toks], v["w_gate"], v["w1"], v["w3"],
+                               v["w2"], cfg.renorm)
+    assert_close("y", host(y)[toks], fw["y"], "bf16")
+    assert_close("dx", host(g["dx"])[toks], bw["dx"], "bf16")
+    assert_close("d_gates", host(g["d_gates"])[toks], bw["d_gates"], "bf16")
+    tim_g = saved.tim.cpu().numpy()
+    slots_g = tim_g[toks].reshape(-1)                 # device slots, (t, j) order
+    slots_r = fw["ix"].tim.reshape(-1)                # oracle sub-run slots, same order
+    assert_close("A", host(A_fwd[torch.from_numpy(slots_g).long().cuda()]), fw["A"][slots_r], "bf16")
+    assert_close("B", host(B_fwd[torch.from_numpy(slots_g).long().cuda()]), fw["B"][slots_r], "bf16")
+    assert_close("dA", host(saved.A[torch.from_numpy(slots_g).long().cuda()]), bw["dA"][slots_r], "bf16")
+    assert_close("dB", host(saved.B[torch.from_numpy(slots_g).long().cuda()]), bw["dB"][slots_r], "bf16")
+    del A_fwd, B_fwd
+
+    # ---- weight gradients: sampled columns of one expert ------------------------------
+    counts_r = ix_r.counts
+    off_g = saved.offsets.cpu().numpy()
+    eti_g = saved.eti.cpu().numpy()
+    e = None
+    for cand_e in np.argsort(-counts_r):   # most loaded expert whose token set agrees
+        seg_r = ix_r.eti[ix_r.offsets[cand_e]:ix_r.offsets[cand_e + 1]]
+        seg_g = eti_g[off_g[cand_e]:off_g[cand_e + 1]]
+        if counts_r[cand_e] > 0 and np.array_equal(seg_r, seg_g):
+            e = int(cand_e)
+            break
+    assert e is not None
+    cols = np.sort(rng.choice(f, size=NCOL, replace=False))
+    seg = ix_r.eti[ix_r.offsets[e]:ix_r.offsets[e + 1]]
+    jsel = np.argmax(ids_r[seg] == e, axis=1)
+    g_e = gates_r[seg, jsel][:, None]
+    sub_ix = oracle.build_index(np.zeros((seg.size, 1), np.int32), 1)
+    xw = v["x"][seg]
+    W1s = v["w1"][e][:, cols][None]
+    W3s = v["w3"][e][:, cols][None]
+    W2s = v["w2"][e][cols, :][None]
+    As, Bs, _ = oracle.ffn_fwd(xw, W1s, W3s, W2s, sub_ix, 1)
+    sbw = oracle.ffn_bwd(v["dy"][seg], xw, W1s, W3s, W2s, g_e, sub_ix, As, Bs)
+    assert_close("dw1[e][:,cols]", host(g["dw1"][e])[:, cols], sbw["dw1"][0], "bf16")
+    assert_close("dw3[e][:,cols]", host(g["dw3"][e])[:, cols], sbw["dw3"][0], "bf16")
+    assert_close("dw2[e][cols,:]", host(g["dw2"][e])[cols, :], sbw["dw2"][0], "bf16")
+    if cfg.n_dead:
+        dead = np.nonzero(~np.isfinite(v["bias"]))[0]
+        assert np.all(host(g["dw1"][dead[0]]) == 0) and np.all(host(g["dw2"][dead[0]]) == 0)
+    del y, saved, g
+    torch.cuda.empty_cache()
+
+    # ---- router backward at full size, oracle logits and seeded gate gradients ----------
+    dgates = rng.standard_normal((T, k))
+    dl_r, dwg_r, dxr_r = oracle.route_bwd(dgates, logits_r, ids_r, v["x"], v["w_gate"], cfg.renorm)
+    flags = B.MOE_BF16 | (B.MOE_RENORM if cfg.renorm else 0)
+    dwg = torch.empty((E, d), dtype=torch.float32, device="cuda")
+    dxr = torch.empty((T, d), dtype=torch.bfloat16, device="cuda")
+    wsb = B.moe_route_bwd_workspace_size(T, d, E, k, flags)
+    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+    lg = np.where(np.isfinite(logits_r), logits_r, -np.inf).astype(np.float32)
+    B.moe_route_bwd(dev(dgates.astype(np.float32)), dev(lg), dev(ids_r),
+                    dev(gates_r.astype(np.float32)), x, wg, T, d, E, k, flags, dwg, dxr, ws, wsb)
+    torch.cuda.synchronize()
+    assert_close("dw_gate", host(dwg), dwg_r, "bf16")
+    assert_close("dx_router", host(dxr), dxr_r, "bf16")
