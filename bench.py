@@ -36,11 +36,97 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="mid_e64k6")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+    ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="approximate CPU time budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-baseline-memory", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a 1 GiB device copy (reference for HBM byte counters)")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write the per-kernel HBM traffic summary from two rocprofv3 --pmc "
+                         "runs (FETCH_SIZE, WRITE_SIZE) of this script with --copy-calibration")
+    ap.add_argument("--pmc-out", default=None)
     return ap.parse_args()
+
+
+CSRC = os.path.join(ROOT, "paper_2601_05296_amd", "csrc")
+COPY_BYTES = 1 << 30
+
+
+def source_digest() -> str:
+    """sha256 over the HIP sources: a traffic summary is valid only for them."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(CSRC)):
+        with open(os.path.join(CSRC, name), "rb") as fh:
+            h.update(name.encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def traffic_path(workload):
+    return os.path.join(ROOT, "profiles", "hbm_traffic_%s.txt" % workload)
+
+
+def kernel_short_name(full: str) -> str:
+    """'void moe::(anonymous namespace)::g5_kernel(...)' -> 'g5_kernel'."""
+    name = full.replace("(anonymous namespace)", "")
+    return name.split("(")[0].split("::")[-1].split("<")[0].split()[-1]
+
+
+def summarize_pmc(fetch_csv, write_csv, out, workload, cmd):
+    """Average FETCH_SIZE / WRITE_SIZE (KiB per dispatch) per kernel, and the
+    scale factors that make the copy kernel read and write exactly the bytes
+    it moved."""
+    import csv
+    def load(path, counter):
+        acc = {}
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            acc.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return {k: float(np.mean(v)) for k, v in acc.items()}
+    fetch, write = load(fetch_csv, "FETCH_SIZE"), load(write_csv, "WRITE_SIZE")
+    copy = [k for k in fetch if "copy" in k.lower() or "elementwise" in k.lower()]
+    copy = max(copy, key=lambda k: fetch[k])
+    ff = COPY_BYTES / 1024.0 / fetch[copy]
+    wf = COPY_BYTES / 1024.0 / write[copy]
+    lines = ["# HBM traffic per dispatch (rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE)",
+             "# workload: %s" % workload,
+             "# command: %s" % cmd,
+             "# copy kernel (%d bytes read and written): %s" % (COPY_BYTES, kernel_short_name(copy)),
+             "# scale factors: fetch %.4f, write %.4f (bytes = KiB * 1024 * factor)" % (ff, wf),
+             "source_sha256 %s" % source_digest(),
+             "fetch_factor %.6f" % ff, "write_factor %.6f" % wf,
+             "# kernel fetch_KiB write_KiB"]
+    for k in sorted(fetch, key=lambda k: -fetch[k]):
+        short = kernel_short_name(k)
+        if k == copy:
+            short = "copy_calibration"
+        lines.append("kernel %s %.1f %.1f" % (short, fetch[k], write.get(k, float("nan"))))
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("wrote", out)
+
+
+def read_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` from the committed summary, or None if
+    absent or taken on different sources."""
+    p = traffic_path(workload)
+    if not os.path.exists(p):
+        return None
+    vals, kern = {}, {}
+    for line in open(p):
+        parts = line.split()
+        if not parts or parts[0].startswith("#"):
+            continue
+        if parts[0] == "kernel":
+            kern[parts[1]] = (float(parts[2]), float(parts[3]))
+        else:
+            vals[parts[0]] = parts[1]
+    if vals.get("source_sha256") != source_digest() or kernel not in kern:
+        return None
+    f_kib, w_kib = kern[kernel]
+    return round((f_kib * float(vals["fetch_factor"]) + w_kib * float(vals["write_factor"])) * 1024.0)
 
 
 def kernel_model(name, cfg, elem):
@@ -73,11 +159,12 @@ def materialised_saved_bytes(x, w_gate, bias, w1, w3, w2, k, renorm):
     the permuted tokens and every SwiGLU intermediate (plain PyTorch autograd,
     forward only; weights are parameters and not counted)."""
     import torch
-    params = {t.data_ptr() for t in (w_gate, w1, w3, w2)}
+    # storages of the parameters and of the caller's input: not activations
+    excluded = {t.untyped_storage().data_ptr() for t in (x, w_gate, w1, w3, w2)}
     seen = {}
 
     def pack(t):
-        if t.data_ptr() not in params:
+        if t.untyped_storage().data_ptr() not in excluded:
             seen[(t.data_ptr(), t.dtype, tuple(t.shape))] = t.numel() * t.element_size()
         return t
 
@@ -87,7 +174,7 @@ def materialised_saved_bytes(x, w_gate, bias, w1, w3, w2, k, renorm):
     wg = w_gate.detach().requires_grad_(True)
     W1, W3, W2 = (w.detach().requires_grad_(True) for w in (w1, w3, w2))
     with torch.autograd.graph.saved_tensors_hooks(pack, lambda t: t):
-        logits = xs.float() @ wg.float().t()
+        logits = (xs @ wg.t()).float()
         if bias is not None:
             logits = logits + bias
         p = torch.softmax(logits, dim=1)
@@ -142,6 +229,11 @@ def cpu_oracle_baseline(inp, cfg, budget_s):
 
 def main():
     args = parse()
+    if args.summarize_pmc:
+        summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1],
+                      args.pmc_out or traffic_path(args.workload), args.workload,
+                      " ".join(sys.argv))
+        return
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
               "(see the sharding note in DESIGN.md); run with --gpus 1", file=sys.stderr)
@@ -220,7 +312,7 @@ def main():
     amount, unit, bound = kernel_model(dom, cfg, elem)
     roofline = {"bound": bound, "achieved": kd["achieved"], "unit": unit,
                 "peak": PEAK_BF16_TFLOPS if unit == "TFLOP/s" else PEAK_HBM_GBS,
-                "frac": kd["frac"], "traffic": None, "kernel": dom,
+                "frac": kd["frac"], "traffic": read_traffic(cfg.name, dom), "kernel": dom,
                 "per_launch": amount, "avg_ms": kd["avg_ms"]}
     gemm_ms = sum(kernels[n]["ms_per_step"] for n in kernels if n.startswith("g") and n[1].isdigit())
     gemm_flops = 18.0 * T * k * d * f
@@ -239,6 +331,13 @@ def main():
                  "frac": round(gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)},
         "kernels": kernels,
     }
+    if args.copy_calibration:
+        src = torch.empty(COPY_BYTES // 2, dtype=torch.bfloat16, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     if not args.no_baseline_memory:
         mb = materialised_saved_bytes(x, wg, bias, w1, w3, w2, k, cfg.renorm)
         out["materialised_baseline_saved_bytes_per_token"] = round(mb / T, 1)
