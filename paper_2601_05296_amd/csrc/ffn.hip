@@ -50,6 +50,7 @@ __device__ __forceinline__ void store4_bf16(bf16_t* p, float a, float b, float c
     *reinterpret_cast<uint2*>(p) = make_uint2(pack_bf2(a, b), pack_bf2(c, d));
 }
 __device__ __forceinline__ float silu_bf(float a) { return a * sigmoidf_(a); }
+__device__ __forceinline__ void store8_bf16(bf16_t* p, const float (&v)[8]) { st16(p, pack8(v)); }
 
 // ============================ kernels ==============================================
 
@@ -80,22 +81,26 @@ g1_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w1,
         if (m >= t.mrows) continue;
         const int64_t s = (int64_t)t.off + t.m0 + m;
 #pragma unroll
-        for (int j = 0; j < C::FN; ++j)
+        for (int j = 0; j < C::FN; ++j) {
+            float va[2][8], vb[2][8];
+            frag_cols8(acc[0][i][j], va);
+            frag_cols8(acc[1][i][j], vb);
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int n = t.n0 + wc.col(j, q);
+            for (int p = 0; p < 2; ++p) {
+                const int n = t.n0 + wc.col8(j, p);
                 if (n >= f) continue;
-                float a[4], b[4];
+                float a[8], b[8], h[8];
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    a[r] = bf2f(f2bf(acc[0][i][j][4 * q + r]));
-                    b[r] = bf2f(f2bf(acc[1][i][j][4 * q + r]));
+                for (int r = 0; r < 8; ++r) {
+                    a[r] = bf2f(f2bf(va[p][r]));
+                    b[r] = bf2f(f2bf(vb[p][r]));
+                    h[r] = silu_bf(a[r]) * b[r];
                 }
-                store4_bf16(A + s * f + n, a[0], a[1], a[2], a[3]);
-                store4_bf16(B + s * f + n, b[0], b[1], b[2], b[3]);
-                store4_bf16(H + s * f + n, silu_bf(a[0]) * b[0], silu_bf(a[1]) * b[1],
-                            silu_bf(a[2]) * b[2], silu_bf(a[3]) * b[3]);
+                store8_bf16(A + s * f + n, a);
+                store8_bf16(B + s * f + n, b);
+                store8_bf16(H + s * f + n, h);
             }
+        }
     }
 }
 
@@ -123,14 +128,15 @@ g2_kernel(const bf16_t* __restrict__ H, const bf16_t* __restrict__ w2,
         if (m >= t.mrows) continue;
         const int64_t s = (int64_t)t.off + t.m0 + m;
 #pragma unroll
-        for (int j = 0; j < C::FN; ++j)
+        for (int j = 0; j < C::FN; ++j) {
+            float v[2][8];
+            frag_cols8(acc[0][i][j], v);
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int n = t.n0 + wc.col(j, q);
-                if (n >= d) continue;
-                const f32x16& v = acc[0][i][j];
-                store4_bf16(O + s * d + n, v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+            for (int p = 0; p < 2; ++p) {
+                const int n = t.n0 + wc.col8(j, p);
+                if (n < d) store8_bf16(O + s * d + n, v[p]);
             }
+        }
     }
 }
 
@@ -166,28 +172,30 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
         const int64_t s = (int64_t)t.off + t.m0 + (valid ? m : 0);
         const float g = gates[slot_src[s]];
         // all A/B loads of this row block first (they alias the stores below)
-        uint2 av[C::FN][4], bv[C::FN][4];
+        uint4 av[C::FN][2], bv[C::FN][2];
 #pragma unroll
         for (int j = 0; j < C::FN; ++j)
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                int n = t.n0 + wc.col(j, q);
-                n = n < f ? n : f - 4;
-                av[j][q] = *reinterpret_cast<const uint2*>(A + s * f + n);
-                bv[j][q] = *reinterpret_cast<const uint2*>(B + s * f + n);
+            for (int p = 0; p < 2; ++p) {
+                int n = t.n0 + wc.col8(j, p);
+                n = n < f ? n : f - 8;
+                av[j][p] = ld16(A + s * f + n);
+                bv[j][p] = ld16(B + s * f + n);
             }
         float dg = 0.f;
 #pragma unroll
-        for (int j = 0; j < C::FN; ++j)
+        for (int j = 0; j < C::FN; ++j) {
+            float u8[2][8];
+            frag_cols8(acc[0][i][j], u8);
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int n = t.n0 + wc.col(j, q);
-                const float a[4] = {bf_lo(av[j][q].x), bf_hi(av[j][q].x), bf_lo(av[j][q].y), bf_hi(av[j][q].y)};
-                const float b[4] = {bf_lo(bv[j][q].x), bf_hi(bv[j][q].x), bf_lo(bv[j][q].y), bf_hi(bv[j][q].y)};
-                float da[4], db[4], hg[4];
+            for (int p = 0; p < 2; ++p) {
+                const int n = t.n0 + wc.col8(j, p);
+                float a[8], b[8], da[8], db[8], hg[8];
+                unpack8(av[j][p], a);
+                unpack8(bv[j][p], b);
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const float u = acc[0][i][j][4 * q + r];
+                for (int r = 0; r < 8; ++r) {
+                    const float u = u8[p][r];
                     const float sg = sigmoidf_(a[r]);
                     const float sl = a[r] * sg;
                     const float h = sl * b[r];
@@ -198,11 +206,12 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
                     db[r] = dh * sl;
                 }
                 if (valid && n < f) {
-                    store4_bf16(A + s * f + n, da[0], da[1], da[2], da[3]);
-                    store4_bf16(B + s * f + n, db[0], db[1], db[2], db[3]);
-                    store4_bf16(HG + s * f + n, hg[0], hg[1], hg[2], hg[3]);
+                    store8_bf16(A + s * f + n, da);
+                    store8_bf16(B + s * f + n, db);
+                    store8_bf16(HG + s * f + n, hg);
                 }
             }
+        }
         dg += __shfl_xor(dg, 32, 64);
         if (valid && wc.lane < 32) part[s * nparts + pidx] = dg;
     }
@@ -216,11 +225,10 @@ g3_kernel(const bf16_t* __restrict__ HG, const bf16_t* __restrict__ dy,
     extern __shared__ __align__(16) char lds[];
     using C = CS;
     const int MT = (f + C::BM - 1) / C::BM, NT = (d + C::BN - 1) / C::BN;
-    const int bid = blockIdx.x;
-    const int e = bid / (MT * NT);
-    const int rem = bid % (MT * NT);
-    const int m0 = (rem % MT) * C::BM;
-    const int n0 = (rem / MT) * C::BN;
+    int e, mt, nt;
+    if (!wgrad_tile(blockIdx.x, MT, NT, e, mt, nt)) return;
+    const int m0 = mt * C::BM;
+    const int n0 = nt * C::BN;
     const int off = offsets[e];
     const int cnt = offsets[e + 1] - off;
     SlotMC<C, C::BM> la;
@@ -260,11 +268,10 @@ g5_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ dA,
     extern __shared__ __align__(16) char lds[];
     using C = CD;
     const int MT = (d + C::BM - 1) / C::BM, NT = (f + C::BN - 1) / C::BN;
-    const int bid = blockIdx.x;
-    const int e = bid / (MT * NT);
-    const int rem = bid % (MT * NT);
-    const int m0 = (rem % MT) * C::BM;
-    const int n0 = (rem / MT) * C::BN;
+    int e, mt, nt;
+    if (!wgrad_tile(blockIdx.x, MT, NT, e, mt, nt)) return;
+    const int m0 = mt * C::BM;
+    const int n0 = nt * C::BN;
     const int off = offsets[e];
     const int cnt = offsets[e + 1] - off;
     GatherMC<C, C::BM> la;
@@ -323,14 +330,15 @@ g6_kernel(const bf16_t* __restrict__ dA, const bf16_t* __restrict__ dB,
         if (m >= t.mrows) continue;
         const int64_t s = (int64_t)t.off + t.m0 + m;
 #pragma unroll
-        for (int j = 0; j < C::FN; ++j)
+        for (int j = 0; j < C::FN; ++j) {
+            float v[2][8];
+            frag_cols8(acc[0][i][j], v);
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int n = t.n0 + wc.col(j, q);
-                if (n >= d) continue;
-                const f32x16& v = acc[0][i][j];
-                store4_bf16(dX + s * d + n, v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+            for (int p = 0; p < 2; ++p) {
+                const int n = t.n0 + wc.col8(j, p);
+                if (n < d) store8_bf16(dX + s * d + n, v[p]);
             }
+        }
     }
 }
 
@@ -566,11 +574,11 @@ hipError_t ffn_bwd(const FfnArgs& a, bool f32, hipStream_t st) {
     hipLaunchKernelGGL(dgate_reduce, grid1d(S, 256), dim3(256), 0, st, part, nparts, a.slot_src,
                        S, a.dgates);
     probe::mark("dgate_reduce", st);
-    hipLaunchKernelGGL(g3_kernel, dim3(a.E * cdiv(a.f, CS::BM) * cdiv(a.d, CS::BN)),
+    hipLaunchKernelGGL(g3_kernel, dim3(wgrad_grid(a.E, cdiv(a.f, CS::BM), cdiv(a.d, CS::BN))),
                        dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)HG, (const bf16_t*)a.dy,
                        a.offsets, a.eti, a.d, a.f, a.dw2);
     probe::mark("g3_kernel", st);
-    hipLaunchKernelGGL(g5_kernel, dim3(a.E * cdiv(a.d, CD::BM) * cdiv(a.f, CD::BN)),
+    hipLaunchKernelGGL(g5_kernel, dim3(wgrad_grid(a.E, cdiv(a.d, CD::BM), cdiv(a.f, CD::BN))),
                        dim3(CD::THREADS), CD::LDS, st, (const bf16_t*)a.x, (const bf16_t*)a.A,
                        (const bf16_t*)a.B, a.offsets, a.eti, a.d, a.f, a.dw1, a.dw3);
     probe::mark("g5_kernel", st);

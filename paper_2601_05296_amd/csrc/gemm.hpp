@@ -262,6 +262,24 @@ struct NoLoader {
     __device__ void issue(int, uint32_t) {}
 };
 
+// ---- 16-byte epilogue layout ----------------------------------------------------------
+// In a 32x32 accumulator fragment lane L holds row L%32 at four runs of four
+// columns, 8q + 4*(L/32) + 0..3 (q = 0..3). gfx950's v_permlane32_swap trades
+// values between lanes L and L+32 so that, for p = 0, 1, lane L holds the
+// eight consecutive columns 16p + 8*(L/32) + 0..7 instead: epilogues then load
+// and store 16 bytes of bf16 per lane, whole 32-byte sectors per row.
+__device__ __forceinline__ void frag_cols8(const f32x16& a, float (&v)[2][8]) {
+#pragma unroll
+    for (int p = 0; p < 2; ++p)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const auto s = __builtin_amdgcn_permlane32_swap(
+                __float_as_uint(a[8 * p + r]), __float_as_uint(a[8 * p + 4 + r]), false, false);
+            v[p][r] = __uint_as_float(s[0]);
+            v[p][4 + r] = __uint_as_float(s[1]);
+        }
+}
+
 // ---- output coordinates of a lane ------------------------------------------------
 template <class C>
 struct WaveCoord {
@@ -276,7 +294,30 @@ struct WaveCoord {
     __device__ int row(int i) const { return wm * C::WTM + i * 32 + (lane & 31); }
     // tile-local first column of run q (0..3) of fragment column-block j
     __device__ int col(int j, int q) const { return wn * C::WTN + j * 32 + q * 8 + (lane >> 5) * 4; }
+    // tile-local first column of eight-column group p (0, 1) after frag_cols8
+    __device__ int col8(int j, int p) const { return wn * C::WTN + j * 32 + p * 16 + (lane >> 5) * 8; }
 };
+
+// ---- weight-gradient tile order ---------------------------------------------------------
+// The weight-gradient GEMMs have P = MT*NT output tiles per expert, each looping
+// over the expert's tokens. Workgroup ids are dealt round-robin to the 8 XCDs
+// (each with its own L2). Every XCD takes, for every expert, one band of
+// ceil(P/8) consecutive tiles in row-major (m, n) order: the tiles of a band
+// share the left operand's token stream in that XCD's L2, and every XCD gets
+// the same share of every expert, whatever the experts' token counts.
+// Returns false for the padding tiles of the last band.
+__device__ __forceinline__ bool wgrad_tile(int bid, int MT, int NT, int& e, int& mt, int& nt) {
+    const int P = MT * NT;
+    const int G = (P + 7) >> 3;
+    const int x = bid & 7, j = bid >> 3;
+    e = j / G;
+    const int lt = x * G + j % G;
+    if (lt >= P) return false;
+    mt = lt / NT;
+    nt = lt % NT;
+    return true;
+}
+inline int wgrad_grid(int E, int MT, int NT) { return E * 8 * ((MT * NT + 7) / 8); }
 
 // ---- grouped tile lookup ------------------------------------------------------------
 // Tiles of expert e: ceil(M_e / BM) * NT, laid out expert after expert, with

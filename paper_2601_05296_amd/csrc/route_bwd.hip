@@ -212,20 +212,22 @@ rb_dx_mfma(const bf16_t* __restrict__ hl, const bf16_t* __restrict__ wg, int64_t
         if (m >= rows) continue;
         bf16_t* row = dx + (m0 + m) * d;
 #pragma unroll
-        for (int j = 0; j < C::FN; ++j)
+        for (int j = 0; j < C::FN; ++j) {
+            float v[2][8];
+            frag_cols8(acc[0][i][j], v);
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int n = n0 + wc.col(j, q);
+            for (int p = 0; p < 2; ++p) {
+                const int n = n0 + wc.col8(j, p);
                 if (n >= d) continue;
-                float v[4];
-#pragma unroll
-                for (int r = 0; r < 4; ++r) v[r] = acc[0][i][j][4 * q + r];
                 if (accumulate) {
-                    const uint2 o = *reinterpret_cast<const uint2*>(row + n);
-                    v[0] += bf_lo(o.x); v[1] += bf_hi(o.x); v[2] += bf_lo(o.y); v[3] += bf_hi(o.y);
+                    float o[8];
+                    unpack8(ld16(row + n), o);
+#pragma unroll
+                    for (int r = 0; r < 8; ++r) v[p][r] += o[r];
                 }
-                *reinterpret_cast<uint2*>(row + n) = make_uint2(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]));
+                st16(row + n, pack8(v[p]));
             }
+        }
     }
 }
 
