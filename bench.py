@@ -46,6 +46,10 @@ def parse():
                     help="write the per-kernel HBM traffic summary from two rocprofv3 --pmc "
                          "runs (FETCH_SIZE, WRITE_SIZE) of this script with --copy-calibration")
     ap.add_argument("--pmc-out", default=None)
+    ap.add_argument("--sweep", action="store_true",
+                    help="memory-capacity sweep: double T from the workload's T until out of "
+                         "memory, for this path and for the materialised-permutation baseline")
+    ap.add_argument("--sweep-max-doublings", type=int, default=8)
     return ap.parse_args()
 
 
@@ -202,6 +206,73 @@ def materialised_saved_bytes(x, w_gate, bias, w1, w3, w2, k, renorm):
     return sum(seen.values())
 
 
+def memory_sweep(cfg, max_doublings):
+    """Peak activation bytes per token and the largest T that fits, for this
+    path (one forward + backward) and for the materialised-permutation
+    baseline (forward only: its saved tensors plus forward temporaries, a
+    lower bound on its training peak). Inputs are drawn on the device from a
+    seeded generator with the workload's distributions."""
+    import torch
+    from paper_2601_05296_amd import layer
+    dev = torch.device("cuda:0")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(cfg.seed)
+    d, f, E, k = cfg.d, cfg.f, cfg.E, cfg.k
+    bf = torch.bfloat16
+    wg = (torch.randn((E, d), generator=gen, device=dev) * 0.02).to(bf)
+    w1 = (torch.randn((E, d, f), generator=gen, device=dev) * d ** -0.5).to(bf)
+    w3 = (torch.randn((E, d, f), generator=gen, device=dev) * d ** -0.5).to(bf)
+    w2 = (torch.randn((E, f, d), generator=gen, device=dev) * f ** -0.5).to(bf)
+    grad_bytes = 4 * (3 * E * d * f + E * d)
+    rows = []
+    ours_ok = base_ok = True
+    for n in range(max_doublings + 1):
+        T = cfg.T << n
+        row = {"T": T}
+        for which in ("ours", "baseline"):
+            if (which == "ours" and not ours_ok) or (which == "baseline" and not base_ok):
+                continue
+            torch.cuda.empty_cache()
+            try:
+                x = torch.randn((T, d), generator=gen, device=dev).to(bf)
+                dy = torch.randn((T, d), generator=gen, device=dev).to(bf) if which == "ours" else None
+                torch.cuda.synchronize()
+                torch.cuda.reset_peak_memory_stats(dev)
+                base = torch.cuda.memory_allocated(dev)
+                if which == "ours":
+                    y, saved = layer.forward(x, wg, None, w1, w3, w2, k, cfg.renorm)
+                    sb = saved.nbytes()
+                    g = layer.backward(saved, dy, x, wg, w1, w3, w2)
+                    torch.cuda.synchronize()
+                    peak = torch.cuda.max_memory_allocated(dev) - base - grad_bytes
+                    del y, saved, g
+                    row["ours_peak_bytes_per_token"] = round(peak / T, 1)
+                    row["ours_saved_bytes_per_token"] = round(sb / T, 1)
+                else:
+                    sb = materialised_saved_bytes(x, wg, None, w1, w3, w2, k, cfg.renorm)
+                    torch.cuda.synchronize()
+                    peak = torch.cuda.max_memory_allocated(dev) - base
+                    row["baseline_fwd_peak_bytes_per_token"] = round(peak / T, 1)
+                    row["baseline_saved_bytes_per_token"] = round(sb / T, 1)
+                del x, dy
+            except torch.cuda.OutOfMemoryError:
+                row[which + "_oom"] = True
+                if which == "ours":
+                    ours_ok = False
+                else:
+                    base_ok = False
+            torch.cuda.empty_cache()
+        rows.append(row)
+        print(json.dumps(row), flush=True)
+        if not ours_ok and not base_ok:
+            break
+    fits = lambda key: max([r["T"] for r in rows if key in r], default=0)
+    return {"workload": cfg.name, "points": rows,
+            "max_T_ours": fits("ours_peak_bytes_per_token"),
+            "max_T_baseline_fwd": fits("baseline_fwd_peak_bytes_per_token"),
+            "hbm_bytes": torch.cuda.get_device_properties(dev).total_memory}
+
+
 def cpu_oracle_baseline(inp, cfg, budget_s):
     """Time the CPU oracle (fwd + bwd of the whole layer) on the first tokens
     of the same workload; the sample grows until about budget_s of work."""
@@ -233,6 +304,12 @@ def main():
         summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1],
                       args.pmc_out or traffic_path(args.workload), args.workload,
                       " ".join(sys.argv))
+        return
+    if args.sweep:
+        from paper_2601_05296_amd import synth
+        res = memory_sweep(synth.CONFIGS[args.workload if args.workload != "mid_e64k6" else
+                                         "mem_sweep_e64k8"], args.sweep_max_doublings)
+        print(json.dumps({"sweep": res}), flush=True)
         return
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
