@@ -416,8 +416,14 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     if not args.no_baseline_memory:
+        torch.cuda.synchronize()
+        torch.cuda.reset_peak_memory_stats(dev)
+        base = torch.cuda.memory_allocated(dev)
         mb = materialised_saved_bytes(x, wg, bias, w1, w3, w2, k, cfg.renorm)
+        torch.cuda.synchronize()
         out["materialised_baseline_saved_bytes_per_token"] = round(mb / T, 1)
+        out["materialised_baseline_fwd_peak_bytes_per_token"] = round(
+            (torch.cuda.max_memory_allocated(dev) - base) / T, 1)
         torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_oracle_baseline(inp, cfg, args.cpu_seconds)
