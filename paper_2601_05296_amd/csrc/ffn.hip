@@ -73,7 +73,7 @@ g1_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w1,
     lb0.init(w1 + (int64_t)t.e * d * f, f, t.n0, f);
     lb1.init(w3 + (int64_t)t.e * d * f, f, t.n0, f);
     Acc<C> acc;
-    gemm_mainloop<C>(la, lb0, lb1, d / GBK, GBK, lds, acc);
+    gemm_mainloop<C>(la, lb0, lb1, d / GBK, GBK, lds, acc, t.mrows);
     WaveCoord<C> wc;
 #pragma unroll
     for (int i = 0; i < C::FM; ++i) {
@@ -120,7 +120,7 @@ g2_kernel(const bf16_t* __restrict__ H, const bf16_t* __restrict__ w2,
     lb.init(w2 + (int64_t)t.e * f * d, d, t.n0, d);
     NoLoader nl;
     Acc<C> acc;
-    gemm_mainloop<C>(la, lb, nl, f / GBK, GBK, lds, acc);
+    gemm_mainloop<C>(la, lb, nl, f / GBK, GBK, lds, acc, t.mrows);
     WaveCoord<C> wc;
 #pragma unroll
     for (int i = 0; i < C::FM; ++i) {
@@ -161,7 +161,7 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
     lb.init(W2e, W2e, d, t.n0, min(C::BN, f - t.n0), d);
     NoLoader nl;
     Acc<C> acc;
-    gemm_mainloop<C>(la, lb, nl, d / GBK, GBK, lds, acc);
+    gemm_mainloop<C>(la, lb, nl, d / GBK, GBK, lds, acc, t.mrows, f - t.n0);
     WaveCoord<C> wc;
     const int nparts = NT * C::WN;
     const int pidx = (t.n0 / C::BN) * C::WN + wc.wn;
@@ -217,6 +217,12 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
     }
 }
 
+// Weight gradients are written once and not read again by this layer:
+// nontemporal stores keep them from displacing the operands in L2.
+__device__ __forceinline__ void st_nt(float* p, const f32x4& v) {
+    __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(p));
+}
+
 // G3: dW2[e] = sum_s HG[s]^T dY[eti[s]]   (M = f, N = d, K = slots of e)
 __global__ void __launch_bounds__(CS::THREADS)
 g3_kernel(const bf16_t* __restrict__ HG, const bf16_t* __restrict__ dy,
@@ -239,24 +245,13 @@ g3_kernel(const bf16_t* __restrict__ HG, const bf16_t* __restrict__ dy,
         lb.init(dy, d, n0, d, eti + off, cnt);
     }
     Acc<C> acc;
-    gemm_mainloop<C>(la, lb, nl, (cnt + GBK - 1) / GBK, tail_from(cnt), lds, acc);
-    WaveCoord<C> wc;
+    gemm_mainloop<C>(la, lb, nl, (cnt + GBK - 1) / GBK, tail_from(cnt), lds, acc, f - m0,
+                     d - n0);
     float* out = dw2 + (int64_t)e * f * d;
-#pragma unroll
-    for (int i = 0; i < C::FM; ++i) {
-        const int m = m0 + wc.row(i);
-        if (m >= f) continue;
-#pragma unroll
-        for (int j = 0; j < C::FN; ++j)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int n = n0 + wc.col(j, q);
-                if (n >= d) continue;
-                const f32x16& v = acc[0][i][j];
-                *reinterpret_cast<f32x4*>(out + (int64_t)m * d + n) =
-                    f32x4{v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
-            }
-    }
+    RowStage<C, 1>::run(acc, lds, [&](int, int r, int c, const f32x4& v) {
+        const int m = m0 + r, n = n0 + c;
+        if (m < f && n < d) st_nt(out + (int64_t)m * d + n, v);
+    });
 }
 
 // G5: dW1[e] = x[eti]^T dA, dW3[e] = x[eti]^T dB   (M = d, N = f, K = slots of e)
@@ -282,27 +277,14 @@ g5_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ dA,
         lb1.init(dB, f, off, n0, f, cnt);
     }
     Acc<C> acc;
-    gemm_mainloop<C>(la, lb0, lb1, (cnt + GBK - 1) / GBK, tail_from(cnt), lds, acc);
-    WaveCoord<C> wc;
+    gemm_mainloop<C>(la, lb0, lb1, (cnt + GBK - 1) / GBK, tail_from(cnt), lds, acc, d - m0,
+                     f - n0);
     float* o1 = dw1 + (int64_t)e * d * f;
     float* o3 = dw3 + (int64_t)e * d * f;
-#pragma unroll
-    for (int i = 0; i < C::FM; ++i) {
-        const int m = m0 + wc.row(i);
-        if (m >= d) continue;
-#pragma unroll
-        for (int j = 0; j < C::FN; ++j)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int n = n0 + wc.col(j, q);
-                if (n >= f) continue;
-                const int64_t o = (int64_t)m * f + n;
-                const f32x16& v1 = acc[0][i][j];
-                const f32x16& v3 = acc[1][i][j];
-                *reinterpret_cast<f32x4*>(o1 + o) = f32x4{v1[4 * q], v1[4 * q + 1], v1[4 * q + 2], v1[4 * q + 3]};
-                *reinterpret_cast<f32x4*>(o3 + o) = f32x4{v3[4 * q], v3[4 * q + 1], v3[4 * q + 2], v3[4 * q + 3]};
-            }
-    }
+    RowStage<C, 2>::run(acc, lds, [&](int b, int r, int c, const f32x4& v) {
+        const int m = m0 + r, n = n0 + c;
+        if (m < d && n < f) st_nt((b ? o3 : o1) + (int64_t)m * f + n, v);
+    });
 }
 
 // G6: dX_slot = dA W1[e]^T + dB W3[e]^T   (K = 2f)
@@ -322,7 +304,7 @@ g6_kernel(const bf16_t* __restrict__ dA, const bf16_t* __restrict__ dB,
     lb.init(w1 + (int64_t)t.e * d * f, w3 + (int64_t)t.e * d * f, f, t.n0, min(C::BN, d - t.n0), f);
     NoLoader nl;
     Acc<C> acc;
-    gemm_mainloop<C>(la, lb, nl, 2 * f / GBK, GBK, lds, acc);
+    gemm_mainloop<C>(la, lb, nl, 2 * f / GBK, GBK, lds, acc, t.mrows);
     WaveCoord<C> wc;
 #pragma unroll
     for (int i = 0; i < C::FM; ++i) {

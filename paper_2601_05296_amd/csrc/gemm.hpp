@@ -41,6 +41,8 @@
 //    row q, lane l receives column l of k rows 0..3.
 #pragma once
 
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace moe {
@@ -180,9 +182,13 @@ __device__ __forceinline__ void zero_mc_rows(char* tile, int from) {
 // (the left operand is then MC; used for the weight gradients' token tails).
 // On return acc[b][i][j] holds sum_k A[m][k] B_b[k][n] for the fragment at
 // rows wm*WTM + 32i, columns wn*WTN + 32j.
+// arows / bcols: rows of the left operand tile and columns of the right one
+// that hold real outputs. A wave whose fragments lie wholly beyond them skips
+// their LDS reads and MFMAs (its loads still land: the copies are shared).
 template <class C, class LA, class LB0, class LB1>
 __device__ __forceinline__ void gemm_mainloop(LA& la, LB0& lb0, LB1& lb1, int nk, int zero_from,
-                                              char* lds, Acc<C>& acc) {
+                                              char* lds, Acc<C>& acc, int arows = C::BM,
+                                              int bcols = C::BN) {
 #pragma unroll
     for (int b = 0; b < C::NB; ++b)
 #pragma unroll
@@ -193,7 +199,7 @@ __device__ __forceinline__ void gemm_mainloop(LA& la, LB0& lb0, LB1& lb1, int nk
                 for (int r = 0; r < 16; ++r) acc[b][i][j][r] = 0.f;
     if (nk <= 0) return;
     const int lane = threadIdx.x & 63;
-    const int wv = threadIdx.x >> 6;
+    const int wv = wave_id();
     const int wm = wv / C::WN, wn = wv % C::WN;
     constexpr int PER = LA::NQ + LB0::NQ + (C::NB == 2 ? LB1::NQ : 0);  // copies per slice
 
@@ -220,37 +226,48 @@ __device__ __forceinline__ void gemm_mainloop(LA& la, LB0& lb0, LB1& lb1, int nk
     barrier_only();
     fix_tail(0);
 
-    for (int kt = 0; kt < nk; ++kt) {
-        if (kt + NST - 1 < nk) issue(kt + NST - 1);
-        const char* cur = lds + (kt % NST) * C::STAGE;
+    // fragments of this wave that hold real outputs (wave-uniform)
+    const int nfm = min(C::FM, max(0, (arows - wm * C::WTM + 31) >> 5));
+    const int nfn = min(C::FN, max(0, (bcols - wn * C::WTN + 31) >> 5));
+    auto loop = [&](auto partial) {
+        constexpr bool PART = decltype(partial)::value;
+        for (int kt = 0; kt < nk; ++kt) {
+            if (kt + NST - 1 < nk) issue(kt + NST - 1);
+            const char* cur = lds + (kt % NST) * C::STAGE;
 #pragma unroll
-        for (int kk = 0; kk < GBK / 16; ++kk) {
-            bf16x8 fa[C::FM];
-#pragma unroll
-            for (int i = 0; i < C::FM; ++i)
-                fa[i] = frag<LA::MC, C::BM>(cur, wm * C::WTM + i * 32, kk, lane);
-#pragma unroll
-            for (int b = 0; b < C::NB; ++b) {
-                const char* bt = cur + C::A_BYTES + b * C::B_BYTES;
-                bf16x8 fb[C::FN];
-#pragma unroll
-                for (int j = 0; j < C::FN; ++j)
-                    fb[j] = frag<LB0::MC, C::BN>(bt, wn * C::WTN + j * 32, kk, lane);
+            for (int kk = 0; kk < GBK / 16; ++kk) {
+                bf16x8 fa[C::FM];
 #pragma unroll
                 for (int i = 0; i < C::FM; ++i)
+                    if (!PART || (i < nfm && nfn > 0))
+                        fa[i] = frag<LA::MC, C::BM>(cur, wm * C::WTM + i * 32, kk, lane);
+#pragma unroll
+                for (int b = 0; b < C::NB; ++b) {
+                    const char* bt = cur + C::A_BYTES + b * C::B_BYTES;
+                    bf16x8 fb[C::FN];
 #pragma unroll
                     for (int j = 0; j < C::FN; ++j)
-                        acc[b][i][j] = mfma32x32x16(fb[j], fa[i], acc[b][i][j]);
+                        if (!PART || (j < nfn && nfm > 0))
+                            fb[j] = frag<LB0::MC, C::BN>(bt, wn * C::WTN + j * 32, kk, lane);
+#pragma unroll
+                    for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+                        for (int j = 0; j < C::FN; ++j)
+                            if (!PART || (i < nfm && j < nfn))
+                                acc[b][i][j] = mfma32x32x16(fb[j], fa[i], acc[b][i][j]);
+                }
+            }
+            if (kt + 1 < nk) {
+                // slice kt+1 has landed once only the copies of later slices remain
+                if (kt + NST - 1 < nk) wait_vmcnt<PER * (NST - 2)>();
+                else wait_vmcnt<0>();
+                barrier_only();
+                fix_tail(kt + 1);
             }
         }
-        if (kt + 1 < nk) {
-            // slice kt+1 has landed once only the copies of later slices remain
-            if (kt + NST - 1 < nk) wait_vmcnt<PER * (NST - 2)>();
-            else wait_vmcnt<0>();
-            barrier_only();
-            fix_tail(kt + 1);
-        }
-    }
+    };
+    if (nfm == C::FM && nfn == C::FN) loop(std::false_type{});
+    else loop(std::true_type{});
     // every wave is done reading LDS before an epilogue reuses it
     __syncthreads();
 }
@@ -296,6 +313,66 @@ struct WaveCoord {
     __device__ int col(int j, int q) const { return wn * C::WTN + j * 32 + q * 8 + (lane >> 5) * 4; }
     // tile-local first column of eight-column group p (0, 1) after frag_cols8
     __device__ int col8(int j, int p) const { return wn * C::WTN + j * 32 + p * 16 + (lane >> 5) * 8; }
+};
+
+// ---- f32 tile output through LDS -------------------------------------------------------
+// The accumulators go through LDS, IPR fragment row-blocks of every wave per
+// round, and leave as whole rows of the tile: a wave's store instruction covers
+// 1 KB of consecutive output bytes (or two rows of 512 B), so every 128-byte
+// line is written by a single instruction. LDS rows are padded by 16 bytes,
+// which keeps both the fragment writes and the row reads free of bank conflicts.
+// Call after gemm_mainloop (whose final barrier frees the LDS ring). Between
+// rounds only the LDS accesses are ordered: the global stores of a round stay
+// in flight while the next round is staged.
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+template <class C, int IPR>
+struct RowStage {
+    static constexpr int ROWS = C::WM * 32 * IPR;
+    static constexpr int PITCH = C::BN * 4 + 16;
+    static constexpr int V4_PER_ROW = C::BN / 4;
+    static constexpr int PASSES = ROWS * V4_PER_ROW / C::THREADS;
+    static constexpr int ROUNDS = C::NB * C::FM / IPR;
+    static_assert(ROWS * PITCH <= C::LDS, "staging fits the LDS ring");
+    static_assert(C::FM % IPR == 0 && (ROWS * V4_PER_ROW) % C::THREADS == 0, "even split");
+    // store(b, tile_row, tile_col, f32x4) is called for every 4 consecutive outputs
+    template <class F>
+    __device__ static void run(const Acc<C>& acc, char* lds, F&& store) {
+        const WaveCoord<C> wc;
+#pragma unroll
+        for (int rd = 0; rd < ROUNDS; ++rd) {
+            const int b = rd / (C::FM / IPR), i0 = (rd % (C::FM / IPR)) * IPR;
+            if (rd > 0) lds_barrier();
+#pragma unroll
+            for (int ii = 0; ii < IPR; ++ii)
+#pragma unroll
+                for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int cr = wc.wm * 32 * IPR + ii * 32 + (wc.lane & 31);
+                        const f32x16& v = acc[b][i0 + ii][j];
+                        *reinterpret_cast<f32x4*>(lds + cr * PITCH + wc.col(j, q) * 4) =
+                            f32x4{v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
+                    }
+            lds_barrier();
+            f32x4 v[PASSES];
+#pragma unroll
+            for (int p = 0; p < PASSES; ++p) {
+                const int t = threadIdx.x + p * C::THREADS;
+                v[p] = *reinterpret_cast<const f32x4*>(lds + (t / V4_PER_ROW) * PITCH +
+                                                       (t % V4_PER_ROW) * 16);
+            }
+#pragma unroll
+            for (int p = 0; p < PASSES; ++p) {
+                const int t = threadIdx.x + p * C::THREADS;
+                const int cr = t / V4_PER_ROW, c4 = t % V4_PER_ROW;
+                const int row = (cr / (32 * IPR)) * C::WTM + (i0 + (cr / 32) % IPR) * 32 + (cr & 31);
+                store(b, row, c4 * 4, v[p]);
+            }
+        }
+    }
 };
 
 // ---- weight-gradient tile order ---------------------------------------------------------

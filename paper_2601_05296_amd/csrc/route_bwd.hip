@@ -204,7 +204,7 @@ rb_dx_mfma(const bf16_t* __restrict__ hl, const bf16_t* __restrict__ wg, int64_t
     lb.init(wg, d, n0, d, Ep, E);
     NoLoader nl;
     Acc<C> acc;
-    gemm_mainloop<C>(la, lb, nl, 2 * Ep / GBK, GBK, lds, acc);
+    gemm_mainloop<C>(la, lb, nl, 2 * Ep / GBK, GBK, lds, acc, rows, d - n0);
     WaveCoord<C> wc;
 #pragma unroll
     for (int i = 0; i < C::FM; ++i) {
@@ -249,7 +249,8 @@ rb_dwg_mfma(const bf16_t* __restrict__ hl, const bf16_t* __restrict__ x, int64_t
     lb.init(x, d, t0, n0, d, cnt);
     NoLoader nl;
     Acc<C> acc;
-    gemm_mainloop<C>(la, lb, nl, (cnt + GBK - 1) / GBK, tail_from(cnt), lds, acc);
+    gemm_mainloop<C>(la, lb, nl, (cnt + GBK - 1) / GBK, tail_from(cnt), lds, acc, M - m0,
+                     d - n0);
     WaveCoord<C> wc;
     float* out = part + (int64_t)split * M * d;
 #pragma unroll
