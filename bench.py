@@ -392,6 +392,16 @@ def main():
                 "frac": kd["frac"], "traffic": read_traffic(cfg.name, dom), "kernel": dom,
                 "per_launch": amount, "avg_ms": kd["avg_ms"]}
     gemm_ms = sum(kernels[n]["ms_per_step"] for n in kernels if n.startswith("g") and n[1].isdigit())
+    # per-stage kernel time (ms per step); the router's two stages are the part
+    # a sparse-to-sparse timing leaves out
+    stage_of = {"route": ("route_",), "build": ("tile_",), "ffn_fwd": ("g1_", "g2_", "f32_g1", "f32_g2"),
+                "combine": ("combine",), "ffn_bwd": ("g3_", "g4_", "g5_", "g6_", "dgate", "f32_g3",
+                                                      "f32_g4", "f32_g5", "f32_g6"),
+                "route_bwd": ("rb_",)}
+    stages = {st: round(sum(v["ms_per_step"] for n, v in kernels.items()
+                            if any(n.startswith(p) for p in pre)), 4)
+              for st, pre in stage_of.items()}
+    router_ms = stages["route"] + stages["route_bwd"]
     gemm_flops = 18.0 * T * k * d * f
     out = {
         "metric": "MoE layer fwd+bwd tokens/sec + peak activation bytes/token, 1 MI355X",
@@ -406,6 +416,10 @@ def main():
         "gemm": {"ms_per_step": round(gemm_ms, 4),
                  "tflops": round(gemm_flops / (gemm_ms * 1e-3) / 1e12, 1),
                  "frac": round(gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)},
+        "stages_ms": stages,
+        "dispatch_us": {"route_plus_build": round((stages["route"] + stages["build"]) * 1e3, 1),
+                        "build": round(stages["build"] * 1e3, 1)},
+        "sparse_to_sparse_tokens_per_s": round(T / ((ms_step - router_ms) * 1e-3), 1),
         "kernels": kernels,
     }
     if args.copy_calibration:
