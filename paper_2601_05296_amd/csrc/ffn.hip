@@ -162,37 +162,63 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
     NoLoader nl;
     Acc<C> acc;
     gemm_mainloop<C>(la, lb, nl, d / GBK, GBK, lds, acc, t.mrows, f - t.n0);
-    WaveCoord<C> wc;
+    // ---- epilogue, one round per fragment row-block (64 rows of the tile) ----
+    // The A and B rows of the round come into LDS by DMA (1 KB copies, many in
+    // flight); every lane reads its values there, writes dA and dB back in
+    // place, and the rows then leave LDS as whole 512-byte runs. g*h follows
+    // through the same buffer. 16-byte chunks are XOR-swizzled by row, so the
+    // fragment-ordered LDS accesses (32 rows, one column) are conflict-free.
+    constexpr int RR = C::WM * 32;       // rows per round
+    constexpr int RB = C::BN * 2;        // bytes per row
+    constexpr int CPR = RB / 16;         // 16-byte chunks per row (32)
+    constexpr int ARR = RR * RB;         // bytes of one array in LDS
+    static_assert(CPR == 32 && 2 * ARR <= C::LDS, "G4 staging layout");
+    const WaveCoord<C> wc;
     const int nparts = NT * C::WN;
     const int pidx = (t.n0 / C::BN) * C::WN + wc.wn;
+    const uint32_t lds_base = lds_offset(lds);
+    const int wv = wave_id();
+    auto tile_row = [&](int rr, int i) { return (rr / 32) * C::WTM + i * 32 + (rr & 31); };
 #pragma unroll
     for (int i = 0; i < C::FM; ++i) {
+        // DMA the round's A and B rows: copy q covers rows 2q', 2q'+1 of array q / (ARR/1024)
+#pragma unroll
+        for (int c = 0; c < 2 * ARR / 1024 / C::NW; ++c) {
+            const int q = wv + c * C::NW;
+            const int arr = q / (ARR / 1024), qq = q % (ARR / 1024);
+            const int rr = 2 * qq + (wc.lane >> 5);
+            const int lc = (wc.lane & 31) ^ (rr & 31);
+            int m = tile_row(rr, i);
+            m = m < t.mrows ? m : 0;
+            int n = t.n0 + lc * 8;
+            n = n < f ? n : f - 8;
+            const bf16_t* src = (arr ? B : A) + ((int64_t)t.off + t.m0 + m) * f + n;
+            dma16(src, lds_base + arr * ARR + qq * 1024);
+        }
+        wait_vmcnt<0>();
+        barrier_only();
+        // this lane's row of the round and its gate
+        const int rr = wc.wm * 32 + (wc.lane & 31);
         const int m = wc.row(i);
         const bool valid = m < t.mrows;
         const int64_t s = (int64_t)t.off + t.m0 + (valid ? m : 0);
         const float g = gates[slot_src[s]];
-        // all A/B loads of this row block first (they alias the stores below)
-        uint4 av[C::FN][2], bv[C::FN][2];
-#pragma unroll
-        for (int j = 0; j < C::FN; ++j)
-#pragma unroll
-            for (int p = 0; p < 2; ++p) {
-                int n = t.n0 + wc.col8(j, p);
-                n = n < f ? n : f - 8;
-                av[j][p] = ld16(A + s * f + n);
-                bv[j][p] = ld16(B + s * f + n);
-            }
+        char* rowA = lds + rr * RB;
+        char* rowB = lds + ARR + rr * RB;
         float dg = 0.f;
+        uint4 hgv[C::FN][2];
 #pragma unroll
         for (int j = 0; j < C::FN; ++j) {
             float u8[2][8];
             frag_cols8(acc[0][i][j], u8);
 #pragma unroll
             for (int p = 0; p < 2; ++p) {
-                const int n = t.n0 + wc.col8(j, p);
+                const int cl = wc.col8(j, p);                       // tile column
+                const int off = (((cl >> 3) ^ (rr & 31)) << 4);     // swizzled chunk
+                const int n = t.n0 + cl;
                 float a[8], b[8], da[8], db[8], hg[8];
-                unpack8(av[j][p], a);
-                unpack8(bv[j][p], b);
+                unpack8(*reinterpret_cast<const uint4*>(rowA + off), a);
+                unpack8(*reinterpret_cast<const uint4*>(rowB + off), b);
 #pragma unroll
                 for (int r = 0; r < 8; ++r) {
                     const float u = u8[p][r];
@@ -205,15 +231,45 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
                     da[r] = dh * b[r] * sg * (1.0f + a[r] * (1.0f - sg));
                     db[r] = dh * sl;
                 }
-                if (valid && n < f) {
-                    store8_bf16(A + s * f + n, da);
-                    store8_bf16(B + s * f + n, db);
-                    store8_bf16(HG + s * f + n, hg);
-                }
+                *reinterpret_cast<uint4*>(rowA + off) = pack8(da);
+                *reinterpret_cast<uint4*>(rowB + off) = pack8(db);
+                hgv[j][p] = pack8(hg);
             }
         }
         dg += __shfl_xor(dg, 32, 64);
         if (valid && wc.lane < 32) part[s * nparts + pidx] = dg;
+        // rows out of LDS: chunk id -> (array, row, physical chunk)
+        auto store_rows = [&](int narr, bf16_t* const* dst) {
+#pragma unroll
+            for (int ps = 0; ps < narr * RR * CPR / C::THREADS; ++ps) {
+                const int cid = ps * C::THREADS + threadIdx.x;
+                const int arr = cid / (RR * CPR);
+                const int r2 = (cid / CPR) % RR, pc = cid % CPR;
+                const int mm = tile_row(r2, i);
+                const int n = t.n0 + ((pc ^ (r2 & 31)) << 3);
+                const uint4 v = *reinterpret_cast<const uint4*>(lds + arr * ARR + r2 * RB + pc * 16);
+                if (mm < t.mrows && n < f) st16_nt(dst[arr] + ((int64_t)t.off + t.m0 + mm) * f + n, v);
+            }
+        };
+        lds_barrier();
+        {
+            bf16_t* const dst[2] = {A, B};
+            store_rows(2, dst);
+        }
+        lds_barrier();
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+            for (int p = 0; p < 2; ++p) {
+                const int off = (((wc.col8(j, p) >> 3) ^ (rr & 31)) << 4);
+                *reinterpret_cast<uint4*>(rowA + off) = hgv[j][p];
+            }
+        lds_barrier();
+        {
+            bf16_t* const dst[1] = {HG};
+            store_rows(1, dst);
+        }
+        lds_barrier();
     }
 }
 
