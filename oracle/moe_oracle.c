@@ -33,6 +33,10 @@
  *     with SiLU recomputed, and token gradients sum the k slot gradients.
  *   - Router backward: the paper gives none; the closed form of the softmax
  *     (or renormalised softmax) Jacobian is used.
+ *   - Non-gated experts (Section 2.2, E_i(x) = W2 act(W1 x); the experiments
+ *     of Section 6 use ReLU and SiLU): a = x W1 is the one saved activation,
+ *     act is recomputed from it in the backward (the checkpoint of Section
+ *     5.2 applied to a single projection). ReLU'(0) is taken as 0.
  */
 #include <math.h>
 #include <stddef.h>
@@ -44,6 +48,16 @@
 
 static double sigmoid(double u) { return 1.0 / (1.0 + exp(-u)); }
 static double silu(double u) { return u * sigmoid(u); }
+
+/* activation codes of the non-gated experts */
+enum { ACT_SILU = 1, ACT_RELU = 2 };
+static double act_f(int act, double u) { return act == ACT_RELU ? (u > 0.0 ? u : 0.0) : silu(u); }
+static double act_d(int act, double u)
+{
+    if (act == ACT_RELU) return u > 0.0 ? 1.0 : 0.0;
+    const double sg = sigmoid(u);
+    return sg * (1.0 + u * (1.0 - sg));
+}
 
 /* ---------------------------------------------------------------------------
  * Gating (Section 2.1): logits = x W_g^T (+ bias), p = softmax(logits),
@@ -345,6 +359,106 @@ ORACLE_API void oracle_route_bwd(const double* d_gates, const double* logits,
         for (int64_t t = 0; t < T; ++t) {
             const double c = dlogits[t * E + e];
             for (int i = 0; i < d; ++i) dw[i] += c * x[t * d + i];
+        }
+    }
+}
+
+/* ---------------------------------------------------------------------------
+ * Non-gated expert forward (Section 2.2): per slot s of expert e, token
+ * t = eti[s]:  a = x[t] W1[e],  h = act(a),  o = h W2[e].
+ * Outputs A [S,f] (the saved pre-activation) and O [S,d].
+ * ------------------------------------------------------------------------- */
+ORACLE_API void oracle_ffn_fwd_act(const double* x, const double* w1, const double* w2,
+                                   const int32_t* offsets, const int32_t* eti, int64_t T,
+                                   int d, int f, int E, int k, int act, double* A, double* O)
+{
+    const int64_t S = T * k;
+    #pragma omp parallel for schedule(static)
+    for (int64_t s = 0; s < S; ++s) {
+        const int e = expert_of_slot(offsets, E, s);
+        const double* xt = x + (int64_t)eti[s] * d;
+        const double* W1 = w1 + (int64_t)e * d * f;
+        const double* W2 = w2 + (int64_t)e * f * d;
+        double* a = A + s * f;
+        double* o = O + s * d;
+        for (int n = 0; n < f; ++n) a[n] = 0.0;
+        for (int i = 0; i < d; ++i) {
+            const double xi = xt[i];
+            for (int n = 0; n < f; ++n) a[n] += xi * W1[(int64_t)i * f + n];
+        }
+        for (int n = 0; n < d; ++n) o[n] = 0.0;
+        for (int c = 0; c < f; ++c) {
+            const double h = act_f(act, a[c]);
+            for (int n = 0; n < d; ++n) o[n] += h * W2[(int64_t)c * d + n];
+        }
+    }
+}
+
+/* ---------------------------------------------------------------------------
+ * Non-gated expert backward (Section 3.2 with the expert of Section 2.2), per
+ * slot s of expert e, token t, gate g = gates[slot_src[s]]:
+ *   d_gates[slot_src[s]] = <dY[t], O[s]>,  O[s] = act(A[s]) W2[e] recomputed
+ *   dh = (g dY[t]) W2[e]^T,   dA = dh * act'(A)
+ *   dW2[e] += act(A)^T (g dY[t]),   dW1[e] += x[t]^T dA,   dX_slot[s] = dA W1[e]^T
+ * Weight gradients are summed over the expert's slots in slot order.
+ * ------------------------------------------------------------------------- */
+ORACLE_API void oracle_ffn_bwd_act(const double* dy, const double* x, const double* w1,
+                                   const double* w2, const double* gates,
+                                   const int32_t* offsets, const int32_t* eti,
+                                   const int32_t* slot_src, const double* A, int64_t T, int d,
+                                   int f, int E, int k, int act, double* dA, double* dw1,
+                                   double* dw2, double* d_gates, double* dX_slot)
+{
+    const int64_t S = T * k;
+    #pragma omp parallel for schedule(static)
+    for (int64_t s = 0; s < S; ++s) {
+        const int e = expert_of_slot(offsets, E, s);
+        const int64_t t = eti[s];
+        const double g = gates[slot_src[s]];
+        const double* W1 = w1 + (int64_t)e * d * f;
+        const double* W2 = w2 + (int64_t)e * f * d;
+        const double* a = A + s * f;
+        const double* dyt = dy + t * d;
+        double* o = (double*)calloc((size_t)d, sizeof(double));
+        for (int c = 0; c < f; ++c) {
+            const double h = act_f(act, a[c]);
+            for (int n = 0; n < d; ++n) o[n] += h * W2[(int64_t)c * d + n];
+        }
+        double dg = 0.0;
+        for (int n = 0; n < d; ++n) dg += dyt[n] * o[n];
+        free(o);
+        d_gates[slot_src[s]] = dg;
+        for (int c = 0; c < f; ++c) {
+            double dh = 0.0;
+            for (int n = 0; n < d; ++n) dh += g * dyt[n] * W2[(int64_t)c * d + n];
+            dA[s * f + c] = dh * act_d(act, a[c]);
+        }
+        double* dxs = dX_slot + s * d;
+        for (int i = 0; i < d; ++i) {
+            double acc = 0.0;
+            for (int c = 0; c < f; ++c) acc += dA[s * f + c] * W1[(int64_t)i * f + c];
+            dxs[i] = acc;
+        }
+    }
+    #pragma omp parallel for schedule(dynamic, 1)
+    for (int e = 0; e < E; ++e) {
+        double* DW1 = dw1 + (int64_t)e * d * f;
+        double* DW2 = dw2 + (int64_t)e * f * d;
+        memset(DW1, 0, sizeof(double) * (size_t)d * f);
+        memset(DW2, 0, sizeof(double) * (size_t)f * d);
+        for (int64_t s = offsets[e]; s < offsets[e + 1]; ++s) {
+            const int64_t t = eti[s];
+            const double g = gates[slot_src[s]];
+            const double* xt = x + t * d;
+            const double* dyt = dy + t * d;
+            for (int c = 0; c < f; ++c) {
+                const double h = act_f(act, A[s * f + c]);
+                for (int n = 0; n < d; ++n) DW2[(int64_t)c * d + n] += h * g * dyt[n];
+            }
+            for (int i = 0; i < d; ++i) {
+                const double xi = xt[i];
+                for (int c = 0; c < f; ++c) DW1[(int64_t)i * f + c] += xi * dA[s * f + c];
+            }
         }
     }
 }

@@ -46,6 +46,8 @@ def _load():
         _lib.oracle_combine.argtypes = [P, P, P, I64, I, I, P]
         _lib.oracle_ffn_bwd.argtypes = [P] * 11 + [I64, I, I, I, I] + [P] * 7
         _lib.oracle_route_bwd.argtypes = [P, P, P, P, P, I64, I, I, I, I, P, P, P]
+        _lib.oracle_ffn_fwd_act.argtypes = [P, P, P, P, P, I64, I, I, I, I, I, P, P]
+        _lib.oracle_ffn_bwd_act.argtypes = [P] * 9 + [I64, I, I, I, I, I] + [P] * 5
         for fn in ("oracle_route", "oracle_build_index", "oracle_ffn_fwd",
                    "oracle_combine", "oracle_ffn_bwd", "oracle_route_bwd"):
             getattr(_lib, fn).restype = None
@@ -113,6 +115,42 @@ def ffn_fwd(x, w1, w3, w2, ix: Index, k: int):
     return A, B, O
 
 
+# expert activations: "swiglu" (Section 5.1, gated, W3 branch) or the non-gated
+# "silu" / "relu" experts of Section 2.2 (E(x) = W2 act(W1 x))
+ACTS = {"silu": 1, "relu": 2}
+
+
+def ffn_fwd_act(x, w1, w2, ix: Index, k: int, act: str):
+    """Per-slot non-gated expert forward (Section 2.2). Returns A [S,f] (the
+    saved pre-activation) and O [S,d]."""
+    x, w1, w2 = _f64(x), _f64(w1), _f64(w2)
+    T, d = x.shape
+    E, _, f = w1.shape
+    S = T * k
+    A = np.empty((S, f)); O = np.empty((S, d))
+    _load().oracle_ffn_fwd_act(_p(x), _p(w1), _p(w2), _p(ix.offsets), _p(ix.eti), T, d, f, E, k,
+                               ACTS[act], _p(A), _p(O))
+    return A, O
+
+
+def ffn_bwd_act(dy, x, w1, w2, gates, ix: Index, A, act: str):
+    """Non-gated expert backward (Section 3.2 with the Section 2.2 expert).
+    Returns dict with dA [S,f], dw1 [E,d,f], dw2 [E,f,d], d_gates [T,k],
+    dX_slot [S,d]."""
+    dy, x, w1, w2, gates, A = map(_f64, (dy, x, w1, w2, gates, A))
+    T, d = x.shape
+    E, _, f = w1.shape
+    k = gates.shape[1]
+    S = T * k
+    out = dict(dA=np.empty((S, f)), dw1=np.empty((E, d, f)), dw2=np.empty((E, f, d)),
+               d_gates=np.empty((T, k)), dX_slot=np.empty((S, d)))
+    _load().oracle_ffn_bwd_act(_p(dy), _p(x), _p(w1), _p(w2), _p(gates), _p(ix.offsets),
+                               _p(ix.eti), _p(ix.slot_src), _p(A), T, d, f, E, k, ACTS[act],
+                               _p(out["dA"]), _p(out["dw1"]), _p(out["dw2"]),
+                               _p(out["d_gates"]), _p(out["dX_slot"]))
+    return out
+
+
 def combine(src, weights, tim):
     """out[t] = sum_j w[t,j] src[tim[t,j]] (Section 2.3; weights None = 1)."""
     src, weights, tim = _f64(src), _f64(weights), _i32(tim)
@@ -154,9 +192,11 @@ def route_bwd(d_gates, logits, ids, x, w_gate, renorm: bool):
     return dl, dwg, dxr
 
 
-def layer_forward(x, w_gate, bias, w1, w3, w2, k: int, renorm: bool, ids=None):
+def layer_forward(x, w_gate, bias, w1, w3, w2, k: int, renorm: bool, ids=None,
+                  act: str = "swiglu"):
     """Whole layer forward. ``ids`` pins the routing decision (used when a
-    caller compares against a device run that already routed)."""
+    caller compares against a device run that already routed). For a
+    non-gated ``act`` w3 is unused and B is None."""
     r_ids, gates, logits, probs = route(x, w_gate, bias, k, renorm)
     if ids is not None:
         ids = _i32(ids)
@@ -166,15 +206,23 @@ def layer_forward(x, w_gate, bias, w1, w3, w2, k: int, renorm: bool, ids=None):
         ids = r_ids
     E = w_gate.shape[0]
     ix = build_index(ids, E)
-    A, B, O = ffn_fwd(x, w1, w3, w2, ix, k)
+    if act == "swiglu":
+        A, B, O = ffn_fwd(x, w1, w3, w2, ix, k)
+    else:
+        (A, O), B = ffn_fwd_act(x, w1, w2, ix, k, act), None
     y = combine(O, gates, ix.tim)
-    return dict(ids=ids, gates=gates, logits=logits, probs=probs, ix=ix, A=A, B=B, O=O, y=y)
+    return dict(ids=ids, gates=gates, logits=logits, probs=probs, ix=ix, A=A, B=B, O=O, y=y,
+                act=act)
 
 
 def layer_backward(fw: dict, dy, x, w_gate, w1, w3, w2, renorm: bool):
     """Whole layer backward from a ``layer_forward`` result: expert backward,
     token gradient accumulation (Section 3.2 step 3) and router backward."""
-    bw = ffn_bwd(dy, x, w1, w3, w2, fw["gates"], fw["ix"], fw["A"], fw["B"])
+    act = fw.get("act", "swiglu")
+    if act == "swiglu":
+        bw = ffn_bwd(dy, x, w1, w3, w2, fw["gates"], fw["ix"], fw["A"], fw["B"])
+    else:
+        bw = ffn_bwd_act(dy, x, w1, w2, fw["gates"], fw["ix"], fw["A"], act)
     dx_ffn = combine(bw["dX_slot"], None, fw["ix"].tim)
     dl, dwg, dxr = route_bwd(bw["d_gates"], fw["logits"], fw["ids"], x, w_gate, renorm)
     bw.update(dx_ffn=dx_ffn, dlogits=dl, dw_gate=dwg, dx_router=dxr, dx=dx_ffn + dxr)

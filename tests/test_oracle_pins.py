@@ -313,3 +313,117 @@ def test_swiglu_derivative_closed_form():
     assert bw["dA"][0, 0] == pytest.approx(dh * (-0.28) * sg * (1 + a * (1 - sg)), rel=1e-14)
     assert bw["dB"][0, 0] == pytest.approx(dh * a * sg, rel=1e-14)
     assert O[0, 0] == pytest.approx(a * sg * (-0.28) * 2.0, rel=1e-14)
+
+
+# --------------------------------------------------------------------------
+# Non-gated experts (Section 2.2: E(x) = W2 act(W1 x); ReLU and SiLU as in the
+# experiments of Section 6)
+# --------------------------------------------------------------------------
+
+_TORCH_ACT = {"silu": torch.nn.functional.silu, "relu": torch.relu}
+
+
+def _torch_dense_act(v, ids, renorm, act, dy=None):
+    """Dense all-experts evaluation in float64 torch (routing fixed by ids);
+    returns y, and the input/weight gradients when dy is given."""
+    t = {n: torch.tensor(v[n], dtype=torch.float64, requires_grad=dy is not None)
+         for n in ("x", "w_gate", "w1", "w2")}
+    logits = t["x"] @ t["w_gate"].T
+    if v.get("bias") is not None:
+        logits = logits + torch.tensor(v["bias"], dtype=torch.float64)
+    p = torch.softmax(logits, dim=1)
+    idx = torch.tensor(ids, dtype=torch.int64)
+    g = torch.gather(p, 1, idx)
+    if renorm:
+        g = g / g.sum(dim=1, keepdim=True)
+    G = torch.zeros_like(p).scatter(1, idx, g)
+    y = torch.zeros_like(t["x"])
+    for e in range(v["w1"].shape[0]):
+        y = y + G[:, e:e + 1] * (_TORCH_ACT[act](t["x"] @ t["w1"][e]) @ t["w2"][e])
+    if dy is None:
+        return y.detach().numpy(), None
+    (y * torch.tensor(dy)).sum().backward()
+    return y.detach().numpy(), {n: tt.grad.numpy() for n, tt in t.items()}
+
+
+@pytest.mark.parametrize("act", ["silu", "relu"])
+@pytest.mark.parametrize("renorm,zipf", [(False, 0.0), (True, 0.0), (False, 1.2)])
+def test_nongated_forward_matches_dense_bruteforce(act, renorm, zipf):
+    v = _tiny_layer(T=30, d=16, f=24, E=6, k=3, zipf=zipf)
+    fw = oracle.layer_forward(v["x"], v["w_gate"], v["bias"], v["w1"], None, v["w2"], 3, renorm,
+                              act=act)
+    assert fw["B"] is None
+    y_ref, _ = _torch_dense_act(v, fw["ids"], renorm, act)
+    np.testing.assert_allclose(fw["y"], y_ref, rtol=1e-11, atol=1e-12)
+
+
+@pytest.mark.parametrize("act", ["silu", "relu"])
+def test_single_expert_is_textbook_mlp(act):
+    # E = 1, k = 1: a plain two-layer MLP W2 act(W1 x) (Section 2.2).
+    v = _tiny_layer(T=9, d=16, f=20, E=1, k=1)
+    fw = oracle.layer_forward(v["x"], v["w_gate"], None, v["w1"], None, v["w2"], 1, False, act=act)
+    a = v["x"] @ v["w1"][0]
+    h = np.maximum(a, 0.0) if act == "relu" else _silu(a)
+    np.testing.assert_allclose(fw["A"], a, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(fw["y"], h @ v["w2"][0], rtol=1e-12, atol=1e-13)
+
+
+@pytest.mark.parametrize("act", ["silu", "relu"])
+@pytest.mark.parametrize("renorm,zipf", [(False, 0.0), (True, 0.0), (False, 1.2)])
+def test_nongated_backward_matches_torch_autograd_dense(act, renorm, zipf):
+    v = _tiny_layer(T=14, d=12, f=16, E=5, k=2, zipf=zipf)
+    dy = v["dy"]
+    fw = oracle.layer_forward(v["x"], v["w_gate"], v["bias"], v["w1"], None, v["w2"], 2, renorm,
+                              act=act)
+    assert np.abs(fw["A"]).min() > 1e-9   # no pre-activation at the ReLU kink
+    bw = oracle.layer_backward(fw, dy, v["x"], v["w_gate"], v["w1"], None, v["w2"], renorm)
+    _, ref = _torch_dense_act(v, fw["ids"], renorm, act, dy)
+    for mine, theirs in (("dx", "x"), ("dw_gate", "w_gate"), ("dw1", "w1"), ("dw2", "w2")):
+        np.testing.assert_allclose(bw[mine], ref[theirs], rtol=1e-10, atol=1e-12, err_msg=mine)
+    assert "dw3" not in bw and "dB" not in bw
+
+
+@pytest.mark.parametrize("act", ["silu", "relu"])
+def test_nongated_backward_central_finite_differences(act):
+    k = 2
+    v = _tiny_layer(T=10, d=8, f=12, E=4, k=k, seed=5)
+    dy = v["dy"]
+    fw = oracle.layer_forward(v["x"], v["w_gate"], None, v["w1"], None, v["w2"], k, False, act=act)
+    bw = oracle.layer_backward(fw, dy, v["x"], v["w_gate"], v["w1"], None, v["w2"], False)
+    ids = fw["ids"]
+    h = 1e-6
+    assert np.abs(fw["A"]).min() > 1e3 * h   # steps never cross the ReLU kink
+
+    def loss(vv):
+        f2 = oracle.layer_forward(vv["x"], vv["w_gate"], None, vv["w1"], None, vv["w2"], k, False,
+                                  ids=ids, act=act)
+        return float((f2["y"] * dy).sum())
+
+    rng = np.random.default_rng(1)
+    for name, gname in (("x", "dx"), ("w_gate", "dw_gate"), ("w1", "dw1"), ("w2", "dw2")):
+        for _ in range(6):
+            idx = tuple(rng.integers(0, s) for s in v[name].shape)
+            vp = dict(v); vm = dict(v)
+            vp[name] = v[name].copy(); vm[name] = v[name].copy()
+            vp[name][idx] += h
+            vm[name][idx] -= h
+            fd = (loss(vp) - loss(vm)) / (2 * h)
+            an = bw[gname][idx]
+            assert abs(fd - an) <= 1e-6 * max(1.0, abs(an)), (name, idx, fd, an)
+
+
+def test_relu_derivative_closed_form():
+    # 1x1 expert: dA = dh * [a > 0] with dh = g dy w2; at a = 0 exactly the
+    # derivative is taken as 0 (h = 0 there, so dW2 and d_gate vanish too).
+    w2 = np.array([[[2.0]]]); dy = np.array([[0.5]])
+    ix = oracle.build_index(np.zeros((1, 1), np.int32), 1)
+    for xv, w1v, want in ((0.7, 1.3, 1.0), (0.7, -1.3, 0.0), (0.0, 1.3, 0.0)):
+        x = np.array([[xv]]); w1 = np.array([[[w1v]]])
+        A, O = oracle.ffn_fwd_act(x, w1, w2, ix, 1, "relu")
+        bw = oracle.ffn_bwd_act(dy, x, w1, w2, np.ones((1, 1)), ix, A, "relu")
+        a = xv * w1v
+        assert A[0, 0] == a and O[0, 0] == max(a, 0.0) * 2.0
+        assert bw["dA"][0, 0] == 0.5 * 2.0 * want
+        assert bw["dw2"][0, 0, 0] == max(a, 0.0) * 0.5
+        assert bw["dw1"][0, 0, 0] == xv * 0.5 * 2.0 * want
+        assert bw["d_gates"][0, 0] == 0.5 * O[0, 0]
