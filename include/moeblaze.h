@@ -56,6 +56,15 @@ extern "C" {
 #define MOE_F32         1u   /* float32 activations and weights (debug mode) */
 #define MOE_RENORM      2u   /* moe_route / moe_route_bwd: renormalise the k gates */
 #define MOE_ACCUMULATE  4u   /* moe_combine / moe_route_bwd: add into the output */
+/* moe_ffn_fwd / moe_ffn_bwd: expert activation. Default (neither flag): the
+ * gated SwiGLU expert of Section 5.1. MOE_ACT_SILU / MOE_ACT_RELU select the
+ * non-gated expert of Section 2.2, E(x) = w2 act(x w1) (ReLU and SiLU are the
+ * activations of the experiments, Section 6): w3, B and dw3 are then unused
+ * and may be NULL, A = x w1 is the only saved activation and act is
+ * recomputed from it in the backward. ReLU'(0) is taken as 0. At most one of
+ * the two may be set (else MOE_ERR_INVALID_ARG). */
+#define MOE_ACT_SILU    8u
+#define MOE_ACT_RELU    16u
 
 /* Human-readable name of a status code (static storage). */
 const char* moe_strerror(int status);
@@ -114,6 +123,8 @@ int moe_build_index(const int32_t* topk_ids, int64_t T, int E, int k,
  * In:  x, w1, w3, w2, offsets [E+1], expert_token_indices [T*k] (from
  *      moe_build_index).
  * Out: A, B [T*k, f], O [T*k, d] (element type per flags).
+ * Non-gated (MOE_ACT_SILU / MOE_ACT_RELU): A[s] = x[t] w1[e], h[s] = act(A[s]),
+ *      O[s] = h[s] w2[e]; w3 and B are not touched.
  * workspace: moe_ffn_fwd_workspace_size(T,d,f,E,k,flags) bytes (holds h
  *      between the two GEMMs; 0 in MOE_F32 mode, where NULL is accepted).
  */
@@ -153,6 +164,8 @@ int moe_combine(const void* src, const float* weights, const int32_t* token_inde
  * The token gradient is then moe_combine(dX_slot, NULL, token_index_map).
  * In:  dy [T,d], x, w1, w3, w2, gates [T,k], offsets, expert_token_indices,
  *      slot_src; A, B [T*k,f] as written by moe_ffn_fwd.
+ * Non-gated (MOE_ACT_SILU / MOE_ACT_RELU): h = act(A), dA = g u act'(A)
+ *      (written over A), dw1 and dX_slot from dA alone; w3, B, dw3 unused.
  * Out: A, B overwritten with dA, dB; dw1, dw3 [E,d,f], dw2 [E,f,d] float32
  *      (overwritten, zero for experts with no tokens); d_gates [T,k] float32;
  *      dX_slot [T*k, d].

@@ -25,6 +25,9 @@ MOE_BF16 = 0
 MOE_F32 = 1
 MOE_RENORM = 2
 MOE_ACCUMULATE = 4
+MOE_ACT_SILU = 8
+MOE_ACT_RELU = 16
+ACT_FLAG = {"swiglu": 0, "silu": MOE_ACT_SILU, "relu": MOE_ACT_RELU}
 
 # Every symbol declared in include/moeblaze.h.
 EXPORTS = ("moe_strerror", "moe_last_error", "moe_route", "moe_build_index_workspace_size",

@@ -32,7 +32,14 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
             return fail(MOE_ERR_INVALID_ARG, "%s: %s is not 16-byte aligned", fn, #p); \
     } while (0)
 
-const unsigned KNOWN_FLAGS = MOE_F32 | MOE_RENORM | MOE_ACCUMULATE;
+const unsigned KNOWN_FLAGS = MOE_F32 | MOE_RENORM | MOE_ACCUMULATE | MOE_ACT_SILU | MOE_ACT_RELU;
+const unsigned ACT_FLAGS = MOE_ACT_SILU | MOE_ACT_RELU;
+
+// expert activation code of the FFN calls (0 SwiGLU, 1 SiLU, 2 ReLU), or -1
+int act_of(unsigned flags) {
+    const unsigned a = flags & ACT_FLAGS;
+    return a == 0 ? 0 : a == MOE_ACT_SILU ? 1 : a == MOE_ACT_RELU ? 2 : -1;
+}
 
 int check_common(const char* fn, int64_t T, int E, int k, unsigned flags) {
     if (T < 0) return fail(MOE_ERR_INVALID_ARG, "%s: T = %lld < 0", fn, (long long)T);
@@ -100,6 +107,7 @@ int moe_route(const void* x, const void* w_gate, const float* bias, int64_t T, i
     const char* fn = "moe_route";
     int r;
     if ((r = check_common(fn, T, E, k, flags)) || (r = check_dim(fn, "d", d))) return r;
+    if (flags & ACT_FLAGS) return fail(MOE_ERR_INVALID_ARG, "%s: activation flags apply to the FFN calls only", fn);
     if (flags & MOE_ACCUMULATE) return fail(MOE_ERR_INVALID_ARG, "%s: MOE_ACCUMULATE not valid here", fn);
     if (T == 0) return MOE_OK;
     REQUIRE_PTR(x); REQUIRE_PTR(w_gate); OPT_PTR(bias); REQUIRE_PTR(topk_ids); REQUIRE_PTR(gates);
@@ -148,10 +156,14 @@ int moe_ffn_fwd(const void* x, const void* w1, const void* w3, const void* w2,
         (r = check_dim(fn, "f", f)))
         return r;
     if (flags & (MOE_RENORM | MOE_ACCUMULATE))
-        return fail(MOE_ERR_INVALID_ARG, "%s: only MOE_F32 / MOE_BF16 are valid flags", fn);
+        return fail(MOE_ERR_INVALID_ARG, "%s: only MOE_F32 / MOE_BF16 and an activation flag are valid", fn);
+    const int act = act_of(flags);
+    if (act < 0) return fail(MOE_ERR_INVALID_ARG, "%s: MOE_ACT_SILU and MOE_ACT_RELU both set", fn);
     if (T == 0) return MOE_OK;
-    REQUIRE_PTR(x); REQUIRE_PTR(w1); REQUIRE_PTR(w3); REQUIRE_PTR(w2); REQUIRE_PTR(offsets);
-    REQUIRE_PTR(expert_token_indices); REQUIRE_PTR(A); REQUIRE_PTR(B); REQUIRE_PTR(O);
+    REQUIRE_PTR(x); REQUIRE_PTR(w1); REQUIRE_PTR(w2); REQUIRE_PTR(offsets);
+    REQUIRE_PTR(expert_token_indices); REQUIRE_PTR(A); REQUIRE_PTR(O);
+    if (act == 0) { REQUIRE_PTR(w3); REQUIRE_PTR(B); }
+    else { OPT_PTR(w3); OPT_PTR(B); }
     const size_t need = moe::ffn_fwd_workspace(T, d, f, E, k, flags & MOE_F32);
     if (need && (!workspace || workspace_bytes < need))
         return fail(MOE_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, workspace_bytes, need);
@@ -159,6 +171,7 @@ int moe_ffn_fwd(const void* x, const void* w1, const void* w3, const void* w2,
     moe::FfnArgs a{};
     a.x = x; a.w1 = w1; a.w3 = w3; a.w2 = w2; a.offsets = offsets; a.eti = expert_token_indices;
     a.A = A; a.B = B; a.O = O; a.T = T; a.d = d; a.f = f; a.E = E; a.k = k; a.ws = workspace;
+    a.act = act;
     moe::probe::begin(stream);
     return hip_status(fn, moe::ffn_fwd(a, flags & MOE_F32, stream));
 }
@@ -168,6 +181,7 @@ int moe_combine(const void* src, const float* weights, const int32_t* token_inde
     const char* fn = "moe_combine";
     int r;
     if ((r = check_common(fn, T, k, k, flags)) || (r = check_dim(fn, "d", d))) return r;
+    if (flags & ACT_FLAGS) return fail(MOE_ERR_INVALID_ARG, "%s: activation flags apply to the FFN calls only", fn);
     if (flags & MOE_RENORM) return fail(MOE_ERR_INVALID_ARG, "%s: MOE_RENORM not valid here", fn);
     if (T == 0) return MOE_OK;
     REQUIRE_PTR(src); OPT_PTR(weights); REQUIRE_PTR(token_index_map); REQUIRE_PTR(out);
@@ -192,12 +206,16 @@ int moe_ffn_bwd(const void* dy, const void* x, const void* w1, const void* w3, c
         (r = check_dim(fn, "f", f)))
         return r;
     if (flags & (MOE_RENORM | MOE_ACCUMULATE))
-        return fail(MOE_ERR_INVALID_ARG, "%s: only MOE_F32 / MOE_BF16 are valid flags", fn);
+        return fail(MOE_ERR_INVALID_ARG, "%s: only MOE_F32 / MOE_BF16 and an activation flag are valid", fn);
+    const int act = act_of(flags);
+    if (act < 0) return fail(MOE_ERR_INVALID_ARG, "%s: MOE_ACT_SILU and MOE_ACT_RELU both set", fn);
     if (T == 0) return MOE_OK;
-    REQUIRE_PTR(dy); REQUIRE_PTR(x); REQUIRE_PTR(w1); REQUIRE_PTR(w3); REQUIRE_PTR(w2);
+    REQUIRE_PTR(dy); REQUIRE_PTR(x); REQUIRE_PTR(w1); REQUIRE_PTR(w2);
     REQUIRE_PTR(gates); REQUIRE_PTR(offsets); REQUIRE_PTR(expert_token_indices);
-    REQUIRE_PTR(slot_src); REQUIRE_PTR(A); REQUIRE_PTR(B); REQUIRE_PTR(dw1); REQUIRE_PTR(dw3);
+    REQUIRE_PTR(slot_src); REQUIRE_PTR(A); REQUIRE_PTR(dw1);
     REQUIRE_PTR(dw2); REQUIRE_PTR(d_gates); REQUIRE_PTR(dX_slot);
+    if (act == 0) { REQUIRE_PTR(w3); REQUIRE_PTR(B); REQUIRE_PTR(dw3); }
+    else { OPT_PTR(w3); OPT_PTR(B); OPT_PTR(dw3); }
     const size_t need = moe::ffn_bwd_workspace(T, d, f, E, k, flags & MOE_F32);
     if (need && (!workspace || workspace_bytes < need))
         return fail(MOE_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, workspace_bytes, need);
@@ -206,7 +224,7 @@ int moe_ffn_bwd(const void* dy, const void* x, const void* w1, const void* w3, c
     a.x = x; a.w1 = w1; a.w3 = w3; a.w2 = w2; a.offsets = offsets; a.eti = expert_token_indices;
     a.slot_src = slot_src; a.gates = gates; a.dy = dy; a.A = A; a.B = B; a.dX = dX_slot;
     a.dw1 = dw1; a.dw3 = dw3; a.dw2 = dw2; a.dgates = d_gates; a.T = T; a.d = d; a.f = f;
-    a.E = E; a.k = k; a.ws = workspace;
+    a.E = E; a.k = k; a.ws = workspace; a.act = act;
     moe::probe::begin(stream);
     return hip_status(fn, moe::ffn_bwd(a, flags & MOE_F32, stream));
 }
@@ -223,6 +241,7 @@ int moe_route_bwd(const float* d_gates, const float* logits, const int32_t* topk
     const char* fn = "moe_route_bwd";
     int r;
     if ((r = check_common(fn, T, E, k, flags)) || (r = check_dim(fn, "d", d))) return r;
+    if (flags & ACT_FLAGS) return fail(MOE_ERR_INVALID_ARG, "%s: activation flags apply to the FFN calls only", fn);
     if (T == 0) return MOE_OK;
     REQUIRE_PTR(d_gates); REQUIRE_PTR(logits); REQUIRE_PTR(topk_ids); REQUIRE_PTR(gates);
     REQUIRE_PTR(x); REQUIRE_PTR(w_gate); REQUIRE_PTR(dw_gate); REQUIRE_PTR(dx);

@@ -50,30 +50,60 @@ __device__ __forceinline__ void store4_bf16(bf16_t* p, float a, float b, float c
     *reinterpret_cast<uint2*>(p) = make_uint2(pack_bf2(a, b), pack_bf2(c, d));
 }
 __device__ __forceinline__ float silu_bf(float a) { return a * sigmoidf_(a); }
+
+// Expert activation: SwiGLU (gated, Section 5.1) or the non-gated SiLU / ReLU
+// experts of Section 2.2, E(x) = W2 act(W1 x), whose only saved activation is
+// A = x W1. ReLU'(0) is taken as 0.
+enum : int { ACT_SWIGLU = 0, ACT_SILU = 1, ACT_RELU = 2 };
+template <int ACT>
+__device__ __forceinline__ float act_f(float a) {
+    if constexpr (ACT == ACT_RELU) return a > 0.f ? a : 0.f;
+    else return a * sigmoidf_(a);
+}
+template <int ACT>
+__device__ __forceinline__ float act_d(float a) {
+    if constexpr (ACT == ACT_RELU) return a > 0.f ? 1.f : 0.f;
+    else {
+        const float sg = sigmoidf_(a);
+        return sg * (1.0f + a * (1.0f - sg));
+    }
+}
+// tile configuration of the first-layer and dW1 GEMMs: two right operands
+// when gated (W1|W3, dA|dB), one otherwise
+template <int ACT> using CFirst = std::conditional_t<ACT == ACT_SWIGLU, CD, CS>;
+static_assert(CD::THREADS == CS::THREADS && CD::LDS == CS::LDS, "CD and CS launch alike");
 __device__ __forceinline__ void store8_bf16(bf16_t* p, const float (&v)[8]) { st16(p, pack8(v)); }
 
 // ============================ kernels ==============================================
 
 // G1: A = x[eti] W1[e], B = x[eti] W3[e]; also H = SiLU(A) * B (from the
-// bf16-rounded A and B, exactly as the backward recomputes it).
+// bf16-rounded A and B, exactly as the backward recomputes it). Non-gated:
+// A = x[eti] W1[e] and H = act(A).
+template <int ACT>
 __global__ void __launch_bounds__(CD::THREADS)
 g1_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w1,
           const bf16_t* __restrict__ w3, const int32_t* __restrict__ offsets,
           const int32_t* __restrict__ eti, int d, int f, int E, bf16_t* __restrict__ A,
           bf16_t* __restrict__ B, bf16_t* __restrict__ H) {
     extern __shared__ __align__(16) char lds[];
-    using C = CD;
+    using C = CFirst<ACT>;
     SlotTile t;
     const int NT = (f + C::BN - 1) / C::BN;
     if (!find_slot_tile<C::THREADS>(offsets, E, C::BM, NT, xcd_remap(blockIdx.x, gridDim.x), C::BN, t))
         return;
     GatherKC<C, C::BM> la;
     la.init(x, d, eti + t.off + t.m0, t.mrows);
-    DenseMC<C, C::BN> lb0, lb1;
+    DenseMC<C, C::BN> lb0;
     lb0.init(w1 + (int64_t)t.e * d * f, f, t.n0, f);
-    lb1.init(w3 + (int64_t)t.e * d * f, f, t.n0, f);
     Acc<C> acc;
-    gemm_mainloop<C>(la, lb0, lb1, d / GBK, GBK, lds, acc, t.mrows);
+    if constexpr (ACT == ACT_SWIGLU) {
+        DenseMC<C, C::BN> lb1;
+        lb1.init(w3 + (int64_t)t.e * d * f, f, t.n0, f);
+        gemm_mainloop<C>(la, lb0, lb1, d / GBK, GBK, lds, acc, t.mrows);
+    } else {
+        NoLoader nl;
+        gemm_mainloop<C>(la, lb0, nl, d / GBK, GBK, lds, acc, t.mrows, f - t.n0);
+    }
     WaveCoord<C> wc;
 #pragma unroll
     for (int i = 0; i < C::FM; ++i) {
@@ -84,7 +114,7 @@ g1_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w1,
         for (int j = 0; j < C::FN; ++j) {
             float va[2][8], vb[2][8];
             frag_cols8(acc[0][i][j], va);
-            frag_cols8(acc[1][i][j], vb);
+            if constexpr (ACT == ACT_SWIGLU) frag_cols8(acc[1][i][j], vb);
 #pragma unroll
             for (int p = 0; p < 2; ++p) {
                 const int n = t.n0 + wc.col8(j, p);
@@ -93,11 +123,15 @@ g1_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w1,
 #pragma unroll
                 for (int r = 0; r < 8; ++r) {
                     a[r] = bf2f(f2bf(va[p][r]));
-                    b[r] = bf2f(f2bf(vb[p][r]));
-                    h[r] = silu_bf(a[r]) * b[r];
+                    if constexpr (ACT == ACT_SWIGLU) {
+                        b[r] = bf2f(f2bf(vb[p][r]));
+                        h[r] = silu_bf(a[r]) * b[r];
+                    } else {
+                        h[r] = act_f<ACT>(a[r]);
+                    }
                 }
                 store8_bf16(A + s * f + n, a);
-                store8_bf16(B + s * f + n, b);
+                if constexpr (ACT == ACT_SWIGLU) store8_bf16(B + s * f + n, b);
                 store8_bf16(H + s * f + n, h);
             }
         }
@@ -141,7 +175,9 @@ g2_kernel(const bf16_t* __restrict__ H, const bf16_t* __restrict__ w2,
 }
 
 // G4: u = dY[eti] W2[e]^T; epilogue: d_gate partials sum(u*h), dA/dB over
-// A/B, and HG = g * h (h recomputed from A, B) for G3.
+// A/B, and HG = g * h (h recomputed from A, B) for G3. Non-gated: dA = g u
+// act'(A) over A, h = act(A).
+template <int ACT>
 __global__ void __launch_bounds__(C4::THREADS, 2)
 g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
           const float* __restrict__ gates, const int32_t* __restrict__ offsets,
@@ -172,6 +208,7 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
     constexpr int RB = C::BN * 2;        // bytes per row
     constexpr int CPR = RB / 16;         // 16-byte chunks per row (32)
     constexpr int ARR = RR * RB;         // bytes of one array in LDS
+    constexpr int NARR = ACT == ACT_SWIGLU ? 2 : 1;   // A, B or A alone
     static_assert(CPR == 32 && 2 * ARR <= C::LDS, "G4 staging layout");
     const WaveCoord<C> wc;
     const int nparts = NT * C::WN;
@@ -183,7 +220,7 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
     for (int i = 0; i < C::FM; ++i) {
         // DMA the round's A and B rows: copy q covers rows 2q', 2q'+1 of array q / (ARR/1024)
 #pragma unroll
-        for (int c = 0; c < 2 * ARR / 1024 / C::NW; ++c) {
+        for (int c = 0; c < NARR * ARR / 1024 / C::NW; ++c) {
             const int q = wv + c * C::NW;
             const int arr = q / (ARR / 1024), qq = q % (ARR / 1024);
             const int rr = 2 * qq + (wc.lane >> 5);
@@ -218,21 +255,28 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
                 const int n = t.n0 + cl;
                 float a[8], b[8], da[8], db[8], hg[8];
                 unpack8(*reinterpret_cast<const uint4*>(rowA + off), a);
-                unpack8(*reinterpret_cast<const uint4*>(rowB + off), b);
+                if constexpr (ACT == ACT_SWIGLU)
+                    unpack8(*reinterpret_cast<const uint4*>(rowB + off), b);
 #pragma unroll
                 for (int r = 0; r < 8; ++r) {
                     const float u = u8[p][r];
-                    const float sg = sigmoidf_(a[r]);
-                    const float sl = a[r] * sg;
-                    const float h = sl * b[r];
+                    const float dh = g * u;
+                    float h;
+                    if constexpr (ACT == ACT_SWIGLU) {
+                        const float sg = sigmoidf_(a[r]);
+                        const float sl = a[r] * sg;
+                        h = sl * b[r];
+                        da[r] = dh * b[r] * sg * (1.0f + a[r] * (1.0f - sg));
+                        db[r] = dh * sl;
+                    } else {
+                        h = act_f<ACT>(a[r]);
+                        da[r] = dh * act_d<ACT>(a[r]);
+                    }
                     dg += n < f ? u * h : 0.f;
                     hg[r] = g * h;
-                    const float dh = g * u;
-                    da[r] = dh * b[r] * sg * (1.0f + a[r] * (1.0f - sg));
-                    db[r] = dh * sl;
                 }
                 *reinterpret_cast<uint4*>(rowA + off) = pack8(da);
-                *reinterpret_cast<uint4*>(rowB + off) = pack8(db);
+                if constexpr (ACT == ACT_SWIGLU) *reinterpret_cast<uint4*>(rowB + off) = pack8(db);
                 hgv[j][p] = pack8(hg);
             }
         }
@@ -254,7 +298,7 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
         lds_barrier();
         {
             bf16_t* const dst[2] = {A, B};
-            store_rows(2, dst);
+            store_rows(NARR, dst);
         }
         lds_barrier();
 #pragma unroll
@@ -311,13 +355,15 @@ g3_kernel(const bf16_t* __restrict__ HG, const bf16_t* __restrict__ dy,
 }
 
 // G5: dW1[e] = x[eti]^T dA, dW3[e] = x[eti]^T dB   (M = d, N = f, K = slots of e)
+// (non-gated: dW1 alone)
+template <int ACT>
 __global__ void __launch_bounds__(CD::THREADS)
 g5_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ dA,
           const bf16_t* __restrict__ dB, const int32_t* __restrict__ offsets,
           const int32_t* __restrict__ eti, int d, int f, float* __restrict__ dw1,
           float* __restrict__ dw3) {
     extern __shared__ __align__(16) char lds[];
-    using C = CD;
+    using C = CFirst<ACT>;
     const int MT = (d + C::BM - 1) / C::BM, NT = (f + C::BN - 1) / C::BN;
     int e, mt, nt;
     if (!wgrad_tile(blockIdx.x, MT, NT, e, mt, nt)) return;
@@ -326,28 +372,31 @@ g5_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ dA,
     const int off = offsets[e];
     const int cnt = offsets[e + 1] - off;
     GatherMC<C, C::BM> la;
-    SlotMC<C, C::BN> lb0, lb1;
+    SlotMC<C, C::BN> lb0;
+    std::conditional_t<ACT == ACT_SWIGLU, SlotMC<C, C::BN>, NoLoader> lb1;
     if (cnt > 0) {
         la.init(x, d, m0, d, eti + off, cnt);
         lb0.init(dA, f, off, n0, f, cnt);
-        lb1.init(dB, f, off, n0, f, cnt);
+        if constexpr (ACT == ACT_SWIGLU) lb1.init(dB, f, off, n0, f, cnt);
     }
     Acc<C> acc;
     gemm_mainloop<C>(la, lb0, lb1, (cnt + GBK - 1) / GBK, tail_from(cnt), lds, acc, d - m0,
                      f - n0);
     float* o1 = dw1 + (int64_t)e * d * f;
-    float* o3 = dw3 + (int64_t)e * d * f;
-    RowStage<C, 2>::run(acc, lds, [&](int b, int r, int c, const f32x4& v) {
+    float* o3 = ACT == ACT_SWIGLU ? dw3 + (int64_t)e * d * f : o1;  // dw3 is NULL when non-gated
+    RowStage<C, ACT == ACT_SWIGLU ? 2 : 1>::run(acc, lds, [&](int b, int r, int c, const f32x4& v) {
         const int m = m0 + r, n = n0 + c;
         if (m < d && n < f) st_nt((b ? o3 : o1) + (int64_t)m * f + n, v);
     });
 }
 
-// G6: dX_slot = dA W1[e]^T + dB W3[e]^T   (K = 2f)
+// G6: dX_slot = dA W1[e]^T + dB W3[e]^T   (K = 2f; non-gated: dA W1[e]^T, K = f,
+// called with dB = dA and W3 = W1, whose second halves are then never reached)
 __global__ void __launch_bounds__(CS::THREADS)
 g6_kernel(const bf16_t* __restrict__ dA, const bf16_t* __restrict__ dB,
           const bf16_t* __restrict__ w1, const bf16_t* __restrict__ w3,
-          const int32_t* __restrict__ offsets, int d, int f, int E, bf16_t* __restrict__ dX) {
+          const int32_t* __restrict__ offsets, int d, int f, int E, int kslices,
+          bf16_t* __restrict__ dX) {
     extern __shared__ __align__(16) char lds[];
     using C = CS;
     SlotTile t;
@@ -360,7 +409,7 @@ g6_kernel(const bf16_t* __restrict__ dA, const bf16_t* __restrict__ dB,
     lb.init(w1 + (int64_t)t.e * d * f, w3 + (int64_t)t.e * d * f, f, t.n0, min(C::BN, d - t.n0), f);
     NoLoader nl;
     Acc<C> acc;
-    gemm_mainloop<C>(la, lb, nl, 2 * f / GBK, GBK, lds, acc, t.mrows);
+    gemm_mainloop<C>(la, lb, nl, kslices, GBK, lds, acc, t.mrows);
     WaveCoord<C> wc;
 #pragma unroll
     for (int i = 0; i < C::FM; ++i) {
@@ -403,6 +452,15 @@ __device__ int expert_of(const int32_t* offsets, int E, int64_t s) {
 }
 __device__ float silu32(float a) { return a / (1.0f + __expf(-a)); }
 
+// h and its derivatives from the first-layer outputs (b unused when non-gated)
+template <int ACT>
+__device__ float f32_h(float a, float b) {
+    if constexpr (ACT == ACT_SWIGLU) return silu32(a) * b;
+    else if constexpr (ACT == ACT_RELU) return a > 0.f ? a : 0.f;
+    else return silu32(a);
+}
+
+template <int ACT>
 __global__ void f32_g1(const float* x, const float* w1, const float* w3, const int32_t* offsets,
                        const int32_t* eti, int64_t S, int d, int f, int E, float* A, float* B) {
     const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -414,12 +472,13 @@ __global__ void f32_g1(const float* x, const float* w1, const float* w3, const i
     float a = 0.f, b = 0.f;
     for (int i = 0; i < d; ++i) {
         a = fmaf(xr[i], w1[((int64_t)e * d + i) * f + n], a);
-        b = fmaf(xr[i], w3[((int64_t)e * d + i) * f + n], b);
+        if constexpr (ACT == ACT_SWIGLU) b = fmaf(xr[i], w3[((int64_t)e * d + i) * f + n], b);
     }
     A[id] = a;
-    B[id] = b;
+    if constexpr (ACT == ACT_SWIGLU) B[id] = b;
 }
 
+template <int ACT>
 __global__ void f32_g2(const float* A, const float* B, const float* w2, const int32_t* offsets,
                        int64_t S, int d, int f, int E, float* O) {
     const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -429,10 +488,12 @@ __global__ void f32_g2(const float* A, const float* B, const float* w2, const in
     const int e = expert_of(offsets, E, s);
     float o = 0.f;
     for (int c = 0; c < f; ++c)
-        o = fmaf(silu32(A[s * f + c]) * B[s * f + c], w2[((int64_t)e * f + c) * d + n], o);
+        o = fmaf(f32_h<ACT>(A[s * f + c], ACT == ACT_SWIGLU ? B[s * f + c] : 0.f),
+                 w2[((int64_t)e * f + c) * d + n], o);
     O[id] = o;
 }
 
+template <int ACT>
 __global__ void f32_g3(const float* A, const float* B, const float* dy, const float* gates,
                        const int32_t* offsets, const int32_t* eti, const int32_t* slot_src,
                        int d, int f, int E, float* dw2) {
@@ -442,13 +503,16 @@ __global__ void f32_g3(const float* A, const float* B, const float* dy, const fl
     const int c = (int)((id / d) % f);
     const int n = (int)(id % d);
     float acc = 0.f;
-    for (int s = offsets[e]; s < offsets[e + 1]; ++s)
-        acc = fmaf(gates[slot_src[s]] * silu32(A[(int64_t)s * f + c]) * B[(int64_t)s * f + c],
-                   dy[(int64_t)eti[s] * d + n], acc);
+    for (int s = offsets[e]; s < offsets[e + 1]; ++s) {
+        const float h = f32_h<ACT>(A[(int64_t)s * f + c],
+                                   ACT == ACT_SWIGLU ? B[(int64_t)s * f + c] : 0.f);
+        acc = fmaf(gates[slot_src[s]] * h, dy[(int64_t)eti[s] * d + n], acc);
+    }
     dw2[id] = acc;
 }
 
 // one thread per slot: u, d_gate, dA, dB (in place)
+template <int ACT>
 __global__ void f32_g4(const float* dy, const float* w2, const float* gates,
                        const int32_t* offsets, const int32_t* eti, const int32_t* slot_src,
                        int64_t S, int d, int f, int E, float* A, float* B, float* dgates) {
@@ -462,16 +526,27 @@ __global__ void f32_g4(const float* dy, const float* w2, const float* gates,
         float u = 0.f;
         const float* wr = w2 + ((int64_t)e * f + c) * d;
         for (int n = 0; n < d; ++n) u = fmaf(dyr[n], wr[n], u);
-        const float a = A[s * f + c], b = B[s * f + c];
-        const float sg = 1.0f / (1.0f + __expf(-a));
-        dg = fmaf(u, a * sg * b, dg);
+        const float a = A[s * f + c];
         const float dh = g * u;
-        A[s * f + c] = dh * b * sg * (1.0f + a * (1.0f - sg));
-        B[s * f + c] = dh * a * sg;
+        if constexpr (ACT == ACT_SWIGLU) {
+            const float b = B[s * f + c];
+            const float sg = 1.0f / (1.0f + __expf(-a));
+            dg = fmaf(u, a * sg * b, dg);
+            A[s * f + c] = dh * b * sg * (1.0f + a * (1.0f - sg));
+            B[s * f + c] = dh * a * sg;
+        } else if constexpr (ACT == ACT_RELU) {
+            dg = fmaf(u, a > 0.f ? a : 0.f, dg);
+            A[s * f + c] = a > 0.f ? dh : 0.f;
+        } else {
+            const float sg = 1.0f / (1.0f + __expf(-a));
+            dg = fmaf(u, a * sg, dg);
+            A[s * f + c] = dh * sg * (1.0f + a * (1.0f - sg));
+        }
     }
     dgates[slot_src[s]] = dg;
 }
 
+template <int ACT>
 __global__ void f32_g5(const float* x, const float* dA, const float* dB, const int32_t* offsets,
                        const int32_t* eti, int d, int f, int E, float* dw1, float* dw3) {
     const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -483,12 +558,13 @@ __global__ void f32_g5(const float* x, const float* dA, const float* dB, const i
     for (int s = offsets[e]; s < offsets[e + 1]; ++s) {
         const float xv = x[(int64_t)eti[s] * d + i];
         a1 = fmaf(xv, dA[(int64_t)s * f + c], a1);
-        a3 = fmaf(xv, dB[(int64_t)s * f + c], a3);
+        if constexpr (ACT == ACT_SWIGLU) a3 = fmaf(xv, dB[(int64_t)s * f + c], a3);
     }
     dw1[id] = a1;
-    dw3[id] = a3;
+    if constexpr (ACT == ACT_SWIGLU) dw3[id] = a3;
 }
 
+template <int ACT>
 __global__ void f32_g6(const float* dA, const float* dB, const float* w1, const float* w3,
                        const int32_t* offsets, int64_t S, int d, int f, int E, float* dX) {
     const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -501,7 +577,7 @@ __global__ void f32_g6(const float* dA, const float* dB, const float* w1, const 
     float acc = 0.f;
     for (int c = 0; c < f; ++c) {
         acc = fmaf(dA[s * f + c], r1[c], acc);
-        acc = fmaf(dB[s * f + c], r3[c], acc);
+        if constexpr (ACT == ACT_SWIGLU) acc = fmaf(dB[s * f + c], r3[c], acc);
     }
     dX[id] = acc;
 }
@@ -522,11 +598,17 @@ hipError_t set_lds_limits() {
             if (e == hipSuccess)
                 e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
         };
-        set(reinterpret_cast<const void*>(g1_kernel), CD::LDS);
+        auto per_act = [&](auto act) {
+            constexpr int ACT = decltype(act)::value;
+            set(reinterpret_cast<const void*>(g1_kernel<ACT>), CFirst<ACT>::LDS);
+            set(reinterpret_cast<const void*>(g4_kernel<ACT>), C4::LDS);
+            set(reinterpret_cast<const void*>(g5_kernel<ACT>), CFirst<ACT>::LDS);
+        };
+        per_act(std::integral_constant<int, ACT_SWIGLU>{});
+        per_act(std::integral_constant<int, ACT_SILU>{});
+        per_act(std::integral_constant<int, ACT_RELU>{});
         set(reinterpret_cast<const void*>(g2_kernel), CS::LDS);
         set(reinterpret_cast<const void*>(g3_kernel), CS::LDS);
-        set(reinterpret_cast<const void*>(g4_kernel), C4::LDS);
-        set(reinterpret_cast<const void*>(g5_kernel), CD::LDS);
         set(reinterpret_cast<const void*>(g6_kernel), CS::LDS);
         return e;
     }();
@@ -544,23 +626,27 @@ size_t ffn_fwd_workspace(int64_t T, int d, int f, int E, int k, bool f32) {
     return align256((size_t)T * k * f * sizeof(bf16_t));  // H
 }
 
-hipError_t ffn_fwd(const FfnArgs& a, bool f32, hipStream_t st) {
+namespace {
+
+template <int ACT>
+hipError_t ffn_fwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
     const int64_t S = a.T * a.k;
     if (f32) {
-        hipLaunchKernelGGL(f32_g1, grid1d(S * a.f, 256), dim3(256), 0, st,
+        hipLaunchKernelGGL(f32_g1<ACT>, grid1d(S * a.f, 256), dim3(256), 0, st,
                            (const float*)a.x, (const float*)a.w1, (const float*)a.w3, a.offsets,
                            a.eti, S, a.d, a.f, a.E, (float*)a.A, (float*)a.B);
         probe::mark("f32_g1", st);
-        hipLaunchKernelGGL(f32_g2, grid1d(S * a.d, 256), dim3(256), 0, st,
+        hipLaunchKernelGGL(f32_g2<ACT>, grid1d(S * a.d, 256), dim3(256), 0, st,
                            (const float*)a.A, (const float*)a.B, (const float*)a.w2, a.offsets, S,
                            a.d, a.f, a.E, (float*)a.O);
         probe::mark("f32_g2", st);
         return hipGetLastError();
     }
     if (hipError_t e = set_lds_limits(); e != hipSuccess) return e;
+    using C1 = CFirst<ACT>;
     bf16_t* H = static_cast<bf16_t*>(a.ws);
-    hipLaunchKernelGGL(g1_kernel, dim3(slot_grid(S, a.E, CD::BM, cdiv(a.f, CD::BN))),
-                       dim3(CD::THREADS), CD::LDS, st, (const bf16_t*)a.x, (const bf16_t*)a.w1,
+    hipLaunchKernelGGL(g1_kernel<ACT>, dim3(slot_grid(S, a.E, C1::BM, cdiv(a.f, C1::BN))),
+                       dim3(C1::THREADS), C1::LDS, st, (const bf16_t*)a.x, (const bf16_t*)a.w1,
                        (const bf16_t*)a.w3, a.offsets, a.eti, a.d, a.f, a.E, (bf16_t*)a.A,
                        (bf16_t*)a.B, H);
     probe::mark("g1_kernel", st);
@@ -571,6 +657,16 @@ hipError_t ffn_fwd(const FfnArgs& a, bool f32, hipStream_t st) {
     return hipGetLastError();
 }
 
+}  // namespace
+
+hipError_t ffn_fwd(const FfnArgs& a, bool f32, hipStream_t st) {
+    switch (a.act) {
+    case ACT_SILU: return ffn_fwd_act<ACT_SILU>(a, f32, st);
+    case ACT_RELU: return ffn_fwd_act<ACT_RELU>(a, f32, st);
+    default: return ffn_fwd_act<ACT_SWIGLU>(a, f32, st);
+    }
+}
+
 size_t ffn_bwd_workspace(int64_t T, int d, int f, int E, int k, bool f32) {
     (void)d; (void)E;
     if (f32) return 0;
@@ -578,33 +674,41 @@ size_t ffn_bwd_workspace(int64_t T, int d, int f, int E, int k, bool f32) {
     return align256((size_t)S * g4_nparts(f) * sizeof(float)) + align256((size_t)S * f * sizeof(bf16_t));
 }
 
-hipError_t ffn_bwd(const FfnArgs& a, bool f32, hipStream_t st) {
+namespace {
+
+template <int ACT>
+hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
     const int64_t S = a.T * a.k;
+    constexpr bool GATED = ACT == ACT_SWIGLU;
     if (f32) {
-        hipLaunchKernelGGL(f32_g3, grid1d((int64_t)a.E * a.f * a.d, 256), dim3(256), 0, st,
+        hipLaunchKernelGGL(f32_g3<ACT>, grid1d((int64_t)a.E * a.f * a.d, 256), dim3(256), 0, st,
                            (const float*)a.A, (const float*)a.B, (const float*)a.dy, a.gates,
                            a.offsets, a.eti, a.slot_src, a.d, a.f, a.E, a.dw2);
         probe::mark("f32_g3", st);
-        hipLaunchKernelGGL(f32_g4, grid1d(S, 64), dim3(64), 0, st, (const float*)a.dy,
+        hipLaunchKernelGGL(f32_g4<ACT>, grid1d(S, 64), dim3(64), 0, st, (const float*)a.dy,
                            (const float*)a.w2, a.gates, a.offsets, a.eti, a.slot_src, S, a.d, a.f,
                            a.E, (float*)a.A, (float*)a.B, a.dgates);
         probe::mark("f32_g4", st);
-        hipLaunchKernelGGL(f32_g5, grid1d((int64_t)a.E * a.d * a.f, 256), dim3(256), 0, st,
+        hipLaunchKernelGGL(f32_g5<ACT>, grid1d((int64_t)a.E * a.d * a.f, 256), dim3(256), 0, st,
                            (const float*)a.x, (const float*)a.A, (const float*)a.B, a.offsets,
                            a.eti, a.d, a.f, a.E, a.dw1, a.dw3);
         probe::mark("f32_g5", st);
-        hipLaunchKernelGGL(f32_g6, grid1d(S * a.d, 256), dim3(256), 0, st, (const float*)a.A,
+        hipLaunchKernelGGL(f32_g6<ACT>, grid1d(S * a.d, 256), dim3(256), 0, st, (const float*)a.A,
                            (const float*)a.B, (const float*)a.w1, (const float*)a.w3, a.offsets,
                            S, a.d, a.f, a.E, (float*)a.dX);
         probe::mark("f32_g6", st);
         return hipGetLastError();
     }
     if (hipError_t e = set_lds_limits(); e != hipSuccess) return e;
+    using C5 = CFirst<ACT>;
     const int nparts = g4_nparts(a.f);
     float* part = static_cast<float*>(a.ws);
     bf16_t* HG = reinterpret_cast<bf16_t*>(static_cast<char*>(a.ws) +
                                            align256((size_t)S * nparts * sizeof(float)));
-    hipLaunchKernelGGL(g4_kernel, dim3(slot_grid(S, a.E, C4::BM, cdiv(a.f, C4::BN))),
+    // non-gated: the second operand of the two-branch kernels is the first again
+    const void* Bx = GATED ? a.B : a.A;
+    const void* w3x = GATED ? a.w3 : a.w1;
+    hipLaunchKernelGGL(g4_kernel<ACT>, dim3(slot_grid(S, a.E, C4::BM, cdiv(a.f, C4::BN))),
                        dim3(C4::THREADS), C4::LDS, st, (const bf16_t*)a.dy, (const bf16_t*)a.w2,
                        a.gates, a.offsets, a.eti, a.slot_src, a.d, a.f, a.E, (bf16_t*)a.A,
                        (bf16_t*)a.B, HG, part);
@@ -616,16 +720,26 @@ hipError_t ffn_bwd(const FfnArgs& a, bool f32, hipStream_t st) {
                        dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)HG, (const bf16_t*)a.dy,
                        a.offsets, a.eti, a.d, a.f, a.dw2);
     probe::mark("g3_kernel", st);
-    hipLaunchKernelGGL(g5_kernel, dim3(wgrad_grid(a.E, cdiv(a.d, CD::BM), cdiv(a.f, CD::BN))),
-                       dim3(CD::THREADS), CD::LDS, st, (const bf16_t*)a.x, (const bf16_t*)a.A,
+    hipLaunchKernelGGL(g5_kernel<ACT>, dim3(wgrad_grid(a.E, cdiv(a.d, C5::BM), cdiv(a.f, C5::BN))),
+                       dim3(C5::THREADS), C5::LDS, st, (const bf16_t*)a.x, (const bf16_t*)a.A,
                        (const bf16_t*)a.B, a.offsets, a.eti, a.d, a.f, a.dw1, a.dw3);
     probe::mark("g5_kernel", st);
     hipLaunchKernelGGL(g6_kernel, dim3(slot_grid(S, a.E, CS::BM, cdiv(a.d, CS::BN))),
-                       dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)a.A, (const bf16_t*)a.B,
-                       (const bf16_t*)a.w1, (const bf16_t*)a.w3, a.offsets, a.d, a.f, a.E,
-                       (bf16_t*)a.dX);
+                       dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)a.A, (const bf16_t*)Bx,
+                       (const bf16_t*)a.w1, (const bf16_t*)w3x, a.offsets, a.d, a.f, a.E,
+                       (GATED ? 2 : 1) * a.f / GBK, (bf16_t*)a.dX);
     probe::mark("g6_kernel", st);
     return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t ffn_bwd(const FfnArgs& a, bool f32, hipStream_t st) {
+    switch (a.act) {
+    case ACT_SILU: return ffn_bwd_act<ACT_SILU>(a, f32, st);
+    case ACT_RELU: return ffn_bwd_act<ACT_RELU>(a, f32, st);
+    default: return ffn_bwd_act<ACT_SWIGLU>(a, f32, st);
+    }
 }
 
 }  // namespace moe

@@ -36,6 +36,7 @@ struct FfnArgs {
     void* A; void* B; void* O; void* dX;
     float* dw1; float* dw3; float* dw2; float* dgates;
     int64_t T; int d, f, E, k;
+    int act;  // 0 SwiGLU (gated), 1 SiLU, 2 ReLU (non-gated: w3, B, dw3 unused)
     void* ws;
 };
 size_t ffn_fwd_workspace(int64_t T, int d, int f, int E, int k, bool f32);

@@ -10,9 +10,10 @@ Backward (Section 3.2):
   -> moe_route_bwd (router gradient, added into dx)
 
 What the forward keeps for the backward (the "saved activations"): the first
-layer outputs A and B [S, f], the routing decision (ids, gates, logits) and the
-dispatch maps (offsets, expert_token_indices, token_index_map, slot_src). No
-permuted copy of x, no SiLU(A), no h and no expert output O is kept.
+layer outputs A and B [S, f] (A alone for the non-gated SiLU / ReLU experts),
+the routing decision (ids, gates, logits) and the dispatch maps (offsets,
+expert_token_indices, token_index_map, slot_src). No permuted copy of x, no
+SiLU(A), no h and no expert output O is kept.
 """
 from __future__ import annotations
 
@@ -32,7 +33,8 @@ class Saved:
     f: int
     E: int
     k: int
-    flags: int
+    flags: int        # element type flag
+    act: str          # "swiglu", "silu" or "relu"
     renorm: bool
     ids: torch.Tensor
     gates: torch.Tensor
@@ -43,25 +45,33 @@ class Saved:
     tim: torch.Tensor
     slot_src: torch.Tensor
     A: torch.Tensor
-    B: torch.Tensor
+    B: torch.Tensor | None
+
+    @property
+    def ffn_flags(self) -> int:
+        return self.flags | B.ACT_FLAG[self.act]
 
     def tensors(self):
-        return [self.ids, self.gates, self.logits, self.counts, self.offsets, self.eti,
-                self.tim, self.slot_src, self.A, self.B]
+        return [t for t in (self.ids, self.gates, self.logits, self.counts, self.offsets,
+                            self.eti, self.tim, self.slot_src, self.A, self.B) if t is not None]
 
     def nbytes(self) -> int:
         return sum(t.numel() * t.element_size() for t in self.tensors())
 
 
-def saved_bytes_per_token(d: int, f: int, E: int, k: int, elem: int, T: int) -> float:
-    """Closed form of Saved.nbytes() / T: A and B (2 k f elem), ids, gates,
-    token_index_map, expert_token_indices and slot_src (5 x 4k), logits (4E),
-    counts and offsets (4(2E+1) per layer)."""
-    return 2.0 * k * f * elem + 20.0 * k + 4.0 * E + 4.0 * (2 * E + 1) / T
+def saved_bytes_per_token(d: int, f: int, E: int, k: int, elem: int, T: int,
+                          act: str = "swiglu") -> float:
+    """Closed form of Saved.nbytes() / T: A and B (2 k f elem; A alone, k f elem,
+    for a non-gated expert), ids, gates, token_index_map, expert_token_indices
+    and slot_src (5 x 4k), logits (4E), counts and offsets (4(2E+1) per layer)."""
+    n_first = 2 if act == "swiglu" else 1
+    return n_first * k * f * elem + 20.0 * k + 4.0 * E + 4.0 * (2 * E + 1) / T
 
 
-def forward(x, w_gate, bias, w1, w3, w2, k: int, renorm: bool, stream=None, keep_O=False):
-    """Returns (y, saved[, O])."""
+def forward(x, w_gate, bias, w1, w3, w2, k: int, renorm: bool, stream=None, keep_O=False,
+            act: str = "swiglu"):
+    """Returns (y, saved[, O]). ``act`` picks the expert: "swiglu" (gated, w3
+    used) or the non-gated "silu" / "relu" (w3 ignored, may be None)."""
     T, d = x.shape
     E, _, f = w1.shape
     dev = x.device
@@ -83,17 +93,20 @@ def forward(x, w_gate, bias, w1, w3, w2, k: int, renorm: bool, stream=None, keep
     ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
     B.moe_build_index(ids, T, E, k, counts, offsets, eti, tim, slot_src, ws, wsb, stream)
     del ws
+    gated = act == "swiglu"
+    fflags = flags | B.ACT_FLAG[act]
     A = torch.empty((S, f), dtype=x.dtype, device=dev)
-    Bm = torch.empty((S, f), dtype=x.dtype, device=dev)
+    Bm = torch.empty((S, f), dtype=x.dtype, device=dev) if gated else None
     O = torch.empty((S, d), dtype=x.dtype, device=dev)
-    wsb = B.moe_ffn_fwd_workspace_size(T, d, f, E, k, flags)
+    wsb = B.moe_ffn_fwd_workspace_size(T, d, f, E, k, fflags)
     ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
-    B.moe_ffn_fwd(x, w1, w3, w2, offsets, eti, T, d, f, E, k, flags, A, Bm, O, ws, wsb, stream)
+    B.moe_ffn_fwd(x, w1, w3 if gated else None, w2, offsets, eti, T, d, f, E, k, fflags, A, Bm,
+                  O, ws, wsb, stream)
     del ws
     y = torch.empty((T, d), dtype=x.dtype, device=dev)
     B.moe_combine(O, gates, tim, T, d, k, flags, y, stream)
-    saved = Saved(T, d, f, E, k, flags, renorm, ids, gates, logits, counts, offsets, eti, tim,
-                  slot_src, A, Bm)
+    saved = Saved(T, d, f, E, k, flags, act, renorm, ids, gates, logits, counts, offsets, eti,
+                  tim, slot_src, A, Bm)
     if keep_O:
         return y, saved, O
     del O
@@ -102,20 +115,22 @@ def forward(x, w_gate, bias, w1, w3, w2, k: int, renorm: bool, stream=None, keep
 
 def backward(saved: Saved, dy, x, w_gate, w1, w3, w2, stream=None, keep=False):
     """Returns dict(dx, dw_gate, dw1, dw3, dw2, d_gates[, dX_slot]). Overwrites
-    saved.A / saved.B with dA / dB."""
+    saved.A / saved.B with dA / dB. dw3 is None for a non-gated expert."""
     s = saved
     T, d, f, E, k = s.T, s.d, s.f, s.E, s.k
     dev = dy.device
     f32 = dict(dtype=torch.float32, device=dev)
     dw1 = torch.empty((E, d, f), **f32)
-    dw3 = torch.empty((E, d, f), **f32)
+    gated = s.act == "swiglu"
+    dw3 = torch.empty((E, d, f), **f32) if gated else None
     dw2 = torch.empty((E, f, d), **f32)
     d_gates = torch.empty((T, k), **f32)
     dX = torch.empty((T * k, d), dtype=dy.dtype, device=dev)
-    wsb = B.moe_ffn_bwd_workspace_size(T, d, f, E, k, s.flags)
+    wsb = B.moe_ffn_bwd_workspace_size(T, d, f, E, k, s.ffn_flags)
     ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
-    B.moe_ffn_bwd(dy, x, w1, w3, w2, s.gates, s.offsets, s.eti, s.slot_src, s.A, s.B, T, d, f,
-                  E, k, s.flags, dw1, dw3, dw2, d_gates, dX, ws, wsb, stream)
+    B.moe_ffn_bwd(dy, x, w1, w3 if gated else None, w2, s.gates, s.offsets, s.eti, s.slot_src,
+                  s.A, s.B, T, d, f, E, k, s.ffn_flags, dw1, dw3, dw2, d_gates, dX, ws, wsb,
+                  stream)
     del ws
     dx = torch.empty((T, d), dtype=dy.dtype, device=dev)
     B.moe_combine(dX, None, s.tim, T, d, k, s.flags, dx, stream)

@@ -82,3 +82,31 @@ def test_workspace_checks_and_zero_tokens():
     r = lib.moe_ffn_fwd(*([FAKE] * 6), 1000, 128, 128, 8, 2, 0, FAKE, FAKE, FAKE, FAKE, need - 1, None)
     assert r == B.MOE_ERR_WORKSPACE
     assert lib.moe_build_index_workspace_size(0, 8, 2) == 0
+
+
+def test_activation_flags():
+    lib = B.load_library()
+    S, f = 1000 * 2, 128
+    # both activation flags at once
+    r = lib.moe_ffn_fwd(FAKE, FAKE, None, FAKE, FAKE, FAKE, 1000, 128, f, 8, 2,
+                        B.MOE_ACT_SILU | B.MOE_ACT_RELU, FAKE, None, FAKE, FAKE, 1 << 30, None)
+    assert r == B.MOE_ERR_INVALID_ARG and b"both" in lib.moe_last_error()
+    # the activation flags belong to the FFN calls only
+    assert lib.moe_combine(FAKE, None, FAKE, 10, 128, 2, B.MOE_ACT_RELU, FAKE, None) == B.MOE_ERR_INVALID_ARG
+    assert lib.moe_route(FAKE, FAKE, None, 10, 128, 8, 2, B.MOE_ACT_SILU, FAKE, FAKE, None,
+                         None) == B.MOE_ERR_INVALID_ARG
+    # SwiGLU needs w3 and B; a non-gated expert accepts NULL for them (a short
+    # workspace then stops the call before any launch)
+    r = lib.moe_ffn_fwd(FAKE, FAKE, None, FAKE, FAKE, FAKE, 1000, 128, f, 8, 2, 0, FAKE, FAKE,
+                        FAKE, FAKE, 1 << 30, None)
+    assert r == B.MOE_ERR_INVALID_ARG and b"w3 is NULL" in lib.moe_last_error()
+    for act in (B.MOE_ACT_SILU, B.MOE_ACT_RELU):
+        r = lib.moe_ffn_fwd(FAKE, FAKE, None, FAKE, FAKE, FAKE, 1000, 128, f, 8, 2, act, FAKE,
+                            None, FAKE, FAKE, 16, None)
+        assert r == B.MOE_ERR_WORKSPACE, lib.moe_last_error()
+        r = lib.moe_ffn_bwd(*([FAKE] * 3), None, FAKE, *([FAKE] * 5), None, 1000, 128, f, 8, 2,
+                            act, FAKE, None, FAKE, FAKE, FAKE, FAKE, 16, None)
+        assert r == B.MOE_ERR_WORKSPACE, lib.moe_last_error()
+    # the non-gated workspaces hold the same buffers (h; partials and g*h)
+    assert lib.moe_ffn_fwd_workspace_size(1000, 128, f, 8, 2, B.MOE_ACT_SILU) == \
+        lib.moe_ffn_fwd_workspace_size(1000, 128, f, 8, 2, 0) >= S * f * 2

@@ -257,6 +257,102 @@ def test_route_bwd_parity(dtype, T, d, E, k, renorm, accumulate):
 
 
 # ---------------------------------------------------------------------------
+NONGATED_CASES = [
+    # dtype, T, d, f, E, k, renorm, ids pattern, activation
+    ("bf16", 300, 256, 384, 8, 2, False, None, "silu"),
+    ("bf16", 700, 256, 256, 16, 4, True, "zipf", "relu"),
+    ("bf16", 500, 384, 128, 12, 3, False, "dead", "silu"),
+    ("f32", 300, 256, 384, 8, 2, False, None, "relu"),
+    ("f32", 257, 128, 256, 16, 4, True, "dead", "silu"),
+]
+
+
+@pytest.mark.parametrize("dtype,T,d,f,E,k,renorm,pattern,act", NONGATED_CASES)
+def test_ffn_nongated_parity(dtype, T, d, f, E, k, renorm, pattern, act):
+    """Non-gated SiLU / ReLU experts (MOE_ACT_SILU / MOE_ACT_RELU): w3, B and
+    dw3 are passed as NULL."""
+    inp, ids, g = _layer_case(dtype, T, d, f, E, k, renorm, pattern)
+    v, st = inp.vals, inp.store
+    S = T * k
+    ix = oracle.build_index(ids, E)
+    A_r, O_r = oracle.ffn_fwd_act(v["x"], v["w1"], v["w2"], ix, k, act)
+    y_r = oracle.combine(O_r, g, ix.tim)
+    bw = oracle.ffn_bwd_act(v["dy"], v["x"], v["w1"], v["w2"], g, ix, A_r, act)
+    dx_r = oracle.combine(bw["dX_slot"], None, ix.tim)
+    gi = _gpu_index(ids, E)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    x, w1, w2, dy = (dev(st[n]) for n in ("x", "w1", "w2", "dy"))
+    offsets, eti, tim, ss = (dev(gi[n]) for n in ("offsets", "eti", "tim", "slot_src"))
+    gates = dev(g)
+    flags = B.dtype_flag(x) | B.ACT_FLAG[act]
+    A = torch.empty((S, f), dtype=tdt, device="cuda")
+    O = torch.empty((S, d), dtype=tdt, device="cuda")
+    wsf = B.moe_ffn_fwd_workspace_size(T, d, f, E, k, flags)
+    wsf_t = torch.empty(max(wsf, 16), dtype=torch.uint8, device="cuda")
+    B.moe_ffn_fwd(x, w1, None, w2, offsets, eti, T, d, f, E, k, flags, A, None, O, wsf_t, wsf)
+    y = torch.empty((T, d), dtype=tdt, device="cuda")
+    B.moe_combine(O, gates, tim, T, d, k, B.dtype_flag(x), y)
+    torch.cuda.synchronize()
+    assert_close("A", host(A), A_r, dtype)
+    assert_close("O", host(O), O_r, dtype)
+    assert_close("y", host(y), y_r, dtype)
+    f32 = dict(dtype=torch.float32, device="cuda")
+    dw1 = torch.full((E, d, f), float("nan"), **f32)
+    dw2 = torch.full((E, f, d), float("nan"), **f32)
+    dg = torch.full((T, k), float("nan"), **f32)
+    dX = torch.empty((S, d), dtype=tdt, device="cuda")
+    wsb = B.moe_ffn_bwd_workspace_size(T, d, f, E, k, flags)
+    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+    B.moe_ffn_bwd(dy, x, w1, None, w2, gates, offsets, eti, ss, A, None, T, d, f, E, k, flags,
+                  dw1, None, dw2, dg, dX, ws, wsb)
+    dx = torch.empty((T, d), dtype=tdt, device="cuda")
+    B.moe_combine(dX, None, tim, T, d, k, B.dtype_flag(x), dx)
+    torch.cuda.synchronize()
+    dA = host(A)
+    if act == "relu":
+        # the derivative is a decision on the sign of A; where A is within the
+        # device's accumulation error of 0 either decision is valid
+        tie = np.abs(A_r) < 1e-4 * np.abs(A_r).max()
+        assert tie.mean() < 1e-3
+        assert_close("dA", np.where(tie, 0, dA), np.where(tie, 0, bw["dA"]), dtype)
+    else:
+        assert_close("dA", dA, bw["dA"], dtype)
+    assert_close("dw2", host(dw2), bw["dw2"], dtype)
+    assert_close("dw1", host(dw1), bw["dw1"], dtype)
+    assert_close("d_gates", host(dg), bw["d_gates"], dtype)
+    assert_close("dX_slot", host(dX), bw["dX_slot"], dtype)
+    assert_close("dx_ffn", host(dx), dx_r, dtype)
+    if pattern == "dead":
+        empty = np.nonzero(gi["counts"] == 0)[0]
+        assert empty.size > 0
+        assert np.all(host(dw1)[empty] == 0) and np.all(host(dw2)[empty] == 0)
+
+
+@pytest.mark.parametrize("act", ["silu", "relu"])
+def test_layer_nongated_end_to_end(act):
+    """Whole layer through layer.forward / layer.backward with a non-gated
+    expert, routing included, on a small bf16 problem."""
+    cfg = synth.MoEConfig("ng", T=600, d=256, f=512, E=8, k=2, dtype="bf16", renorm=False)
+    inp = synth.make_inputs(cfg)
+    v, st = inp.vals, inp.store
+    fw_r = oracle.layer_forward(v["x"], v["w_gate"], None, v["w1"], None, v["w2"], cfg.k, False,
+                                act=act)
+    bw_r = oracle.layer_backward(fw_r, v["dy"], v["x"], v["w_gate"], v["w1"], None, v["w2"], False)
+    x, wg, w1, w2, dy = (dev(st[n]) for n in ("x", "w_gate", "w1", "w2", "dy"))
+    y, saved = layer.forward(x, wg, None, w1, None, w2, cfg.k, False, act=act)
+    assert saved.B is None
+    assert saved.nbytes() == pytest.approx(
+        layer.saved_bytes_per_token(cfg.d, cfg.f, cfg.E, cfg.k, 2, cfg.T, act) * cfg.T)
+    ids_g = saved.ids.cpu().numpy()
+    assert np.array_equal(ids_g, fw_r["ids"])
+    g = layer.backward(saved, dy, x, wg, w1, None, w2)
+    torch.cuda.synchronize()
+    assert g["dw3"] is None
+    assert_close("y", host(y), fw_r["y"], "bf16")
+    for n in ("dw1", "dw2", "dw_gate", "dx", "d_gates"):
+        assert_close(n, host(g[n]), bw_r[n], "bf16")
+
+
 # whole layer (routing included) on the tiny float32 workload
 # ---------------------------------------------------------------------------
 
@@ -302,5 +398,17 @@ def test_error_codes_launch_nothing():
     with pytest.raises(B.MoEError) as ei:
         B.moe_build_index(x, 4, 8, 2, x, x, x, x, x, x, 0)
     assert ei.value.status == B.MOE_ERR_WORKSPACE
+    # activation flags: both at once, or on a call other than the FFN
+    with pytest.raises(B.MoEError) as ei:
+        B.moe_ffn_fwd(x, x, None, x, x, x, 4, 128, 128, 2, 1,
+                      B.MOE_ACT_SILU | B.MOE_ACT_RELU, x, None, x, x, 1 << 20)
+    assert ei.value.status == B.MOE_ERR_INVALID_ARG
+    with pytest.raises(B.MoEError) as ei:
+        B.moe_combine(x, None, x, 4, 128, 2, B.MOE_ACT_SILU, x)
+    assert ei.value.status == B.MOE_ERR_INVALID_ARG
+    # SwiGLU needs w3 and B
+    with pytest.raises(B.MoEError) as ei:
+        B.moe_ffn_fwd(x, x, None, x, x, x, 4, 128, 128, 2, 1, 0, x, None, x, x, 1 << 20)
+    assert ei.value.status == B.MOE_ERR_INVALID_ARG
     # T == 0 is a no-op
     B.moe_combine(x, None, x, 0, 128, 2, 0, x)
