@@ -36,6 +36,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="mid_e64k6")
+    ap.add_argument("--act", choices=("swiglu", "silu", "relu"), default=None,
+                    help="expert activation (default: the workload's own)")
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="approximate CPU time budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -138,8 +140,9 @@ def kernel_model(name, cfg, elem):
     T, d, f, E, k = cfg.T, cfg.d, cfg.f, cfg.E, cfg.k
     S = T * k
     g = 2.0 * S * d * f  # flops of one [S x d] x [d x f] product
-    flops = {"g1_kernel": 2 * g, "g2_kernel": g, "g3_kernel": g, "g4_kernel": g,
-             "g5_kernel": 2 * g, "g6_kernel": 2 * g}
+    nb = 2 if cfg.act == "swiglu" else 1   # right operands of g1, g5, g6
+    flops = {"g1_kernel": nb * g, "g2_kernel": g, "g3_kernel": g, "g4_kernel": g,
+             "g5_kernel": nb * g, "g6_kernel": nb * g}
     if name in flops:
         return flops[name], "TFLOP/s", "mfma"
     nparts = (f // 128) * 2
@@ -158,13 +161,13 @@ def kernel_model(name, cfg, elem):
     return float(byts.get(name, 0)), "GB/s", "hbm"
 
 
-def materialised_saved_bytes(x, w_gate, bias, w1, w3, w2, k, renorm):
+def materialised_saved_bytes(x, w_gate, bias, w1, w3, w2, k, renorm, act="swiglu"):
     """Saved-for-backward bytes of a conventional MoE layer that materialises
-    the permuted tokens and every SwiGLU intermediate (plain PyTorch autograd,
+    the permuted tokens and every expert intermediate (plain PyTorch autograd,
     forward only; weights are parameters and not counted)."""
     import torch
     # storages of the parameters and of the caller's input: not activations
-    excluded = {t.untyped_storage().data_ptr() for t in (x, w_gate, w1, w3, w2)}
+    excluded = {t.untyped_storage().data_ptr() for t in (x, w_gate, w1, w3, w2) if t is not None}
     seen = {}
 
     def pack(t):
@@ -176,7 +179,7 @@ def materialised_saved_bytes(x, w_gate, bias, w1, w3, w2, k, renorm):
     E = w1.shape[0]
     xs = x.detach().requires_grad_(True)
     wg = w_gate.detach().requires_grad_(True)
-    W1, W3, W2 = (w.detach().requires_grad_(True) for w in (w1, w3, w2))
+    W1, W3, W2 = (None if w is None else w.detach().requires_grad_(True) for w in (w1, w3, w2))
     with torch.autograd.graph.saved_tensors_hooks(pack, lambda t: t):
         logits = (xs @ wg.t()).float()
         if bias is not None:
@@ -195,8 +198,12 @@ def materialised_saved_bytes(x, w_gate, bias, w1, w3, w2, k, renorm):
         for e in range(E):
             xe = x_perm[o0:o0 + counts[e]]
             a = xe @ W1[e]
-            b = xe @ W3[e]
-            h = torch.nn.functional.silu(a) * b
+            if act == "swiglu":
+                h = torch.nn.functional.silu(a) * (xe @ W3[e])
+            elif act == "relu":
+                h = torch.relu(a)
+            else:
+                h = torch.nn.functional.silu(a)
             outs.append(h @ W2[e])
             o0 += counts[e]
         O = torch.cat(outs, 0)
@@ -221,9 +228,10 @@ def memory_sweep(cfg, max_doublings):
     bf = torch.bfloat16
     wg = (torch.randn((E, d), generator=gen, device=dev) * 0.02).to(bf)
     w1 = (torch.randn((E, d, f), generator=gen, device=dev) * d ** -0.5).to(bf)
-    w3 = (torch.randn((E, d, f), generator=gen, device=dev) * d ** -0.5).to(bf)
+    gated = cfg.act == "swiglu"
+    w3 = (torch.randn((E, d, f), generator=gen, device=dev) * d ** -0.5).to(bf) if gated else None
     w2 = (torch.randn((E, f, d), generator=gen, device=dev) * f ** -0.5).to(bf)
-    grad_bytes = 4 * (3 * E * d * f + E * d)
+    grad_bytes = 4 * ((3 if gated else 2) * E * d * f + E * d)
     rows = []
     ours_ok = base_ok = True
     for n in range(max_doublings + 1):
@@ -240,7 +248,7 @@ def memory_sweep(cfg, max_doublings):
                 torch.cuda.reset_peak_memory_stats(dev)
                 base = torch.cuda.memory_allocated(dev)
                 if which == "ours":
-                    y, saved = layer.forward(x, wg, None, w1, w3, w2, k, cfg.renorm)
+                    y, saved = layer.forward(x, wg, None, w1, w3, w2, k, cfg.renorm, act=cfg.act)
                     sb = saved.nbytes()
                     g = layer.backward(saved, dy, x, wg, w1, w3, w2)
                     torch.cuda.synchronize()
@@ -249,7 +257,7 @@ def memory_sweep(cfg, max_doublings):
                     row["ours_peak_bytes_per_token"] = round(peak / T, 1)
                     row["ours_saved_bytes_per_token"] = round(sb / T, 1)
                 else:
-                    sb = materialised_saved_bytes(x, wg, None, w1, w3, w2, k, cfg.renorm)
+                    sb = materialised_saved_bytes(x, wg, None, w1, w3, w2, k, cfg.renorm, cfg.act)
                     torch.cuda.synchronize()
                     peak = torch.cuda.max_memory_allocated(dev) - base
                     row["baseline_fwd_peak_bytes_per_token"] = round(peak / T, 1)
@@ -282,7 +290,7 @@ def cpu_oracle_baseline(inp, cfg, budget_s):
     def run(n):
         t0 = time.perf_counter()
         fw = oracle.layer_forward(v["x"][:n], v["w_gate"], v["bias"], v["w1"], v["w3"], v["w2"],
-                                  cfg.k, cfg.renorm)
+                                  cfg.k, cfg.renorm, act=cfg.act)
         oracle.layer_backward(fw, v["dy"][:n], v["x"][:n], v["w_gate"], v["w1"], v["w3"],
                               v["w2"], cfg.renorm)
         return time.perf_counter() - t0
@@ -320,6 +328,8 @@ def main():
     from paper_2601_05296_amd import layer, synth
 
     cfg = synth.CONFIGS[args.workload]
+    if args.act:
+        cfg = cfg.with_(act=args.act)
     assert cfg.dtype == "bf16", "the benchmark workloads are bf16"
     elem = 2
     dev = torch.device("cuda:0")
@@ -337,7 +347,7 @@ def main():
     T, d, f, E, k = cfg.T, cfg.d, cfg.f, cfg.E, cfg.k
 
     def step():
-        y, saved = layer.forward(x, wg, bias, w1, w3, w2, k, cfg.renorm)
+        y, saved = layer.forward(x, wg, bias, w1, w3, w2, k, cfg.renorm, act=cfg.act)
         g = layer.backward(saved, dy, x, wg, w1, w3, w2)
         return y, saved, g
 
@@ -351,9 +361,9 @@ def main():
     y, saved, g = step()
     torch.cuda.synchronize()
     peak = torch.cuda.max_memory_allocated(dev) - base
-    grad_bytes = sum(g[n].numel() * 4 for n in ("dw1", "dw3", "dw2", "dw_gate"))
+    grad_bytes = sum(g[n].numel() * 4 for n in ("dw1", "dw3", "dw2", "dw_gate") if g[n] is not None)
     saved_bytes = saved.nbytes()
-    formula = layer.saved_bytes_per_token(d, f, E, k, elem, T) * T
+    formula = layer.saved_bytes_per_token(d, f, E, k, elem, T, cfg.act) * T
     assert abs(saved_bytes - formula) < 1, (saved_bytes, formula)
     del y, saved, g
 
@@ -402,14 +412,15 @@ def main():
                             if any(n.startswith(p) for p in pre)), 4)
               for st, pre in stage_of.items()}
     router_ms = stages["route"] + stages["route_bwd"]
-    gemm_flops = 18.0 * T * k * d * f
+    gemm_flops = (18.0 if cfg.act == "swiglu" else 12.0) * T * k * d * f
     out = {
         "metric": "MoE layer fwd+bwd tokens/sec + peak activation bytes/token, 1 MI355X",
         "value": round(tokens_per_s, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": cfg.name, "T": T, "d": d, "f": f, "E": E, "k": k,
-                   "renorm": cfg.renorm, "zipf_s": cfg.zipf_s, "parallelism": "none"},
+                   "renorm": cfg.renorm, "zipf_s": cfg.zipf_s, "act": cfg.act,
+                   "parallelism": "none"},
         "peak_activation_bytes_per_token": round((peak - grad_bytes) / T, 1),
         "saved_activation_bytes_per_token": round(saved_bytes / T, 1),
         "roofline": roofline,
@@ -433,7 +444,7 @@ def main():
         torch.cuda.synchronize()
         torch.cuda.reset_peak_memory_stats(dev)
         base = torch.cuda.memory_allocated(dev)
-        mb = materialised_saved_bytes(x, wg, bias, w1, w3, w2, k, cfg.renorm)
+        mb = materialised_saved_bytes(x, wg, bias, w1, w3, w2, k, cfg.renorm, cfg.act)
         torch.cuda.synchronize()
         out["materialised_baseline_saved_bytes_per_token"] = round(mb / T, 1)
         out["materialised_baseline_fwd_peak_bytes_per_token"] = round(

@@ -51,6 +51,7 @@ class MoEConfig:
     zipf_s: float = 0.0          # > 0: per-expert Zipf-shaped router bias
     n_dead: int = 0              # experts whose bias is -inf (never chosen)
     seed: int = 0
+    act: str = "swiglu"          # expert: "swiglu" (gated) or non-gated "silu" / "relu"
 
     @property
     def S(self) -> int:
@@ -74,6 +75,23 @@ CONFIGS = {
     "mem_sweep_e64k8": MoEConfig("mem_sweep_e64k8", T=16384, d=4096, f=2048, E=64,
                                  k=8, dtype="bf16"),
 }
+
+# The seven configurations of the paper's Table 1 (Section 6.1): input width
+# d, experts E, top-k, batch x sequence length tokens, FFN hidden width 4d,
+# with the non-gated SiLU expert of its SiLU experiments (select another
+# expert with MoEConfig.with_(act=...)).
+TABLE1 = {  # name: (d, E, k, batch, seq_len)
+    "conf1": (512, 4, 1, 32, 2048),
+    "conf2": (1024, 8, 2, 32, 2048),
+    "conf3": (1024, 16, 4, 32, 2048),
+    "conf4": (2048, 16, 4, 32, 1024),
+    "conf5": (512, 16, 4, 32, 1024),
+    "conf6": (1024, 16, 4, 16, 1024),
+    "conf7": (2048, 8, 4, 16, 512),
+}
+for _n, (_d, _E, _k, _b, _l) in TABLE1.items():
+    CONFIGS["table1_" + _n] = MoEConfig("table1_" + _n, T=_b * _l, d=_d, f=4 * _d, E=_E, k=_k,
+                                        dtype="bf16", act="silu")
 
 
 def bf16_round(a: np.ndarray) -> np.ndarray:
@@ -140,14 +158,18 @@ def make_inputs(cfg: MoEConfig, T: int | None = None, with_dy: bool = True) -> L
         "x": _normal(rng(s_x), (T, d), 1.0),
         "w_gate": _normal(rng(s_g), (E, d), 0.02),
         "w1": _normal(rng(s_w1), (E, d, f), 1.0 / math.sqrt(d)),
-        "w3": _normal(rng(s_w3), (E, d, f), 1.0 / math.sqrt(d)),
+        # (the W3 stream is spawned for every expert type, so the other
+        # draws do not depend on it)
+        "w3": _normal(rng(s_w3), (E, d, f), 1.0 / math.sqrt(d)) if cfg.act == "swiglu" else None,
         "w2": _normal(rng(s_w2), (E, f, d), 1.0 / math.sqrt(f)),
     }
     if with_dy:
         raw["dy"] = _normal(rng(s_dy), (T, d), 1.0)
     out = LayerInputs(cfg.with_(T=T))
     for name, a in raw.items():
-        if cfg.dtype == "bf16":
+        if a is None:
+            out.store[name] = out.vals[name] = None
+        elif cfg.dtype == "bf16":
             b = bf16_round(a)
             out.store[name] = b
             out.vals[name] = bf16_to_f32(b)
