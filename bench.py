@@ -52,6 +52,9 @@ def parse():
                     help="memory-capacity sweep: double T from the workload's T until out of "
                          "memory, for this path and for the materialised-permutation baseline")
     ap.add_argument("--sweep-max-doublings", type=int, default=8)
+    ap.add_argument("--table1", action="store_true",
+                    help="the seven shapes of the paper's Table 1 (SiLU and SwiGLU experts): "
+                         "this path against a materialised PyTorch layer, time and memory")
     return ap.parse_args()
 
 
@@ -213,6 +216,124 @@ def materialised_saved_bytes(x, w_gate, bias, w1, w3, w2, k, renorm, act="swiglu
     return sum(seen.values())
 
 
+def materialised_step(x, w_gate, bias, w1, w3, w2, dy, k, renorm, act):
+    """One forward + backward of a conventional MoE layer in plain PyTorch: the
+    permuted tokens and every expert intermediate are materialised, one matmul
+    per expert, autograd for the backward. Returns the gradients."""
+    import torch
+    xs = x.detach().requires_grad_(True)
+    wg = w_gate.detach().requires_grad_(True)
+    W1, W3, W2 = (None if w is None else w.detach().requires_grad_(True) for w in (w1, w3, w2))
+    E = w1.shape[0]
+    logits = (xs @ wg.t()).float()
+    if bias is not None:
+        logits = logits + bias
+    p = torch.softmax(logits, dim=1)
+    g, ids = torch.topk(p, k, dim=1)
+    if renorm:
+        g = g / g.sum(dim=1, keepdim=True)
+    flat = ids.reshape(-1)
+    order = torch.argsort(flat, stable=True)
+    tok = order // k
+    x_perm = xs.index_select(0, tok)
+    counts = torch.bincount(flat, minlength=E).tolist()
+    outs = []
+    o0 = 0
+    for e in range(E):
+        xe = x_perm[o0:o0 + counts[e]]
+        a = xe @ W1[e]
+        if act == "swiglu":
+            h = torch.nn.functional.silu(a) * (xe @ W3[e])
+        elif act == "relu":
+            h = torch.relu(a)
+        else:
+            h = torch.nn.functional.silu(a)
+        outs.append(h @ W2[e])
+        o0 += counts[e]
+    O = torch.cat(outs, 0)
+    gw = g.reshape(-1)[order].to(O.dtype)
+    y = torch.zeros_like(xs).index_add_(0, tok, O * gw[:, None])
+    y.backward(dy)
+    return [t.grad for t in (xs, wg, W1, W3, W2) if t is not None]
+
+
+def table1_sweep(args):
+    """The seven shapes of the paper's Table 1 (Section 6.1), with the
+    non-gated SiLU expert and with SwiGLU: time per fwd+bwd step, saved and
+    peak activation bytes per token, for this path and for the materialised
+    PyTorch layer (materialised_step). Inputs are drawn on the device from a
+    seeded generator with the workloads' distributions."""
+    import torch
+    from paper_2601_05296_amd import layer, synth
+    dev = torch.device("cuda:0")
+    bf = torch.bfloat16
+    rows = []
+    for act in ("silu", "swiglu"):
+        for name in synth.TABLE1:
+            cfg = synth.CONFIGS["table1_" + name].with_(act=act)
+            T, d, f, E, k = cfg.T, cfg.d, cfg.f, cfg.E, cfg.k
+            gated = act == "swiglu"
+            gen = torch.Generator(device=dev)
+            gen.manual_seed(cfg.seed)
+            rnd = lambda shape, std: (torch.randn(shape, generator=gen, device=dev) * std).to(bf)
+            wg = rnd((E, d), 0.02)
+            w1 = rnd((E, d, f), d ** -0.5)
+            w3 = rnd((E, d, f), d ** -0.5) if gated else None
+            w2 = rnd((E, f, d), f ** -0.5)
+            x = rnd((T, d), 1.0)
+            dy = rnd((T, d), 1.0)
+            row = {"conf": name, "act": act, "T": T, "d": d, "f": f, "E": E, "k": k}
+
+            def timed(fn, steps, warm):
+                for _ in range(warm):
+                    fn()
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for _ in range(steps):
+                    fn()
+                e1.record()
+                torch.cuda.synchronize()
+                return e0.elapsed_time(e1) / steps
+
+            def ours():
+                y, saved = layer.forward(x, wg, None, w1, w3, w2, k, False, act=act)
+                return layer.backward(saved, dy, x, wg, w1, w3, w2)
+
+            def base():
+                return materialised_step(x, wg, None, w1, w3, w2, dy, k, False, act)
+
+            for which, fn in (("ours", ours), ("base", base)):
+                torch.cuda.empty_cache()
+                row[which + "_ms"] = round(timed(fn, args.steps, args.warmup), 4)
+                torch.cuda.synchronize()
+                torch.cuda.reset_peak_memory_stats(dev)
+                m0 = torch.cuda.memory_allocated(dev)
+                out = fn()
+                torch.cuda.synchronize()
+                peak = torch.cuda.max_memory_allocated(dev) - m0
+                grads = sum(t.numel() * t.element_size()
+                            for t in (out.values() if isinstance(out, dict) else out)
+                            if t is not None and t.dim() == 3)  # weight gradients
+                row[which + "_peak_bytes_per_token"] = round((peak - grads) / T, 1)
+                del out
+            torch.cuda.empty_cache()
+            y, saved = layer.forward(x, wg, None, w1, w3, w2, k, False, act=act)
+            row["ours_saved_bytes_per_token"] = round(saved.nbytes() / T, 1)
+            del y, saved
+            row["base_saved_bytes_per_token"] = round(
+                materialised_saved_bytes(x, wg, None, w1, w3, w2, k, False, act) / T, 1)
+            row["speedup"] = round(row["base_ms"] / row["ours_ms"], 3)
+            row["saved_ratio"] = round(row["base_saved_bytes_per_token"] /
+                                       row["ours_saved_bytes_per_token"], 3)
+            row["ours_tokens_per_s"] = round(T / (row["ours_ms"] * 1e-3), 1)
+            rows.append(row)
+            print(json.dumps(row), flush=True)
+            del x, dy, w1, w2, w3, wg
+            torch.cuda.empty_cache()
+    return rows
+
+
 def memory_sweep(cfg, max_doublings):
     """Peak activation bytes per token and the largest T that fits, for this
     path (one forward + backward) and for the materialised-permutation
@@ -312,6 +433,9 @@ def main():
         summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1],
                       args.pmc_out or traffic_path(args.workload), args.workload,
                       " ".join(sys.argv))
+        return
+    if args.table1:
+        print(json.dumps({"table1": table1_sweep(args)}), flush=True)
         return
     if args.sweep:
         from paper_2601_05296_amd import synth
