@@ -181,6 +181,47 @@ int moe_ffn_bwd(const void* dy, const void* x, const void* w1, const void* w3, c
                 void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * moe_ffn_fwd_combine -- moe_ffn_fwd followed by moe_combine(O, gates,
+ * token_index_map) without the [T*k, d] expert-output buffer: the second GEMM
+ * runs one column strip of O at a time (512 columns) into the workspace and
+ * each strip is combined into y before the next one is computed (Section 2.3
+ * aggregation, Section 3.1). Same arithmetic and summation order as the two
+ * separate calls, so the result is identical and deterministic.
+ * In:  as moe_ffn_fwd, plus gates [T,k] float32 and token_index_map [T,k].
+ * Out: A, B as moe_ffn_fwd; y [T,d] (element type per flags).
+ * workspace: moe_ffn_fwd_combine_workspace_size(T,d,f,E,k,flags) bytes (h and
+ *      one [T*k, 512] strip; in MOE_F32 mode the whole [T*k, d] output).
+ */
+size_t moe_ffn_fwd_combine_workspace_size(int64_t T, int d, int f, int E, int k, unsigned flags);
+int moe_ffn_fwd_combine(const void* x, const void* w1, const void* w3, const void* w2,
+                        const int32_t* offsets, const int32_t* expert_token_indices,
+                        const float* gates, const int32_t* token_index_map,
+                        int64_t T, int d, int f, int E, int k, unsigned flags,
+                        void* A, void* B, void* y, void* workspace, size_t workspace_bytes,
+                        hipStream_t stream);
+
+/*
+ * moe_ffn_bwd_combine -- moe_ffn_bwd followed by the token gradient
+ * accumulation moe_combine(dX_slot, NULL, token_index_map) of Section 3.2
+ * step 3, without the [T*k, d] dX_slot buffer: dX_slot is produced one column
+ * strip at a time in the workspace (reusing the space of g*h, which the dw2
+ * GEMM has consumed by then) and each strip is summed into dx. Identical to
+ * the two separate calls.
+ * In:  as moe_ffn_bwd, plus token_index_map [T,k].
+ * Out: as moe_ffn_bwd, with dx [T,d] in place of dX_slot; MOE_ACCUMULATE adds
+ *      into dx instead of overwriting it.
+ * workspace: moe_ffn_bwd_combine_workspace_size(T,d,f,E,k,flags) bytes.
+ */
+size_t moe_ffn_bwd_combine_workspace_size(int64_t T, int d, int f, int E, int k, unsigned flags);
+int moe_ffn_bwd_combine(const void* dy, const void* x, const void* w1, const void* w3,
+                        const void* w2, const float* gates, const int32_t* offsets,
+                        const int32_t* expert_token_indices, const int32_t* slot_src,
+                        const int32_t* token_index_map, void* A, void* B, int64_t T, int d,
+                        int f, int E, int k, unsigned flags, float* dw1, float* dw3, float* dw2,
+                        float* d_gates, void* dx, void* workspace, size_t workspace_bytes,
+                        hipStream_t stream);
+
+/*
  * moe_route_bwd -- router backward. The paper does not state it; this is the
  * closed form of the gating Jacobian for the forward of moe_route:
  *   without MOE_RENORM: dl = p * (dp - <p, dp>), dp[e] = d_gates[t,j] where

@@ -32,7 +32,9 @@ ACT_FLAG = {"swiglu": 0, "silu": MOE_ACT_SILU, "relu": MOE_ACT_RELU}
 # Every symbol declared in include/moeblaze.h.
 EXPORTS = ("moe_strerror", "moe_last_error", "moe_route", "moe_build_index_workspace_size",
            "moe_build_index", "moe_ffn_fwd_workspace_size", "moe_ffn_fwd", "moe_combine", "moe_ffn_bwd_workspace_size",
-           "moe_ffn_bwd", "moe_route_bwd_workspace_size", "moe_route_bwd", "moe_probe_enable",
+           "moe_ffn_bwd", "moe_ffn_fwd_combine_workspace_size", "moe_ffn_fwd_combine",
+           "moe_ffn_bwd_combine_workspace_size", "moe_ffn_bwd_combine",
+           "moe_route_bwd_workspace_size", "moe_route_bwd", "moe_probe_enable",
            "moe_probe_disable", "moe_probe_count", "moe_probe_get")
 
 
@@ -71,6 +73,10 @@ def load_library(path: str = LIB):
         "moe_combine": (I, [P, P, P, I64, I, I, U, P, P]),
         "moe_ffn_bwd_workspace_size": (SZ, [I64, I, I, I, I, U]),
         "moe_ffn_bwd": (I, [P] * 11 + [I64, I, I, I, I, U] + [P] * 6 + [SZ, P]),
+        "moe_ffn_fwd_combine_workspace_size": (SZ, [I64, I, I, I, I, U]),
+        "moe_ffn_fwd_combine": (I, [P] * 8 + [I64, I, I, I, I, U] + [P] * 4 + [SZ, P]),
+        "moe_ffn_bwd_combine_workspace_size": (SZ, [I64, I, I, I, I, U]),
+        "moe_ffn_bwd_combine": (I, [P] * 12 + [I64, I, I, I, I, U] + [P] * 6 + [SZ, P]),
         "moe_route_bwd_workspace_size": (SZ, [I64, I, I, I, U]),
         "moe_route_bwd": (I, [P] * 6 + [I64, I, I, I, U, P, P, P, SZ, P]),
         "moe_probe_enable": (I, [I]),
@@ -144,6 +150,32 @@ def moe_ffn_fwd(x, w1, w3, w2, offsets, expert_token_indices, T, d, f, E, k, fla
                                       _ptr(expert_token_indices), T, d, f, E, k, flags, _ptr(A),
                                       _ptr(B), _ptr(O), _ptr(workspace), workspace_bytes,
                                       _stream(stream)))
+
+
+def moe_ffn_fwd_combine_workspace_size(T, d, f, E, k, flags) -> int:
+    return load_library().moe_ffn_fwd_combine_workspace_size(T, d, f, E, k, flags)
+
+
+def moe_ffn_fwd_combine(x, w1, w3, w2, offsets, expert_token_indices, gates, token_index_map,
+                        T, d, f, E, k, flags, A, B, y, workspace, workspace_bytes, stream=None):
+    _check(load_library().moe_ffn_fwd_combine(
+        _ptr(x), _ptr(w1), _ptr(w3), _ptr(w2), _ptr(offsets), _ptr(expert_token_indices),
+        _ptr(gates), _ptr(token_index_map), T, d, f, E, k, flags, _ptr(A), _ptr(B), _ptr(y),
+        _ptr(workspace), workspace_bytes, _stream(stream)))
+
+
+def moe_ffn_bwd_combine_workspace_size(T, d, f, E, k, flags) -> int:
+    return load_library().moe_ffn_bwd_combine_workspace_size(T, d, f, E, k, flags)
+
+
+def moe_ffn_bwd_combine(dy, x, w1, w3, w2, gates, offsets, expert_token_indices, slot_src,
+                        token_index_map, A, B, T, d, f, E, k, flags, dw1, dw3, dw2, d_gates, dx,
+                        workspace, workspace_bytes, stream=None):
+    _check(load_library().moe_ffn_bwd_combine(
+        _ptr(dy), _ptr(x), _ptr(w1), _ptr(w3), _ptr(w2), _ptr(gates), _ptr(offsets),
+        _ptr(expert_token_indices), _ptr(slot_src), _ptr(token_index_map), _ptr(A), _ptr(B), T, d,
+        f, E, k, flags, _ptr(dw1), _ptr(dw3), _ptr(dw2), _ptr(d_gates), _ptr(dx), _ptr(workspace),
+        workspace_bytes, _stream(stream)))
 
 
 def moe_combine(src, weights, token_index_map, T, d, k, flags, out, stream=None):

@@ -68,6 +68,101 @@ int hip_status(const char* fn, hipError_t e) {
 
 }  // namespace
 
+namespace {
+
+// moe_ffn_fwd and moe_ffn_fwd_combine: O (plain) or y via gates and
+// token_index_map (combined)
+int ffn_fwd_impl(const char* fn, bool combined, const void* x, const void* w1, const void* w3,
+                 const void* w2, const int32_t* offsets, const int32_t* expert_token_indices,
+                 const float* gates, const int32_t* token_index_map, int64_t T, int d, int f,
+                 int E, int k, unsigned flags, void* A, void* B, void* out, void* workspace,
+                 size_t workspace_bytes, hipStream_t stream) {
+    int r;
+    if ((r = check_common(fn, T, E, k, flags)) || (r = check_dim(fn, "d", d)) ||
+        (r = check_dim(fn, "f", f)))
+        return r;
+    if (flags & (MOE_RENORM | MOE_ACCUMULATE))
+        return fail(MOE_ERR_INVALID_ARG, "%s: only MOE_F32 / MOE_BF16 and an activation flag are valid", fn);
+    const int act = act_of(flags);
+    if (act < 0) return fail(MOE_ERR_INVALID_ARG, "%s: MOE_ACT_SILU and MOE_ACT_RELU both set", fn);
+    if (T == 0) return MOE_OK;
+    REQUIRE_PTR(x); REQUIRE_PTR(w1); REQUIRE_PTR(w2); REQUIRE_PTR(offsets);
+    REQUIRE_PTR(expert_token_indices); REQUIRE_PTR(A);
+    if (combined) {
+        const void* y = out;
+        REQUIRE_PTR(gates); REQUIRE_PTR(token_index_map); REQUIRE_PTR(y);
+    } else {
+        const void* O = out;
+        REQUIRE_PTR(O);
+    }
+    if (act == 0) { REQUIRE_PTR(w3); REQUIRE_PTR(B); }
+    else { OPT_PTR(w3); OPT_PTR(B); }
+    const size_t need = moe::ffn_fwd_workspace(T, d, f, E, k, flags & MOE_F32, combined);
+    if (need && (!workspace || workspace_bytes < need))
+        return fail(MOE_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, workspace_bytes, need);
+    OPT_PTR(workspace);
+    moe::FfnArgs a{};
+    a.x = x; a.w1 = w1; a.w3 = w3; a.w2 = w2; a.offsets = offsets; a.eti = expert_token_indices;
+    a.A = A; a.B = B; a.T = T; a.d = d; a.f = f; a.E = E; a.k = k; a.ws = workspace;
+    a.act = act;
+    if (combined) { a.y = out; a.gates = gates; a.tim = token_index_map; }
+    else a.O = out;
+    moe::probe::begin(stream);
+    return hip_status(fn, moe::ffn_fwd(a, flags & MOE_F32, stream));
+}
+
+}  // namespace
+
+namespace {
+
+// moe_ffn_bwd and moe_ffn_bwd_combine: dX_slot (plain) or dx through
+// token_index_map (combined; MOE_ACCUMULATE adds into dx)
+int ffn_bwd_impl(const char* fn, bool combined, const void* dy, const void* x, const void* w1,
+                 const void* w3, const void* w2, const float* gates, const int32_t* offsets,
+                 const int32_t* expert_token_indices, const int32_t* slot_src,
+                 const int32_t* token_index_map, void* A, void* B, int64_t T, int d, int f,
+                 int E, int k, unsigned flags, float* dw1, float* dw3, float* dw2,
+                 float* d_gates, void* out, void* workspace, size_t workspace_bytes,
+                 hipStream_t stream) {
+    int r;
+    if ((r = check_common(fn, T, E, k, flags)) || (r = check_dim(fn, "d", d)) ||
+        (r = check_dim(fn, "f", f)))
+        return r;
+    if ((flags & MOE_RENORM) || (!combined && (flags & MOE_ACCUMULATE)))
+        return fail(MOE_ERR_INVALID_ARG, "%s: flag not valid here", fn);
+    const int act = act_of(flags);
+    if (act < 0) return fail(MOE_ERR_INVALID_ARG, "%s: MOE_ACT_SILU and MOE_ACT_RELU both set", fn);
+    if (T == 0) return MOE_OK;
+    REQUIRE_PTR(dy); REQUIRE_PTR(x); REQUIRE_PTR(w1); REQUIRE_PTR(w2);
+    REQUIRE_PTR(gates); REQUIRE_PTR(offsets); REQUIRE_PTR(expert_token_indices);
+    REQUIRE_PTR(slot_src); REQUIRE_PTR(A); REQUIRE_PTR(dw1);
+    REQUIRE_PTR(dw2); REQUIRE_PTR(d_gates);
+    if (combined) {
+        const void* dx = out;
+        REQUIRE_PTR(token_index_map); REQUIRE_PTR(dx);
+    } else {
+        const void* dX_slot = out;
+        REQUIRE_PTR(dX_slot);
+    }
+    if (act == 0) { REQUIRE_PTR(w3); REQUIRE_PTR(B); REQUIRE_PTR(dw3); }
+    else { OPT_PTR(w3); OPT_PTR(B); OPT_PTR(dw3); }
+    const size_t need = moe::ffn_bwd_workspace(T, d, f, E, k, flags & MOE_F32, combined);
+    if (need && (!workspace || workspace_bytes < need))
+        return fail(MOE_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, workspace_bytes, need);
+    OPT_PTR(workspace);
+    moe::FfnArgs a{};
+    a.x = x; a.w1 = w1; a.w3 = w3; a.w2 = w2; a.offsets = offsets; a.eti = expert_token_indices;
+    a.slot_src = slot_src; a.gates = gates; a.dy = dy; a.A = A; a.B = B;
+    a.dw1 = dw1; a.dw3 = dw3; a.dw2 = dw2; a.dgates = d_gates; a.T = T; a.d = d; a.f = f;
+    a.E = E; a.k = k; a.ws = workspace; a.act = act;
+    if (combined) { a.y = out; a.tim = token_index_map; a.accumulate = flags & MOE_ACCUMULATE; }
+    else a.dX = out;
+    moe::probe::begin(stream);
+    return hip_status(fn, moe::ffn_bwd(a, flags & MOE_F32, stream));
+}
+
+}  // namespace
+
 extern "C" {
 
 const char* moe_strerror(int status) {
@@ -141,39 +236,34 @@ int moe_build_index(const int32_t* topk_ids, int64_t T, int E, int k, int32_t* c
                                            token_index_map, slot_src, workspace, stream));
 }
 
+
 size_t moe_ffn_fwd_workspace_size(int64_t T, int d, int f, int E, int k, unsigned flags) {
     if (T <= 0 || d < 1 || f < 1 || E < 1 || k < 1) return 0;
-    return moe::ffn_fwd_workspace(T, d, f, E, k, flags & MOE_F32);
+    return moe::ffn_fwd_workspace(T, d, f, E, k, flags & MOE_F32, false);
 }
 
 int moe_ffn_fwd(const void* x, const void* w1, const void* w3, const void* w2,
                 const int32_t* offsets, const int32_t* expert_token_indices, int64_t T, int d,
                 int f, int E, int k, unsigned flags, void* A, void* B, void* O, void* workspace,
                 size_t workspace_bytes, hipStream_t stream) {
-    const char* fn = "moe_ffn_fwd";
-    int r;
-    if ((r = check_common(fn, T, E, k, flags)) || (r = check_dim(fn, "d", d)) ||
-        (r = check_dim(fn, "f", f)))
-        return r;
-    if (flags & (MOE_RENORM | MOE_ACCUMULATE))
-        return fail(MOE_ERR_INVALID_ARG, "%s: only MOE_F32 / MOE_BF16 and an activation flag are valid", fn);
-    const int act = act_of(flags);
-    if (act < 0) return fail(MOE_ERR_INVALID_ARG, "%s: MOE_ACT_SILU and MOE_ACT_RELU both set", fn);
-    if (T == 0) return MOE_OK;
-    REQUIRE_PTR(x); REQUIRE_PTR(w1); REQUIRE_PTR(w2); REQUIRE_PTR(offsets);
-    REQUIRE_PTR(expert_token_indices); REQUIRE_PTR(A); REQUIRE_PTR(O);
-    if (act == 0) { REQUIRE_PTR(w3); REQUIRE_PTR(B); }
-    else { OPT_PTR(w3); OPT_PTR(B); }
-    const size_t need = moe::ffn_fwd_workspace(T, d, f, E, k, flags & MOE_F32);
-    if (need && (!workspace || workspace_bytes < need))
-        return fail(MOE_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, workspace_bytes, need);
-    OPT_PTR(workspace);
-    moe::FfnArgs a{};
-    a.x = x; a.w1 = w1; a.w3 = w3; a.w2 = w2; a.offsets = offsets; a.eti = expert_token_indices;
-    a.A = A; a.B = B; a.O = O; a.T = T; a.d = d; a.f = f; a.E = E; a.k = k; a.ws = workspace;
-    a.act = act;
-    moe::probe::begin(stream);
-    return hip_status(fn, moe::ffn_fwd(a, flags & MOE_F32, stream));
+    return ffn_fwd_impl("moe_ffn_fwd", false, x, w1, w3, w2, offsets, expert_token_indices,
+                        nullptr, nullptr, T, d, f, E, k, flags, A, B, O, workspace,
+                        workspace_bytes, stream);
+}
+
+size_t moe_ffn_fwd_combine_workspace_size(int64_t T, int d, int f, int E, int k, unsigned flags) {
+    if (T <= 0 || d < 1 || f < 1 || E < 1 || k < 1) return 0;
+    return moe::ffn_fwd_workspace(T, d, f, E, k, flags & MOE_F32, true);
+}
+
+int moe_ffn_fwd_combine(const void* x, const void* w1, const void* w3, const void* w2,
+                        const int32_t* offsets, const int32_t* expert_token_indices,
+                        const float* gates, const int32_t* token_index_map, int64_t T, int d,
+                        int f, int E, int k, unsigned flags, void* A, void* B, void* y,
+                        void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    return ffn_fwd_impl("moe_ffn_fwd_combine", true, x, w1, w3, w2, offsets,
+                        expert_token_indices, gates, token_index_map, T, d, f, E, k, flags, A, B,
+                        y, workspace, workspace_bytes, stream);
 }
 
 int moe_combine(const void* src, const float* weights, const int32_t* token_index_map,
@@ -190,9 +280,10 @@ int moe_combine(const void* src, const float* weights, const int32_t* token_inde
                                        flags & MOE_ACCUMULATE, out, stream));
 }
 
+
 size_t moe_ffn_bwd_workspace_size(int64_t T, int d, int f, int E, int k, unsigned flags) {
     if (T <= 0 || d < 1 || f < 1 || E < 1 || k < 1) return 0;
-    return moe::ffn_bwd_workspace(T, d, f, E, k, flags & MOE_F32);
+    return moe::ffn_bwd_workspace(T, d, f, E, k, flags & MOE_F32, false);
 }
 
 int moe_ffn_bwd(const void* dy, const void* x, const void* w1, const void* w3, const void* w2,
@@ -200,33 +291,26 @@ int moe_ffn_bwd(const void* dy, const void* x, const void* w1, const void* w3, c
                 const int32_t* slot_src, void* A, void* B, int64_t T, int d, int f, int E, int k,
                 unsigned flags, float* dw1, float* dw3, float* dw2, float* d_gates,
                 void* dX_slot, void* workspace, size_t workspace_bytes, hipStream_t stream) {
-    const char* fn = "moe_ffn_bwd";
-    int r;
-    if ((r = check_common(fn, T, E, k, flags)) || (r = check_dim(fn, "d", d)) ||
-        (r = check_dim(fn, "f", f)))
-        return r;
-    if (flags & (MOE_RENORM | MOE_ACCUMULATE))
-        return fail(MOE_ERR_INVALID_ARG, "%s: only MOE_F32 / MOE_BF16 and an activation flag are valid", fn);
-    const int act = act_of(flags);
-    if (act < 0) return fail(MOE_ERR_INVALID_ARG, "%s: MOE_ACT_SILU and MOE_ACT_RELU both set", fn);
-    if (T == 0) return MOE_OK;
-    REQUIRE_PTR(dy); REQUIRE_PTR(x); REQUIRE_PTR(w1); REQUIRE_PTR(w2);
-    REQUIRE_PTR(gates); REQUIRE_PTR(offsets); REQUIRE_PTR(expert_token_indices);
-    REQUIRE_PTR(slot_src); REQUIRE_PTR(A); REQUIRE_PTR(dw1);
-    REQUIRE_PTR(dw2); REQUIRE_PTR(d_gates); REQUIRE_PTR(dX_slot);
-    if (act == 0) { REQUIRE_PTR(w3); REQUIRE_PTR(B); REQUIRE_PTR(dw3); }
-    else { OPT_PTR(w3); OPT_PTR(B); OPT_PTR(dw3); }
-    const size_t need = moe::ffn_bwd_workspace(T, d, f, E, k, flags & MOE_F32);
-    if (need && (!workspace || workspace_bytes < need))
-        return fail(MOE_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, workspace_bytes, need);
-    OPT_PTR(workspace);
-    moe::FfnArgs a{};
-    a.x = x; a.w1 = w1; a.w3 = w3; a.w2 = w2; a.offsets = offsets; a.eti = expert_token_indices;
-    a.slot_src = slot_src; a.gates = gates; a.dy = dy; a.A = A; a.B = B; a.dX = dX_slot;
-    a.dw1 = dw1; a.dw3 = dw3; a.dw2 = dw2; a.dgates = d_gates; a.T = T; a.d = d; a.f = f;
-    a.E = E; a.k = k; a.ws = workspace; a.act = act;
-    moe::probe::begin(stream);
-    return hip_status(fn, moe::ffn_bwd(a, flags & MOE_F32, stream));
+    return ffn_bwd_impl("moe_ffn_bwd", false, dy, x, w1, w3, w2, gates, offsets,
+                        expert_token_indices, slot_src, nullptr, A, B, T, d, f, E, k, flags, dw1,
+                        dw3, dw2, d_gates, dX_slot, workspace, workspace_bytes, stream);
+}
+
+size_t moe_ffn_bwd_combine_workspace_size(int64_t T, int d, int f, int E, int k, unsigned flags) {
+    if (T <= 0 || d < 1 || f < 1 || E < 1 || k < 1) return 0;
+    return moe::ffn_bwd_workspace(T, d, f, E, k, flags & MOE_F32, true);
+}
+
+int moe_ffn_bwd_combine(const void* dy, const void* x, const void* w1, const void* w3,
+                        const void* w2, const float* gates, const int32_t* offsets,
+                        const int32_t* expert_token_indices, const int32_t* slot_src,
+                        const int32_t* token_index_map, void* A, void* B, int64_t T, int d,
+                        int f, int E, int k, unsigned flags, float* dw1, float* dw3, float* dw2,
+                        float* d_gates, void* dx, void* workspace, size_t workspace_bytes,
+                        hipStream_t stream) {
+    return ffn_bwd_impl("moe_ffn_bwd_combine", true, dy, x, w1, w3, w2, gates, offsets,
+                        expert_token_indices, slot_src, token_index_map, A, B, T, d, f, E, k,
+                        flags, dw1, dw3, dw2, d_gates, dx, workspace, workspace_bytes, stream);
 }
 
 size_t moe_route_bwd_workspace_size(int64_t T, int d, int E, int k, unsigned flags) {

@@ -6,9 +6,10 @@
 // into y, with no routed-token buffer. With unit weights the same kernel is the
 // token gradient accumulation of Section 3.2, step 3.
 //
-// HBM-bound gather-reduce: one workgroup per token, 16-byte vector loads
-// along d, all k source rows of a chunk in flight before the float32
-// accumulation, which adds the k terms in order j = 0..k-1.
+// HBM-bound gather-reduce: one workgroup per token (several for narrow column
+// strips), 16-byte vector loads along d, all k source rows of a chunk in
+// flight before the float32 accumulation, which adds the k terms in order
+// j = 0..k-1.
 #include "common.hpp"
 #include "launch.hpp"
 #include "probe.hpp"
@@ -19,35 +20,40 @@ namespace {
 constexpr int CMB_THREADS = 256;
 constexpr int KMAX = 16;
 
-// One workgroup per token; thread c owns 16-byte column chunks c and c + 256
-// (d <= 4096 bf16 / 2048 float32 per pass; wider rows loop). The token's k
-// slot rows and weights are wave-uniform (scalar loads); all k source chunks
-// of a thread are loaded before the float32 sum, which runs in order j = 0..k-1.
+// A workgroup handles TPB tokens (TPB = 256 / LPT) with LPT lanes per token;
+// lane c owns 16-byte column chunks c, c + LPT, ... of its token's ncols
+// columns. Source rows are src_ld elements apart and output rows out_ld, so
+// the kernel also combines one column strip of a wider matrix. The token's k
+// slot rows and weights are read once; all k source chunks of a lane are
+// loaded before the float32 sum, which runs in order j = 0..k-1.
 template <bool F32, int NC>
 __global__ void __launch_bounds__(CMB_THREADS)
-combine_kernel(const void* __restrict__ src_, const float* __restrict__ w,
-               const int32_t* __restrict__ tim, int64_t T, int d, int k, int accumulate,
-               void* __restrict__ out_) {
-    const int64_t t = blockIdx.x;
+combine_kernel(const void* __restrict__ src_, int64_t src_ld, const float* __restrict__ w,
+               const int32_t* __restrict__ tim, int64_t T, int ncols, int k, int accumulate,
+               void* __restrict__ out_, int64_t out_ld, int lpt_log2) {
+    const int lpt = 1 << lpt_log2;
+    const int64_t t = (int64_t)blockIdx.x * (CMB_THREADS >> lpt_log2) + (threadIdx.x >> lpt_log2);
+    const int lane = threadIdx.x & (lpt - 1);
+    if (t >= T) return;
     constexpr int EPV = F32 ? 4 : 8;  // elements per 16-byte vector
-    const int nchunk = d / EPV;
+    const int nchunk = ncols / EPV;
     int64_t row[KMAX];
     float g[KMAX];
 #pragma unroll
     for (int j = 0; j < KMAX; ++j) {
         if (j < k) {
-            row[j] = (int64_t)tim[t * k + j] * d;
+            row[j] = (int64_t)tim[t * k + j] * src_ld;
             g[j] = w ? w[t * k + j] : 1.0f;
         }
     }
     const char* src = static_cast<const char*>(src_);
     char* out = static_cast<char*>(out_);
     const int esz = F32 ? 4 : 2;
-    for (int c0 = 0; c0 < nchunk; c0 += NC * CMB_THREADS) {
+    for (int c0 = 0; c0 < nchunk; c0 += NC * lpt) {
         uint4 v[NC][KMAX];
 #pragma unroll
         for (int u = 0; u < NC; ++u) {
-            const int c = c0 + u * CMB_THREADS + threadIdx.x;
+            const int c = c0 + u * lpt + lane;
 #pragma unroll
             for (int j = 0; j < KMAX; ++j)
                 if (j < k && c < nchunk)
@@ -60,7 +66,7 @@ combine_kernel(const void* __restrict__ src_, const float* __restrict__ w,
         }
 #pragma unroll
         for (int u = 0; u < NC; ++u) {
-            const int c = c0 + u * CMB_THREADS + threadIdx.x;
+            const int c = c0 + u * lpt + lane;
             if (c >= nchunk) continue;
             float acc[8];
 #pragma unroll
@@ -81,7 +87,7 @@ combine_kernel(const void* __restrict__ src_, const float* __restrict__ w,
                     }
                 }
             }
-            char* dst = out + (t * d + (int64_t)c * EPV) * esz;
+            char* dst = out + (t * out_ld + (int64_t)c * EPV) * esz;
             if (accumulate) {
                 const uint4 o = ld16(dst);
                 if (F32) {
@@ -105,24 +111,35 @@ combine_kernel(const void* __restrict__ src_, const float* __restrict__ w,
 
 }  // namespace
 
-hipError_t combine(const void* src, const float* w, const int32_t* tim, int64_t T, int d,
-                   int k, bool f32, bool accumulate, void* out, hipStream_t st) {
-    const dim3 grid((unsigned)T);
-    const int nchunk = d / (f32 ? 4 : 8);
+hipError_t combine_cols(const void* src, int64_t src_ld, const float* w, const int32_t* tim,
+                        int64_t T, int ncols, int k, bool f32, bool accumulate, void* out,
+                        int64_t out_ld, hipStream_t st) {
+    const int nchunk = ncols / (f32 ? 4 : 8);
+    // lanes per token: the smallest power of two covering the row's chunks
+    // (at most the whole workgroup; wider rows loop)
+    int lpt_log2 = 0;
+    while ((1 << lpt_log2) < nchunk && (1 << lpt_log2) < CMB_THREADS) ++lpt_log2;
+    const int64_t tpb = CMB_THREADS >> lpt_log2;
+    const dim3 grid((unsigned)((T + tpb - 1) / tpb));
     if (f32) {
-        hipLaunchKernelGGL((combine_kernel<true, 2>), grid, dim3(CMB_THREADS), 0, st, src, w, tim,
-                           T, d, k, (int)accumulate, out);
+        hipLaunchKernelGGL((combine_kernel<true, 2>), grid, dim3(CMB_THREADS), 0, st, src, src_ld,
+                           w, tim, T, ncols, k, (int)accumulate, out, out_ld, lpt_log2);
         probe::mark("combine_f32", st);
     } else if (nchunk <= CMB_THREADS) {
-        hipLaunchKernelGGL((combine_kernel<false, 1>), grid, dim3(CMB_THREADS), 0, st, src, w,
-                           tim, T, d, k, (int)accumulate, out);
+        hipLaunchKernelGGL((combine_kernel<false, 1>), grid, dim3(CMB_THREADS), 0, st, src,
+                           src_ld, w, tim, T, ncols, k, (int)accumulate, out, out_ld, lpt_log2);
         probe::mark("combine", st);
     } else {
-        hipLaunchKernelGGL((combine_kernel<false, 2>), grid, dim3(CMB_THREADS), 0, st, src, w,
-                           tim, T, d, k, (int)accumulate, out);
+        hipLaunchKernelGGL((combine_kernel<false, 2>), grid, dim3(CMB_THREADS), 0, st, src,
+                           src_ld, w, tim, T, ncols, k, (int)accumulate, out, out_ld, lpt_log2);
         probe::mark("combine", st);
     }
     return hipGetLastError();
+}
+
+hipError_t combine(const void* src, const float* w, const int32_t* tim, int64_t T, int d,
+                   int k, bool f32, bool accumulate, void* out, hipStream_t st) {
+    return combine_cols(src, d, w, tim, T, d, k, f32, accumulate, out, d, st);
 }
 
 }  // namespace moe

@@ -138,23 +138,24 @@ g1_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w1,
     }
 }
 
-// G2: O = H W2[e]
+// G2: O = H W2[e], output columns [n_base, n_base + ncols) into rows ldo apart
 __global__ void __launch_bounds__(CS::THREADS)
 g2_kernel(const bf16_t* __restrict__ H, const bf16_t* __restrict__ w2,
-          const int32_t* __restrict__ offsets, int d, int f, int E, bf16_t* __restrict__ O) {
+          const int32_t* __restrict__ offsets, int d, int f, int E, int n_base, int ncols,
+          int64_t ldo, bf16_t* __restrict__ O) {
     extern __shared__ __align__(16) char lds[];
     using C = CS;
     SlotTile t;
-    const int NT = (d + C::BN - 1) / C::BN;
+    const int NT = (ncols + C::BN - 1) / C::BN;
     if (!find_slot_tile<C::THREADS>(offsets, E, C::BM, NT, xcd_remap(blockIdx.x, gridDim.x), C::BN, t))
         return;
     DenseKC2<C, C::BM> la;
     la.init(H, H, f, (int64_t)t.off + t.m0, t.mrows, f);
     DenseMC<C, C::BN> lb;
-    lb.init(w2 + (int64_t)t.e * f * d, d, t.n0, d);
+    lb.init(w2 + (int64_t)t.e * f * d, d, n_base + t.n0, n_base + ncols);
     NoLoader nl;
     Acc<C> acc;
-    gemm_mainloop<C>(la, lb, nl, f / GBK, GBK, lds, acc, t.mrows);
+    gemm_mainloop<C>(la, lb, nl, f / GBK, GBK, lds, acc, t.mrows, ncols - t.n0);
     WaveCoord<C> wc;
 #pragma unroll
     for (int i = 0; i < C::FM; ++i) {
@@ -168,7 +169,7 @@ g2_kernel(const bf16_t* __restrict__ H, const bf16_t* __restrict__ w2,
 #pragma unroll
             for (int p = 0; p < 2; ++p) {
                 const int n = t.n0 + wc.col8(j, p);
-                if (n < d) store8_bf16(O + s * d + n, v[p]);
+                if (n < ncols) store8_bf16(O + s * ldo + n, v[p]);
             }
         }
     }
@@ -390,26 +391,28 @@ g5_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ dA,
     });
 }
 
-// G6: dX_slot = dA W1[e]^T + dB W3[e]^T   (K = 2f; non-gated: dA W1[e]^T, K = f,
+// G6: dX_slot = dA W1[e]^T + dB W3[e]^T, output columns [n_base, n_base + ncols)
+// into rows ldo apart   (K = 2f; non-gated: dA W1[e]^T, K = f,
 // called with dB = dA and W3 = W1, whose second halves are then never reached)
 __global__ void __launch_bounds__(CS::THREADS)
 g6_kernel(const bf16_t* __restrict__ dA, const bf16_t* __restrict__ dB,
           const bf16_t* __restrict__ w1, const bf16_t* __restrict__ w3,
-          const int32_t* __restrict__ offsets, int d, int f, int E, int kslices,
-          bf16_t* __restrict__ dX) {
+          const int32_t* __restrict__ offsets, int d, int f, int E, int kslices, int n_base,
+          int ncols, int64_t ldo, bf16_t* __restrict__ dX) {
     extern __shared__ __align__(16) char lds[];
     using C = CS;
     SlotTile t;
-    const int NT = (d + C::BN - 1) / C::BN;
+    const int NT = (ncols + C::BN - 1) / C::BN;
     if (!find_slot_tile<C::THREADS>(offsets, E, C::BM, NT, xcd_remap(blockIdx.x, gridDim.x), C::BN, t))
         return;
     DenseKC2<C, C::BM> la;
     la.init(dA, dB, f, (int64_t)t.off + t.m0, t.mrows, f);
     DenseKC2<C, C::BN> lb;  // rows i of W1[e] / W3[e] ([d][f]), K = f then f
-    lb.init(w1 + (int64_t)t.e * d * f, w3 + (int64_t)t.e * d * f, f, t.n0, min(C::BN, d - t.n0), f);
+    lb.init(w1 + (int64_t)t.e * d * f, w3 + (int64_t)t.e * d * f, f, n_base + t.n0,
+            min(C::BN, ncols - t.n0), f);
     NoLoader nl;
     Acc<C> acc;
-    gemm_mainloop<C>(la, lb, nl, kslices, GBK, lds, acc, t.mrows);
+    gemm_mainloop<C>(la, lb, nl, kslices, GBK, lds, acc, t.mrows, ncols - t.n0);
     WaveCoord<C> wc;
 #pragma unroll
     for (int i = 0; i < C::FM; ++i) {
@@ -423,7 +426,7 @@ g6_kernel(const bf16_t* __restrict__ dA, const bf16_t* __restrict__ dB,
 #pragma unroll
             for (int p = 0; p < 2; ++p) {
                 const int n = t.n0 + wc.col8(j, p);
-                if (n < d) store8_bf16(dX + s * d + n, v[p]);
+                if (n < ncols) store8_bf16(dX + s * ldo + n, v[p]);
             }
         }
     }
@@ -617,13 +620,18 @@ hipError_t set_lds_limits() {
 
 inline size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 inline int g4_nparts(int f) { return cdiv(f, C4::BN) * C4::WN; }
+// column strip of the expert output (or of dX_slot) when the combine follows
+// strip by strip: 512 columns, two GEMM tiles wide
+inline int strip_width(int d) { return d < 512 ? d : 512; }
 
 }  // namespace
 
-size_t ffn_fwd_workspace(int64_t T, int d, int f, int E, int k, bool f32) {
-    (void)d; (void)E;
-    if (f32) return 0;
-    return align256((size_t)T * k * f * sizeof(bf16_t));  // H
+size_t ffn_fwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool combined) {
+    (void)E;
+    const size_t S = (size_t)T * k;
+    if (f32) return combined ? align256(S * d * sizeof(float)) : 0;  // O
+    const size_t h = align256(S * f * sizeof(bf16_t));                // H
+    return combined ? h + align256(S * strip_width(d) * sizeof(bf16_t)) : h;
 }
 
 namespace {
@@ -636,10 +644,12 @@ hipError_t ffn_fwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
                            (const float*)a.x, (const float*)a.w1, (const float*)a.w3, a.offsets,
                            a.eti, S, a.d, a.f, a.E, (float*)a.A, (float*)a.B);
         probe::mark("f32_g1", st);
+        float* O = a.y ? static_cast<float*>(a.ws) : (float*)a.O;
         hipLaunchKernelGGL(f32_g2<ACT>, grid1d(S * a.d, 256), dim3(256), 0, st,
                            (const float*)a.A, (const float*)a.B, (const float*)a.w2, a.offsets, S,
-                           a.d, a.f, a.E, (float*)a.O);
+                           a.d, a.f, a.E, O);
         probe::mark("f32_g2", st);
+        if (a.y) return combine(O, a.gates, a.tim, a.T, a.d, a.k, true, false, a.y, st);
         return hipGetLastError();
     }
     if (hipError_t e = set_lds_limits(); e != hipSuccess) return e;
@@ -650,10 +660,28 @@ hipError_t ffn_fwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
                        (const bf16_t*)a.w3, a.offsets, a.eti, a.d, a.f, a.E, (bf16_t*)a.A,
                        (bf16_t*)a.B, H);
     probe::mark("g1_kernel", st);
-    hipLaunchKernelGGL(g2_kernel, dim3(slot_grid(S, a.E, CS::BM, cdiv(a.d, CS::BN))),
-                       dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)H, (const bf16_t*)a.w2,
-                       a.offsets, a.d, a.f, a.E, (bf16_t*)a.O);
-    probe::mark("g2_kernel", st);
+    if (!a.y) {   // O [S, d] for the caller's combine
+        hipLaunchKernelGGL(g2_kernel, dim3(slot_grid(S, a.E, CS::BM, cdiv(a.d, CS::BN))),
+                           dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)H, (const bf16_t*)a.w2,
+                           a.offsets, a.d, a.f, a.E, 0, a.d, (int64_t)a.d, (bf16_t*)a.O);
+        probe::mark("g2_kernel", st);
+        return hipGetLastError();
+    }
+    // combined: one column strip of O at a time, straight into y
+    const int sw = strip_width(a.d);
+    bf16_t* strip = reinterpret_cast<bf16_t*>(static_cast<char*>(a.ws) +
+                                              align256((size_t)S * a.f * sizeof(bf16_t)));
+    for (int c0 = 0; c0 < a.d; c0 += sw) {
+        const int nc = min(sw, a.d - c0);
+        hipLaunchKernelGGL(g2_kernel, dim3(slot_grid(S, a.E, CS::BM, cdiv(nc, CS::BN))),
+                           dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)H, (const bf16_t*)a.w2,
+                           a.offsets, a.d, a.f, a.E, c0, nc, (int64_t)nc, strip);
+        probe::mark("g2_kernel", st);
+        if (hipError_t e = combine_cols(strip, nc, a.gates, a.tim, a.T, nc, a.k, false, false,
+                                        static_cast<bf16_t*>(a.y) + c0, a.d, st);
+            e != hipSuccess)
+            return e;
+    }
     return hipGetLastError();
 }
 
@@ -667,11 +695,13 @@ hipError_t ffn_fwd(const FfnArgs& a, bool f32, hipStream_t st) {
     }
 }
 
-size_t ffn_bwd_workspace(int64_t T, int d, int f, int E, int k, bool f32) {
-    (void)d; (void)E;
-    if (f32) return 0;
-    const int64_t S = T * k;
-    return align256((size_t)S * g4_nparts(f) * sizeof(float)) + align256((size_t)S * f * sizeof(bf16_t));
+size_t ffn_bwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool combined) {
+    (void)E;
+    const size_t S = (size_t)T * k;
+    if (f32) return combined ? align256(S * d * sizeof(float)) : 0;  // dX_slot
+    const size_t hg = S * f * sizeof(bf16_t);                         // g*h, then dX strips
+    const size_t strip = combined ? S * strip_width(d) * sizeof(bf16_t) : 0;
+    return align256(S * g4_nparts(f) * sizeof(float)) + align256(hg > strip ? hg : strip);
 }
 
 namespace {
@@ -693,10 +723,12 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
                            (const float*)a.x, (const float*)a.A, (const float*)a.B, a.offsets,
                            a.eti, a.d, a.f, a.E, a.dw1, a.dw3);
         probe::mark("f32_g5", st);
+        float* dX = a.y ? static_cast<float*>(a.ws) : (float*)a.dX;
         hipLaunchKernelGGL(f32_g6<ACT>, grid1d(S * a.d, 256), dim3(256), 0, st, (const float*)a.A,
                            (const float*)a.B, (const float*)a.w1, (const float*)a.w3, a.offsets,
-                           S, a.d, a.f, a.E, (float*)a.dX);
+                           S, a.d, a.f, a.E, dX);
         probe::mark("f32_g6", st);
+        if (a.y) return combine(dX, nullptr, a.tim, a.T, a.d, a.k, true, a.accumulate, a.y, st);
         return hipGetLastError();
     }
     if (hipError_t e = set_lds_limits(); e != hipSuccess) return e;
@@ -724,11 +756,30 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
                        dim3(C5::THREADS), C5::LDS, st, (const bf16_t*)a.x, (const bf16_t*)a.A,
                        (const bf16_t*)a.B, a.offsets, a.eti, a.d, a.f, a.dw1, a.dw3);
     probe::mark("g5_kernel", st);
-    hipLaunchKernelGGL(g6_kernel, dim3(slot_grid(S, a.E, CS::BM, cdiv(a.d, CS::BN))),
-                       dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)a.A, (const bf16_t*)Bx,
-                       (const bf16_t*)a.w1, (const bf16_t*)w3x, a.offsets, a.d, a.f, a.E,
-                       (GATED ? 2 : 1) * a.f / GBK, (bf16_t*)a.dX);
-    probe::mark("g6_kernel", st);
+    const int kslices = (GATED ? 2 : 1) * a.f / GBK;
+    if (!a.y) {   // dX_slot [S, d] for the caller's combine
+        hipLaunchKernelGGL(g6_kernel, dim3(slot_grid(S, a.E, CS::BM, cdiv(a.d, CS::BN))),
+                           dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)a.A, (const bf16_t*)Bx,
+                           (const bf16_t*)a.w1, (const bf16_t*)w3x, a.offsets, a.d, a.f, a.E,
+                           kslices, 0, a.d, (int64_t)a.d, (bf16_t*)a.dX);
+        probe::mark("g6_kernel", st);
+        return hipGetLastError();
+    }
+    // combined: one column strip of dX_slot at a time, summed straight into dx;
+    // the strip reuses g*h's workspace, which G3 has finished with
+    const int sw = strip_width(a.d);
+    for (int c0 = 0; c0 < a.d; c0 += sw) {
+        const int nc = min(sw, a.d - c0);
+        hipLaunchKernelGGL(g6_kernel, dim3(slot_grid(S, a.E, CS::BM, cdiv(nc, CS::BN))),
+                           dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)a.A, (const bf16_t*)Bx,
+                           (const bf16_t*)a.w1, (const bf16_t*)w3x, a.offsets, a.d, a.f, a.E,
+                           kslices, c0, nc, (int64_t)nc, HG);
+        probe::mark("g6_kernel", st);
+        if (hipError_t e = combine_cols(HG, nc, nullptr, a.tim, a.T, nc, a.k, false,
+                                        a.accumulate, static_cast<bf16_t*>(a.y) + c0, a.d, st);
+            e != hipSuccess)
+            return e;
+    }
     return hipGetLastError();
 }
 

@@ -27,6 +27,11 @@ hipError_t route_bwd(const float* dgates, const float* logits, const int32_t* id
 // ---- combine ----
 hipError_t combine(const void* src, const float* w, const int32_t* tim, int64_t T, int d,
                    int k, bool f32, bool accumulate, void* out, hipStream_t st);
+// the same on one column strip: ncols columns of source rows src_ld elements
+// apart into output rows out_ld elements apart
+hipError_t combine_cols(const void* src, int64_t src_ld, const float* w, const int32_t* tim,
+                        int64_t T, int ncols, int k, bool f32, bool accumulate, void* out,
+                        int64_t out_ld, hipStream_t st);
 
 // ---- expert FFN ----
 struct FfnArgs {
@@ -38,10 +43,13 @@ struct FfnArgs {
     int64_t T; int d, f, E, k;
     int act;  // 0 SwiGLU (gated), 1 SiLU, 2 ReLU (non-gated: w3, B, dw3 unused)
     void* ws;
+    // combined calls: y (forward) or dx (backward) [T, d] written through
+    // token_index_map instead of O / dX_slot; accumulate adds into dx
+    void* y; const int32_t* tim; bool accumulate;
 };
-size_t ffn_fwd_workspace(int64_t T, int d, int f, int E, int k, bool f32);
+size_t ffn_fwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool combined);
 hipError_t ffn_fwd(const FfnArgs& a, bool f32, hipStream_t st);
-size_t ffn_bwd_workspace(int64_t T, int d, int f, int E, int k, bool f32);
+size_t ffn_bwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool combined);
 hipError_t ffn_bwd(const FfnArgs& a, bool f32, hipStream_t st);
 
 }  // namespace moe

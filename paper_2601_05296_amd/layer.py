@@ -4,10 +4,12 @@ This module only allocates device buffers with torch and calls the library's
 entry points in order; every arithmetic step runs in the HIP kernels.
 
 Forward (MoEBlaze paper, Sections 2-5):
-  moe_route -> moe_build_index -> moe_ffn_fwd -> moe_combine
+  moe_route -> moe_build_index -> moe_ffn_fwd_combine
+  (= moe_ffn_fwd + moe_combine, strip by strip, with no [T*k, d] output buffer)
 Backward (Section 3.2):
-  moe_ffn_bwd -> moe_combine (unit weights: token gradient accumulation)
-  -> moe_route_bwd (router gradient, added into dx)
+  moe_ffn_bwd_combine (= moe_ffn_bwd + the unit-weight combine that sums the
+  token gradient) -> moe_route_bwd (router gradient, added into dx)
+``separate=True`` runs the four separate calls instead (same results).
 
 What the forward keeps for the backward (the "saved activations"): the first
 layer outputs A and B [S, f] (A alone for the non-gated SiLU / ReLU experts),
@@ -69,9 +71,10 @@ def saved_bytes_per_token(d: int, f: int, E: int, k: int, elem: int, T: int,
 
 
 def forward(x, w_gate, bias, w1, w3, w2, k: int, renorm: bool, stream=None, keep_O=False,
-            act: str = "swiglu"):
+            act: str = "swiglu", separate: bool = False):
     """Returns (y, saved[, O]). ``act`` picks the expert: "swiglu" (gated, w3
-    used) or the non-gated "silu" / "relu" (w3 ignored, may be None)."""
+    used) or the non-gated "silu" / "relu" (w3 ignored, may be None).
+    ``keep_O`` (returns the expert outputs) implies ``separate``."""
     T, d = x.shape
     E, _, f = w1.shape
     dev = x.device
@@ -97,25 +100,34 @@ def forward(x, w_gate, bias, w1, w3, w2, k: int, renorm: bool, stream=None, keep
     fflags = flags | B.ACT_FLAG[act]
     A = torch.empty((S, f), dtype=x.dtype, device=dev)
     Bm = torch.empty((S, f), dtype=x.dtype, device=dev) if gated else None
+    y = torch.empty((T, d), dtype=x.dtype, device=dev)
+    saved = Saved(T, d, f, E, k, flags, act, renorm, ids, gates, logits, counts, offsets, eti,
+                  tim, slot_src, A, Bm)
+    w3g = w3 if gated else None
+    if not (separate or keep_O):
+        wsb = B.moe_ffn_fwd_combine_workspace_size(T, d, f, E, k, fflags)
+        ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
+        B.moe_ffn_fwd_combine(x, w1, w3g, w2, offsets, eti, gates, tim, T, d, f, E, k, fflags, A,
+                              Bm, y, ws, wsb, stream)
+        del ws
+        return y, saved
     O = torch.empty((S, d), dtype=x.dtype, device=dev)
     wsb = B.moe_ffn_fwd_workspace_size(T, d, f, E, k, fflags)
     ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
-    B.moe_ffn_fwd(x, w1, w3 if gated else None, w2, offsets, eti, T, d, f, E, k, fflags, A, Bm,
-                  O, ws, wsb, stream)
+    B.moe_ffn_fwd(x, w1, w3g, w2, offsets, eti, T, d, f, E, k, fflags, A, Bm, O, ws, wsb, stream)
     del ws
-    y = torch.empty((T, d), dtype=x.dtype, device=dev)
     B.moe_combine(O, gates, tim, T, d, k, flags, y, stream)
-    saved = Saved(T, d, f, E, k, flags, act, renorm, ids, gates, logits, counts, offsets, eti,
-                  tim, slot_src, A, Bm)
     if keep_O:
         return y, saved, O
     del O
     return y, saved
 
 
-def backward(saved: Saved, dy, x, w_gate, w1, w3, w2, stream=None, keep=False):
+def backward(saved: Saved, dy, x, w_gate, w1, w3, w2, stream=None, keep=False,
+             separate: bool = False):
     """Returns dict(dx, dw_gate, dw1, dw3, dw2, d_gates[, dX_slot]). Overwrites
-    saved.A / saved.B with dA / dB. dw3 is None for a non-gated expert."""
+    saved.A / saved.B with dA / dB. dw3 is None for a non-gated expert.
+    ``keep`` (returns dX_slot and the FFN part of dx) implies ``separate``."""
     s = saved
     T, d, f, E, k = s.T, s.d, s.f, s.E, s.k
     dev = dy.device
@@ -125,20 +137,28 @@ def backward(saved: Saved, dy, x, w_gate, w1, w3, w2, stream=None, keep=False):
     dw3 = torch.empty((E, d, f), **f32) if gated else None
     dw2 = torch.empty((E, f, d), **f32)
     d_gates = torch.empty((T, k), **f32)
-    dX = torch.empty((T * k, d), dtype=dy.dtype, device=dev)
-    wsb = B.moe_ffn_bwd_workspace_size(T, d, f, E, k, s.ffn_flags)
-    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
-    B.moe_ffn_bwd(dy, x, w1, w3 if gated else None, w2, s.gates, s.offsets, s.eti, s.slot_src,
-                  s.A, s.B, T, d, f, E, k, s.ffn_flags, dw1, dw3, dw2, d_gates, dX, ws, wsb,
-                  stream)
-    del ws
     dx = torch.empty((T, d), dtype=dy.dtype, device=dev)
-    B.moe_combine(dX, None, s.tim, T, d, k, s.flags, dx, stream)
+    w3g = w3 if gated else None
     out = dict(dw1=dw1, dw3=dw3, dw2=dw2, d_gates=d_gates)
-    if keep:
-        out["dX_slot"] = dX
-        out["dx_ffn"] = dx.clone()
-    del dX
+    if not (separate or keep):
+        wsb = B.moe_ffn_bwd_combine_workspace_size(T, d, f, E, k, s.ffn_flags)
+        ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
+        B.moe_ffn_bwd_combine(dy, x, w1, w3g, w2, s.gates, s.offsets, s.eti, s.slot_src, s.tim,
+                              s.A, s.B, T, d, f, E, k, s.ffn_flags, dw1, dw3, dw2, d_gates, dx,
+                              ws, wsb, stream)
+        del ws
+    else:
+        dX = torch.empty((T * k, d), dtype=dy.dtype, device=dev)
+        wsb = B.moe_ffn_bwd_workspace_size(T, d, f, E, k, s.ffn_flags)
+        ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
+        B.moe_ffn_bwd(dy, x, w1, w3g, w2, s.gates, s.offsets, s.eti, s.slot_src, s.A, s.B, T, d,
+                      f, E, k, s.ffn_flags, dw1, dw3, dw2, d_gates, dX, ws, wsb, stream)
+        del ws
+        B.moe_combine(dX, None, s.tim, T, d, k, s.flags, dx, stream)
+        if keep:
+            out["dX_slot"] = dX
+            out["dx_ffn"] = dx.clone()
+        del dX
     dwg = torch.empty((E, d), **f32)
     rflags = s.flags | B.MOE_ACCUMULATE | (B.MOE_RENORM if s.renorm else 0)
     wsb = B.moe_route_bwd_workspace_size(T, d, E, k, rflags)

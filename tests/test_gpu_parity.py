@@ -353,6 +353,99 @@ def test_layer_nongated_end_to_end(act):
         assert_close(n, host(g[n]), bw_r[n], "bf16")
 
 
+COMBINED_CASES = [
+    # dtype, T, d, f, E, k, ids pattern, activation
+    ("bf16", 400, 1280, 256, 8, 2, None, "swiglu"),     # three column strips, the last 256 wide
+    ("bf16", 333, 384, 256, 12, 3, "dead", "silu"),     # one strip narrower than 512
+    ("bf16", 500, 640, 384, 16, 4, "zipf", "relu"),
+    ("f32", 257, 256, 256, 8, 2, None, "swiglu"),
+]
+
+
+@pytest.mark.parametrize("dtype,T,d,f,E,k,pattern,act", COMBINED_CASES)
+def test_ffn_combined_equals_separate(dtype, T, d, f, E, k, pattern, act):
+    """moe_ffn_fwd_combine / moe_ffn_bwd_combine against moe_ffn_fwd / moe_ffn_bwd
+    followed by moe_combine: the same kernels in the same order, so the results
+    are bit-identical; and against the oracle."""
+    inp, ids, g = _layer_case(dtype, T, d, f, E, k, False, pattern)
+    v, st = inp.vals, inp.store
+    gated = act == "swiglu"
+    S = T * k
+    gi = _gpu_index(ids, E)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    x, w1, w2, dy = (dev(st[n]) for n in ("x", "w1", "w2", "dy"))
+    w3 = dev(st["w3"]) if gated else None
+    offsets, eti, tim, ss = (dev(gi[n]) for n in ("offsets", "eti", "tim", "slot_src"))
+    gates = dev(g)
+    flags = B.dtype_flag(x) | B.ACT_FLAG[act]
+    f32 = dict(dtype=torch.float32, device="cuda")
+
+    def fwd(combined):
+        A = torch.empty((S, f), dtype=tdt, device="cuda")
+        Bm = torch.empty((S, f), dtype=tdt, device="cuda") if gated else None
+        y = torch.empty((T, d), dtype=tdt, device="cuda")
+        if combined:
+            wsb = B.moe_ffn_fwd_combine_workspace_size(T, d, f, E, k, flags)
+            ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+            B.moe_ffn_fwd_combine(x, w1, w3, w2, offsets, eti, gates, tim, T, d, f, E, k, flags,
+                                  A, Bm, y, ws, wsb)
+        else:
+            O = torch.empty((S, d), dtype=tdt, device="cuda")
+            wsb = B.moe_ffn_fwd_workspace_size(T, d, f, E, k, flags)
+            ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+            B.moe_ffn_fwd(x, w1, w3, w2, offsets, eti, T, d, f, E, k, flags, A, Bm, O, ws, wsb)
+            B.moe_combine(O, gates, tim, T, d, k, B.dtype_flag(x), y)
+        return A, Bm, y
+
+    def bwd(A, Bm, combined, dx0=None):
+        dw1 = torch.empty((E, d, f), **f32)
+        dw3 = torch.empty((E, d, f), **f32) if gated else None
+        dw2 = torch.empty((E, f, d), **f32)
+        dg = torch.empty((T, k), **f32)
+        dx = torch.empty((T, d), dtype=tdt, device="cuda") if dx0 is None else dx0.clone()
+        if combined:
+            fl = flags | (B.MOE_ACCUMULATE if dx0 is not None else 0)
+            wsb = B.moe_ffn_bwd_combine_workspace_size(T, d, f, E, k, flags)
+            ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+            B.moe_ffn_bwd_combine(dy, x, w1, w3, w2, gates, offsets, eti, ss, tim, A, Bm, T, d, f,
+                                  E, k, fl, dw1, dw3, dw2, dg, dx, ws, wsb)
+        else:
+            dX = torch.empty((S, d), dtype=tdt, device="cuda")
+            wsb = B.moe_ffn_bwd_workspace_size(T, d, f, E, k, flags)
+            ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+            B.moe_ffn_bwd(dy, x, w1, w3, w2, gates, offsets, eti, ss, A, Bm, T, d, f, E, k, flags,
+                          dw1, dw3, dw2, dg, dX, ws, wsb)
+            B.moe_combine(dX, None, tim, T, d, k,
+                          B.dtype_flag(x) | (B.MOE_ACCUMULATE if dx0 is not None else 0), dx)
+        return dict(dw1=dw1, dw3=dw3, dw2=dw2, d_gates=dg, dx=dx)
+
+    res = {}
+    for combined in (False, True):
+        A, Bm, y = fwd(combined)
+        A0 = A.clone()
+        Bm0 = Bm.clone() if gated else None
+        r = bwd(A, Bm, combined)
+        r2 = bwd(A0, Bm0, combined, dx0=y)   # MOE_ACCUMULATE: dx = y + token gradient
+        torch.cuda.synchronize()
+        res[combined] = (A0, y, r, r2)
+    (A_s, y_s, r_s, r2_s), (A_c, y_c, r_c, r2_c) = res[False], res[True]
+    assert torch.equal(A_s, A_c) and torch.equal(y_s, y_c)
+    for n in ("dw1", "dw2", "d_gates", "dx") + (("dw3",) if gated else ()):
+        assert torch.equal(r_s[n], r_c[n]), n
+    assert torch.equal(r2_s["dx"], r2_c["dx"])
+    # and the oracle
+    ix = oracle.build_index(ids, E)
+    if gated:
+        A_r, B_r, O_r = oracle.ffn_fwd(v["x"], v["w1"], v["w3"], v["w2"], ix, k)
+        bw = oracle.ffn_bwd(v["dy"], v["x"], v["w1"], v["w3"], v["w2"], g, ix, A_r, B_r)
+    else:
+        A_r, O_r = oracle.ffn_fwd_act(v["x"], v["w1"], v["w2"], ix, k, act)
+        bw = oracle.ffn_bwd_act(v["dy"], v["x"], v["w1"], v["w2"], g, ix, A_r, act)
+    assert_close("y", host(y_c), oracle.combine(O_r, g, ix.tim), dtype)
+    assert_close("dx", host(r_c["dx"]), oracle.combine(bw["dX_slot"], None, ix.tim), dtype)
+    assert_close("dw1", host(r_c["dw1"]), bw["dw1"], dtype)
+
+
 # whole layer (routing included) on the tiny float32 workload
 # ---------------------------------------------------------------------------
 
