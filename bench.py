@@ -307,15 +307,25 @@ def table1_sweep(args):
                 torch.cuda.empty_cache()
                 row[which + "_ms"] = round(timed(fn, args.steps, args.warmup), 4)
                 torch.cuda.synchronize()
+                # forward peak, then the peak of the whole step less the weight
+                # gradients (which live only in the backward); the larger counts
                 torch.cuda.reset_peak_memory_stats(dev)
                 m0 = torch.cuda.memory_allocated(dev)
+                if which == "ours":
+                    y, saved = layer.forward(x, wg, None, w1, w3, w2, k, False, act=act)
+                    del y, saved
+                else:
+                    materialised_saved_bytes(x, wg, None, w1, w3, w2, k, False, act)
+                torch.cuda.synchronize()
+                fwd_peak = torch.cuda.max_memory_allocated(dev) - m0
+                torch.cuda.reset_peak_memory_stats(dev)
                 out = fn()
                 torch.cuda.synchronize()
                 peak = torch.cuda.max_memory_allocated(dev) - m0
                 grads = sum(t.numel() * t.element_size()
                             for t in (out.values() if isinstance(out, dict) else out)
                             if t is not None and t.dim() == 3)  # weight gradients
-                row[which + "_peak_bytes_per_token"] = round((peak - grads) / T, 1)
+                row[which + "_peak_bytes_per_token"] = round(max(fwd_peak, peak - grads) / T, 1)
                 del out
             torch.cuda.empty_cache()
             y, saved = layer.forward(x, wg, None, w1, w3, w2, k, False, act=act)
@@ -371,9 +381,12 @@ def memory_sweep(cfg, max_doublings):
                 if which == "ours":
                     y, saved = layer.forward(x, wg, None, w1, w3, w2, k, cfg.renorm, act=cfg.act)
                     sb = saved.nbytes()
+                    torch.cuda.synchronize()
+                    fwd_peak = torch.cuda.max_memory_allocated(dev) - base
+                    torch.cuda.reset_peak_memory_stats(dev)
                     g = layer.backward(saved, dy, x, wg, w1, w3, w2)
                     torch.cuda.synchronize()
-                    peak = torch.cuda.max_memory_allocated(dev) - base - grad_bytes
+                    peak = max(fwd_peak, torch.cuda.max_memory_allocated(dev) - base - grad_bytes)
                     del y, saved, g
                     row["ours_peak_bytes_per_token"] = round(peak / T, 1)
                     row["ours_saved_bytes_per_token"] = round(sb / T, 1)
@@ -479,13 +492,19 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    # peak activation bytes of one step (weights, inputs and weight gradients excluded)
+    # peak activation bytes of one step (weights, inputs and weight gradients
+    # excluded): the forward's peak and the backward's, the larger one counts
     torch.cuda.reset_peak_memory_stats(dev)
     base = torch.cuda.memory_allocated(dev)
-    y, saved, g = step()
+    y, saved = layer.forward(x, wg, bias, w1, w3, w2, k, cfg.renorm, act=cfg.act)
     torch.cuda.synchronize()
-    peak = torch.cuda.max_memory_allocated(dev) - base
+    fwd_peak = torch.cuda.max_memory_allocated(dev) - base
+    torch.cuda.reset_peak_memory_stats(dev)
+    g = layer.backward(saved, dy, x, wg, w1, w3, w2)
+    torch.cuda.synchronize()
     grad_bytes = sum(g[n].numel() * 4 for n in ("dw1", "dw3", "dw2", "dw_gate") if g[n] is not None)
+    bwd_peak = torch.cuda.max_memory_allocated(dev) - base - grad_bytes
+    peak = max(fwd_peak, bwd_peak)
     saved_bytes = saved.nbytes()
     formula = layer.saved_bytes_per_token(d, f, E, k, elem, T, cfg.act) * T
     assert abs(saved_bytes - formula) < 1, (saved_bytes, formula)
@@ -545,7 +564,8 @@ def main():
         "config": {"workload": cfg.name, "T": T, "d": d, "f": f, "E": E, "k": k,
                    "renorm": cfg.renorm, "zipf_s": cfg.zipf_s, "act": cfg.act,
                    "parallelism": "none"},
-        "peak_activation_bytes_per_token": round((peak - grad_bytes) / T, 1),
+        "peak_activation_bytes_per_token": round(peak / T, 1),
+        "peak_activation_bytes_per_token_fwd_bwd": [round(fwd_peak / T, 1), round(bwd_peak / T, 1)],
         "saved_activation_bytes_per_token": round(saved_bytes / T, 1),
         "roofline": roofline,
         "gemm": {"ms_per_step": round(gemm_ms, 4),

@@ -621,8 +621,9 @@ hipError_t set_lds_limits() {
 inline size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 inline int g4_nparts(int f) { return cdiv(f, C4::BN) * C4::WN; }
 // column strip of the expert output (or of dX_slot) when the combine follows
-// strip by strip: 512 columns, two GEMM tiles wide
-inline int strip_width(int d) { return d < 512 ? d : 512; }
+// strip by strip: 1024 columns, four GEMM tiles wide (narrower strips leave
+// too few tiles per launch to fill the GPU evenly)
+inline int strip_width(int d) { return d < 1024 ? d : 1024; }
 
 }  // namespace
 
