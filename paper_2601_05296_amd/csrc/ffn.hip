@@ -620,19 +620,28 @@ hipError_t set_lds_limits() {
 
 inline size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 inline int g4_nparts(int f) { return cdiv(f, C4::BN) * C4::WN; }
-// column strip of the expert output (or of dX_slot) when the combine follows
-// strip by strip: 1024 columns, four GEMM tiles wide (narrower strips leave
-// too few tiles per launch to fill the GPU evenly)
-inline int strip_width(int d) { return d < 1024 ? d : 1024; }
+// Column strip of the expert output (or of dX_slot) when the combine follows
+// strip by strip. Narrow strips save memory, but a launch needs enough tiles
+// (here about six waves of 256) or its last partial wave leaves CUs idle, so
+// the strips are as narrow as that allows, in whole 256-column tiles, and of
+// equal width: about 1024 columns for 98k slots and 64 experts, 2048 for 65k
+// slots and 8 experts, 256 for 524k slots.
+inline int strip_width(int64_t S, int E, int d) {
+    const int64_t mtiles = (S + CS::BM - 1) / CS::BM + E / 2;   // tiles per column of tiles
+    const int64_t want = 6 * 256;
+    const int64_t w = (int64_t)CS::BN * ((want + mtiles - 1) / mtiles);
+    const int n = (int)(d / (w < d ? w : d));                    // strips
+    const int width = ((d + n - 1) / n + CS::BN - 1) / CS::BN * CS::BN;
+    return width < d ? width : d;
+}
 
 }  // namespace
 
 size_t ffn_fwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool combined) {
-    (void)E;
     const size_t S = (size_t)T * k;
     if (f32) return combined ? align256(S * d * sizeof(float)) : 0;  // O
     const size_t h = align256(S * f * sizeof(bf16_t));                // H
-    return combined ? h + align256(S * strip_width(d) * sizeof(bf16_t)) : h;
+    return combined ? h + align256(S * strip_width(S, E, d) * sizeof(bf16_t)) : h;
 }
 
 namespace {
@@ -669,7 +678,7 @@ hipError_t ffn_fwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
         return hipGetLastError();
     }
     // combined: one column strip of O at a time, straight into y
-    const int sw = strip_width(a.d);
+    const int sw = strip_width(S, a.E, a.d);
     bf16_t* strip = reinterpret_cast<bf16_t*>(static_cast<char*>(a.ws) +
                                               align256((size_t)S * a.f * sizeof(bf16_t)));
     for (int c0 = 0; c0 < a.d; c0 += sw) {
@@ -697,11 +706,10 @@ hipError_t ffn_fwd(const FfnArgs& a, bool f32, hipStream_t st) {
 }
 
 size_t ffn_bwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool combined) {
-    (void)E;
     const size_t S = (size_t)T * k;
     if (f32) return combined ? align256(S * d * sizeof(float)) : 0;  // dX_slot
     const size_t hg = S * f * sizeof(bf16_t);                         // g*h, then dX strips
-    const size_t strip = combined ? S * strip_width(d) * sizeof(bf16_t) : 0;
+    const size_t strip = combined ? S * strip_width(S, E, d) * sizeof(bf16_t) : 0;
     return align256(S * g4_nparts(f) * sizeof(float)) + align256(hg > strip ? hg : strip);
 }
 
@@ -768,7 +776,7 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
     }
     // combined: one column strip of dX_slot at a time, summed straight into dx;
     // the strip reuses g*h's workspace, which G3 has finished with
-    const int sw = strip_width(a.d);
+    const int sw = strip_width(S, a.E, a.d);
     for (int c0 = 0; c0 < a.d; c0 += sw) {
         const int nc = min(sw, a.d - c0);
         hipLaunchKernelGGL(g6_kernel, dim3(slot_grid(S, a.E, CS::BM, cdiv(nc, CS::BN))),

@@ -355,10 +355,13 @@ def test_layer_nongated_end_to_end(act):
 
 COMBINED_CASES = [
     # dtype, T, d, f, E, k, ids pattern, activation
-    ("bf16", 400, 1280, 256, 8, 2, None, "swiglu"),     # three column strips, the last 256 wide
-    ("bf16", 333, 384, 256, 12, 3, "dead", "silu"),     # one strip narrower than 512
+    ("bf16", 400, 1280, 256, 8, 2, None, "swiglu"),
+    ("bf16", 333, 384, 256, 12, 3, "dead", "silu"),
     ("bf16", 500, 640, 384, 16, 4, "zipf", "relu"),
     ("f32", 257, 256, 256, 8, 2, None, "swiglu"),
+    # 393k slots: three strips of 256 columns (bit-exactness only; the
+    # full-size tests check multi-strip workloads against the oracle)
+    ("bf16", 49152, 768, 256, 16, 8, None, "swiglu"),
 ]
 
 
@@ -433,6 +436,8 @@ def test_ffn_combined_equals_separate(dtype, T, d, f, E, k, pattern, act):
     for n in ("dw1", "dw2", "d_gates", "dx") + (("dw3",) if gated else ()):
         assert torch.equal(r_s[n], r_c[n]), n
     assert torch.equal(r2_s["dx"], r2_c["dx"])
+    if S > 20000:
+        return
     # and the oracle
     ix = oracle.build_index(ids, E)
     if gated:
