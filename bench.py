@@ -38,6 +38,9 @@ def parse():
     ap.add_argument("--workload", default="mid_e64k6")
     ap.add_argument("--act", choices=("swiglu", "silu", "relu"), default=None,
                     help="expert activation (default: the workload's own)")
+    ap.add_argument("--recompute", action="store_true",
+                    help="full-recompute checkpoint policy: save only the routing decision and "
+                         "maps, recompute the first layer in the backward")
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="approximate CPU time budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -484,7 +487,8 @@ def main():
     T, d, f, E, k = cfg.T, cfg.d, cfg.f, cfg.E, cfg.k
 
     def step():
-        y, saved = layer.forward(x, wg, bias, w1, w3, w2, k, cfg.renorm, act=cfg.act)
+        y, saved = layer.forward(x, wg, bias, w1, w3, w2, k, cfg.renorm, act=cfg.act,
+                                 recompute=args.recompute)
         g = layer.backward(saved, dy, x, wg, w1, w3, w2)
         return y, saved, g
 
@@ -496,17 +500,18 @@ def main():
     # excluded): the forward's peak and the backward's, the larger one counts
     torch.cuda.reset_peak_memory_stats(dev)
     base = torch.cuda.memory_allocated(dev)
-    y, saved = layer.forward(x, wg, bias, w1, w3, w2, k, cfg.renorm, act=cfg.act)
+    y, saved = layer.forward(x, wg, bias, w1, w3, w2, k, cfg.renorm, act=cfg.act,
+                             recompute=args.recompute)
     torch.cuda.synchronize()
     fwd_peak = torch.cuda.max_memory_allocated(dev) - base
+    saved_bytes = saved.nbytes()   # before the backward (which may recompute A, B into it)
     torch.cuda.reset_peak_memory_stats(dev)
     g = layer.backward(saved, dy, x, wg, w1, w3, w2)
     torch.cuda.synchronize()
     grad_bytes = sum(g[n].numel() * 4 for n in ("dw1", "dw3", "dw2", "dw_gate") if g[n] is not None)
     bwd_peak = torch.cuda.max_memory_allocated(dev) - base - grad_bytes
     peak = max(fwd_peak, bwd_peak)
-    saved_bytes = saved.nbytes()
-    formula = layer.saved_bytes_per_token(d, f, E, k, elem, T, cfg.act) * T
+    formula = layer.saved_bytes_per_token(d, f, E, k, elem, T, cfg.act, args.recompute) * T
     assert abs(saved_bytes - formula) < 1, (saved_bytes, formula)
     del y, saved, g
 
@@ -556,6 +561,8 @@ def main():
               for st, pre in stage_of.items()}
     router_ms = stages["route"] + stages["route_bwd"]
     gemm_flops = (18.0 if cfg.act == "swiglu" else 12.0) * T * k * d * f
+    if args.recompute:   # the first layer runs again in the backward
+        gemm_flops += (4.0 if cfg.act == "swiglu" else 2.0) * T * k * d * f
     out = {
         "metric": "MoE layer fwd+bwd tokens/sec + peak activation bytes/token, 1 MI355X",
         "value": round(tokens_per_s, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
@@ -563,6 +570,7 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": cfg.name, "T": T, "d": d, "f": f, "E": E, "k": k,
                    "renorm": cfg.renorm, "zipf_s": cfg.zipf_s, "act": cfg.act,
+                   "checkpoint": "recompute" if args.recompute else "A,B",
                    "parallelism": "none"},
         "peak_activation_bytes_per_token": round(peak / T, 1),
         "peak_activation_bytes_per_token_fwd_bwd": [round(fwd_peak / T, 1), round(bwd_peak / T, 1)],

@@ -181,6 +181,21 @@ int moe_ffn_bwd(const void* dy, const void* x, const void* w1, const void* w3, c
                 void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * moe_ffn_recompute -- the first-layer outputs alone: A[s] = x[t] w1[e] and
+ * B[s] = x[t] w3[e] (non-gated: A alone), bit-identical to what moe_ffn_fwd
+ * writes. It serves a full-recompute checkpoint policy (Section 5.2 carried
+ * one step further): the forward keeps only the routing decision and the
+ * dispatch maps, and the backward recomputes A and B with this call before
+ * moe_ffn_bwd, for 2*T*k*d*f (non-gated: T*k*d*f) extra multiply-adds.
+ * In:  x, w1, w3, offsets, expert_token_indices as moe_ffn_fwd.
+ * Out: A, B [T*k, f]. No workspace.
+ */
+int moe_ffn_recompute(const void* x, const void* w1, const void* w3,
+                      const int32_t* offsets, const int32_t* expert_token_indices,
+                      int64_t T, int d, int f, int E, int k, unsigned flags,
+                      void* A, void* B, hipStream_t stream);
+
+/*
  * moe_ffn_fwd_combine -- moe_ffn_fwd followed by moe_combine(O, gates,
  * token_index_map) without the [T*k, d] expert-output buffer: the second GEMM
  * runs one column strip of O at a time (512 columns) into the workspace and

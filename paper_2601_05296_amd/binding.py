@@ -32,7 +32,8 @@ ACT_FLAG = {"swiglu": 0, "silu": MOE_ACT_SILU, "relu": MOE_ACT_RELU}
 # Every symbol declared in include/moeblaze.h.
 EXPORTS = ("moe_strerror", "moe_last_error", "moe_route", "moe_build_index_workspace_size",
            "moe_build_index", "moe_ffn_fwd_workspace_size", "moe_ffn_fwd", "moe_combine", "moe_ffn_bwd_workspace_size",
-           "moe_ffn_bwd", "moe_ffn_fwd_combine_workspace_size", "moe_ffn_fwd_combine",
+           "moe_ffn_bwd", "moe_ffn_recompute", "moe_ffn_fwd_combine_workspace_size",
+           "moe_ffn_fwd_combine",
            "moe_ffn_bwd_combine_workspace_size", "moe_ffn_bwd_combine",
            "moe_route_bwd_workspace_size", "moe_route_bwd", "moe_probe_enable",
            "moe_probe_disable", "moe_probe_count", "moe_probe_get")
@@ -73,6 +74,7 @@ def load_library(path: str = LIB):
         "moe_combine": (I, [P, P, P, I64, I, I, U, P, P]),
         "moe_ffn_bwd_workspace_size": (SZ, [I64, I, I, I, I, U]),
         "moe_ffn_bwd": (I, [P] * 11 + [I64, I, I, I, I, U] + [P] * 6 + [SZ, P]),
+        "moe_ffn_recompute": (I, [P] * 5 + [I64, I, I, I, I, U, P, P, P]),
         "moe_ffn_fwd_combine_workspace_size": (SZ, [I64, I, I, I, I, U]),
         "moe_ffn_fwd_combine": (I, [P] * 8 + [I64, I, I, I, I, U] + [P] * 4 + [SZ, P]),
         "moe_ffn_bwd_combine_workspace_size": (SZ, [I64, I, I, I, I, U]),
@@ -150,6 +152,13 @@ def moe_ffn_fwd(x, w1, w3, w2, offsets, expert_token_indices, T, d, f, E, k, fla
                                       _ptr(expert_token_indices), T, d, f, E, k, flags, _ptr(A),
                                       _ptr(B), _ptr(O), _ptr(workspace), workspace_bytes,
                                       _stream(stream)))
+
+
+def moe_ffn_recompute(x, w1, w3, offsets, expert_token_indices, T, d, f, E, k, flags, A, B,
+                      stream=None):
+    _check(load_library().moe_ffn_recompute(_ptr(x), _ptr(w1), _ptr(w3), _ptr(offsets),
+                                            _ptr(expert_token_indices), T, d, f, E, k, flags,
+                                            _ptr(A), _ptr(B), _stream(stream)))
 
 
 def moe_ffn_fwd_combine_workspace_size(T, d, f, E, k, flags) -> int:

@@ -251,6 +251,31 @@ int moe_ffn_fwd(const void* x, const void* w1, const void* w3, const void* w2,
                         workspace_bytes, stream);
 }
 
+int moe_ffn_recompute(const void* x, const void* w1, const void* w3,
+                      const int32_t* offsets, const int32_t* expert_token_indices, int64_t T,
+                      int d, int f, int E, int k, unsigned flags, void* A, void* B,
+                      hipStream_t stream) {
+    const char* fn = "moe_ffn_recompute";
+    int r;
+    if ((r = check_common(fn, T, E, k, flags)) || (r = check_dim(fn, "d", d)) ||
+        (r = check_dim(fn, "f", f)))
+        return r;
+    if (flags & (MOE_RENORM | MOE_ACCUMULATE))
+        return fail(MOE_ERR_INVALID_ARG, "%s: only MOE_F32 / MOE_BF16 and an activation flag are valid", fn);
+    const int act = act_of(flags);
+    if (act < 0) return fail(MOE_ERR_INVALID_ARG, "%s: MOE_ACT_SILU and MOE_ACT_RELU both set", fn);
+    if (T == 0) return MOE_OK;
+    REQUIRE_PTR(x); REQUIRE_PTR(w1); REQUIRE_PTR(offsets); REQUIRE_PTR(expert_token_indices);
+    REQUIRE_PTR(A);
+    if (act == 0) { REQUIRE_PTR(w3); REQUIRE_PTR(B); }
+    else { OPT_PTR(w3); OPT_PTR(B); }
+    moe::FfnArgs a{};
+    a.x = x; a.w1 = w1; a.w3 = w3; a.offsets = offsets; a.eti = expert_token_indices;
+    a.A = A; a.B = B; a.T = T; a.d = d; a.f = f; a.E = E; a.k = k; a.act = act;
+    moe::probe::begin(stream);
+    return hip_status(fn, moe::ffn_first(a, flags & MOE_F32, stream));
+}
+
 size_t moe_ffn_fwd_combine_workspace_size(int64_t T, int d, int f, int E, int k, unsigned flags) {
     if (T <= 0 || d < 1 || f < 1 || E < 1 || k < 1) return 0;
     return moe::ffn_fwd_workspace(T, d, f, E, k, flags & MOE_F32, true);

@@ -78,7 +78,8 @@ __device__ __forceinline__ void store8_bf16(bf16_t* p, const float (&v)[8]) { st
 
 // G1: A = x[eti] W1[e], B = x[eti] W3[e]; also H = SiLU(A) * B (from the
 // bf16-rounded A and B, exactly as the backward recomputes it). Non-gated:
-// A = x[eti] W1[e] and H = act(A).
+// A = x[eti] W1[e] and H = act(A). H == NULL: A and B only (the backward's
+// recompute under the full-recompute policy).
 template <int ACT>
 __global__ void __launch_bounds__(CD::THREADS)
 g1_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w1,
@@ -132,7 +133,7 @@ g1_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w1,
                 }
                 store8_bf16(A + s * f + n, a);
                 if constexpr (ACT == ACT_SWIGLU) store8_bf16(B + s * f + n, b);
-                store8_bf16(H + s * f + n, h);
+                if (H) store8_bf16(H + s * f + n, h);
             }
         }
     }
@@ -695,7 +696,35 @@ hipError_t ffn_fwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
     return hipGetLastError();
 }
 
+template <int ACT>
+hipError_t ffn_first_act(const FfnArgs& a, bool f32, hipStream_t st) {
+    const int64_t S = a.T * a.k;
+    if (f32) {
+        hipLaunchKernelGGL(f32_g1<ACT>, grid1d(S * a.f, 256), dim3(256), 0, st,
+                           (const float*)a.x, (const float*)a.w1, (const float*)a.w3, a.offsets,
+                           a.eti, S, a.d, a.f, a.E, (float*)a.A, (float*)a.B);
+        probe::mark("f32_g1", st);
+        return hipGetLastError();
+    }
+    if (hipError_t e = set_lds_limits(); e != hipSuccess) return e;
+    using C1 = CFirst<ACT>;
+    hipLaunchKernelGGL(g1_kernel<ACT>, dim3(slot_grid(S, a.E, C1::BM, cdiv(a.f, C1::BN))),
+                       dim3(C1::THREADS), C1::LDS, st, (const bf16_t*)a.x, (const bf16_t*)a.w1,
+                       (const bf16_t*)a.w3, a.offsets, a.eti, a.d, a.f, a.E, (bf16_t*)a.A,
+                       (bf16_t*)a.B, (bf16_t*)nullptr);
+    probe::mark("g1_kernel", st);
+    return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t ffn_first(const FfnArgs& a, bool f32, hipStream_t st) {
+    switch (a.act) {
+    case ACT_SILU: return ffn_first_act<ACT_SILU>(a, f32, st);
+    case ACT_RELU: return ffn_first_act<ACT_RELU>(a, f32, st);
+    default: return ffn_first_act<ACT_SWIGLU>(a, f32, st);
+    }
+}
 
 hipError_t ffn_fwd(const FfnArgs& a, bool f32, hipStream_t st) {
     switch (a.act) {

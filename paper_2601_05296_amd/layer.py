@@ -10,6 +10,9 @@ Backward (Section 3.2):
   moe_ffn_bwd_combine (= moe_ffn_bwd + the unit-weight combine that sums the
   token gradient) -> moe_route_bwd (router gradient, added into dx)
 ``separate=True`` runs the four separate calls instead (same results).
+``recompute=True`` is the full-recompute checkpoint policy: the forward keeps
+only the routing decision and the maps, and the backward first recomputes A
+and B with moe_ffn_recompute (bit-identical to the forward's).
 
 What the forward keeps for the backward (the "saved activations"): the first
 layer outputs A and B [S, f] (A alone for the non-gated SiLU / ReLU experts),
@@ -46,7 +49,7 @@ class Saved:
     eti: torch.Tensor
     tim: torch.Tensor
     slot_src: torch.Tensor
-    A: torch.Tensor
+    A: torch.Tensor | None      # None under the full-recompute policy
     B: torch.Tensor | None
 
     @property
@@ -62,16 +65,17 @@ class Saved:
 
 
 def saved_bytes_per_token(d: int, f: int, E: int, k: int, elem: int, T: int,
-                          act: str = "swiglu") -> float:
+                          act: str = "swiglu", recompute: bool = False) -> float:
     """Closed form of Saved.nbytes() / T: A and B (2 k f elem; A alone, k f elem,
-    for a non-gated expert), ids, gates, token_index_map, expert_token_indices
-    and slot_src (5 x 4k), logits (4E), counts and offsets (4(2E+1) per layer)."""
-    n_first = 2 if act == "swiglu" else 1
+    for a non-gated expert; none under full recompute), ids, gates,
+    token_index_map, expert_token_indices and slot_src (5 x 4k), logits (4E),
+    counts and offsets (4(2E+1) per layer)."""
+    n_first = 0 if recompute else (2 if act == "swiglu" else 1)
     return n_first * k * f * elem + 20.0 * k + 4.0 * E + 4.0 * (2 * E + 1) / T
 
 
 def forward(x, w_gate, bias, w1, w3, w2, k: int, renorm: bool, stream=None, keep_O=False,
-            act: str = "swiglu", separate: bool = False):
+            act: str = "swiglu", separate: bool = False, recompute: bool = False):
     """Returns (y, saved[, O]). ``act`` picks the expert: "swiglu" (gated, w3
     used) or the non-gated "silu" / "relu" (w3 ignored, may be None).
     ``keep_O`` (returns the expert outputs) implies ``separate``."""
@@ -104,6 +108,8 @@ def forward(x, w_gate, bias, w1, w3, w2, k: int, renorm: bool, stream=None, keep
     saved = Saved(T, d, f, E, k, flags, act, renorm, ids, gates, logits, counts, offsets, eti,
                   tim, slot_src, A, Bm)
     w3g = w3 if gated else None
+    if recompute:   # A and B live only for this call
+        saved.A = saved.B = None
     if not (separate or keep_O):
         wsb = B.moe_ffn_fwd_combine_workspace_size(T, d, f, E, k, fflags)
         ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
@@ -134,6 +140,11 @@ def backward(saved: Saved, dy, x, w_gate, w1, w3, w2, stream=None, keep=False,
     f32 = dict(dtype=torch.float32, device=dev)
     dw1 = torch.empty((E, d, f), **f32)
     gated = s.act == "swiglu"
+    if s.A is None:   # full-recompute policy: the first layer again
+        s.A = torch.empty((T * k, f), dtype=dy.dtype, device=dev)
+        s.B = torch.empty((T * k, f), dtype=dy.dtype, device=dev) if gated else None
+        B.moe_ffn_recompute(x, w1, w3 if gated else None, s.offsets, s.eti, T, d, f, E, k,
+                            s.ffn_flags, s.A, s.B, stream)
     dw3 = torch.empty((E, d, f), **f32) if gated else None
     dw2 = torch.empty((E, f, d), **f32)
     d_gates = torch.empty((T, k), **f32)

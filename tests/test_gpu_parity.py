@@ -473,6 +473,30 @@ def test_layer_end_to_end_tiny_f32():
         assert_close(n, host(g[n]), bw_r[n], "f32")
 
 
+@pytest.mark.parametrize("act", ["swiglu", "silu"])
+def test_layer_recompute_policy_bit_identical(act):
+    """Full-recompute policy (moe_ffn_recompute in the backward) against the
+    default policy that saves A and B: identical outputs and gradients, and
+    only the routing decision and maps saved."""
+    cfg = synth.MoEConfig("rc", T=1500, d=256, f=384, E=16, k=4, dtype="bf16", renorm=True,
+                          act=act)
+    inp = synth.make_inputs(cfg)
+    st = inp.store
+    x, wg, w1, w2, dy = (dev(st[n]) for n in ("x", "w_gate", "w1", "w2", "dy"))
+    w3 = dev(st["w3"]) if act == "swiglu" else None
+    outs = []
+    for rc in (False, True):
+        y, saved = layer.forward(x, wg, None, w1, w3, w2, cfg.k, cfg.renorm, act=act, recompute=rc)
+        assert (saved.A is None) == rc
+        assert saved.nbytes() == pytest.approx(layer.saved_bytes_per_token(
+            cfg.d, cfg.f, cfg.E, cfg.k, 2, cfg.T, act, recompute=rc) * cfg.T)
+        g = layer.backward(saved, dy, x, wg, w1, w3, w2)
+        torch.cuda.synchronize()
+        outs.append([y] + [g[n] for n in ("dx", "dw1", "dw2", "dw_gate", "d_gates")])
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+
+
 def test_layer_deterministic_bf16():
     cfg = synth.MoEConfig("det", T=2000, d=256, f=256, E=16, k=4, dtype="bf16", renorm=True)
     inp = synth.make_inputs(cfg)
