@@ -141,14 +141,16 @@ def read_traffic(workload, kernel):
     return round((f_kib * float(vals["fetch_factor"]) + w_kib * float(vals["write_factor"])) * 1024.0)
 
 
-def kernel_model(name, cfg, elem):
-    """Algorithmic work of one launch: (amount, unit, bound)."""
+def kernel_model(name, cfg, elem, recompute=False):
+    """Algorithmic work of one kernel over one whole step (all its launches:
+    the strips of the second GEMM, of the dX GEMM and of the combine, both
+    combine passes, the recomputed first GEMM): (amount, unit, bound)."""
     T, d, f, E, k = cfg.T, cfg.d, cfg.f, cfg.E, cfg.k
     S = T * k
     g = 2.0 * S * d * f  # flops of one [S x d] x [d x f] product
     nb = 2 if cfg.act == "swiglu" else 1   # right operands of g1, g5, g6
-    flops = {"g1_kernel": nb * g, "g2_kernel": g, "g3_kernel": g, "g4_kernel": g,
-             "g5_kernel": nb * g, "g6_kernel": nb * g}
+    flops = {"g1_kernel": nb * g * (2 if recompute else 1), "g2_kernel": g, "g3_kernel": g,
+             "g4_kernel": g, "g5_kernel": nb * g, "g6_kernel": nb * g}
     if name in flops:
         return flops[name], "TFLOP/s", "mfma"
     nparts = (f // 128) * 2
@@ -157,7 +159,7 @@ def kernel_model(name, cfg, elem):
         "tile_hist": S * 4,
         "tile_scan": 0,
         "tile_rank": S * 4 + 3 * S * 4,
-        "combine": S * d * elem + T * d * elem + T * k * 8,
+        "combine": 2 * (S * d * elem + T * d * elem + T * k * 8),   # forward and backward
         "dgate_reduce": S * nparts * 4 + S * 8,
         "rb_dlogits": T * E * 4 * 2 + T * k * 12,
         "rb_dx": T * E * 4 + E * d * elem + 2 * T * d * elem,
@@ -535,20 +537,26 @@ def main():
     kernels = {}
     for name, lst in kern.items():
         avg = float(np.mean(lst))
-        amount, unit, bound = kernel_model(name, cfg, elem)
-        rate = amount / (avg * 1e-3) / (1e12 if unit == "TFLOP/s" else 1e9) if amount else None
+        per_step_ms = float(np.sum(lst)) / args.steps
+        launches = len(lst) / args.steps
+        amount, unit, bound = kernel_model(name, cfg, elem, args.recompute)
+        # work of all the step's launches over their total time = the
+        # per-launch work over the average launch
+        rate = amount / (per_step_ms * 1e-3) / (1e12 if unit == "TFLOP/s" else 1e9) if amount else None
         peak_ = PEAK_BF16_TFLOPS if unit == "TFLOP/s" else PEAK_HBM_GBS
-        kernels[name] = {"avg_ms": round(avg, 4), "launches_per_step": len(lst) / args.steps,
-                         "ms_per_step": round(avg * len(lst) / args.steps, 4),
+        kernels[name] = {"avg_ms": round(avg, 4), "launches_per_step": launches,
+                         "ms_per_step": round(per_step_ms, 4),
+                         "per_launch": amount / launches,
                          "bound": bound, "achieved": None if rate is None else round(rate, 1),
                          "unit": unit, "frac": None if rate is None else round(rate / peak_, 4)}
     dom = max(kernels, key=lambda n: kernels[n]["ms_per_step"])
     kd = kernels[dom]
-    amount, unit, bound = kernel_model(dom, cfg, elem)
+    unit, bound = kd["unit"], kd["bound"]
     roofline = {"bound": bound, "achieved": kd["achieved"], "unit": unit,
                 "peak": PEAK_BF16_TFLOPS if unit == "TFLOP/s" else PEAK_HBM_GBS,
                 "frac": kd["frac"], "traffic": read_traffic(cfg.name, dom), "kernel": dom,
-                "per_launch": amount, "avg_ms": kd["avg_ms"]}
+                "per_launch": kd["per_launch"], "avg_ms": kd["avg_ms"],
+                "launches_per_step": kd["launches_per_step"]}
     gemm_ms = sum(kernels[n]["ms_per_step"] for n in kernels if n.startswith("g") and n[1].isdigit())
     # per-stage kernel time (ms per step); the router's two stages are the part
     # a sparse-to-sparse timing leaves out

@@ -6,7 +6,8 @@
 // matrix cores: each wave owns 16 tokens and all E experts, x fragments are
 // loaded straight from global memory (every x element is read exactly once)
 // and W_g is staged through LDS in 64-wide K slices shared by the 4 waves of a
-// workgroup. Softmax and the top-k selection run on the accumulators in
+// workgroup, double-buffered: the next slice's W_g and x are in flight while
+// the current one is multiplied. Softmax and the top-k selection run on the accumulators in
 // registers: the 4 lanes holding one token's logits find the k largest by k
 // rounds of (local best, two cross-lane exchanges), ties going to the lower
 // expert id.
@@ -50,26 +51,55 @@ route_bf16(const bf16_t* __restrict__ x, const bf16_t* __restrict__ wg,
 
     const int Ep = NE * 16;
     const int nchunks = Ep * 8;  // 16-byte chunks of one W_g slice
-    for (int k0 = 0; k0 < d; k0 += RT_BK) {
-        __syncthreads();
-        for (int c = tid; c < nchunks; c += RT_THREADS) {
+    constexpr int WPT = (NE * 16 * 8 + RT_THREADS - 1) / RT_THREADS;  // chunks per thread
+    // software pipeline: the W_g slice and the x fragments of slice s+1 are
+    // loaded into registers while slice s is multiplied; W_g alternates
+    // between two LDS buffers
+    uint4 wreg[WPT], xreg[2];
+    auto load_w = [&](int k0) {
+#pragma unroll
+        for (int i = 0; i < WPT; ++i) {
+            const int c = tid + i * RT_THREADS;
             const int r = c >> 3, cc = c & 7;
-            uint4 v = zero16();
-            if (r < E) v = ld16(wg + (int64_t)r * d + k0 + cc * 8);
-            st16(lds + kc64_off(r, cc), v);
+            wreg[i] = (c < nchunks && r < E) ? ld16(wg + (int64_t)r * d + k0 + cc * 8) : zero16();
         }
-        __syncthreads();
+    };
+    auto store_w = [&](char* buf) {
+#pragma unroll
+        for (int i = 0; i < WPT; ++i) {
+            const int c = tid + i * RT_THREADS;
+            if (c < nchunks) st16(buf + kc64_off(c >> 3, c & 7), wreg[i]);
+        }
+    };
+    auto load_x = [&](int k0) {
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) xreg[kk] = ld16(xrow + k0 + kk * 32 + grp * 8);
+    };
+    char* const buf1 = lds + Ep * 128;
+    load_w(0);
+    load_x(0);
+    store_w(lds);
+    __syncthreads();
+    for (int k0 = 0, s = 0; k0 < d; k0 += RT_BK, ++s) {
+        const char* cur = (s & 1) ? buf1 : lds;
+        const uint4 xc0 = xreg[0], xc1 = xreg[1];
+        const bool more = k0 + RT_BK < d;
+        if (more) {
+            load_w(k0 + RT_BK);
+            load_x(k0 + RT_BK);
+        }
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
-            const uint4 xv = ld16(xrow + k0 + kk * 32 + grp * 8);
-            const bf16x8 q = __builtin_bit_cast(bf16x8, xv);
+            const bf16x8 q = __builtin_bit_cast(bf16x8, kk ? xc1 : xc0);
 #pragma unroll
             for (int fe = 0; fe < NE; ++fe) {
                 const bf16x8 p = *reinterpret_cast<const bf16x8*>(
-                    lds + kc64_off(fe * 16 + col, kk * 4 + grp));
+                    cur + kc64_off(fe * 16 + col, kk * 4 + grp));
                 acc[fe] = mfma16x16x32(p, q, acc[fe]);
             }
         }
+        if (more) store_w((s & 1) ? lds : buf1);
+        __syncthreads();
     }
     // lane holds logits of token t0+col, experts fe*16 + 4*grp + r
     const int64_t t = t0 + col;
@@ -180,7 +210,7 @@ hipError_t launch_route_bf16(const void* x, const void* wg, const float* bias, i
                              int d, int E, int k, bool renorm, int32_t* ids, float* gates,
                              float* logits, hipStream_t st) {
     const dim3 grid((unsigned)((T + RT_TOK - 1) / RT_TOK));
-    const size_t lds = (size_t)NE * 16 * 128;
+    const size_t lds = (size_t)2 * NE * 16 * 128;   // two W_g slices
     hipLaunchKernelGGL(route_bf16<NE>, grid, dim3(RT_THREADS), lds, st,
                        static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(wg), bias, T,
                        d, E, k, (int)renorm, ids, gates, logits);
