@@ -18,15 +18,17 @@ namespace moe {
 namespace {
 
 constexpr int CMB_THREADS = 256;
-constexpr int KMAX = 16;
 
 // A workgroup handles TPB tokens (TPB = 256 / LPT) with LPT lanes per token;
 // lane c owns 16-byte column chunks c, c + LPT, ... of its token's ncols
 // columns. Source rows are src_ld elements apart and output rows out_ld, so
 // the kernel also combines one column strip of a wider matrix. The token's k
 // slot rows and weights are read once; all k source chunks of a lane are
-// loaded before the float32 sum, which runs in order j = 0..k-1.
-template <bool F32, int NC>
+// loaded before the float32 sum, which runs in order j = 0..k-1. KMAX >= k
+// sizes the per-lane arrays: the smallest bound that fits keeps the register
+// count, and with it the number of loads in flight per CU, where it belongs
+// (KMAX = 16 would hold 135 VGPRs and three waves per SIMD for any k).
+template <bool F32, int NC, int KMAX>
 __global__ void __launch_bounds__(CMB_THREADS)
 combine_kernel(const void* __restrict__ src_, int64_t src_ld, const float* __restrict__ w,
                const int32_t* __restrict__ tim, int64_t T, int ncols, int k, int accumulate,
@@ -109,11 +111,10 @@ combine_kernel(const void* __restrict__ src_, int64_t src_ld, const float* __res
     }
 }
 
-}  // namespace
-
-hipError_t combine_cols(const void* src, int64_t src_ld, const float* w, const int32_t* tim,
-                        int64_t T, int ncols, int k, bool f32, bool accumulate, void* out,
-                        int64_t out_ld, hipStream_t st) {
+template <int KMAX>
+void launch_combine(const void* src, int64_t src_ld, const float* w, const int32_t* tim,
+                    int64_t T, int ncols, int k, bool f32, bool accumulate, void* out,
+                    int64_t out_ld, hipStream_t st) {
     const int nchunk = ncols / (f32 ? 4 : 8);
     // lanes per token: the smallest power of two covering the row's chunks
     // (at most the whole workgroup; wider rows loop)
@@ -122,18 +123,31 @@ hipError_t combine_cols(const void* src, int64_t src_ld, const float* w, const i
     const int64_t tpb = CMB_THREADS >> lpt_log2;
     const dim3 grid((unsigned)((T + tpb - 1) / tpb));
     if (f32) {
-        hipLaunchKernelGGL((combine_kernel<true, 2>), grid, dim3(CMB_THREADS), 0, st, src, src_ld,
-                           w, tim, T, ncols, k, (int)accumulate, out, out_ld, lpt_log2);
+        hipLaunchKernelGGL((combine_kernel<true, 2, KMAX>), grid, dim3(CMB_THREADS), 0, st, src,
+                           src_ld, w, tim, T, ncols, k, (int)accumulate, out, out_ld, lpt_log2);
         probe::mark("combine_f32", st);
     } else if (nchunk <= CMB_THREADS) {
-        hipLaunchKernelGGL((combine_kernel<false, 1>), grid, dim3(CMB_THREADS), 0, st, src,
+        hipLaunchKernelGGL((combine_kernel<false, 1, KMAX>), grid, dim3(CMB_THREADS), 0, st, src,
                            src_ld, w, tim, T, ncols, k, (int)accumulate, out, out_ld, lpt_log2);
         probe::mark("combine", st);
     } else {
-        hipLaunchKernelGGL((combine_kernel<false, 2>), grid, dim3(CMB_THREADS), 0, st, src,
+        hipLaunchKernelGGL((combine_kernel<false, 2, KMAX>), grid, dim3(CMB_THREADS), 0, st, src,
                            src_ld, w, tim, T, ncols, k, (int)accumulate, out, out_ld, lpt_log2);
         probe::mark("combine", st);
     }
+}
+
+}  // namespace
+
+hipError_t combine_cols(const void* src, int64_t src_ld, const float* w, const int32_t* tim,
+                        int64_t T, int ncols, int k, bool f32, bool accumulate, void* out,
+                        int64_t out_ld, hipStream_t st) {
+    if (k <= 4)
+        launch_combine<4>(src, src_ld, w, tim, T, ncols, k, f32, accumulate, out, out_ld, st);
+    else if (k <= 8)
+        launch_combine<8>(src, src_ld, w, tim, T, ncols, k, f32, accumulate, out, out_ld, st);
+    else
+        launch_combine<16>(src, src_ld, w, tim, T, ncols, k, f32, accumulate, out, out_ld, st);
     return hipGetLastError();
 }
 

@@ -117,7 +117,11 @@ def test_route_parity(dtype, T, d, E, k, renorm, bias):
 @pytest.mark.parametrize("dtype,T,d,k,weighted,accumulate", [
     ("bf16", 1000, 256, 2, True, False), ("bf16", 333, 2048, 6, True, True),
     ("bf16", 257, 512, 8, False, False), ("f32", 1000, 256, 2, True, False),
-    ("f32", 100, 128, 16, False, True)])
+    ("f32", 100, 128, 16, False, True),
+    # per-token array bounds 4 / 8 / 16 (the kernel is sized by the smallest
+    # bound >= k): both sides of each edge, and bf16 rows wider than 256 chunks
+    ("bf16", 129, 256, 4, True, False), ("bf16", 200, 4096, 5, False, True),
+    ("bf16", 300, 1024, 12, True, True), ("f32", 150, 512, 3, True, False)])
 def test_combine_parity(dtype, T, d, k, weighted, accumulate):
     rng = np.random.default_rng(T + d + k)
     E = max(k, 8)
