@@ -51,6 +51,18 @@ def parse():
                     help="write the per-kernel HBM traffic summary from two rocprofv3 --pmc "
                          "runs (FETCH_SIZE, WRITE_SIZE) of this script with --copy-calibration")
     ap.add_argument("--pmc-out", default=None)
+    ap.add_argument("--summarize-stats", metavar="KERNEL_STATS_CSV",
+                    help="write the short per-kernel timing summary of a rocprofv3 "
+                         "--kernel-trace --stats run of this script")
+    ap.add_argument("--summarize-counters", nargs=2, metavar=("TCP_CSV", "SQ_CSV"),
+                    help="write the per-kernel L1-to-L2 request and MFMA-busy summary from two "
+                         "rocprofv3 --pmc runs of this script (TCP_TCC_READ_REQ_sum "
+                         "TCP_TCC_READ_REQ_LATENCY_sum TCP_TCC_WRITE_REQ_sum "
+                         "TCP_PENDING_STALL_CYCLES_sum, then SQ_VALU_MFMA_BUSY_CYCLES "
+                         "SQ_BUSY_CYCLES GRBM_GUI_ACTIVE)")
+    ap.add_argument("--profile-command", default="",
+                    help="the rocprofv3 command(s) the summarised files came from")
+    ap.add_argument("--summary-out", default=None)
     ap.add_argument("--sweep", action="store_true",
                     help="memory-capacity sweep: double T from the workload's T until out of "
                          "memory, for this path and for the materialised-permutation baseline")
@@ -115,6 +127,74 @@ def summarize_pmc(fetch_csv, write_csv, out, workload, cmd):
         if k == copy:
             short = "copy_calibration"
         lines.append("kernel %s %.1f %.1f" % (short, fetch[k], write.get(k, float("nan"))))
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("wrote", out)
+
+
+def summarize_stats(stats_csv, out, workload, cmd, profile_cmd):
+    """Per-kernel calls and durations from rocprofv3's kernel_stats.csv."""
+    import csv
+    from paper_2601_05296_amd import synth
+    cfg = synth.CONFIGS[workload]
+    rows = list(csv.DictReader(open(stats_csv)))
+    lines = ["# rocprofv3 kernel statistics, workload %s (T=%d d=%d f=%d E=%d k=%d, %s)"
+             % (workload, cfg.T, cfg.d, cfg.f, cfg.E, cfg.k, cfg.dtype),
+             "# profile: %s" % profile_cmd,
+             "# summary: python %s" % cmd,
+             "# kernel calls avg_us total_ms pct min_us max_us"]
+    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
+        lines.append("%-22s %4d %10.1f %9.3f %6.2f %9.1f %9.1f" % (
+            kernel_short_name(r["Name"])[:22], int(r["Calls"]), float(r["AverageNs"]) / 1e3,
+            float(r["TotalDurationNs"]) / 1e6, float(r["Percentage"]),
+            float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3))
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("wrote", out)
+
+
+N_CU, N_XCD, SIMD_PER_CU = 256, 8, 4
+
+
+def summarize_counters(tcp_csv, sq_csv, out, workload, cmd, profile_cmd):
+    """Per-kernel means per launch of the L1-to-L2 request counters and of
+    the MFMA busy cycles. GRBM_GUI_ACTIVE is summed over the XCDs, so one
+    XCD's cycles are GUI/8; the mean number of read requests in flight per CU
+    is the latency sum (request-cycles) over CU-cycles."""
+    import csv
+    acc, launches = {}, {}
+    for path in (tcp_csv, sq_csv):
+        seen = {}
+        for r in csv.DictReader(open(path)):
+            name = kernel_short_name(r["Kernel_Name"])
+            a = acc.setdefault(name, {})
+            a[r["Counter_Name"]] = a.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+            seen.setdefault(name, set()).add(r["Dispatch_Id"])
+        for name, ids in seen.items():
+            launches[name] = max(launches.get(name, 0), len(ids))
+    lines = ["# L1-to-L2 requests and MFMA busy time per launch, workload %s" % workload,
+             "# profile: %s" % profile_cmd,
+             "# summary: python %s" % cmd,
+             "# cycles = GRBM_GUI_ACTIVE / %d (one XCD); %d CUs, %d SIMDs per CU" % (N_XCD, N_CU, SIMD_PER_CU),
+             "# rd_req: TCP_TCC_READ_REQ; lat: mean read latency in cycles; inflight: mean read "
+             "requests in flight per CU; pend: share of CU-cycles the L1 stalls on pending "
+             "requests; wr_req: TCP_TCC_WRITE_REQ; mfma: MFMA busy share of SIMD-cycles",
+             "# kernel launches cycles rd_req lat inflight pend wr_req mfma"]
+    def per(a, key, n):
+        return a.get(key, 0.0) / n
+    order = sorted(acc, key=lambda k: -acc[k].get("GRBM_GUI_ACTIVE", 0.0))
+    for name in order:
+        a, n = acc[name], launches[name]
+        cyc = per(a, "GRBM_GUI_ACTIVE", n) / N_XCD
+        if cyc <= 0:
+            continue
+        rq = per(a, "TCP_TCC_READ_REQ_sum", n)
+        lat_sum = per(a, "TCP_TCC_READ_REQ_LATENCY_sum", n)
+        lines.append("%-20s %4d %9.0f %10.3g %6.0f %8.1f %6.2f %10.3g %6.2f" % (
+            name, n, cyc, rq, lat_sum / rq if rq else float("nan"), lat_sum / (N_CU * cyc),
+            per(a, "TCP_PENDING_STALL_CYCLES_sum", n) / (N_CU * cyc),
+            per(a, "TCP_TCC_WRITE_REQ_sum", n),
+            per(a, "SQ_VALU_MFMA_BUSY_CYCLES", n) / (N_CU * SIMD_PER_CU * cyc)))
     with open(out, "w") as fh:
         fh.write("\n".join(lines) + "\n")
     print("wrote", out)
@@ -451,6 +531,16 @@ def main():
         summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1],
                       args.pmc_out or traffic_path(args.workload), args.workload,
                       " ".join(sys.argv))
+        return
+    if args.summarize_stats:
+        summarize_stats(args.summarize_stats,
+                        args.summary_out or os.path.join(ROOT, "profiles", "kernel_stats_%s.txt" % args.workload),
+                        args.workload, " ".join(sys.argv), args.profile_command)
+        return
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters[0], args.summarize_counters[1],
+                           args.summary_out or os.path.join(ROOT, "profiles", "l2_requests_mfma_%s.txt" % args.workload),
+                           args.workload, " ".join(sys.argv), args.profile_command)
         return
     if args.table1:
         print(json.dumps({"table1": table1_sweep(args)}), flush=True)
