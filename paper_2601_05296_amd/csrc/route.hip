@@ -3,17 +3,17 @@
 //
 // bf16 path: the router product logits[T,E] = x W_g^T is a skinny GEMM
 // (E <= 256 columns) whose cost is reading x once from HBM, so it runs on the
-// matrix cores: each wave owns 16 tokens and all E experts, x fragments are
-// loaded straight from global memory (every x element is read exactly once)
-// and W_g is staged through LDS in 64-wide K slices shared by the 4 waves of a
-// workgroup, double-buffered: the next slice's W_g and x are in flight while
-// the current one is multiplied. Softmax and the top-k selection run on the accumulators in
-// registers: the 4 lanes holding one token's logits find the k largest by k
+// matrix cores: each wave owns 16 tokens and all E experts. The 64 x rows of
+// a workgroup (every x element is read exactly once) and W_g come through an
+// LDS ring of 64-wide K slices filled by direct-to-LDS copies, three slices
+// ahead of the one being multiplied. Softmax and the top-k selection run on
+// the accumulators in registers: the 4 lanes holding one token's logits find the k largest by k
 // rounds of (local best, two cross-lane exchanges), ties going to the lower
 // expert id.
 //
 // f32 path (debug mode): one thread per token, float32 FMA.
 #include "common.hpp"
+#include "gemm.hpp"
 #include "launch.hpp"
 #include "probe.hpp"
 
@@ -23,6 +23,9 @@ namespace {
 constexpr int RT_THREADS = 256;
 constexpr int RT_TOK = 64;   // tokens per workgroup (16 per wave)
 constexpr int RT_BK = 64;    // K slice staged in LDS
+// LDS ring depth (slices): four, three for E > 128 (a stage is then 40 KB)
+template <int NE> constexpr int rt_nst() { return NE >= 16 ? 3 : 4; }
+template <int NE> constexpr int rt_lds() { return rt_nst<NE>() * (RT_TOK + NE * 16) * 128; }
 
 // LDS offset (bytes) of 16-byte chunk `c` (0..7) of row `r` in a row-major
 // [rows][64] bf16 tile; the chunk index is XOR-swizzled with the row so that
@@ -41,65 +44,75 @@ route_bf16(const bf16_t* __restrict__ x, const bf16_t* __restrict__ wg,
     const int grp = lane >> 4;    // which 4-column group of each 16-expert fragment
     const int col = lane & 15;    // token within the wave's 16
     const int64_t t0 = (int64_t)blockIdx.x * RT_TOK + wv * 16;
-    int64_t trow = t0 + col;
-    if (trow >= T) trow = T - 1;  // clamp: valid memory, result discarded
-    const bf16_t* xrow = x + trow * d;
 
     f32x4 acc[NE];
 #pragma unroll
     for (int i = 0; i < NE; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    const int Ep = NE * 16;
-    const int nchunks = Ep * 8;  // 16-byte chunks of one W_g slice
-    constexpr int WPT = (NE * 16 * 8 + RT_THREADS - 1) / RT_THREADS;  // chunks per thread
-    // software pipeline: the W_g slice and the x fragments of slice s+1 are
-    // loaded into registers while slice s is multiplied; W_g alternates
-    // between two LDS buffers
-    uint4 wreg[WPT], xreg[2];
-    auto load_w = [&](int k0) {
+    // LDS ring of RT_NST stages; a stage holds the 64-wide K slice of the
+    // workgroup's 64 x rows and of all Ep W_g rows, 128-byte rows swizzled by
+    // kc64_off. Both arrive by direct-to-LDS copies of 1 KB (8 rows, lane l
+    // fetching the 16-byte chunk that lands at byte 16l), so every request is
+    // a whole 128-byte line and the copies of the next RT_NST-1 slices are in
+    // flight while a slice is multiplied. Rows past T or E repeat the last
+    // valid row: their products are never read.
+    constexpr int RT_NST = rt_nst<NE>();
+    constexpr int Ep = NE * 16;
+    constexpr int XB = RT_TOK * 128, STAGE = XB + Ep * 128;
+    constexpr int NCOPY = STAGE / 1024, PER = NCOPY / 4;   // 1 KB copies per slice, per wave
+    static_assert(NCOPY % 4 == 0, "copies split evenly over the four waves");
+    const int nk = d / RT_BK;
+    const uint32_t lds_base = lds_offset(lds);
+    const int wvu = wave_id();                        // wave index, uniform (SGPR)
+    const int64_t xrow0 = (int64_t)blockIdx.x * RT_TOK;
+    auto issue = [&](int s) {
+        const uint32_t dst = lds_base + (s % RT_NST) * STAGE;
+        const int k0 = s * RT_BK;
 #pragma unroll
-        for (int i = 0; i < WPT; ++i) {
-            const int c = tid + i * RT_THREADS;
-            const int r = c >> 3, cc = c & 7;
-            wreg[i] = (c < nchunks && r < E) ? ld16(wg + (int64_t)r * d + k0 + cc * 8) : zero16();
+        for (int c = 0; c < PER; ++c) {
+            const int q = wvu + 4 * c;                // copy index within the stage
+            const int r = q * 8 + (lane >> 3);        // stage row (x rows first, then W_g)
+            const int ch = (lane & 7) ^ (r & 7);      // logical chunk at this lane's slot
+            const bf16_t* src;
+            if (r < RT_TOK) {
+                int64_t t = xrow0 + r;
+                t = t < T ? t : T - 1;
+                src = x + t * d + k0 + ch * 8;
+            } else {
+                int e = r - RT_TOK;
+                e = e < E ? e : E - 1;
+                src = wg + (int64_t)e * d + k0 + ch * 8;
+            }
+            dma16(src, dst + q * 1024);
         }
     };
-    auto store_w = [&](char* buf) {
 #pragma unroll
-        for (int i = 0; i < WPT; ++i) {
-            const int c = tid + i * RT_THREADS;
-            if (c < nchunks) st16(buf + kc64_off(c >> 3, c & 7), wreg[i]);
-        }
-    };
-    auto load_x = [&](int k0) {
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk) xreg[kk] = ld16(xrow + k0 + kk * 32 + grp * 8);
-    };
-    char* const buf1 = lds + Ep * 128;
-    load_w(0);
-    load_x(0);
-    store_w(lds);
-    __syncthreads();
-    for (int k0 = 0, s = 0; k0 < d; k0 += RT_BK, ++s) {
-        const char* cur = (s & 1) ? buf1 : lds;
-        const uint4 xc0 = xreg[0], xc1 = xreg[1];
-        const bool more = k0 + RT_BK < d;
-        if (more) {
-            load_w(k0 + RT_BK);
-            load_x(k0 + RT_BK);
-        }
+    for (int s = 0; s < RT_NST - 1; ++s)
+        if (s < nk) issue(s);
+    if (nk >= RT_NST - 1) wait_vmcnt<PER * (RT_NST - 2)>();
+    else wait_vmcnt<0>();
+    barrier_only();
+    for (int s = 0; s < nk; ++s) {
+        if (s + RT_NST - 1 < nk) issue(s + RT_NST - 1);
+        const char* xt = lds + (s % RT_NST) * STAGE;
+        const char* wt = xt + XB;
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
-            const bf16x8 q = __builtin_bit_cast(bf16x8, kk ? xc1 : xc0);
+            const bf16x8 q = *reinterpret_cast<const bf16x8*>(
+                xt + kc64_off(wv * 16 + col, kk * 4 + grp));
 #pragma unroll
             for (int fe = 0; fe < NE; ++fe) {
                 const bf16x8 p = *reinterpret_cast<const bf16x8*>(
-                    cur + kc64_off(fe * 16 + col, kk * 4 + grp));
+                    wt + kc64_off(fe * 16 + col, kk * 4 + grp));
                 acc[fe] = mfma16x16x32(p, q, acc[fe]);
             }
         }
-        if (more) store_w((s & 1) ? lds : buf1);
-        __syncthreads();
+        if (s + 1 < nk) {
+            // slice s+1 has landed once only the copies of later slices remain
+            if (s + RT_NST - 1 < nk) wait_vmcnt<PER * (RT_NST - 2)>();
+            else wait_vmcnt<0>();
+            lds_barrier();
+        }
     }
     // lane holds logits of token t0+col, experts fe*16 + 4*grp + r
     const int64_t t = t0 + col;
@@ -209,9 +222,12 @@ template <int NE>
 hipError_t launch_route_bf16(const void* x, const void* wg, const float* bias, int64_t T,
                              int d, int E, int k, bool renorm, int32_t* ids, float* gates,
                              float* logits, hipStream_t st) {
+    static const hipError_t attr = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(route_bf16<NE>), hipFuncAttributeMaxDynamicSharedMemorySize,
+        rt_lds<NE>());
+    if (attr != hipSuccess) return attr;
     const dim3 grid((unsigned)((T + RT_TOK - 1) / RT_TOK));
-    const size_t lds = (size_t)2 * NE * 16 * 128;   // two W_g slices
-    hipLaunchKernelGGL(route_bf16<NE>, grid, dim3(RT_THREADS), lds, st,
+    hipLaunchKernelGGL(route_bf16<NE>, grid, dim3(RT_THREADS), rt_lds<NE>(), st,
                        static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(wg), bias, T,
                        d, E, k, (int)renorm, ids, gates, logits);
     probe::mark("route_bf16", st);
@@ -231,7 +247,6 @@ hipError_t route(const void* x, const void* wg, const float* bias, int64_t T, in
         probe::mark("route_f32", st);
         return hipGetLastError();
     }
-    if (E <= 16) return launch_route_bf16<1>(x, wg, bias, T, d, E, k, renorm, ids, gates, logits, st);
     if (E <= 32) return launch_route_bf16<2>(x, wg, bias, T, d, E, k, renorm, ids, gates, logits, st);
     if (E <= 64) return launch_route_bf16<4>(x, wg, bias, T, d, E, k, renorm, ids, gates, logits, st);
     if (E <= 128) return launch_route_bf16<8>(x, wg, bias, T, d, E, k, renorm, ids, gates, logits, st);
