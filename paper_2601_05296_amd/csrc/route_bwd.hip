@@ -206,6 +206,23 @@ rb_dx_mfma(const bf16_t* __restrict__ hl, const bf16_t* __restrict__ wg, int64_t
     Acc<C> acc;
     gemm_mainloop<C>(la, lb, nl, 2 * Ep / GBK, GBK, lds, acc, rows, d - n0);
     WaveCoord<C> wc;
+    // The lane's dx values are all loaded before the first store: loads placed
+    // after a store to the same rows would each wait for the previous one.
+    // (rows >= 1 and d >= 8 hold for every launched tile.)
+    uint4 old[C::FM][C::FN][2];
+    if (accumulate) {
+#pragma unroll
+        for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+            for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+                for (int p = 0; p < 2; ++p) {
+                    // clamped into the tile's valid rows and columns, so that
+                    // the loads need no branch (values off the tile are unused)
+                    const int m = min(wc.row(i), rows - 1), n = min(n0 + wc.col8(j, p), d - 8);
+                    old[i][j][p] = ld16(dx + (m0 + m) * d + n);
+                }
+    }
 #pragma unroll
     for (int i = 0; i < C::FM; ++i) {
         const int m = wc.row(i);
@@ -221,7 +238,7 @@ rb_dx_mfma(const bf16_t* __restrict__ hl, const bf16_t* __restrict__ wg, int64_t
                 if (n >= d) continue;
                 if (accumulate) {
                     float o[8];
-                    unpack8(ld16(row + n), o);
+                    unpack8(old[i][j][p], o);
 #pragma unroll
                     for (int r = 0; r < 8; ++r) v[p][r] += o[r];
                 }
