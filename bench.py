@@ -552,8 +552,9 @@ def main():
         print(json.dumps({"sweep": res}), flush=True)
         return
     if args.gpus != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
-              "(see the sharding note in DESIGN.md); run with --gpus 1", file=sys.stderr)
+        print("bench.py runs on one GPU only: the MoE layer here has no multi-GPU path "
+              "(expert or data parallelism is not implemented); run with --gpus 1",
+              file=sys.stderr)
         sys.exit(2)
     import torch
     from paper_2601_05296_amd import binding as B
