@@ -38,6 +38,9 @@ def parse():
     ap.add_argument("--workload", default="mid_e64k6")
     ap.add_argument("--act", choices=("swiglu", "silu", "relu"), default=None,
                     help="expert activation (default: the workload's own)")
+    ap.add_argument("--h-on-load", action="store_true",
+                    help="MOE_H_ON_LOAD: no h buffer between the GEMMs; the second GEMM forms h "
+                         "from A and B as it loads them")
     ap.add_argument("--recompute", action="store_true",
                     help="full-recompute checkpoint policy: save only the routing decision and "
                          "maps, recompute the first layer in the backward")
@@ -229,7 +232,8 @@ def kernel_model(name, cfg, elem, recompute=False):
     S = T * k
     g = 2.0 * S * d * f  # flops of one [S x d] x [d x f] product
     nb = 2 if cfg.act == "swiglu" else 1   # right operands of g1, g5, g6
-    flops = {"g1_kernel": nb * g * (2 if recompute else 1), "g2_kernel": g, "g3_kernel": g,
+    flops = {"g1_kernel": nb * g * (2 if recompute else 1), "g2_kernel": g, "g2h_kernel": g,
+             "g3_kernel": g,
              "g4_kernel": g, "g5_kernel": nb * g, "g6_kernel": nb * g}
     if name in flops:
         return flops[name], "TFLOP/s", "mfma"
@@ -581,7 +585,7 @@ def main():
 
     def step():
         y, saved = layer.forward(x, wg, bias, w1, w3, w2, k, cfg.renorm, act=cfg.act,
-                                 recompute=args.recompute)
+                                 recompute=args.recompute, h_on_load=args.h_on_load)
         g = layer.backward(saved, dy, x, wg, w1, w3, w2)
         return y, saved, g
 
@@ -594,7 +598,7 @@ def main():
     torch.cuda.reset_peak_memory_stats(dev)
     base = torch.cuda.memory_allocated(dev)
     y, saved = layer.forward(x, wg, bias, w1, w3, w2, k, cfg.renorm, act=cfg.act,
-                             recompute=args.recompute)
+                             recompute=args.recompute, h_on_load=args.h_on_load)
     torch.cuda.synchronize()
     fwd_peak = torch.cuda.max_memory_allocated(dev) - base
     saved_bytes = saved.nbytes()   # before the backward (which may recompute A, B into it)
@@ -651,7 +655,7 @@ def main():
     gemm_ms = sum(kernels[n]["ms_per_step"] for n in kernels if n.startswith("g") and n[1].isdigit())
     # per-stage kernel time (ms per step); the router's two stages are the part
     # a sparse-to-sparse timing leaves out
-    stage_of = {"route": ("route_",), "build": ("tile_",), "ffn_fwd": ("g1_", "g2_", "f32_g1", "f32_g2"),
+    stage_of = {"route": ("route_",), "build": ("tile_",), "ffn_fwd": ("g1_", "g2_", "g2h_", "f32_g1", "f32_g2"),
                 "combine": ("combine",), "ffn_bwd": ("g3_", "g4_", "g5_", "g6_", "dgate", "f32_g3",
                                                       "f32_g4", "f32_g5", "f32_g6"),
                 "route_bwd": ("rb_",)}
@@ -670,6 +674,7 @@ def main():
         "config": {"workload": cfg.name, "T": T, "d": d, "f": f, "E": E, "k": k,
                    "renorm": cfg.renorm, "zipf_s": cfg.zipf_s, "act": cfg.act,
                    "checkpoint": "recompute" if args.recompute else "A,B",
+                   "h_on_load": bool(args.h_on_load),
                    "parallelism": "none"},
         "peak_activation_bytes_per_token": round(peak / T, 1),
         "peak_activation_bytes_per_token_fwd_bwd": [round(fwd_peak / T, 1), round(bwd_peak / T, 1)],

@@ -32,8 +32,10 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
             return fail(MOE_ERR_INVALID_ARG, "%s: %s is not 16-byte aligned", fn, #p); \
     } while (0)
 
-const unsigned KNOWN_FLAGS = MOE_F32 | MOE_RENORM | MOE_ACCUMULATE | MOE_ACT_SILU | MOE_ACT_RELU;
+const unsigned KNOWN_FLAGS =
+    MOE_F32 | MOE_RENORM | MOE_ACCUMULATE | MOE_ACT_SILU | MOE_ACT_RELU | MOE_H_ON_LOAD;
 const unsigned ACT_FLAGS = MOE_ACT_SILU | MOE_ACT_RELU;
+const unsigned FFN_ONLY = ACT_FLAGS | MOE_H_ON_LOAD;   // meaningful to the FFN calls only
 
 // expert activation code of the FFN calls (0 SwiGLU, 1 SiLU, 2 ReLU), or -1
 int act_of(unsigned flags) {
@@ -82,7 +84,7 @@ int ffn_fwd_impl(const char* fn, bool combined, const void* x, const void* w1, c
         (r = check_dim(fn, "f", f)))
         return r;
     if (flags & (MOE_RENORM | MOE_ACCUMULATE))
-        return fail(MOE_ERR_INVALID_ARG, "%s: only MOE_F32 / MOE_BF16 and an activation flag are valid", fn);
+        return fail(MOE_ERR_INVALID_ARG, "%s: only MOE_F32 / MOE_BF16, an activation flag and MOE_H_ON_LOAD are valid", fn);
     const int act = act_of(flags);
     if (act < 0) return fail(MOE_ERR_INVALID_ARG, "%s: MOE_ACT_SILU and MOE_ACT_RELU both set", fn);
     if (T == 0) return MOE_OK;
@@ -97,7 +99,8 @@ int ffn_fwd_impl(const char* fn, bool combined, const void* x, const void* w1, c
     }
     if (act == 0) { REQUIRE_PTR(w3); REQUIRE_PTR(B); }
     else { OPT_PTR(w3); OPT_PTR(B); }
-    const size_t need = moe::ffn_fwd_workspace(T, d, f, E, k, flags & MOE_F32, combined);
+    const size_t need =
+        moe::ffn_fwd_workspace(T, d, f, E, k, flags & MOE_F32, combined, flags & MOE_H_ON_LOAD);
     if (need && (!workspace || workspace_bytes < need))
         return fail(MOE_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, workspace_bytes, need);
     OPT_PTR(workspace);
@@ -105,6 +108,7 @@ int ffn_fwd_impl(const char* fn, bool combined, const void* x, const void* w1, c
     a.x = x; a.w1 = w1; a.w3 = w3; a.w2 = w2; a.offsets = offsets; a.eti = expert_token_indices;
     a.A = A; a.B = B; a.T = T; a.d = d; a.f = f; a.E = E; a.k = k; a.ws = workspace;
     a.act = act;
+    a.h_on_load = flags & MOE_H_ON_LOAD;
     if (combined) { a.y = out; a.gates = gates; a.tim = token_index_map; }
     else a.O = out;
     moe::probe::begin(stream);
@@ -202,7 +206,7 @@ int moe_route(const void* x, const void* w_gate, const float* bias, int64_t T, i
     const char* fn = "moe_route";
     int r;
     if ((r = check_common(fn, T, E, k, flags)) || (r = check_dim(fn, "d", d))) return r;
-    if (flags & ACT_FLAGS) return fail(MOE_ERR_INVALID_ARG, "%s: activation flags apply to the FFN calls only", fn);
+    if (flags & FFN_ONLY) return fail(MOE_ERR_INVALID_ARG, "%s: activation and h-on-load flags apply to the FFN calls only", fn);
     if (flags & MOE_ACCUMULATE) return fail(MOE_ERR_INVALID_ARG, "%s: MOE_ACCUMULATE not valid here", fn);
     if (T == 0) return MOE_OK;
     REQUIRE_PTR(x); REQUIRE_PTR(w_gate); OPT_PTR(bias); REQUIRE_PTR(topk_ids); REQUIRE_PTR(gates);
@@ -239,7 +243,7 @@ int moe_build_index(const int32_t* topk_ids, int64_t T, int E, int k, int32_t* c
 
 size_t moe_ffn_fwd_workspace_size(int64_t T, int d, int f, int E, int k, unsigned flags) {
     if (T <= 0 || d < 1 || f < 1 || E < 1 || k < 1) return 0;
-    return moe::ffn_fwd_workspace(T, d, f, E, k, flags & MOE_F32, false);
+    return moe::ffn_fwd_workspace(T, d, f, E, k, flags & MOE_F32, false, flags & MOE_H_ON_LOAD);
 }
 
 int moe_ffn_fwd(const void* x, const void* w1, const void* w3, const void* w2,
@@ -261,7 +265,7 @@ int moe_ffn_recompute(const void* x, const void* w1, const void* w3,
         (r = check_dim(fn, "f", f)))
         return r;
     if (flags & (MOE_RENORM | MOE_ACCUMULATE))
-        return fail(MOE_ERR_INVALID_ARG, "%s: only MOE_F32 / MOE_BF16 and an activation flag are valid", fn);
+        return fail(MOE_ERR_INVALID_ARG, "%s: only MOE_F32 / MOE_BF16, an activation flag and MOE_H_ON_LOAD are valid", fn);
     const int act = act_of(flags);
     if (act < 0) return fail(MOE_ERR_INVALID_ARG, "%s: MOE_ACT_SILU and MOE_ACT_RELU both set", fn);
     if (T == 0) return MOE_OK;
@@ -278,7 +282,7 @@ int moe_ffn_recompute(const void* x, const void* w1, const void* w3,
 
 size_t moe_ffn_fwd_combine_workspace_size(int64_t T, int d, int f, int E, int k, unsigned flags) {
     if (T <= 0 || d < 1 || f < 1 || E < 1 || k < 1) return 0;
-    return moe::ffn_fwd_workspace(T, d, f, E, k, flags & MOE_F32, true);
+    return moe::ffn_fwd_workspace(T, d, f, E, k, flags & MOE_F32, true, flags & MOE_H_ON_LOAD);
 }
 
 int moe_ffn_fwd_combine(const void* x, const void* w1, const void* w3, const void* w2,
@@ -296,7 +300,7 @@ int moe_combine(const void* src, const float* weights, const int32_t* token_inde
     const char* fn = "moe_combine";
     int r;
     if ((r = check_common(fn, T, k, k, flags)) || (r = check_dim(fn, "d", d))) return r;
-    if (flags & ACT_FLAGS) return fail(MOE_ERR_INVALID_ARG, "%s: activation flags apply to the FFN calls only", fn);
+    if (flags & FFN_ONLY) return fail(MOE_ERR_INVALID_ARG, "%s: activation and h-on-load flags apply to the FFN calls only", fn);
     if (flags & MOE_RENORM) return fail(MOE_ERR_INVALID_ARG, "%s: MOE_RENORM not valid here", fn);
     if (T == 0) return MOE_OK;
     REQUIRE_PTR(src); OPT_PTR(weights); REQUIRE_PTR(token_index_map); REQUIRE_PTR(out);
@@ -350,7 +354,7 @@ int moe_route_bwd(const float* d_gates, const float* logits, const int32_t* topk
     const char* fn = "moe_route_bwd";
     int r;
     if ((r = check_common(fn, T, E, k, flags)) || (r = check_dim(fn, "d", d))) return r;
-    if (flags & ACT_FLAGS) return fail(MOE_ERR_INVALID_ARG, "%s: activation flags apply to the FFN calls only", fn);
+    if (flags & FFN_ONLY) return fail(MOE_ERR_INVALID_ARG, "%s: activation and h-on-load flags apply to the FFN calls only", fn);
     if (T == 0) return MOE_OK;
     REQUIRE_PTR(d_gates); REQUIRE_PTR(logits); REQUIRE_PTR(topk_ids); REQUIRE_PTR(gates);
     REQUIRE_PTR(x); REQUIRE_PTR(w_gate); REQUIRE_PTR(dw_gate); REQUIRE_PTR(dx);

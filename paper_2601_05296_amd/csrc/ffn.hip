@@ -43,6 +43,8 @@ using CS = GemmCfg<256, 256, 2, 4, 1>;  // G2, G3, G6
 // workgroups with 72 KB of LDS, so that two share a CU and one's epilogue
 // overlaps the other's main loop.
 using C4 = GemmCfg<128, 256, 2, 2, 1>;
+// G2 with h formed on load: the stage also holds B's tile (144 KB of LDS)
+using CH = GemmCfg<256, 256, 2, 4, 1, 1>;
 
 // ============================ epilogue helpers ===================================
 
@@ -71,6 +73,7 @@ __device__ __forceinline__ float act_d(float a) {
 // tile configuration of the first-layer and dW1 GEMMs: two right operands
 // when gated (W1|W3, dA|dB), one otherwise
 template <int ACT> using CFirst = std::conditional_t<ACT == ACT_SWIGLU, CD, CS>;
+template <int ACT> using CSecondH = std::conditional_t<ACT == ACT_SWIGLU, CH, CS>;
 static_assert(CD::THREADS == CS::THREADS && CD::LDS == CS::LDS, "CD and CS launch alike");
 __device__ __forceinline__ void store8_bf16(bf16_t* p, const float (&v)[8]) { st16(p, pack8(v)); }
 
@@ -157,6 +160,81 @@ g2_kernel(const bf16_t* __restrict__ H, const bf16_t* __restrict__ w2,
     NoLoader nl;
     Acc<C> acc;
     gemm_mainloop<C>(la, lb, nl, f / GBK, GBK, lds, acc, t.mrows, ncols - t.n0);
+    WaveCoord<C> wc;
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i) {
+        const int m = wc.row(i);
+        if (m >= t.mrows) continue;
+        const int64_t s = (int64_t)t.off + t.m0 + m;
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j) {
+            float v[2][8];
+            frag_cols8(acc[0][i][j], v);
+#pragma unroll
+            for (int p = 0; p < 2; ++p) {
+                const int n = t.n0 + wc.col8(j, p);
+                if (n < ncols) store8_bf16(O + s * ldo + n, v[p]);
+            }
+        }
+    }
+}
+
+// Pre-pass of the second GEMM with h formed on load: the slice's A tile (and
+// B's, in the extra tile) become h = SiLU(A) * B (act(A) when non-gated) in
+// place, with the arithmetic of G1's epilogue, so h is bit-identical to the
+// buffered one. Layout-oblivious: A and B tiles share one swizzled layout.
+template <int ACT, class C>
+struct HPass {
+    static constexpr bool active = true;
+    __device__ void operator()(char* stage, int) const {
+        constexpr int NCH = C::A_BYTES / 16;
+        static_assert(NCH % C::THREADS == 0, "whole chunks per thread");
+#pragma unroll
+        for (int it = 0; it < NCH / C::THREADS; ++it) {
+            const int q = threadIdx.x + it * C::THREADS;
+            uint4* pa = reinterpret_cast<uint4*>(stage) + q;
+            float a[8], h[8];
+            unpack8(*pa, a);
+            if constexpr (ACT == ACT_SWIGLU) {
+                float b[8];
+                unpack8(*(reinterpret_cast<const uint4*>(stage + C::A_BYTES) + q), b);
+#pragma unroll
+                for (int r = 0; r < 8; ++r) h[r] = silu_bf(a[r]) * b[r];
+            } else {
+#pragma unroll
+                for (int r = 0; r < 8; ++r) h[r] = act_f<ACT>(a[r]);
+            }
+            *pa = pack8(h);
+        }
+    }
+};
+
+// G2 with h formed on load (the paper's recomputation in the second GEMM,
+// Section 3.1): O = h W2[e] from the saved A (and B), no h buffer.
+template <int ACT>
+__global__ void __launch_bounds__(CS::THREADS)
+g2h_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B,
+           const bf16_t* __restrict__ w2, const int32_t* __restrict__ offsets, int d, int f,
+           int E, int n_base, int ncols, int64_t ldo, bf16_t* __restrict__ O) {
+    extern __shared__ __align__(16) char lds[];
+    using C = CSecondH<ACT>;
+    SlotTile t;
+    const int NT = (ncols + C::BN - 1) / C::BN;
+    if (!find_slot_tile<C::THREADS>(offsets, E, C::BM, NT, xcd_remap(blockIdx.x, gridDim.x), C::BN, t))
+        return;
+    DenseMC<C, C::BN> lb;
+    lb.init(w2 + (int64_t)t.e * f * d, d, n_base + t.n0, n_base + ncols);
+    NoLoader nl;
+    Acc<C> acc;
+    if constexpr (ACT == ACT_SWIGLU) {
+        PairKC<C, C::BM> la;
+        la.init(A, B, f, (int64_t)t.off + t.m0, t.mrows);
+        gemm_mainloop<C>(la, lb, nl, f / GBK, GBK, lds, acc, t.mrows, ncols - t.n0, HPass<ACT, C>{});
+    } else {
+        DenseKC2<C, C::BM> la;
+        la.init(A, A, f, (int64_t)t.off + t.m0, t.mrows, f);
+        gemm_mainloop<C>(la, lb, nl, f / GBK, GBK, lds, acc, t.mrows, ncols - t.n0, HPass<ACT, C>{});
+    }
     WaveCoord<C> wc;
 #pragma unroll
     for (int i = 0; i < C::FM; ++i) {
@@ -607,6 +685,7 @@ hipError_t set_lds_limits() {
             set(reinterpret_cast<const void*>(g1_kernel<ACT>), CFirst<ACT>::LDS);
             set(reinterpret_cast<const void*>(g4_kernel<ACT>), C4::LDS);
             set(reinterpret_cast<const void*>(g5_kernel<ACT>), CFirst<ACT>::LDS);
+            set(reinterpret_cast<const void*>(g2h_kernel<ACT>), CSecondH<ACT>::LDS);
         };
         per_act(std::integral_constant<int, ACT_SWIGLU>{});
         per_act(std::integral_constant<int, ACT_SILU>{});
@@ -638,10 +717,11 @@ inline int strip_width(int64_t S, int E, int d) {
 
 }  // namespace
 
-size_t ffn_fwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool combined) {
+size_t ffn_fwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool combined,
+                         bool h_on_load) {
     const size_t S = (size_t)T * k;
     if (f32) return combined ? align256(S * d * sizeof(float)) : 0;  // O
-    const size_t h = align256(S * f * sizeof(bf16_t));                // H
+    const size_t h = h_on_load ? 0 : align256(S * f * sizeof(bf16_t));   // H
     return combined ? h + align256(S * strip_width(S, E, d) * sizeof(bf16_t)) : h;
 }
 
@@ -665,29 +745,39 @@ hipError_t ffn_fwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
     }
     if (hipError_t e = set_lds_limits(); e != hipSuccess) return e;
     using C1 = CFirst<ACT>;
-    bf16_t* H = static_cast<bf16_t*>(a.ws);
+    using C2H = CSecondH<ACT>;
+    // h buffered between the GEMMs, or (h_on_load) formed again from A, B
+    bf16_t* H = a.h_on_load ? nullptr : static_cast<bf16_t*>(a.ws);
     hipLaunchKernelGGL(g1_kernel<ACT>, dim3(slot_grid(S, a.E, C1::BM, cdiv(a.f, C1::BN))),
                        dim3(C1::THREADS), C1::LDS, st, (const bf16_t*)a.x, (const bf16_t*)a.w1,
                        (const bf16_t*)a.w3, a.offsets, a.eti, a.d, a.f, a.E, (bf16_t*)a.A,
                        (bf16_t*)a.B, H);
     probe::mark("g1_kernel", st);
+    auto second = [&](int c0, int nc, int64_t ldo, bf16_t* out) {
+        if (a.h_on_load) {
+            hipLaunchKernelGGL(g2h_kernel<ACT>, dim3(slot_grid(S, a.E, C2H::BM, cdiv(nc, C2H::BN))),
+                               dim3(C2H::THREADS), C2H::LDS, st, (const bf16_t*)a.A,
+                               (const bf16_t*)a.B, (const bf16_t*)a.w2, a.offsets, a.d, a.f, a.E,
+                               c0, nc, ldo, out);
+            probe::mark("g2h_kernel", st);
+        } else {
+            hipLaunchKernelGGL(g2_kernel, dim3(slot_grid(S, a.E, CS::BM, cdiv(nc, CS::BN))),
+                               dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)H,
+                               (const bf16_t*)a.w2, a.offsets, a.d, a.f, a.E, c0, nc, ldo, out);
+            probe::mark("g2_kernel", st);
+        }
+    };
     if (!a.y) {   // O [S, d] for the caller's combine
-        hipLaunchKernelGGL(g2_kernel, dim3(slot_grid(S, a.E, CS::BM, cdiv(a.d, CS::BN))),
-                           dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)H, (const bf16_t*)a.w2,
-                           a.offsets, a.d, a.f, a.E, 0, a.d, (int64_t)a.d, (bf16_t*)a.O);
-        probe::mark("g2_kernel", st);
+        second(0, a.d, (int64_t)a.d, (bf16_t*)a.O);
         return hipGetLastError();
     }
     // combined: one column strip of O at a time, straight into y
     const int sw = strip_width(S, a.E, a.d);
-    bf16_t* strip = reinterpret_cast<bf16_t*>(static_cast<char*>(a.ws) +
-                                              align256((size_t)S * a.f * sizeof(bf16_t)));
+    bf16_t* strip = reinterpret_cast<bf16_t*>(
+        static_cast<char*>(a.ws) + (a.h_on_load ? 0 : align256((size_t)S * a.f * sizeof(bf16_t))));
     for (int c0 = 0; c0 < a.d; c0 += sw) {
         const int nc = min(sw, a.d - c0);
-        hipLaunchKernelGGL(g2_kernel, dim3(slot_grid(S, a.E, CS::BM, cdiv(nc, CS::BN))),
-                           dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)H, (const bf16_t*)a.w2,
-                           a.offsets, a.d, a.f, a.E, c0, nc, (int64_t)nc, strip);
-        probe::mark("g2_kernel", st);
+        second(c0, nc, (int64_t)nc, strip);
         if (hipError_t e = combine_cols(strip, nc, a.gates, a.tim, a.T, nc, a.k, false, false,
                                         static_cast<bf16_t*>(a.y) + c0, a.d, st);
             e != hipSuccess)

@@ -70,6 +70,11 @@ __device__ __forceinline__ void wait_vmcnt() {
 // __syncthreads() adds; also a compiler memory barrier.
 __device__ __forceinline__ void barrier_only() { asm volatile("s_barrier" ::: "memory"); }
 
+// Barrier after this wave's LDS accesses have completed.
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 // 16-byte global -> LDS copy by one lane: lane l writes LDS bytes
 // lds_off + 16*l .. +15 (lds_off must be wave-uniform; it goes to M0). Issued
 // from inline assembly so that the compiler does not track these copies: it
@@ -90,16 +95,20 @@ __device__ __forceinline__ uint32_t lds_offset(const void* p) {
 // Wave index as a value the compiler knows to be uniform (kept in an SGPR).
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
-template <int BM_, int BN_, int WM_, int WN_, int NB_>
+// XA extra left-operand-shaped tiles per stage follow the left operand's tile
+// (raw inputs that a pre-pass folds into it, e.g. B of h = SiLU(A) * B); the
+// right-operand tiles start after them, at AREG.
+template <int BM_, int BN_, int WM_, int WN_, int NB_, int XA_ = 0>
 struct GemmCfg {
-    static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, NB = NB_;
+    static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, NB = NB_, XA = XA_;
     static constexpr int NW = WM * WN;
     static constexpr int THREADS = NW * WAVE;
     static constexpr int WTM = BM / WM, WTN = BN / WN;   // wave tile
     static constexpr int FM = WTM / 32, FN = WTN / 32;   // 32x32 fragments per wave
     static constexpr int A_BYTES = BM * GBK * 2;
     static constexpr int B_BYTES = BN * GBK * 2;
-    static constexpr int STAGE = A_BYTES + NB * B_BYTES;
+    static constexpr int AREG = (1 + XA) * A_BYTES;
+    static constexpr int STAGE = AREG + NB * B_BYTES;
     static constexpr int LDS = NST * STAGE;
     static_assert(FM >= 1 && FN >= 1, "wave tile too small");
     static_assert(LDS <= 160 * 1024, "LDS budget");
@@ -185,10 +194,18 @@ __device__ __forceinline__ void zero_mc_rows(char* tile, int from) {
 // arows / bcols: rows of the left operand tile and columns of the right one
 // that hold real outputs. A wave whose fragments lie wholly beyond them skips
 // their LDS reads and MFMAs (its loads still land: the copies are shared).
-template <class C, class LA, class LB0, class LB1>
+// PRE: an optional pass over the stage of slice kt (pre(stage, kt)) run by the
+// whole workgroup once the slice is visible and before any fragment is read,
+// followed by a barrier: it turns the raw tiles of the left operand (the XA
+// extra ones included) into the operand the MFMAs consume.
+struct NoPre {
+    static constexpr bool active = false;
+    __device__ void operator()(char*, int) const {}
+};
+template <class C, class LA, class LB0, class LB1, class PRE = NoPre>
 __device__ __forceinline__ void gemm_mainloop(LA& la, LB0& lb0, LB1& lb1, int nk, int zero_from,
                                               char* lds, Acc<C>& acc, int arows = C::BM,
-                                              int bcols = C::BN) {
+                                              int bcols = C::BN, PRE pre = PRE{}) {
 #pragma unroll
     for (int b = 0; b < C::NB; ++b)
 #pragma unroll
@@ -207,12 +224,14 @@ __device__ __forceinline__ void gemm_mainloop(LA& la, LB0& lb0, LB1& lb1, int nk
     auto issue = [&](int kt) {
         const uint32_t t = lds_base + (kt % NST) * C::STAGE;
         la.issue(kt, t);
-        lb0.issue(kt, t + C::A_BYTES);
-        if constexpr (C::NB == 2) lb1.issue(kt, t + C::A_BYTES + C::B_BYTES);
+        lb0.issue(kt, t + C::AREG);
+        if constexpr (C::NB == 2) lb1.issue(kt, t + C::AREG + C::B_BYTES);
     };
     auto fix_tail = [&](int kt) {  // called once slice kt is visible to all waves
         if (kt == nk - 1 && zero_from < GBK) {
-            zero_mc_rows<C, C::BM>(lds + (kt % NST) * C::STAGE, zero_from);
+#pragma unroll
+            for (int x = 0; x <= C::XA; ++x)
+                zero_mc_rows<C, C::BM>(lds + (kt % NST) * C::STAGE + x * C::A_BYTES, zero_from);
             __syncthreads();
         }
     };
@@ -233,6 +252,10 @@ __device__ __forceinline__ void gemm_mainloop(LA& la, LB0& lb0, LB1& lb1, int nk
         constexpr bool PART = decltype(partial)::value;
         for (int kt = 0; kt < nk; ++kt) {
             if (kt + NST - 1 < nk) issue(kt + NST - 1);
+            if constexpr (PRE::active) {
+                pre(lds + (kt % NST) * C::STAGE, kt);
+                lds_barrier();
+            }
             const char* cur = lds + (kt % NST) * C::STAGE;
 #pragma unroll
             for (int kk = 0; kk < GBK / 16; ++kk) {
@@ -243,7 +266,7 @@ __device__ __forceinline__ void gemm_mainloop(LA& la, LB0& lb0, LB1& lb1, int nk
                         fa[i] = frag<LA::MC, C::BM>(cur, wm * C::WTM + i * 32, kk, lane);
 #pragma unroll
                 for (int b = 0; b < C::NB; ++b) {
-                    const char* bt = cur + C::A_BYTES + b * C::B_BYTES;
+                    const char* bt = cur + C::AREG + b * C::B_BYTES;
                     bf16x8 fb[C::FN];
 #pragma unroll
                     for (int j = 0; j < C::FN; ++j)
@@ -324,9 +347,6 @@ struct WaveCoord {
 // Call after gemm_mainloop (whose final barrier frees the LDS ring). Between
 // rounds only the LDS accesses are ordered: the global stores of a round stay
 // in flight while the next round is staged.
-__device__ __forceinline__ void lds_barrier() {
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
 
 template <class C, int IPR>
 struct RowStage {

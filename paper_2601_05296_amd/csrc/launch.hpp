@@ -46,8 +46,11 @@ struct FfnArgs {
     // combined calls: y (forward) or dx (backward) [T, d] written through
     // token_index_map instead of O / dX_slot; accumulate adds into dx
     void* y; const int32_t* tim; bool accumulate;
+    // h is not buffered: the second GEMM forms it again from A (and B) on load
+    bool h_on_load;
 };
-size_t ffn_fwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool combined);
+size_t ffn_fwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool combined,
+                         bool h_on_load);
 hipError_t ffn_fwd(const FfnArgs& a, bool f32, hipStream_t st);
 // first layer only: A (and B) from x, nothing else
 hipError_t ffn_first(const FfnArgs& a, bool f32, hipStream_t st);

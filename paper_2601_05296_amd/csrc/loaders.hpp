@@ -69,6 +69,37 @@ struct DenseKC2 : KCBase<C, R> {
     }
 };
 
+// Two KC tiles of the same rows row0 + r (r < rows, else row0) from two
+// row-major matrices of equal shape: src0 into the left operand's tile, src1
+// into the extra tile after it (GemmCfg XA = 1).
+template <class C, int R>
+struct PairKC : KCBase<C, R> {
+    static constexpr int NQ1 = KCBase<C, R>::NQ;
+    static constexpr int NQ = 2 * NQ1;   // copies per wave per slice, both tiles
+    static_assert(C::XA == 1 && R == C::BM, "pair tiles fill the left operand and its extra tile");
+    const bf16_t* p0[NQ1];
+    const bf16_t* p1[NQ1];
+    __device__ void init(const bf16_t* src0, const bf16_t* src1, int ld, int64_t row0, int rows) {
+        const int lane = threadIdx.x & 63;
+#pragma unroll
+        for (int i = 0; i < NQ1; ++i) {
+            const int q = this->q(i);
+            int r = KCDma::row(q, lane);
+            r = r < rows ? r : 0;
+            const int64_t o = (row0 + r) * (int64_t)ld + KCDma::kcol(q, lane);
+            p0[i] = src0 + o;
+            p1[i] = src1 + o;
+        }
+    }
+    __device__ void issue(int kt, uint32_t t) {
+#pragma unroll
+        for (int i = 0; i < NQ1; ++i) {
+            dma16(p0[i] + kt * GBK, t + this->q(i) * 1024u);
+            dma16(p1[i] + kt * GBK, t + C::A_BYTES + this->q(i) * 1024u);
+        }
+    }
+};
+
 template <class C, int R>
 struct MCBase {
     static constexpr bool MC = true;

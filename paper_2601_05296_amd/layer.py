@@ -13,6 +13,8 @@ Backward (Section 3.2):
 ``recompute=True`` is the full-recompute checkpoint policy: the forward keeps
 only the routing decision and the maps, and the backward first recomputes A
 and B with moe_ffn_recompute (bit-identical to the forward's).
+``h_on_load=True`` (MOE_H_ON_LOAD) buffers no h between the GEMMs: the second
+GEMM forms h again from A and B (bit-identical results, less memory).
 
 What the forward keeps for the backward (the "saved activations"): the first
 layer outputs A and B [S, f] (A alone for the non-gated SiLU / ReLU experts),
@@ -51,10 +53,11 @@ class Saved:
     slot_src: torch.Tensor
     A: torch.Tensor | None      # None under the full-recompute policy
     B: torch.Tensor | None
+    h_on_load: bool = False
 
     @property
     def ffn_flags(self) -> int:
-        return self.flags | B.ACT_FLAG[self.act]
+        return self.flags | B.ACT_FLAG[self.act] | (B.MOE_H_ON_LOAD if self.h_on_load else 0)
 
     def tensors(self):
         return [t for t in (self.ids, self.gates, self.logits, self.counts, self.offsets,
@@ -75,7 +78,8 @@ def saved_bytes_per_token(d: int, f: int, E: int, k: int, elem: int, T: int,
 
 
 def forward(x, w_gate, bias, w1, w3, w2, k: int, renorm: bool, stream=None, keep_O=False,
-            act: str = "swiglu", separate: bool = False, recompute: bool = False):
+            act: str = "swiglu", separate: bool = False, recompute: bool = False,
+            h_on_load: bool = False):
     """Returns (y, saved[, O]). ``act`` picks the expert: "swiglu" (gated, w3
     used) or the non-gated "silu" / "relu" (w3 ignored, may be None).
     ``keep_O`` (returns the expert outputs) implies ``separate``."""
@@ -101,12 +105,12 @@ def forward(x, w_gate, bias, w1, w3, w2, k: int, renorm: bool, stream=None, keep
     B.moe_build_index(ids, T, E, k, counts, offsets, eti, tim, slot_src, ws, wsb, stream)
     del ws
     gated = act == "swiglu"
-    fflags = flags | B.ACT_FLAG[act]
+    fflags = flags | B.ACT_FLAG[act] | (B.MOE_H_ON_LOAD if h_on_load else 0)
     A = torch.empty((S, f), dtype=x.dtype, device=dev)
     Bm = torch.empty((S, f), dtype=x.dtype, device=dev) if gated else None
     y = torch.empty((T, d), dtype=x.dtype, device=dev)
     saved = Saved(T, d, f, E, k, flags, act, renorm, ids, gates, logits, counts, offsets, eti,
-                  tim, slot_src, A, Bm)
+                  tim, slot_src, A, Bm, h_on_load)
     w3g = w3 if gated else None
     if recompute:   # A and B live only for this call
         saved.A = saved.B = None

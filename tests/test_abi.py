@@ -84,6 +84,33 @@ def test_workspace_checks_and_zero_tokens():
     assert lib.moe_build_index_workspace_size(0, 8, 2) == 0
 
 
+def test_h_on_load_flag():
+    lib = B.load_library()
+    T, d, f, E, k = 1000, 256, 384, 8, 2
+    S = T * k
+    h = (S * f * 2 + 255) // 256 * 256
+    for fl in (0, B.MOE_ACT_SILU, B.MOE_ACT_RELU):
+        # the forward workspace drops exactly the bf16 h buffer
+        assert lib.moe_ffn_fwd_workspace_size(T, d, f, E, k, fl) - \
+            lib.moe_ffn_fwd_workspace_size(T, d, f, E, k, fl | B.MOE_H_ON_LOAD) == h
+        assert lib.moe_ffn_fwd_combine_workspace_size(T, d, f, E, k, fl) - \
+            lib.moe_ffn_fwd_combine_workspace_size(T, d, f, E, k, fl | B.MOE_H_ON_LOAD) == h
+    # float32 debug mode buffers no h either way
+    assert lib.moe_ffn_fwd_workspace_size(T, d, f, E, k, B.MOE_F32 | B.MOE_H_ON_LOAD) == \
+        lib.moe_ffn_fwd_workspace_size(T, d, f, E, k, B.MOE_F32)
+    # without h the separate forward needs no workspace at all
+    assert lib.moe_ffn_fwd_workspace_size(T, d, f, E, k, B.MOE_H_ON_LOAD) == 0
+    # the FFN calls accept it (here a short workspace stops the call before any launch)
+    r = lib.moe_ffn_fwd_combine(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, T, d, f, E, k,
+                                B.MOE_H_ON_LOAD, FAKE, FAKE, FAKE, FAKE, 16, None)
+    assert r == B.MOE_ERR_WORKSPACE, lib.moe_last_error()
+    # the other calls reject it
+    assert lib.moe_combine(FAKE, None, FAKE, 10, 128, 2, B.MOE_H_ON_LOAD, FAKE, None) == \
+        B.MOE_ERR_INVALID_ARG
+    assert lib.moe_route(FAKE, FAKE, None, 10, 128, 8, 2, B.MOE_H_ON_LOAD, FAKE, FAKE, None,
+                         None) == B.MOE_ERR_INVALID_ARG
+
+
 def test_activation_flags():
     lib = B.load_library()
     S, f = 1000 * 2, 128

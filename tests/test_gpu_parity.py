@@ -455,6 +455,49 @@ def test_ffn_combined_equals_separate(dtype, T, d, f, E, k, pattern, act):
     assert_close("dw1", host(r_c["dw1"]), bw["dw1"], dtype)
 
 
+@pytest.mark.parametrize("dtype,T,d,f,E,k,pattern,act", [c for c in COMBINED_CASES if c[0] == "bf16"])
+def test_ffn_h_on_load_bit_identical(dtype, T, d, f, E, k, pattern, act):
+    """MOE_H_ON_LOAD: the second GEMM forms h from A (and B) as it loads them,
+    with G1's arithmetic, so A, B, O and y are bit-identical to the buffered
+    path, and the forward workspace drops the S x f bf16 h buffer."""
+    inp, ids, g = _layer_case(dtype, T, d, f, E, k, False, pattern)
+    st = inp.store
+    gated = act == "swiglu"
+    S = T * k
+    gi = _gpu_index(ids, E)
+    x, w1, w2 = (dev(st[n]) for n in ("x", "w1", "w2"))
+    w3 = dev(st["w3"]) if gated else None
+    offsets, eti, tim = (dev(gi[n]) for n in ("offsets", "eti", "tim"))
+    gates = dev(g)
+    base = B.dtype_flag(x) | B.ACT_FLAG[act]
+
+    def fwd(flags, combined):
+        A = torch.empty((S, f), dtype=torch.bfloat16, device="cuda")
+        Bm = torch.empty((S, f), dtype=torch.bfloat16, device="cuda") if gated else None
+        if combined:
+            out = torch.empty((T, d), dtype=torch.bfloat16, device="cuda")
+            wsb = B.moe_ffn_fwd_combine_workspace_size(T, d, f, E, k, flags)
+            ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+            B.moe_ffn_fwd_combine(x, w1, w3, w2, offsets, eti, gates, tim, T, d, f, E, k, flags,
+                                  A, Bm, out, ws, wsb)
+        else:
+            out = torch.empty((S, d), dtype=torch.bfloat16, device="cuda")
+            wsb = B.moe_ffn_fwd_workspace_size(T, d, f, E, k, flags)
+            ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+            B.moe_ffn_fwd(x, w1, w3, w2, offsets, eti, T, d, f, E, k, flags, A, Bm, out, ws, wsb)
+        torch.cuda.synchronize()
+        return A, Bm, out, wsb
+
+    for combined in (False, True):
+        A0, B0, out0, ws0 = fwd(base, combined)
+        A1, B1, out1, ws1 = fwd(base | B.MOE_H_ON_LOAD, combined)
+        assert torch.equal(A0, A1)
+        if gated:
+            assert torch.equal(B0, B1)
+        assert torch.equal(out0, out1), "combined" if combined else "O"
+        assert ws0 - ws1 == (S * f * 2 + 255) // 256 * 256
+
+
 # whole layer (routing included) on the tiny float32 workload
 # ---------------------------------------------------------------------------
 
