@@ -65,14 +65,15 @@ extern "C" {
  * the two may be set (else MOE_ERR_INVALID_ARG). */
 #define MOE_ACT_SILU    8u
 #define MOE_ACT_RELU    16u
-/* moe_ffn_fwd, moe_ffn_fwd_combine (and their workspace queries): do not
- * buffer h = SiLU(A) * B between the two GEMMs; the second GEMM forms h again
- * from A and B as it loads them (Section 3.1 keeps only the first MLP's output;
- * Section 5.2 recomputes the activation). h is bit-identical to the buffered
- * one, so are O and y. The forward workspace shrinks by S*f*2 bytes at the cost
- * of the second GEMM reading A and B instead of h. The other FFN calls accept
- * and ignore it; route, build, combine and route_bwd reject it
- * (MOE_ERR_INVALID_ARG). */
+/* The FFN calls and their workspace queries: buffer no h = SiLU(A) * B.
+ * Forward: the second GEMM forms h again from A and B as it loads them
+ * (Section 3.1 keeps only the first MLP's output; Section 5.2 recomputes the
+ * activation). Backward: the dW2 GEMM runs first and forms g*h from A, B and
+ * the gates as it loads them, before dA and dB overwrite A and B. Every result
+ * is bit-identical to the default path; the forward workspace drops S*f*2
+ * bytes (h) and the backward's the same (g*h), at the cost of those two GEMMs
+ * reading A and B instead of one buffer. moe_ffn_recompute accepts and ignores
+ * it; route, build, combine and route_bwd reject it (MOE_ERR_INVALID_ARG). */
 #define MOE_H_ON_LOAD   32u
 
 /* Human-readable name of a status code (static storage). */

@@ -150,7 +150,8 @@ int ffn_bwd_impl(const char* fn, bool combined, const void* dy, const void* x, c
     }
     if (act == 0) { REQUIRE_PTR(w3); REQUIRE_PTR(B); REQUIRE_PTR(dw3); }
     else { OPT_PTR(w3); OPT_PTR(B); OPT_PTR(dw3); }
-    const size_t need = moe::ffn_bwd_workspace(T, d, f, E, k, flags & MOE_F32, combined);
+    const size_t need =
+        moe::ffn_bwd_workspace(T, d, f, E, k, flags & MOE_F32, combined, flags & MOE_H_ON_LOAD);
     if (need && (!workspace || workspace_bytes < need))
         return fail(MOE_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, workspace_bytes, need);
     OPT_PTR(workspace);
@@ -159,6 +160,7 @@ int ffn_bwd_impl(const char* fn, bool combined, const void* dy, const void* x, c
     a.slot_src = slot_src; a.gates = gates; a.dy = dy; a.A = A; a.B = B;
     a.dw1 = dw1; a.dw3 = dw3; a.dw2 = dw2; a.dgates = d_gates; a.T = T; a.d = d; a.f = f;
     a.E = E; a.k = k; a.ws = workspace; a.act = act;
+    a.h_on_load = flags & MOE_H_ON_LOAD;
     if (combined) { a.y = out; a.tim = token_index_map; a.accumulate = flags & MOE_ACCUMULATE; }
     else a.dX = out;
     moe::probe::begin(stream);
@@ -312,7 +314,7 @@ int moe_combine(const void* src, const float* weights, const int32_t* token_inde
 
 size_t moe_ffn_bwd_workspace_size(int64_t T, int d, int f, int E, int k, unsigned flags) {
     if (T <= 0 || d < 1 || f < 1 || E < 1 || k < 1) return 0;
-    return moe::ffn_bwd_workspace(T, d, f, E, k, flags & MOE_F32, false);
+    return moe::ffn_bwd_workspace(T, d, f, E, k, flags & MOE_F32, false, flags & MOE_H_ON_LOAD);
 }
 
 int moe_ffn_bwd(const void* dy, const void* x, const void* w1, const void* w3, const void* w2,
@@ -327,7 +329,7 @@ int moe_ffn_bwd(const void* dy, const void* x, const void* w1, const void* w3, c
 
 size_t moe_ffn_bwd_combine_workspace_size(int64_t T, int d, int f, int E, int k, unsigned flags) {
     if (T <= 0 || d < 1 || f < 1 || E < 1 || k < 1) return 0;
-    return moe::ffn_bwd_workspace(T, d, f, E, k, flags & MOE_F32, true);
+    return moe::ffn_bwd_workspace(T, d, f, E, k, flags & MOE_F32, true, flags & MOE_H_ON_LOAD);
 }
 
 int moe_ffn_bwd_combine(const void* dy, const void* x, const void* w1, const void* w3,

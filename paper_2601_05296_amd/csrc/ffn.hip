@@ -1,22 +1,29 @@
-// ffn.hip -- SwiGLU expert FFN of the MoE layer as grouped GEMMs that read
-// token rows through the dispatch index maps (MoEBlaze paper, Section 3 and
-// Section 5, Algorithm 1), bf16 MFMA with float32 accumulation on gfx950.
+// ffn.hip -- expert FFN of the MoE layer (SwiGLU, or the non-gated SiLU / ReLU
+// expert) as grouped GEMMs that read token rows through the dispatch index
+// maps (MoEBlaze paper, Section 3 and Section 5, Algorithm 1), bf16 MFMA with
+// float32 accumulation on gfx950.
 //
 // Forward (moe_ffn_fwd):
 //   G1  A|B = x[eti] [W1|W3]      x rows gathered on load, both first-layer
 //                                 projections from one x tile (Section 5.2);
-//                                 A and B are the only saved activations.
-//   G2  O = (SiLU(A) * B) W2      h = SiLU(A)*B formed on load from A, B and
-//                                 never written (SiLU recomputed, Section 5.2).
-// Backward (moe_ffn_bwd), in this order so A and B can be overwritten:
-//   G3  dW2 = h^T (g dY[eti])     h recomputed on load and scaled by the gate,
-//                                 dY rows gathered (the expert-summation
-//                                 backward of Section 3.2, never materialised).
+//                                 A and B are the only saved activations. The
+//                                 epilogue also writes h = SiLU(A)*B into a
+//                                 transient buffer for G2.
+//   G2  O = h W2                  (MOE_H_ON_LOAD: g2h_kernel forms h from A
+//                                 and B as it loads them; no h buffer.)
+// Backward (moe_ffn_bwd):
 //   G4  u = dY[eti] W2^T, then in the epilogue: d_gate partials sum(u*h),
-//       dA = g u B SiLU'(A), dB = g u SiLU(A), written over A and B.
+//       dA = g u B SiLU'(A), dB = g u SiLU(A) written over A and B, and g*h
+//       into a transient buffer (h recomputed from A and B).
+//   G3  dW2 = (g h)^T dY[eti]     dY rows gathered (the expert-summation
+//                                 backward of Section 3.2). MOE_H_ON_LOAD:
+//                                 g3h_kernel runs before G4 and forms g*h from
+//                                 A, B and the gates on load; no g*h buffer.
 //   G5  dW1 = x[eti]^T dA, dW3 = x[eti]^T dB   (one x tile, two products)
 //   G6  dX_slot = [dA|dB] [W1|W3]^T             (both branches in one K loop)
-// The token gradient is then a unit-weight combine (combine.hip).
+// The token gradient is then a unit-weight combine (combine.hip). Forming h
+// on load costs the second GEMMs a second operand stream and an in-LDS pass
+// per K slice; it returns the same bits.
 //
 // Row-wise GEMMs (G1, G2, G4, G6) tile each expert's slot segment; their grid
 // is sized for the worst case (S/BM + E tiles per column block) and each
@@ -257,7 +264,7 @@ g2h_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B,
 // G4: u = dY[eti] W2[e]^T; epilogue: d_gate partials sum(u*h), dA/dB over
 // A/B, and HG = g * h (h recomputed from A, B) for G3. Non-gated: dA = g u
 // act'(A) over A, h = act(A).
-template <int ACT>
+template <int ACT, bool HG_OUT>
 __global__ void __launch_bounds__(C4::THREADS, 2)
 g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
           const float* __restrict__ gates, const int32_t* __restrict__ offsets,
@@ -381,19 +388,21 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
             store_rows(NARR, dst);
         }
         lds_barrier();
+        if constexpr (HG_OUT) {   // false when G3 forms g*h itself (h on load)
 #pragma unroll
-        for (int j = 0; j < C::FN; ++j)
+            for (int j = 0; j < C::FN; ++j)
 #pragma unroll
-            for (int p = 0; p < 2; ++p) {
-                const int off = (((wc.col8(j, p) >> 3) ^ (rr & 31)) << 4);
-                *reinterpret_cast<uint4*>(rowA + off) = hgv[j][p];
+                for (int p = 0; p < 2; ++p) {
+                    const int off = (((wc.col8(j, p) >> 3) ^ (rr & 31)) << 4);
+                    *reinterpret_cast<uint4*>(rowA + off) = hgv[j][p];
+                }
+            lds_barrier();
+            {
+                bf16_t* const dst[1] = {HG};
+                store_rows(1, dst);
             }
-        lds_barrier();
-        {
-            bf16_t* const dst[1] = {HG};
-            store_rows(1, dst);
+            lds_barrier();
         }
-        lds_barrier();
     }
 }
 
@@ -427,6 +436,87 @@ g3_kernel(const bf16_t* __restrict__ HG, const bf16_t* __restrict__ dy,
     Acc<C> acc;
     gemm_mainloop<C>(la, lb, nl, (cnt + GBK - 1) / GBK, tail_from(cnt), lds, acc, f - m0,
                      d - n0);
+    float* out = dw2 + (int64_t)e * f * d;
+    RowStage<C, 1>::run(acc, lds, [&](int, int r, int c, const f32x4& v) {
+        const int m = m0 + r, n = n0 + c;
+        if (m < f && n < d) st_nt(out + (int64_t)m * d + n, v);
+    });
+}
+
+// gs[s] = gates[slot_src[s]] for s < S, 0 for S <= s < S + pad (the gate of
+// each slot in slot order, for the dW2 GEMM's pre-pass)
+__global__ void slot_gates(const float* __restrict__ gates, const int32_t* __restrict__ slot_src,
+                           int64_t S, int64_t pad, float* __restrict__ gs) {
+    const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (s < S) gs[s] = gates[slot_src[s]];
+    else if (s < S + pad) gs[s] = 0.0f;
+}
+constexpr int GS_PAD = 64;   // zero gates past the last slot (a slice reads up to 31 more)
+
+// Pre-pass of the dW2 GEMM with g*h formed on load: the slice's A tile (MC: 32
+// slot rows of 256 columns) and B's, in the extra tile, become g*h = g * SiLU(A)
+// * B in place (g * act(A) when non-gated), with the arithmetic of G4's
+// epilogue, so the result equals the buffered g*h bit for bit. The slot rows'
+// gates sit in the 128-byte gate slot of the stage.
+template <int ACT, class C>
+struct GPass {
+    static constexpr bool active = true;
+    const char* gate_slots;   // NST x 32 floats after the ring
+    __device__ void operator()(char* stage, int kt) const {
+        constexpr int NCH = C::A_BYTES / 16;     // 16-byte chunks of the tile
+        constexpr int CPR = C::BM * 2 / 16;      // chunks per slot row
+        static_assert(NCH % C::THREADS == 0, "whole chunks per thread");
+        const float* g = reinterpret_cast<const float*>(gate_slots + (kt % NST) * 128);
+#pragma unroll
+        for (int it = 0; it < NCH / C::THREADS; ++it) {
+            const int q = threadIdx.x + it * C::THREADS;
+            const float gv = g[q / CPR];
+            uint4* pa = reinterpret_cast<uint4*>(stage) + q;
+            float a[8], hg[8];
+            unpack8(*pa, a);
+            if constexpr (ACT == ACT_SWIGLU) {
+                float b[8];
+                unpack8(*(reinterpret_cast<const uint4*>(stage + C::A_BYTES) + q), b);
+#pragma unroll
+                for (int r = 0; r < 8; ++r) hg[r] = gv * (silu_bf(a[r]) * b[r]);
+            } else {
+#pragma unroll
+                for (int r = 0; r < 8; ++r) hg[r] = gv * act_f<ACT>(a[r]);
+            }
+            *pa = pack8(hg);
+        }
+    }
+};
+
+// G3 with g*h formed on load from the saved A (and B) and the slot-ordered
+// gates gs: dW2[e] = sum_s (g h)[s]^T dY[eti[s]]. Runs before G4, which then
+// writes dA, dB over A, B and no g*h.
+template <int ACT>
+__global__ void __launch_bounds__(CS::THREADS)
+g3h_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B,
+           const float* __restrict__ gs, const bf16_t* __restrict__ dy,
+           const int32_t* __restrict__ offsets, const int32_t* __restrict__ eti, int d, int f,
+           float* __restrict__ dw2) {
+    extern __shared__ __align__(16) char lds[];
+    using C = CSecondH<ACT>;
+    constexpr int NSRC = ACT == ACT_SWIGLU ? 2 : 1;
+    const int MT = (f + C::BM - 1) / C::BM, NT = (d + C::BN - 1) / C::BN;
+    int e, mt, nt;
+    if (!wgrad_tile(blockIdx.x, MT, NT, e, mt, nt)) return;
+    const int m0 = mt * C::BM;
+    const int n0 = nt * C::BN;
+    const int off = offsets[e];
+    const int cnt = offsets[e + 1] - off;
+    SlotMCG<C, C::BM, NSRC> la;
+    GatherMC<C, C::BN> lb;
+    NoLoader nl;
+    if (cnt > 0) {
+        la.init(A, NSRC == 2 ? B : A, f, off, m0, f, cnt, gs, lds_offset(lds) + NST * C::STAGE);
+        lb.init(dy, d, n0, d, eti + off, cnt);
+    }
+    Acc<C> acc;
+    gemm_mainloop<C>(la, lb, nl, (cnt + GBK - 1) / GBK, tail_from(cnt), lds, acc, f - m0,
+                     d - n0, GPass<ACT, C>{lds + NST * C::STAGE});
     float* out = dw2 + (int64_t)e * f * d;
     RowStage<C, 1>::run(acc, lds, [&](int, int r, int c, const f32x4& v) {
         const int m = m0 + r, n = n0 + c;
@@ -683,9 +773,11 @@ hipError_t set_lds_limits() {
         auto per_act = [&](auto act) {
             constexpr int ACT = decltype(act)::value;
             set(reinterpret_cast<const void*>(g1_kernel<ACT>), CFirst<ACT>::LDS);
-            set(reinterpret_cast<const void*>(g4_kernel<ACT>), C4::LDS);
+            set(reinterpret_cast<const void*>(g4_kernel<ACT, true>), C4::LDS);
+            set(reinterpret_cast<const void*>(g4_kernel<ACT, false>), C4::LDS);
             set(reinterpret_cast<const void*>(g5_kernel<ACT>), CFirst<ACT>::LDS);
             set(reinterpret_cast<const void*>(g2h_kernel<ACT>), CSecondH<ACT>::LDS);
+            set(reinterpret_cast<const void*>(g3h_kernel<ACT>), CSecondH<ACT>::LDS + NST * 128);
         };
         per_act(std::integral_constant<int, ACT_SWIGLU>{});
         per_act(std::integral_constant<int, ACT_SILU>{});
@@ -824,12 +916,18 @@ hipError_t ffn_fwd(const FfnArgs& a, bool f32, hipStream_t st) {
     }
 }
 
-size_t ffn_bwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool combined) {
+size_t ffn_bwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool combined,
+                         bool h_on_load) {
     const size_t S = (size_t)T * k;
     if (f32) return combined ? align256(S * d * sizeof(float)) : 0;  // dX_slot
-    const size_t hg = S * f * sizeof(bf16_t);                         // g*h, then dX strips
+    const size_t part = align256(S * g4_nparts(f) * sizeof(float));  // d_gate partials
     const size_t strip = combined ? S * strip_width(S, E, d) * sizeof(bf16_t) : 0;
-    return align256(S * g4_nparts(f) * sizeof(float)) + align256(hg > strip ? hg : strip);
+    if (h_on_load) {   // slot-ordered gates for G3, then (same space) the dX strip
+        const size_t gs = (S + GS_PAD) * sizeof(float);
+        return part + align256(gs > strip ? gs : strip);
+    }
+    const size_t hg = S * f * sizeof(bf16_t);                         // g*h, then dX strips
+    return part + align256(hg > strip ? hg : strip);
 }
 
 namespace {
@@ -861,14 +959,31 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
     }
     if (hipError_t e = set_lds_limits(); e != hipSuccess) return e;
     using C5 = CFirst<ACT>;
+    using C3H = CSecondH<ACT>;
     const int nparts = g4_nparts(a.f);
     float* part = static_cast<float*>(a.ws);
-    bf16_t* HG = reinterpret_cast<bf16_t*>(static_cast<char*>(a.ws) +
-                                           align256((size_t)S * nparts * sizeof(float)));
+    char* const ws2 = static_cast<char*>(a.ws) + align256((size_t)S * nparts * sizeof(float));
+    // default: g*h [S, f] from G4's epilogue for G3; h on load: slot-ordered
+    // gates, and G3 (run first, before G4 overwrites A and B) forms g*h itself.
+    // Either is finished with before the dX strips reuse the space.
+    float* gs = a.h_on_load ? reinterpret_cast<float*>(ws2) : nullptr;
+    bf16_t* HG = a.h_on_load ? nullptr : reinterpret_cast<bf16_t*>(ws2);
+    bf16_t* strip = reinterpret_cast<bf16_t*>(ws2);
     // non-gated: the second operand of the two-branch kernels is the first again
     const void* Bx = GATED ? a.B : a.A;
     const void* w3x = GATED ? a.w3 : a.w1;
-    hipLaunchKernelGGL(g4_kernel<ACT>, dim3(slot_grid(S, a.E, C4::BM, cdiv(a.f, C4::BN))),
+    if (a.h_on_load) {
+        hipLaunchKernelGGL(slot_gates, grid1d(S + GS_PAD, 256), dim3(256), 0, st, a.gates,
+                           a.slot_src, S, (int64_t)GS_PAD, gs);
+        probe::mark("slot_gates", st);
+        hipLaunchKernelGGL(g3h_kernel<ACT>, dim3(wgrad_grid(a.E, cdiv(a.f, C3H::BM), cdiv(a.d, C3H::BN))),
+                           dim3(C3H::THREADS), C3H::LDS + NST * 128, st, (const bf16_t*)a.A,
+                           (const bf16_t*)Bx, (const float*)gs, (const bf16_t*)a.dy, a.offsets,
+                           a.eti, a.d, a.f, a.dw2);
+        probe::mark("g3h_kernel", st);
+    }
+    auto g4 = a.h_on_load ? g4_kernel<ACT, false> : g4_kernel<ACT, true>;
+    hipLaunchKernelGGL(g4, dim3(slot_grid(S, a.E, C4::BM, cdiv(a.f, C4::BN))),
                        dim3(C4::THREADS), C4::LDS, st, (const bf16_t*)a.dy, (const bf16_t*)a.w2,
                        a.gates, a.offsets, a.eti, a.slot_src, a.d, a.f, a.E, (bf16_t*)a.A,
                        (bf16_t*)a.B, HG, part);
@@ -876,10 +991,12 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
     hipLaunchKernelGGL(dgate_reduce, grid1d(S, 256), dim3(256), 0, st, part, nparts, a.slot_src,
                        S, a.dgates);
     probe::mark("dgate_reduce", st);
-    hipLaunchKernelGGL(g3_kernel, dim3(wgrad_grid(a.E, cdiv(a.f, CS::BM), cdiv(a.d, CS::BN))),
-                       dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)HG, (const bf16_t*)a.dy,
-                       a.offsets, a.eti, a.d, a.f, a.dw2);
-    probe::mark("g3_kernel", st);
+    if (!a.h_on_load) {
+        hipLaunchKernelGGL(g3_kernel, dim3(wgrad_grid(a.E, cdiv(a.f, CS::BM), cdiv(a.d, CS::BN))),
+                           dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)HG, (const bf16_t*)a.dy,
+                           a.offsets, a.eti, a.d, a.f, a.dw2);
+        probe::mark("g3_kernel", st);
+    }
     hipLaunchKernelGGL(g5_kernel<ACT>, dim3(wgrad_grid(a.E, cdiv(a.d, C5::BM), cdiv(a.f, C5::BN))),
                        dim3(C5::THREADS), C5::LDS, st, (const bf16_t*)a.x, (const bf16_t*)a.A,
                        (const bf16_t*)a.B, a.offsets, a.eti, a.d, a.f, a.dw1, a.dw3);
@@ -894,16 +1011,16 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
         return hipGetLastError();
     }
     // combined: one column strip of dX_slot at a time, summed straight into dx;
-    // the strip reuses g*h's workspace, which G3 has finished with
+    // by default the strip reuses g*h's workspace, which G3 has finished with
     const int sw = strip_width(S, a.E, a.d);
     for (int c0 = 0; c0 < a.d; c0 += sw) {
         const int nc = min(sw, a.d - c0);
         hipLaunchKernelGGL(g6_kernel, dim3(slot_grid(S, a.E, CS::BM, cdiv(nc, CS::BN))),
                            dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)a.A, (const bf16_t*)Bx,
                            (const bf16_t*)a.w1, (const bf16_t*)w3x, a.offsets, a.d, a.f, a.E,
-                           kslices, c0, nc, (int64_t)nc, HG);
+                           kslices, c0, nc, (int64_t)nc, strip);
         probe::mark("g6_kernel", st);
-        if (hipError_t e = combine_cols(HG, nc, nullptr, a.tim, a.T, nc, a.k, false,
+        if (hipError_t e = combine_cols(strip, nc, nullptr, a.tim, a.T, nc, a.k, false,
                                         a.accumulate, static_cast<bf16_t*>(a.y) + c0, a.d, st);
             e != hipSuccess)
             return e;

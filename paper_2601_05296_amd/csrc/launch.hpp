@@ -54,7 +54,8 @@ size_t ffn_fwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool c
 hipError_t ffn_fwd(const FfnArgs& a, bool f32, hipStream_t st);
 // first layer only: A (and B) from x, nothing else
 hipError_t ffn_first(const FfnArgs& a, bool f32, hipStream_t st);
-size_t ffn_bwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool combined);
+size_t ffn_bwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool combined,
+                         bool h_on_load);
 hipError_t ffn_bwd(const FfnArgs& a, bool f32, hipStream_t st);
 
 }  // namespace moe

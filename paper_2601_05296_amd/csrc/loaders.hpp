@@ -207,6 +207,48 @@ struct SlotMC : MCBase<C, R> {
 // MC tile of a [K][ncols] matrix whose K rows come from two row ranges of the
 // same matrix: k < ksplit -> row k, k >= ksplit -> row k - ksplit; rows at or
 // beyond nrows are clamped (the other operand is zero there).
+// MC tiles of slot rows off + kr (kr < cnt, else cnt - 1) of one or two
+// row-major [S][ld] matrices (NSRC = 2: the second into the extra tile,
+// GemmCfg XA = 1), and the slice's 32 per-slot gates (float32, slot order,
+// padded with zeros past the last slot) into a 128-byte slot of the gate
+// array that follows the LDS ring. Every wave copies the same gate bytes, so
+// that all waves count the same number of copies per slice.
+template <class C, int R, int NSRC>
+struct SlotMCG : MCBase<C, R> {
+    static constexpr int NQ1 = MCBase<C, R>::NQ;
+    static constexpr int NQ = NSRC * NQ1 + 1;
+    static_assert(NSRC == 1 + C::XA && R == C::BM, "one tile per source, left operand shape");
+    const bf16_t* base0[NQ1];
+    const bf16_t* base1[NQ1];
+    const float* gs;        // gates of slots off, off + 1, ...
+    int ld, cnt;
+    uint32_t gate_lds;      // LDS offset of the gate array (NST slots of 128 bytes)
+    __device__ void init(const bf16_t* src0, const bf16_t* src1, int ld_, int64_t off, int col0,
+                         int ncols, int cnt_, const float* gates_slot, uint32_t gate_lds_) {
+        ld = ld_;
+        cnt = cnt_;
+        gs = gates_slot + off;
+        gate_lds = gate_lds_;
+#pragma unroll
+        for (int i = 0; i < NQ1; ++i) {
+            base0[i] = src0 + off * ld_ + this->colc(i, col0, ncols);
+            base1[i] = src1 + off * ld_ + this->colc(i, col0, ncols);
+        }
+    }
+    __device__ void issue(int kt, uint32_t t) {
+#pragma unroll
+        for (int i = 0; i < NQ1; ++i) {
+            int kr = kt * GBK + this->krow(i);
+            kr = kr < cnt ? kr : cnt - 1;
+            dma16(base0[i] + (int64_t)kr * ld, t + this->q(i) * 1024u);
+            if constexpr (NSRC == 2)
+                dma16(base1[i] + (int64_t)kr * ld, t + C::A_BYTES + this->q(i) * 1024u);
+        }
+        const int lane = threadIdx.x & 63;
+        if (lane < GBK / 4) dma16(gs + kt * GBK + lane * 4, gate_lds + (kt % NST) * 128u);
+    }
+};
+
 template <class C, int R>
 struct SplitRowsMC : MCBase<C, R> {
     using MCBase<C, R>::NQ;

@@ -13,8 +13,9 @@ Backward (Section 3.2):
 ``recompute=True`` is the full-recompute checkpoint policy: the forward keeps
 only the routing decision and the maps, and the backward first recomputes A
 and B with moe_ffn_recompute (bit-identical to the forward's).
-``h_on_load=True`` (MOE_H_ON_LOAD) buffers no h between the GEMMs: the second
-GEMM forms h again from A and B (bit-identical results, less memory).
+``h_on_load=True`` (MOE_H_ON_LOAD) buffers neither h in the forward nor g*h in
+the backward: the second GEMM and the dW2 GEMM form them again from A and B as
+they load them (bit-identical results, less memory, more operand traffic).
 
 What the forward keeps for the backward (the "saved activations"): the first
 layer outputs A and B [S, f] (A alone for the non-gated SiLU / ReLU experts),

@@ -95,6 +95,12 @@ def test_h_on_load_flag():
             lib.moe_ffn_fwd_workspace_size(T, d, f, E, k, fl | B.MOE_H_ON_LOAD) == h
         assert lib.moe_ffn_fwd_combine_workspace_size(T, d, f, E, k, fl) - \
             lib.moe_ffn_fwd_combine_workspace_size(T, d, f, E, k, fl | B.MOE_H_ON_LOAD) == h
+    # the backward drops g*h (the dX strip of the combined call may be larger)
+    for fl in (0, B.MOE_ACT_SILU):
+        assert lib.moe_ffn_bwd_workspace_size(T, d, f, E, k, fl) - \
+            lib.moe_ffn_bwd_workspace_size(T, d, f, E, k, fl | B.MOE_H_ON_LOAD) >= h - (S + 64) * 4 - 256
+        assert lib.moe_ffn_bwd_combine_workspace_size(T, d, f, E, k, fl | B.MOE_H_ON_LOAD) <= \
+            lib.moe_ffn_bwd_combine_workspace_size(T, d, f, E, k, fl)
     # float32 debug mode buffers no h either way
     assert lib.moe_ffn_fwd_workspace_size(T, d, f, E, k, B.MOE_F32 | B.MOE_H_ON_LOAD) == \
         lib.moe_ffn_fwd_workspace_size(T, d, f, E, k, B.MOE_F32)

@@ -458,8 +458,10 @@ def test_ffn_combined_equals_separate(dtype, T, d, f, E, k, pattern, act):
 @pytest.mark.parametrize("dtype,T,d,f,E,k,pattern,act", [c for c in COMBINED_CASES if c[0] == "bf16"])
 def test_ffn_h_on_load_bit_identical(dtype, T, d, f, E, k, pattern, act):
     """MOE_H_ON_LOAD: the second GEMM forms h from A (and B) as it loads them,
-    with G1's arithmetic, so A, B, O and y are bit-identical to the buffered
-    path, and the forward workspace drops the S x f bf16 h buffer."""
+    with G1's arithmetic, and the dW2 GEMM forms g*h from A, B and the gates
+    before G4 overwrites them, with G4's arithmetic; so A, B, O, y and every
+    gradient are bit-identical to the buffered path, and the workspaces drop
+    the S x f bf16 h and g*h buffers."""
     inp, ids, g = _layer_case(dtype, T, d, f, E, k, False, pattern)
     st = inp.store
     gated = act == "swiglu"
@@ -488,6 +490,29 @@ def test_ffn_h_on_load_bit_identical(dtype, T, d, f, E, k, pattern, act):
         torch.cuda.synchronize()
         return A, Bm, out, wsb
 
+    dy, ss = dev(st["dy"]), dev(gi["slot_src"])
+    f32 = dict(dtype=torch.float32, device="cuda")
+
+    def bwd(flags, combined, A, Bm, dx0):
+        dw1 = torch.empty((E, d, f), **f32)
+        dw3 = torch.empty((E, d, f), **f32) if gated else None
+        dw2 = torch.empty((E, f, d), **f32)
+        dg = torch.empty((T, k), **f32)
+        if combined:
+            dx = dx0.clone()
+            wsb = B.moe_ffn_bwd_combine_workspace_size(T, d, f, E, k, flags)
+            ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+            B.moe_ffn_bwd_combine(dy, x, w1, w3, w2, gates, offsets, eti, ss, tim, A, Bm, T, d, f,
+                                  E, k, flags | B.MOE_ACCUMULATE, dw1, dw3, dw2, dg, dx, ws, wsb)
+        else:
+            dx = torch.empty((S, d), dtype=torch.bfloat16, device="cuda")
+            wsb = B.moe_ffn_bwd_workspace_size(T, d, f, E, k, flags)
+            ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+            B.moe_ffn_bwd(dy, x, w1, w3, w2, gates, offsets, eti, ss, A, Bm, T, d, f, E, k, flags,
+                          dw1, dw3, dw2, dg, dx, ws, wsb)
+        torch.cuda.synchronize()
+        return dict(dw1=dw1, dw3=dw3, dw2=dw2, d_gates=dg, dx=dx, dA=A, dB=Bm), wsb
+
     for combined in (False, True):
         A0, B0, out0, ws0 = fwd(base, combined)
         A1, B1, out1, ws1 = fwd(base | B.MOE_H_ON_LOAD, combined)
@@ -496,6 +521,12 @@ def test_ffn_h_on_load_bit_identical(dtype, T, d, f, E, k, pattern, act):
             assert torch.equal(B0, B1)
         assert torch.equal(out0, out1), "combined" if combined else "O"
         assert ws0 - ws1 == (S * f * 2 + 255) // 256 * 256
+        dx0 = out0 if combined else None          # combined: accumulate onto y
+        r0, wb0 = bwd(base, combined, A0, B0, dx0)
+        r1, wb1 = bwd(base | B.MOE_H_ON_LOAD, combined, A1, B1, dx0)
+        for n in ("dw1", "dw2", "d_gates", "dx", "dA") + (("dw3", "dB") if gated else ()):
+            assert torch.equal(r0[n], r1[n]), (n, combined)
+        assert wb1 <= wb0 if combined else wb0 - wb1 >= S * f * 2 - (S + 64) * 4 - 256
 
 
 # whole layer (routing included) on the tiny float32 workload
@@ -532,16 +563,19 @@ def test_layer_recompute_policy_bit_identical(act):
     x, wg, w1, w2, dy = (dev(st[n]) for n in ("x", "w_gate", "w1", "w2", "dy"))
     w3 = dev(st["w3"]) if act == "swiglu" else None
     outs = []
-    for rc in (False, True):
-        y, saved = layer.forward(x, wg, None, w1, w3, w2, cfg.k, cfg.renorm, act=act, recompute=rc)
+    # (recompute, h_on_load): default, full recompute, no h / g*h buffers, both
+    for rc, hol in ((False, False), (True, False), (False, True), (True, True)):
+        y, saved = layer.forward(x, wg, None, w1, w3, w2, cfg.k, cfg.renorm, act=act, recompute=rc,
+                                 h_on_load=hol)
         assert (saved.A is None) == rc
         assert saved.nbytes() == pytest.approx(layer.saved_bytes_per_token(
             cfg.d, cfg.f, cfg.E, cfg.k, 2, cfg.T, act, recompute=rc) * cfg.T)
         g = layer.backward(saved, dy, x, wg, w1, w3, w2)
         torch.cuda.synchronize()
         outs.append([y] + [g[n] for n in ("dx", "dw1", "dw2", "dw_gate", "d_gates")])
-    for a, b in zip(*outs):
-        assert torch.equal(a, b)
+    for other in outs[1:]:
+        for a, b in zip(outs[0], other):
+            assert torch.equal(a, b)
 
 
 def test_layer_deterministic_bf16():
