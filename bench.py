@@ -63,6 +63,10 @@ def parse():
                          "TCP_TCC_READ_REQ_LATENCY_sum TCP_TCC_WRITE_REQ_sum "
                          "TCP_PENDING_STALL_CYCLES_sum, then SQ_VALU_MFMA_BUSY_CYCLES "
                          "SQ_BUSY_CYCLES GRBM_GUI_ACTIVE)")
+    ap.add_argument("--summarize-table1", metavar="JSON",
+                    help="write profiles/table1_sweep.txt from the last line of a --table1 run")
+    ap.add_argument("--summarize-sweep", metavar="JSON",
+                    help="write the memory-sweep summary from the last line of a --sweep run")
     ap.add_argument("--profile-command", default="",
                     help="the rocprofv3 command(s) the summarised files came from")
     ap.add_argument("--summary-out", default=None)
@@ -151,6 +155,69 @@ def summarize_stats(stats_csv, out, workload, cmd, profile_cmd):
             kernel_short_name(r["Name"])[:22], int(r["Calls"]), float(r["AverageNs"]) / 1e3,
             float(r["TotalDurationNs"]) / 1e6, float(r["Percentage"]),
             float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3))
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("wrote", out)
+
+
+def summarize_table1(json_path, out, cmd, profile_cmd):
+    """Text summary of a --table1 run (its last output line)."""
+    rows = json.loads(open(json_path).read().strip().splitlines()[-1])["table1"]
+    lines = ["# Table 1 shapes (paper Section 6.1): this path vs a materialised PyTorch MoE layer",
+             "# run: %s" % profile_cmd,
+             "# summary: python %s" % cmd,
+             "# one MI355X, bf16, f = 4d, T = batch x seq_len, plain top-k softmax gates; "
+             "device-side seeded inputs",
+             "# baseline: argsort + index_select routed-token buffer, one torch matmul (hipBLASLt) "
+             "per expert, every",
+             "#   intermediate kept by autograd (bench.materialised_step); saved bytes from "
+             "saved-tensor hooks",
+             "# bytes are per token; peak = max(forward peak, step peak less weight gradients), "
+             "inputs and weights excluded",
+             "# conf act T d f E k | ours_ms base_ms speedup | ours_saved base_saved ratio | "
+             "ours_peak base_peak ratio | ours tokens/s"]
+    for r in rows:
+        lines.append("%s %s %d %d %d %d %d | %.3f %.3f %.2fx | %.0f %.0f %.2fx | %.0f %.0f %.2fx | %.0f" % (
+            r["conf"], r["act"], r["T"], r["d"], r["f"], r["E"], r["k"], r["ours_ms"], r["base_ms"],
+            r["speedup"], r["ours_saved_bytes_per_token"], r["base_saved_bytes_per_token"],
+            r["saved_ratio"], r["ours_peak_bytes_per_token"], r["base_peak_bytes_per_token"],
+            r["base_peak_bytes_per_token"] / r["ours_peak_bytes_per_token"], r["ours_tokens_per_s"]))
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("wrote", out)
+
+
+def summarize_sweep(json_path, out, cmd, profile_cmd):
+    """Text summary of a --sweep run (its last output line)."""
+    from paper_2601_05296_amd import synth
+    res = json.loads(open(json_path).read().strip().splitlines()[-1])["sweep"]
+    c = synth.CONFIGS[res["workload"]]
+    lines = ["# Memory-capacity sweep, workload %s (d=%d f=%d E=%d k=%d, %s), one MI355X"
+             % (c.name, c.d, c.f, c.E, c.k, c.dtype),
+             "# run: %s" % profile_cmd,
+             "# summary: python %s" % cmd,
+             "# ours: one forward + backward through the C ABI (moe_ffn_fwd_combine / "
+             "moe_ffn_bwd_combine); peak =",
+             "#       max(forward allocator peak, backward allocator peak less weight gradients), "
+             "weights and inputs excluded",
+             "# baseline: materialised-permutation PyTorch layer, forward only (saved tensors + "
+             "forward temporaries;",
+             "#           a lower bound on its training peak)",
+             "# HBM: %d bytes" % res["hbm_bytes"],
+             "# T  ours_peak_B/token  ours_saved_B/token  baseline_fwd_peak_B/token  "
+             "baseline_saved_B/token"]
+    def cell(r, key, oom):
+        if key in r:
+            return "%11.1f" % r[key]
+        return "%11s" % ("OOM" if r.get(oom) else "-")
+    for r in res["points"]:
+        lines.append("%8d %s %s %s %s" % (
+            r["T"], cell(r, "ours_peak_bytes_per_token", "ours_oom"),
+            cell(r, "ours_saved_bytes_per_token", "ours_oom"),
+            cell(r, "baseline_fwd_peak_bytes_per_token", "baseline_oom"),
+            cell(r, "baseline_saved_bytes_per_token", "baseline_oom")))
+    lines.append("# largest T that fits: ours %d, materialised baseline (forward alone) %d"
+                 % (res["max_T_ours"], res["max_T_baseline_fwd"]))
     with open(out, "w") as fh:
         fh.write("\n".join(lines) + "\n")
     print("wrote", out)
@@ -541,6 +608,16 @@ def main():
         summarize_stats(args.summarize_stats,
                         args.summary_out or os.path.join(ROOT, "profiles", "kernel_stats_%s.txt" % args.workload),
                         args.workload, " ".join(sys.argv), args.profile_command)
+        return
+    if args.summarize_table1:
+        summarize_table1(args.summarize_table1,
+                         args.summary_out or os.path.join(ROOT, "profiles", "table1_sweep.txt"),
+                         " ".join(sys.argv), args.profile_command)
+        return
+    if args.summarize_sweep:
+        summarize_sweep(args.summarize_sweep,
+                        args.summary_out or os.path.join(ROOT, "profiles", "memory_sweep_mem_sweep_e64k8.txt"),
+                        " ".join(sys.argv), args.profile_command)
         return
     if args.summarize_counters:
         summarize_counters(args.summarize_counters[0], args.summarize_counters[1],
