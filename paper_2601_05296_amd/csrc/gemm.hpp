@@ -87,6 +87,14 @@ __device__ __forceinline__ void dma16(const void* g, uint32_t lds_off) {
                  ::"v"(g), "s"(lds_off) : "memory", "m0");
 }
 
+// 4-byte global -> LDS copy by one lane: lane l writes LDS bytes
+// lds_off + 4*l .. +3 (same rules as dma16; the source needs only 4-byte
+// alignment).
+__device__ __forceinline__ void dma4(const void* g, uint32_t lds_off) {
+    asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
+                 ::"v"(g), "s"(lds_off) : "memory", "m0");
+}
+
 // LDS byte offset of a pointer into the workgroup's shared memory.
 __device__ __forceinline__ uint32_t lds_offset(const void* p) {
     return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const char*)p;

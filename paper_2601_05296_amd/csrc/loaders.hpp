@@ -245,7 +245,7 @@ struct SlotMCG : MCBase<C, R> {
                 dma16(base1[i] + (int64_t)kr * ld, t + C::A_BYTES + this->q(i) * 1024u);
         }
         const int lane = threadIdx.x & 63;
-        if (lane < GBK / 4) dma16(gs + kt * GBK + lane * 4, gate_lds + (kt % NST) * 128u);
+        if (lane < GBK) dma4(gs + kt * GBK + lane, gate_lds + (kt % NST) * 128u);
     }
 };
 
