@@ -288,9 +288,11 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
     // ---- epilogue, one round per fragment row-block (64 rows of the tile) ----
     // The A and B rows of the round come into LDS by DMA (1 KB copies, many in
     // flight); every lane reads its values there, writes dA and dB back in
-    // place, and the rows then leave LDS as whole 512-byte runs. g*h follows
-    // through the same buffer. 16-byte chunks are XOR-swizzled by row, so the
-    // fragment-ordered LDS accesses (32 rows, one column) are conflict-free.
+    // place, and the rows then leave LDS as whole 512-byte runs. g*h goes out
+    // straight from registers, 16 bytes per lane (staging it through LDS as
+    // well took two more barriers per round and spilled registers: 4% slower).
+    // 16-byte chunks are XOR-swizzled by row, so the fragment-ordered LDS
+    // accesses (32 rows, one column) are conflict-free.
     constexpr int RR = C::WM * 32;       // rows per round
     constexpr int RB = C::BN * 2;        // bytes per row
     constexpr int CPR = RB / 16;         // 16-byte chunks per row (32)
@@ -389,19 +391,15 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
         }
         lds_barrier();
         if constexpr (HG_OUT) {   // false when G3 forms g*h itself (h on load)
+            if (valid) {
 #pragma unroll
-            for (int j = 0; j < C::FN; ++j)
+                for (int j = 0; j < C::FN; ++j)
 #pragma unroll
-                for (int p = 0; p < 2; ++p) {
-                    const int off = (((wc.col8(j, p) >> 3) ^ (rr & 31)) << 4);
-                    *reinterpret_cast<uint4*>(rowA + off) = hgv[j][p];
-                }
-            lds_barrier();
-            {
-                bf16_t* const dst[1] = {HG};
-                store_rows(1, dst);
+                    for (int p = 0; p < 2; ++p) {
+                        const int n = t.n0 + wc.col8(j, p);
+                        if (n < f) st16(HG + s * f + n, hgv[j][p]);
+                    }
             }
-            lds_barrier();
         }
     }
 }
