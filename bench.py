@@ -44,7 +44,7 @@ def parse():
     ap.add_argument("--recompute", action="store_true",
                     help="full-recompute checkpoint policy: save only the routing decision and "
                          "maps, recompute the first layer in the backward")
-    ap.add_argument("--cpu-seconds", type=float, default=20.0,
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-baseline-memory", action="store_true")
@@ -586,15 +586,23 @@ def cpu_oracle_baseline(inp, cfg, budget_s):
                               v["w2"], cfg.renorm)
         return time.perf_counter() - t0
 
-    n0 = 8
-    t_small = run(n0)
-    n = int(min(cfg.T, max(n0, n0 * budget_s / max(t_small, 1e-3))))
+    # two calibration runs fit time = a + b*n (a: the per-expert weight
+    # gradient work, independent of n); the timed sample is sized for budget_s
+    n0, n1 = 8, 32
+    t0 = run(n0)
+    t1 = run(n1)
+    b = max((t1 - t0) / (n1 - n0), 1e-6)
+    a = max(t0 - b * n0, 0.0)
+    # the proportional estimate n1 * budget / t1 never overshoots (a >= 0); the
+    # fit may, when the two runs differ by little more than noise: at most 2x
+    n_prop = n1 * budget_s / max(t1, 1e-3)
+    n = int(min(cfg.T, max(n1, min((budget_s - a) / b, 2.0 * n_prop))))
     t = run(n)
     cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
     return {"value": n / t, "unit": "tokens/s", "cores": cores, "kind": "oracle",
             "sample": "first %d of %d tokens of %s, whole-layer fwd+bwd in fp64 "
-                      "(%.1f s; calibration run of %d tokens %.1f s not counted)"
-                      % (n, cfg.T, cfg.name, t, n0, t_small)}
+                      "(%.1f s; calibration runs of %d and %d tokens, %.1f s, not counted)"
+                      % (n, cfg.T, cfg.name, t, n0, n1, t0 + t1)}
 
 
 def main():
@@ -767,6 +775,37 @@ def main():
         "sparse_to_sparse_tokens_per_s": round(T / ((ms_step - router_ms) * 1e-3), 1),
         "kernels": kernels,
     }
+    if not (args.h_on_load or args.recompute or args.no_baseline_memory):
+        # the other operating point of the same layer: MOE_H_ON_LOAD buffers
+        # neither h nor g*h (bit-identical results, less memory, more time)
+        def lean_step():
+            y_, s_ = layer.forward(x, wg, bias, w1, w3, w2, k, cfg.renorm, act=cfg.act,
+                                   h_on_load=True)
+            return y_, s_, layer.backward(s_, dy, x, wg, w1, w3, w2)
+        lean_step()
+        torch.cuda.synchronize()
+        torch.cuda.reset_peak_memory_stats(dev)
+        b0 = torch.cuda.memory_allocated(dev)
+        y_, s_ = layer.forward(x, wg, bias, w1, w3, w2, k, cfg.renorm, act=cfg.act, h_on_load=True)
+        torch.cuda.synchronize()
+        lf = torch.cuda.max_memory_allocated(dev) - b0
+        torch.cuda.reset_peak_memory_stats(dev)
+        g_ = layer.backward(s_, dy, x, wg, w1, w3, w2)
+        torch.cuda.synchronize()
+        lb = torch.cuda.max_memory_allocated(dev) - b0 - grad_bytes
+        del y_, s_, g_
+        n_lean = max(3, args.steps // 2)
+        t2 = time.perf_counter()
+        for _ in range(n_lean):
+            lean_step()
+        torch.cuda.synchronize()
+        t3 = time.perf_counter()
+        out["h_on_load_policy"] = {
+            "checkpoint": "A,B; h and g*h formed on load (MOE_H_ON_LOAD)",
+            "steps": n_lean, "ms_per_step": round((t3 - t2) * 1e3 / n_lean, 4),
+            "tokens_per_s": round(T * n_lean / (t3 - t2), 1),
+            "peak_activation_bytes_per_token": round(max(lf, lb) / T, 1),
+            "peak_activation_bytes_per_token_fwd_bwd": [round(lf / T, 1), round(lb / T, 1)]}
     if args.copy_calibration:
         src = torch.empty(COPY_BYTES // 2, dtype=torch.bfloat16, device=dev)
         dst = torch.empty_like(src)
