@@ -600,13 +600,23 @@ g6_kernel(const bf16_t* __restrict__ dA, const bf16_t* __restrict__ dB,
 }
 
 // d_gates[slot_src[s]] = sum of the G4 partials of slot s (fixed order)
+// (16-byte loads when a slot's nparts partials fill whole 16-byte vectors;
+// the sum runs in order p = 0..nparts-1 either way)
 __global__ void dgate_reduce(const float* __restrict__ part, int nparts,
                              const int32_t* __restrict__ slot_src, int64_t S,
                              float* __restrict__ dgates) {
     const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (s >= S) return;
+    const float* row = part + s * nparts;
     float acc = 0.f;
-    for (int p = 0; p < nparts; ++p) acc += part[s * nparts + p];
+    if ((nparts & 3) == 0) {
+        for (int p = 0; p < nparts; p += 4) {
+            const f32x4 v = *reinterpret_cast<const f32x4*>(row + p);
+            acc += v[0]; acc += v[1]; acc += v[2]; acc += v[3];
+        }
+    } else {
+        for (int p = 0; p < nparts; ++p) acc += row[p];
+    }
     dgates[slot_src[s]] = acc;
 }
 

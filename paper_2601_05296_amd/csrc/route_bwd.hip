@@ -153,16 +153,34 @@ constexpr int RB_MCH = 512;  // tokens per split of the MFMA dW_g kernel
 
 inline int epad(int E) { return (E + 31) / 32 * 32; }
 
-// dl of token t as bf16 hi/lo pairs: hl[t][e] = hi, hl[t][Ep + e] = lo
+// dl of token t as bf16 hi/lo pairs: hl[t][e] = hi, hl[t][Ep + e] = lo.
+// One wave per token. The token's k (id, gate, gate gradient) triples are read
+// once by lanes 0..k-1 and spread through LDS: every expert column then finds
+// its own entry there instead of scanning the k ids in global memory. The
+// gate sum runs in order j = 0..k-1.
 __global__ void __launch_bounds__(256)
 rb_dlogits_hilo(const float* __restrict__ dg, const float* __restrict__ logits,
                 const int32_t* __restrict__ ids, const float* __restrict__ gates, int64_t T,
                 int E, int Ep, int k, int renorm, bf16_t* __restrict__ hl) {
-    const int lane = threadIdx.x & 63;
-    const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (t >= T) return;
+    __shared__ float s_dp[4][256], s_gs[4][256];   // per wave, by expert (Ep <= 256)
+    __shared__ float s_g[4][16], s_dg[4][16];       // per wave, by slot j (k <= 16)
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int64_t t = (int64_t)blockIdx.x * 4 + w;
+    const bool valid = t < T;
+    for (int e = lane; e < Ep; e += 64) { s_dp[w][e] = 0.f; s_gs[w][e] = 0.f; }
+    __syncthreads();
+    if (valid && lane < k) {
+        const int e = ids[t * k + lane];
+        const float gj = gates[t * k + lane], dj = dg[t * k + lane];
+        s_g[w][lane] = gj;
+        s_dg[w][lane] = dj;
+        s_dp[w][e] = dj;
+        s_gs[w][e] = gj;
+    }
+    __syncthreads();
+    if (!valid) return;
     float gdg = 0.f;
-    for (int j = 0; j < k; ++j) gdg += gates[t * k + j] * dg[t * k + j];
+    for (int j = 0; j < k; ++j) gdg += s_g[w][j] * s_dg[w][j];
     const float* lt = logits + t * E;
     float mx = -INFINITY, z = 0.f;
     if (!renorm) {
@@ -175,11 +193,9 @@ rb_dlogits_hilo(const float* __restrict__ dg, const float* __restrict__ logits,
     for (int e = lane; e < Ep; e += 64) {
         float v = 0.f;
         if (e < E) {
-            float dp = 0.f, gsel = 0.f;
-            bool sel = false;
-            for (int j = 0; j < k; ++j)
-                if (ids[t * k + j] == e) { dp = dg[t * k + j]; gsel = gates[t * k + j]; sel = true; }
-            if (renorm) v = sel ? gsel * (dp - gdg) : 0.f;
+            // unselected experts: dp = 0 and (renorm) gate 0
+            const float dp = s_dp[w][e];
+            if (renorm) v = s_gs[w][e] * (dp - gdg);
             else v = (__expf(lt[e] - mx) / z) * (dp - gdg);
         }
         const uint32_t hi = f2bf(v);
@@ -295,6 +311,9 @@ __global__ void rb_dwg_reduce_hilo(const float* __restrict__ part, int nsplit, i
     const int64_t per = (int64_t)2 * Ep * d;
     const int64_t lo_off = (int64_t)Ep * d;
     float acc = 0.f;
+    // unrolled so that the loads of several splits are in flight at once; the
+    // sum still runs in split order
+#pragma unroll 8
     for (int s = 0; s < nsplit; ++s) acc += part[s * per + i] + part[s * per + lo_off + i];
     dwg[i] = acc;
 }
