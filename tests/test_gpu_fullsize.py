@@ -169,3 +169,30 @@ def test_full_size_layer(name):
     torch.cuda.synchronize()
     assert_close("dw_gate", host(dwg), dwg_r, "bf16")
     assert_close("dx_router", host(dxr), dxr_r, "bf16")
+
+
+@pytest.mark.parametrize("name", ["mid_e64k6", "table1_conf1_relu"])
+def test_full_size_h_on_load_bit_identical(name):
+    """MOE_H_ON_LOAD at full size, in the launch configuration bench.py times
+    (multi-strip combined calls): outputs and every gradient bit-identical to
+    the default policy that buffers h and g*h."""
+    cfg = _cfg(name)
+    print("full-size h-on-load case %s: T=%d d=%d f=%d E=%d k=%d act=%s"
+          % (name, cfg.T, cfg.d, cfg.f, cfg.E, cfg.k, cfg.act), flush=True)
+    inp = synth.make_inputs(cfg, with_dy=True)
+    st = inp.store
+    x, wg, w1, w3, w2, dy = (dev(st[n]) if st[n] is not None else None
+                             for n in ("x", "w_gate", "w1", "w3", "w2", "dy"))
+    bias = dev(st["bias"]) if st["bias"] is not None else None
+    outs = []
+    for hol in (False, True):
+        y, saved = layer.forward(x, wg, bias, w1, w3, w2, cfg.k, cfg.renorm, act=cfg.act,
+                                 h_on_load=hol)
+        g = layer.backward(saved, dy, x, wg, w1, w3, w2)
+        torch.cuda.synchronize()
+        outs.append([y] + [g[n] for n in ("dx", "dw1", "dw3", "dw2", "dw_gate", "d_gates")])
+    for n, a, b in zip(("y", "dx", "dw1", "dw3", "dw2", "dw_gate", "d_gates"), *outs):
+        if a is None:
+            assert b is None
+            continue
+        assert torch.equal(a, b), n
