@@ -192,8 +192,9 @@ def summarize_sweep(json_path, out, cmd, profile_cmd):
     from paper_2601_05296_amd import synth
     res = json.loads(open(json_path).read().strip().splitlines()[-1])["sweep"]
     c = synth.CONFIGS[res["workload"]]
-    lines = ["# Memory-capacity sweep, workload %s (d=%d f=%d E=%d k=%d, %s), one MI355X"
-             % (c.name, c.d, c.f, c.E, c.k, c.dtype),
+    lines = ["# Memory-capacity sweep, workload %s (d=%d f=%d E=%d k=%d, %s), one MI355X%s"
+             % (c.name, c.d, c.f, c.E, c.k, c.dtype,
+                ", this path with MOE_H_ON_LOAD (no h / g*h buffers)" if res.get("h_on_load") else ""),
              "# run: %s" % profile_cmd,
              "# summary: python %s" % cmd,
              "# ours: one forward + backward through the C ABI (moe_ffn_fwd_combine / "
@@ -501,7 +502,7 @@ def table1_sweep(args):
     return rows
 
 
-def memory_sweep(cfg, max_doublings):
+def memory_sweep(cfg, max_doublings, h_on_load=False):
     """Peak activation bytes per token and the largest T that fits, for this
     path (one forward + backward) and for the materialised-permutation
     baseline (forward only: its saved tensors plus forward temporaries, a
@@ -536,7 +537,8 @@ def memory_sweep(cfg, max_doublings):
                 torch.cuda.reset_peak_memory_stats(dev)
                 base = torch.cuda.memory_allocated(dev)
                 if which == "ours":
-                    y, saved = layer.forward(x, wg, None, w1, w3, w2, k, cfg.renorm, act=cfg.act)
+                    y, saved = layer.forward(x, wg, None, w1, w3, w2, k, cfg.renorm, act=cfg.act,
+                                             h_on_load=h_on_load)
                     sb = saved.nbytes()
                     torch.cuda.synchronize()
                     fwd_peak = torch.cuda.max_memory_allocated(dev) - base
@@ -566,7 +568,7 @@ def memory_sweep(cfg, max_doublings):
         if not ours_ok and not base_ok:
             break
     fits = lambda key: max([r["T"] for r in rows if key in r], default=0)
-    return {"workload": cfg.name, "points": rows,
+    return {"workload": cfg.name, "h_on_load": bool(h_on_load), "points": rows,
             "max_T_ours": fits("ours_peak_bytes_per_token"),
             "max_T_baseline_fwd": fits("baseline_fwd_peak_bytes_per_token"),
             "hbm_bytes": torch.cuda.get_device_properties(dev).total_memory}
@@ -638,7 +640,8 @@ def main():
     if args.sweep:
         from paper_2601_05296_amd import synth
         res = memory_sweep(synth.CONFIGS[args.workload if args.workload != "mid_e64k6" else
-                                         "mem_sweep_e64k8"], args.sweep_max_doublings)
+                                         "mem_sweep_e64k8"], args.sweep_max_doublings,
+                           h_on_load=args.h_on_load)
         print(json.dumps({"sweep": res}), flush=True)
         return
     if args.gpus != 1:
