@@ -103,7 +103,8 @@ int moe_route(const void* x, const void* w_gate, const float* bias,
  * moe_build_index -- dispatch index maps (Section 4.1 definitions, built
  * without global atomics as in Section 4.2: per-tile expert counts, one
  * prefix sum, then a stable in-tile rank and scatter).
- * In:  topk_ids [T,k] int32, each row k distinct ids in [0,E) (not checked).
+ * In:  topk_ids [T,k] int32, each row k distinct ids in [0,E), as moe_route
+ *      writes them.
  * Out: counts [E]                        tokens routed to each expert
  *      offsets [E+1]                     exclusive prefix sum of counts
  *                                        (expert_token_offsets)
@@ -114,6 +115,15 @@ int moe_route(const void* x, const void* w_gate, const float* bias,
  *      slot_src [T*k]                    t*k + j of each slot (inverse map)
  * workspace: moe_build_index_workspace_size(T,E,k) bytes of device memory.
  * Deterministic: identical inputs give bit-identical outputs.
+ * Other ids are rejected on the device, not reported: a choice whose id is
+ * outside [0,E) or repeats an earlier id of its row gets no slot and a
+ * token_index_map entry of -1, and counts / offsets leave it out, so that
+ * offsets[E] < T*k. The maps stay consistent (slots [0, offsets[E]) each
+ * written once), and every later call stays inside its buffers: moe_combine
+ * adds nothing for a -1 entry, the FFN calls write only slot rows below
+ * offsets[E] and no d_gates entry of a rejected choice, and moe_route_bwd
+ * ignores ids outside [0,E). The router gradients of a token with a rejected
+ * choice are then unspecified.
  */
 size_t moe_build_index_workspace_size(int64_t T, int E, int k);
 int moe_build_index(const int32_t* topk_ids, int64_t T, int E, int k,
@@ -150,7 +160,8 @@ int moe_ffn_fwd(const void* x, const void* w1, const void* w3, const void* w2,
  * per-token slot list (Section 3.1), and, with weights == NULL, the token
  * gradient accumulation of the backward pass (Section 3.2, step 3):
  *   out[t] = sum_{j<k} weights[t,j] * src[token_index_map[t,j]]
- * The k terms are added in order j = 0..k-1 in float32.
+ * The k terms are added in order j = 0..k-1 in float32; a token_index_map
+ * entry of -1 (a choice moe_build_index rejected) adds nothing.
  * MOE_ACCUMULATE: out[t] += (the sum) instead of overwriting.
  * In:  src [T*k, d], weights [T,k] float32 or NULL (all ones),
  *      token_index_map [T,k].

@@ -9,7 +9,8 @@
 // HBM-bound gather-reduce: one workgroup per token (several for narrow column
 // strips), 16-byte vector loads along d, all k source rows of a chunk in
 // flight before the float32 accumulation, which adds the k terms in order
-// j = 0..k-1.
+// j = 0..k-1. A token_index_map entry of -1 (a choice the index build
+// rejected) adds nothing.
 #include "common.hpp"
 #include "launch.hpp"
 #include "probe.hpp"
@@ -44,7 +45,8 @@ combine_kernel(const void* __restrict__ src_, int64_t src_ld, const float* __res
 #pragma unroll
     for (int j = 0; j < KMAX; ++j) {
         if (j < k) {
-            row[j] = (int64_t)tim[t * k + j] * src_ld;
+            const int32_t slot = tim[t * k + j];
+            row[j] = slot < 0 ? -1 : (int64_t)slot * src_ld;
             g[j] = w ? w[t * k + j] : 1.0f;
         }
     }
@@ -58,7 +60,7 @@ combine_kernel(const void* __restrict__ src_, int64_t src_ld, const float* __res
             const int c = c0 + u * lpt + lane;
 #pragma unroll
             for (int j = 0; j < KMAX; ++j)
-                if (j < k && c < nchunk)
+                if (j < k && c < nchunk && row[j] >= 0)
                 {
                     typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
                     const u32x4 x = __builtin_nontemporal_load(
@@ -75,7 +77,7 @@ combine_kernel(const void* __restrict__ src_, int64_t src_ld, const float* __res
             for (int i = 0; i < 8; ++i) acc[i] = 0.0f;
 #pragma unroll
             for (int j = 0; j < KMAX; ++j) {
-                if (j < k) {
+                if (j < k && row[j] >= 0) {
                     if (F32) {
                         acc[0] += g[j] * __uint_as_float(v[u][j].x);
                         acc[1] += g[j] * __uint_as_float(v[u][j].y);

@@ -441,12 +441,15 @@ g3_kernel(const bf16_t* __restrict__ HG, const bf16_t* __restrict__ dy,
     });
 }
 
-// gs[s] = gates[slot_src[s]] for s < S, 0 for S <= s < S + pad (the gate of
-// each slot in slot order, for the dW2 GEMM's pre-pass)
+// gs[s] = gates[slot_src[s]] for the filled slots s < offsets[E], 0 for the
+// rest up to S + pad (the gate of each slot in slot order, for the dW2 GEMM's
+// pre-pass; fewer than S slots are filled only when the index build rejected
+// choices)
 __global__ void slot_gates(const float* __restrict__ gates, const int32_t* __restrict__ slot_src,
-                           int64_t S, int64_t pad, float* __restrict__ gs) {
+                           const int32_t* __restrict__ offsets, int E, int64_t S, int64_t pad,
+                           float* __restrict__ gs) {
     const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (s < S) gs[s] = gates[slot_src[s]];
+    if (s < offsets[E]) gs[s] = gates[slot_src[s]];
     else if (s < S + pad) gs[s] = 0.0f;
 }
 constexpr int GS_PAD = 64;   // zero gates past the last slot (a slice reads up to 31 more)
@@ -603,10 +606,11 @@ g6_kernel(const bf16_t* __restrict__ dA, const bf16_t* __restrict__ dB,
 // (16-byte loads when a slot's nparts partials fill whole 16-byte vectors;
 // the sum runs in order p = 0..nparts-1 either way)
 __global__ void dgate_reduce(const float* __restrict__ part, int nparts,
-                             const int32_t* __restrict__ slot_src, int64_t S,
+                             const int32_t* __restrict__ slot_src,
+                             const int32_t* __restrict__ offsets, int E, int64_t S,
                              float* __restrict__ dgates) {
     const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (s >= S) return;
+    if (s >= S || s >= offsets[E]) return;
     const float* row = part + s * nparts;
     float acc = 0.f;
     if ((nparts & 3) == 0) {
@@ -647,6 +651,7 @@ __global__ void f32_g1(const float* x, const float* w1, const float* w3, const i
     if (id >= S * f) return;
     const int64_t s = id / f;
     const int n = (int)(id % f);
+    if (s >= offsets[E]) return;
     const int e = expert_of(offsets, E, s);
     const float* xr = x + (int64_t)eti[s] * d;
     float a = 0.f, b = 0.f;
@@ -697,7 +702,7 @@ __global__ void f32_g4(const float* dy, const float* w2, const float* gates,
                        const int32_t* offsets, const int32_t* eti, const int32_t* slot_src,
                        int64_t S, int d, int f, int E, float* A, float* B, float* dgates) {
     const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (s >= S) return;
+    if (s >= S || s >= offsets[E]) return;
     const int e = expert_of(offsets, E, s);
     const float* dyr = dy + (int64_t)eti[s] * d;
     const float g = gates[slot_src[s]];
@@ -982,7 +987,7 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
     const void* w3x = GATED ? a.w3 : a.w1;
     if (a.h_on_load) {
         hipLaunchKernelGGL(slot_gates, grid1d(S + GS_PAD, 256), dim3(256), 0, st, a.gates,
-                           a.slot_src, S, (int64_t)GS_PAD, gs);
+                           a.slot_src, a.offsets, a.E, S, (int64_t)GS_PAD, gs);
         probe::mark("slot_gates", st);
         hipLaunchKernelGGL(g3h_kernel<ACT>, dim3(wgrad_grid(a.E, cdiv(a.f, C3H::BM), cdiv(a.d, C3H::BN))),
                            dim3(C3H::THREADS), C3H::LDS + NST * 128, st, (const bf16_t*)a.A,
@@ -997,7 +1002,7 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
                        (bf16_t*)a.B, HG, part);
     probe::mark("g4_kernel", st);
     hipLaunchKernelGGL(dgate_reduce, grid1d(S, 256), dim3(256), 0, st, part, nparts, a.slot_src,
-                       S, a.dgates);
+                       a.offsets, a.E, S, a.dgates);
     probe::mark("dgate_reduce", st);
     if (!a.h_on_load) {
         hipLaunchKernelGGL(g3_kernel, dim3(wgrad_grid(a.E, cdiv(a.f, CS::BM), cdiv(a.d, CS::BN))),

@@ -21,6 +21,11 @@
 //                   earlier waves and chunks. Slots are therefore assigned in
 //                   ascending token order inside every expert, as in the
 //                   paper's worked example, and the result is deterministic.
+//
+// A choice whose id lies outside [0, E) or repeats an earlier id of its row
+// (top-k never produces either) is rejected by both passes alike: it gets no
+// slot and its token_index_map entry is -1. Every slot below offsets[E] is
+// then written exactly once, whatever the ids hold.
 #include "common.hpp"
 #include "launch.hpp"
 #include "probe.hpp"
@@ -32,6 +37,16 @@ constexpr int IDX_THREADS = 256;
 constexpr int MAX_TILES = 1024;
 
 // tokens per tile: a multiple of 256 keeping the number of tiles <= MAX_TILES
+// does choice j of a row take a slot: its id is in [0, E) and differs from the
+// ids of the row's earlier choices
+__device__ inline bool choice_ok(const int32_t* row, int j, int E) {
+    const int e = row[j];
+    if ((unsigned)e >= (unsigned)E) return false;
+    for (int i = 0; i < j; ++i)
+        if (row[i] == e) return false;
+    return true;
+}
+
 inline int64_t tile_tokens(int64_t T) {
     int64_t tb = (T + MAX_TILES - 1) / MAX_TILES;
     tb = ((tb + IDX_THREADS - 1) / IDX_THREADS) * IDX_THREADS;
@@ -46,10 +61,14 @@ tile_hist(const int32_t* __restrict__ ids, int64_t T, int E, int k, int64_t tb, 
     const int b = blockIdx.x;
     for (int e = tid; e < E; e += IDX_THREADS) c[e] = 0;
     __syncthreads();
-    const int64_t lo = (int64_t)b * tb * k;
-    int64_t hi = lo + tb * k;
-    if (hi > T * k) hi = T * k;
-    for (int64_t i = lo + tid; i < hi; i += IDX_THREADS) atomicAdd(&c[ids[i]], 1);
+    const int64_t t_lo = (int64_t)b * tb;
+    int64_t t_hi = t_lo + tb;
+    if (t_hi > T) t_hi = T;
+    for (int64_t t = t_lo + tid; t < t_hi; t += IDX_THREADS) {
+        const int32_t* row = ids + t * k;
+        for (int j = 0; j < k; ++j)
+            if (choice_ok(row, j, E)) atomicAdd(&c[row[j]], 1);
+    }
     __syncthreads();
     for (int e = tid; e < E; e += IDX_THREADS) cnt[(int64_t)e * ntiles + b] = c[e];
 }
@@ -120,13 +139,21 @@ tile_rank(const int32_t* __restrict__ ids, int64_t T, int E, int k, int64_t tb, 
         for (int i = tid; i < nt * k; i += IDX_THREADS) chunk_ids[i] = ids[c0 * k + i];
         __syncthreads();
         const bool valid = tid < nt;
+        unsigned ok = 0;   // bit j: choice j of this lane's token takes a slot
         if (valid)
             for (int j = 0; j < k; ++j)
-                atomicOr(&mask[wv][chunk_ids[tid * k + j]], 1ull << lane);
+                if (choice_ok(chunk_ids + tid * k, j, E)) {
+                    ok |= 1u << j;
+                    atomicOr(&mask[wv][chunk_ids[tid * k + j]], 1ull << lane);
+                }
         __syncthreads();
         if (valid) {
             const int64_t t = c0 + tid;
             for (int j = 0; j < k; ++j) {
+                if (!((ok >> j) & 1u)) {
+                    chunk_tim[tid * k + j] = -1;
+                    continue;
+                }
                 const int e = chunk_ids[tid * k + j];
                 int r = run[e] + __popcll(mask[wv][e] & below);
                 for (int w = 0; w < wv; ++w) r += __popcll(mask[w][e]);

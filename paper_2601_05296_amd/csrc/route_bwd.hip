@@ -174,8 +174,10 @@ rb_dlogits_hilo(const float* __restrict__ dg, const float* __restrict__ logits,
         const float gj = gates[t * k + lane], dj = dg[t * k + lane];
         s_g[w][lane] = gj;
         s_dg[w][lane] = dj;
-        s_dp[w][e] = dj;
-        s_gs[w][e] = gj;
+        if ((unsigned)e < (unsigned)E) {   // ids outside [0, E) address no logit
+            s_dp[w][e] = dj;
+            s_gs[w][e] = gj;
+        }
     }
     __syncthreads();
     if (!valid) return;

@@ -72,6 +72,171 @@ def test_build_index_deterministic():
 
 
 # ---------------------------------------------------------------------------
+# ids top-k never produces (outside [0, E), or repeated within a row): the
+# index build rejects such a choice and every later call stays in bounds.
+# Expected values come from the oracle with each rejected choice sent to an
+# extra, last expert whose weights are zero: its slots come after all others
+# and it adds exactly nothing.
+# ---------------------------------------------------------------------------
+
+def _corrupt_ids(T, E, k, seed, frac):
+    ids = _ids_case(T, E, k, None, seed=seed)
+    rng = np.random.default_rng(seed + 1)
+    bad = [-1, E, 1 << 30, -(1 << 31)]
+    for t in np.nonzero(rng.random(T) < frac)[0]:
+        j = int(rng.integers(k))
+        kind = int(rng.integers(5))
+        ids[t, j] = ids[t, int(rng.integers(j))] if (kind == 4 and j > 0) else bad[kind % 4]
+    return ids
+
+
+def _rejected(ids, E):
+    """Brute force: a choice is rejected when its id is outside [0, E) or
+    equals an earlier id of its row."""
+    T, k = ids.shape
+    rej = np.zeros((T, k), bool)
+    for t in range(T):
+        for j in range(k):
+            e = int(ids[t, j])
+            rej[t, j] = not 0 <= e < E or e in ids[t, :j].tolist()
+    return rej
+
+
+def _sink_index(ids, rej, E):
+    return oracle.build_index(np.where(rej, E, ids), E + 1)
+
+
+@pytest.mark.parametrize("T,E,k,frac", [
+    (300, 8, 2, 0.2), (1000, 64, 6, 0.3), (777, 256, 16, 0.5), (513, 16, 4, 1.0), (1, 4, 2, 1.0),
+    (200, 8, 3, None)])
+def test_build_index_rejects_invalid_ids(T, E, k, frac):
+    if frac is None:   # every choice rejected
+        ids = np.full((T, k), -1, np.int32)
+    else:
+        ids = _corrupt_ids(T, E, k, seed=T, frac=frac)
+    rej = _rejected(ids, E)
+    assert rej.any()
+    ref = _sink_index(ids, rej, E)
+    got = _gpu_index(ids, E)
+    n = int(ref.offsets[E])
+    assert n == T * k - int(rej.sum())
+    assert np.array_equal(got["counts"], ref.counts[:E])
+    assert np.array_equal(got["offsets"], ref.offsets[:E + 1])
+    assert np.array_equal(got["eti"][:n], ref.eti[:n])
+    assert np.array_equal(got["slot_src"][:n], ref.slot_src[:n])
+    assert np.array_equal(got["tim"], np.where(rej, -1, ref.tim))
+
+
+@pytest.mark.parametrize("dtype,act,h_on_load,combined", [
+    ("bf16", "swiglu", False, True), ("bf16", "swiglu", True, True), ("bf16", "swiglu", False, False),
+    ("bf16", "relu", False, True), ("f32", "swiglu", False, False)])
+def test_ffn_with_rejected_choices(dtype, act, h_on_load, combined):
+    T, d, f, E, k = 300, 256, 384, 8, 3
+    inp, _, g = _layer_case(dtype, T, d, f, E, k, False, None)
+    ids = _corrupt_ids(T, E, k, seed=3, frac=0.3)
+    ids[:5] = -1                      # tokens with no valid choice at all
+    rej = _rejected(ids, E)
+    v, st = inp.vals, inp.store
+    gated = act == "swiglu"
+    S = T * k
+    # oracle with the rejected choices on a zero-weight last expert
+    ix = _sink_index(ids, rej, E)
+
+    def z(w):
+        return np.concatenate([w, np.zeros((1,) + w.shape[1:])])
+
+    if gated:
+        A_r, B_r, O_r = oracle.ffn_fwd(v["x"], z(v["w1"]), z(v["w3"]), z(v["w2"]), ix, k)
+        bw = oracle.ffn_bwd(v["dy"], v["x"], z(v["w1"]), z(v["w3"]), z(v["w2"]), g, ix, A_r, B_r)
+    else:
+        A_r, O_r = oracle.ffn_fwd_act(v["x"], z(v["w1"]), z(v["w2"]), ix, k, act)
+        bw = oracle.ffn_bwd_act(v["dy"], v["x"], z(v["w1"]), z(v["w2"]), g, ix, A_r, act)
+    y_r = oracle.combine(O_r, g, ix.tim)
+    dx_r = oracle.combine(bw["dX_slot"], None, ix.tim)
+    # device, on the ids as they are
+    gi = _gpu_index(ids, E)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    x, w1, w2, dy = (dev(st[n]) for n in ("x", "w1", "w2", "dy"))
+    w3 = dev(st["w3"]) if gated else None
+    offsets, eti, tim, ss = (dev(gi[n]) for n in ("offsets", "eti", "tim", "slot_src"))
+    gates = dev(g)
+    flags = B.dtype_flag(x) | B.ACT_FLAG[act] | (B.MOE_H_ON_LOAD if h_on_load else 0)
+    nan = float("nan")
+    A = torch.full((S, f), nan, dtype=tdt, device="cuda")
+    Bm = torch.full((S, f), nan, dtype=tdt, device="cuda") if gated else None
+    y = torch.empty((T, d), dtype=tdt, device="cuda")
+    f32 = dict(dtype=torch.float32, device="cuda")
+    dw1 = torch.full((E, d, f), nan, **f32)
+    dw3 = torch.full((E, d, f), nan, **f32) if gated else None
+    dw2 = torch.full((E, f, d), nan, **f32)
+    dg = torch.full((T, k), nan, **f32)
+    dx = torch.empty((T, d), dtype=tdt, device="cuda")
+    if combined:
+        wsb = B.moe_ffn_fwd_combine_workspace_size(T, d, f, E, k, flags)
+        ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+        B.moe_ffn_fwd_combine(x, w1, w3, w2, offsets, eti, gates, tim, T, d, f, E, k, flags,
+                              A, Bm, y, ws, wsb)
+        wsb = B.moe_ffn_bwd_combine_workspace_size(T, d, f, E, k, flags)
+        ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+        B.moe_ffn_bwd_combine(dy, x, w1, w3, w2, gates, offsets, eti, ss, tim, A, Bm, T, d, f,
+                              E, k, flags, dw1, dw3, dw2, dg, dx, ws, wsb)
+    else:
+        # rows of O and dX_slot past offsets[E] are never written: NaN there
+        # would reach y or dx if the combine read them
+        O = torch.full((S, d), nan, dtype=tdt, device="cuda")
+        wsb = B.moe_ffn_fwd_workspace_size(T, d, f, E, k, flags)
+        ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+        B.moe_ffn_fwd(x, w1, w3, w2, offsets, eti, T, d, f, E, k, flags, A, Bm, O, ws, wsb)
+        B.moe_combine(O, gates, tim, T, d, k, B.dtype_flag(x), y)
+        dX = torch.full((S, d), nan, dtype=tdt, device="cuda")
+        wsb = B.moe_ffn_bwd_workspace_size(T, d, f, E, k, flags)
+        ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+        B.moe_ffn_bwd(dy, x, w1, w3, w2, gates, offsets, eti, ss, A, Bm, T, d, f, E, k, flags,
+                      dw1, dw3, dw2, dg, dX, ws, wsb)
+        B.moe_combine(dX, None, tim, T, d, k, B.dtype_flag(x), dx)
+    torch.cuda.synchronize()
+    assert_close("y", host(y), y_r, dtype)
+    assert np.all(host(y)[:5] == 0)
+    assert_close("dx", host(dx), dx_r, dtype)
+    assert_close("dw1", host(dw1), bw["dw1"][:E], dtype)
+    assert_close("dw2", host(dw2), bw["dw2"][:E], dtype)
+    if gated:
+        assert_close("dw3", host(dw3), bw["dw3"][:E], dtype)
+    got_dg = host(dg)
+    assert_close("d_gates", got_dg[~rej], bw["d_gates"][~rej], dtype)
+    assert np.all(np.isnan(got_dg[rej]))     # not written
+
+
+@pytest.mark.parametrize("renorm", [False, True])
+def test_route_bwd_ignores_invalid_ids(renorm):
+    T, d, E, k = 500, 256, 64, 6
+    cfg = synth.MoEConfig("rb", T=T, d=d, f=128, E=E, k=k, dtype="bf16", renorm=renorm)
+    inp = synth.make_inputs(cfg)
+    v = inp.vals
+    ids, gates, logits, _ = oracle.route(v["x"], v["w_gate"], None, k, renorm)
+    rng = np.random.default_rng(9)
+    bad_rows = rng.random(T) < 0.3
+    bad_ids = ids.copy()
+    for t in np.nonzero(bad_rows)[0]:
+        bad_ids[t, int(rng.integers(k))] = [-1, E, 1 << 30, -(1 << 31)][int(rng.integers(4))]
+    dgates = rng.standard_normal((T, k))
+    clean = ~bad_rows
+    _, _, dx_r = oracle.route_bwd(dgates[clean], logits[clean], ids[clean], v["x"][clean],
+                                  v["w_gate"], renorm)
+    x, wg = dev(inp.store["x"]), dev(inp.store["w_gate"])
+    flags = B.dtype_flag(x) | (B.MOE_RENORM if renorm else 0)
+    dwg = torch.empty((E, d), dtype=torch.float32, device="cuda")
+    dx = torch.empty((T, d), dtype=torch.bfloat16, device="cuda")
+    wsb = B.moe_route_bwd_workspace_size(T, d, E, k, flags)
+    ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+    B.moe_route_bwd(dev(dgates.astype(np.float32)), dev(logits.astype(np.float32)), dev(bad_ids),
+                    dev(gates.astype(np.float32)), x, wg, T, d, E, k, flags, dwg, dx, ws, wsb)
+    torch.cuda.synchronize()
+    assert np.all(np.isfinite(host(dwg))) and np.all(np.isfinite(host(dx)))
+    assert_close("dx (clean tokens)", host(dx)[clean], dx_r, "bf16")
+
+
+# ---------------------------------------------------------------------------
 # moe_route
 # ---------------------------------------------------------------------------
 
