@@ -27,7 +27,7 @@
  *    float32 in both modes; index arrays are int32.
  *  - A slot is one (token, chosen expert) pair; there are S = T*k slots,
  *    grouped by expert and, inside an expert, by ascending token id.
- *  - Limits: 1 <= k <= min(E, 16), 1 <= E <= 256, d and f multiples of 128,
+ *  - Limits: 1 <= k <= min(E, 16), 1 <= E <= 256, d and f multiples of 64,
  *    T*k < 2^31. T == 0 is a no-op returning MOE_OK. All pointers must be
  *    16-byte aligned.
  *  - Calls that share output or workspace buffers must be ordered on one

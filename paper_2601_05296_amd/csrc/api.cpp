@@ -59,7 +59,7 @@ int check_common(const char* fn, int64_t T, int E, int k, unsigned flags) {
 
 int check_dim(const char* fn, const char* name, int v) {
     if (v < 1) return fail(MOE_ERR_INVALID_ARG, "%s: %s = %d < 1", fn, name, v);
-    if (v % 128) return fail(MOE_ERR_UNSUPPORTED, "%s: %s = %d is not a multiple of 128", fn, name, v);
+    if (v % 64) return fail(MOE_ERR_UNSUPPORTED, "%s: %s = %d is not a multiple of 64", fn, name, v);
     return MOE_OK;
 }
 

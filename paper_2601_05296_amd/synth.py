@@ -74,6 +74,10 @@ CONFIGS = {
                                  k=8, dtype="bf16", zipf_s=1.2),
     "mem_sweep_e64k8": MoEConfig("mem_sweep_e64k8", T=16384, d=4096, f=2048, E=64,
                                  k=8, dtype="bf16"),
+    # widths that are multiples of 64 but not of 128 (partial column tiles in
+    # every GEMM), at the shape of a current 128-expert top-4 model layer
+    "d2880_e128k4": MoEConfig("d2880_e128k4", T=16384, d=2880, f=2880, E=128, k=4,
+                              dtype="bf16"),
 }
 
 # The seven configurations of the paper's Table 1 (Section 6.1): input width

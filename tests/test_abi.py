@@ -42,7 +42,8 @@ FAKE = 1 << 20  # an aligned non-null address that is never dereferenced
     (dict(T=10, d=128, E=8, k=9), B.MOE_ERR_INVALID_ARG),    # k > E
     (dict(T=10, d=128, E=8, k=0), B.MOE_ERR_INVALID_ARG),
     (dict(T=-1, d=128, E=8, k=2), B.MOE_ERR_INVALID_ARG),
-    (dict(T=10, d=100, E=8, k=2), B.MOE_ERR_UNSUPPORTED),    # d % 128
+    (dict(T=10, d=100, E=8, k=2), B.MOE_ERR_UNSUPPORTED),    # d % 64
+    (dict(T=10, d=96, E=8, k=2), B.MOE_ERR_UNSUPPORTED),     # d % 64
     (dict(T=10, d=128, E=300, k=2), B.MOE_ERR_UNSUPPORTED),  # E > 256
     (dict(T=10, d=128, E=64, k=17), B.MOE_ERR_UNSUPPORTED),  # k > 16
     (dict(T=1 << 30, d=128, E=64, k=8), B.MOE_ERR_UNSUPPORTED),  # T*k >= 2^31

@@ -26,7 +26,7 @@ from tests.parity import assert_close, dev, host, near_tie_ok
 pytestmark = pytest.mark.gpu
 
 CASES = ["mid_e64k6", "few_large_e8k2", "many_small_zipf", "mem_sweep_e64k8", "zipf_empty",
-         "table1_conf4", "table1_conf1_relu"]
+         "table1_conf4", "table1_conf1_relu", "d2880_e128k4"]
 NTOK = 12      # sampled tokens
 NCOL = 8       # sampled hidden columns
 

@@ -243,7 +243,8 @@ def test_route_bwd_ignores_invalid_ids(renorm):
 @pytest.mark.parametrize("dtype,T,d,E,k,renorm,bias", [
     ("bf16", 1000, 256, 8, 2, False, None), ("bf16", 1000, 512, 64, 6, True, None),
     ("bf16", 777, 256, 128, 8, False, "zipf"), ("bf16", 300, 384, 200, 16, False, "dead"),
-    ("f32", 1000, 256, 8, 2, False, None), ("f32", 500, 256, 64, 6, True, "dead")])
+    ("f32", 1000, 256, 8, 2, False, None), ("f32", 500, 256, 64, 6, True, "dead"),
+    ("bf16", 700, 320, 64, 6, True, None)])
 def test_route_parity(dtype, T, d, E, k, renorm, bias):
     cfg = synth.MoEConfig("r", T=T, d=d, f=128, E=E, k=k, dtype=dtype, renorm=renorm,
                           zipf_s=1.2 if bias == "zipf" else 0.0,
@@ -319,6 +320,9 @@ FFN_CASES = [
     ("bf16", 500, 384, 128, 12, 3, False, "dead"),
     ("f32", 300, 256, 384, 8, 2, False, None),
     ("f32", 257, 128, 256, 16, 4, True, "dead"),
+    # d and f odd multiples of 64: partial column tiles in every GEMM
+    ("bf16", 300, 320, 192, 8, 2, False, None),
+    ("f32", 200, 192, 320, 8, 3, False, None),
 ]
 
 
@@ -393,7 +397,8 @@ def test_ffn_fwd_bwd_parity(dtype, T, d, f, E, k, renorm, pattern):
     ("bf16", 1000, 256, 8, 2, False, False), ("bf16", 2500, 512, 64, 6, True, True),
     ("bf16", 1500, 256, 128, 8, False, True), ("bf16", 777, 384, 200, 16, True, False),
     ("f32", 1000, 256, 8, 2, False, False),
-    ("f32", 700, 128, 32, 4, True, True)])
+    ("f32", 700, 128, 32, 4, True, True),
+    ("bf16", 900, 192, 64, 6, False, True), ("bf16", 600, 320, 256, 8, True, False)])
 def test_route_bwd_parity(dtype, T, d, E, k, renorm, accumulate):
     cfg = synth.MoEConfig("rb", T=T, d=d, f=128, E=E, k=k, dtype=dtype, renorm=renorm)
     inp = synth.make_inputs(cfg)
@@ -433,6 +438,7 @@ NONGATED_CASES = [
     ("bf16", 500, 384, 128, 12, 3, False, "dead", "silu"),
     ("f32", 300, 256, 384, 8, 2, False, None, "relu"),
     ("f32", 257, 128, 256, 16, 4, True, "dead", "silu"),
+    ("bf16", 400, 192, 320, 8, 2, False, "zipf", "relu"),
 ]
 
 
@@ -528,6 +534,7 @@ COMBINED_CASES = [
     ("bf16", 333, 384, 256, 12, 3, "dead", "silu"),
     ("bf16", 500, 640, 384, 16, 4, "zipf", "relu"),
     ("f32", 257, 256, 256, 8, 2, None, "swiglu"),
+    ("bf16", 500, 576, 448, 16, 4, None, "swiglu"),
     # 393k slots: three strips of 256 columns (bit-exactness only; the
     # full-size tests check multi-strip workloads against the oracle)
     ("bf16", 49152, 768, 256, 16, 8, None, "swiglu"),
