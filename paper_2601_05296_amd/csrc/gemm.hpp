@@ -256,49 +256,75 @@ __device__ __forceinline__ void gemm_mainloop(LA& la, LB0& lb0, LB1& lb1, int nk
     // fragments of this wave that hold real outputs (wave-uniform)
     const int nfm = min(C::FM, max(0, (arows - wm * C::WTM + 31) >> 5));
     const int nfn = min(C::FN, max(0, (bcols - wn * C::WTN + 31) >> 5));
-    auto loop = [&](auto partial) {
+    // the MFMAs of slice kt (fragments read from its LDS stage)
+    auto mma = [&](int kt, auto partial) {
         constexpr bool PART = decltype(partial)::value;
-        for (int kt = 0; kt < nk; ++kt) {
-            if (kt + NST - 1 < nk) issue(kt + NST - 1);
-            if constexpr (PRE::active) {
-                pre(lds + (kt % NST) * C::STAGE, kt);
-                lds_barrier();
-            }
-            const char* cur = lds + (kt % NST) * C::STAGE;
+        const char* cur = lds + (kt % NST) * C::STAGE;
 #pragma unroll
-            for (int kk = 0; kk < GBK / 16; ++kk) {
-                bf16x8 fa[C::FM];
+        for (int kk = 0; kk < GBK / 16; ++kk) {
+            bf16x8 fa[C::FM];
+#pragma unroll
+            for (int i = 0; i < C::FM; ++i)
+                if (!PART || (i < nfm && nfn > 0))
+                    fa[i] = frag<LA::MC, C::BM>(cur, wm * C::WTM + i * 32, kk, lane);
+#pragma unroll
+            for (int b = 0; b < C::NB; ++b) {
+                const char* bt = cur + C::AREG + b * C::B_BYTES;
+                bf16x8 fb[C::FN];
+#pragma unroll
+                for (int j = 0; j < C::FN; ++j)
+                    if (!PART || (j < nfn && nfm > 0))
+                        fb[j] = frag<LB0::MC, C::BN>(bt, wn * C::WTN + j * 32, kk, lane);
 #pragma unroll
                 for (int i = 0; i < C::FM; ++i)
-                    if (!PART || (i < nfm && nfn > 0))
-                        fa[i] = frag<LA::MC, C::BM>(cur, wm * C::WTM + i * 32, kk, lane);
-#pragma unroll
-                for (int b = 0; b < C::NB; ++b) {
-                    const char* bt = cur + C::AREG + b * C::B_BYTES;
-                    bf16x8 fb[C::FN];
 #pragma unroll
                     for (int j = 0; j < C::FN; ++j)
-                        if (!PART || (j < nfn && nfm > 0))
-                            fb[j] = frag<LB0::MC, C::BN>(bt, wn * C::WTN + j * 32, kk, lane);
-#pragma unroll
-                    for (int i = 0; i < C::FM; ++i)
-#pragma unroll
-                        for (int j = 0; j < C::FN; ++j)
-                            if (!PART || (i < nfm && j < nfn))
-                                acc[b][i][j] = mfma32x32x16(fb[j], fa[i], acc[b][i][j]);
-                }
-            }
-            if (kt + 1 < nk) {
-                // slice kt+1 has landed once only the copies of later slices remain
-                if (kt + NST - 1 < nk) wait_vmcnt<PER * (NST - 2)>();
-                else wait_vmcnt<0>();
-                barrier_only();
-                fix_tail(kt + 1);
+                        if (!PART || (i < nfm && j < nfn))
+                            acc[b][i][j] = mfma32x32x16(fb[j], fa[i], acc[b][i][j]);
             }
         }
     };
-    if (nfm == C::FM && nfn == C::FN) loop(std::false_type{});
-    else loop(std::true_type{});
+    if constexpr (!PRE::active) {
+        auto loop = [&](auto partial) {
+            for (int kt = 0; kt < nk; ++kt) {
+                if (kt + NST - 1 < nk) issue(kt + NST - 1);
+                mma(kt, partial);
+                if (kt + 1 < nk) {
+                    // slice kt+1 has landed once only the copies of later slices remain
+                    if (kt + NST - 1 < nk) wait_vmcnt<PER * (NST - 2)>();
+                    else wait_vmcnt<0>();
+                    barrier_only();
+                    fix_tail(kt + 1);
+                }
+            }
+        };
+        if (nfm == C::FM && nfn == C::FN) loop(std::false_type{});
+        else loop(std::true_type{});
+    } else {
+        // The pre-pass runs one slice ahead of the MFMAs: slice kt is
+        // multiplied, then slice kt+1 (landed) is transformed in its own stage
+        // while the last MFMAs drain, and slice kt+2 is in flight. (Running the
+        // pre-pass first on every other wave, so that the two waves of a SIMD
+        // overlap vector ALU and MFMA work, measured slower.)
+        static_assert(NST == 3, "stages: multiplied, transformed, in flight");
+        pre(lds, 0);
+        lds_barrier();
+        auto loop = [&](auto partial) {
+            for (int kt = 0; kt < nk; ++kt) {
+                if (kt + 1 < nk) {
+                    wait_vmcnt<0>();   // slice kt+1, the last one issued, has landed
+                    barrier_only();
+                    fix_tail(kt + 1);
+                }
+                if (kt + NST - 1 < nk) issue(kt + NST - 1);   // into the stage slice kt-1 left
+                mma(kt, partial);
+                if (kt + 1 < nk) pre(lds + ((kt + 1) % NST) * C::STAGE, kt + 1);
+                lds_barrier();
+            }
+        };
+        if (nfm == C::FM && nfn == C::FN) loop(std::false_type{});
+        else loop(std::true_type{});
+    }
     // every wave is done reading LDS before an epilogue reuses it
     __syncthreads();
 }
