@@ -190,29 +190,52 @@ g2_kernel(const bf16_t* __restrict__ H, const bf16_t* __restrict__ w2,
 // B's, in the extra tile) become h = SiLU(A) * B (act(A) when non-gated) in
 // place, with the arithmetic of G1's epilogue, so h is bit-identical to the
 // buffered one. Layout-oblivious: A and B tiles share one swizzled layout.
+// Each thread owns NIT 16-byte chunks. The work comes in three parts so that
+// the main loop can spread it between the MFMAs of the previous slice: load
+// (LDS reads), pair(p) (elements 2p and 2p+1 of the thread's chunks) and store.
 template <int ACT, class C>
 struct HPass {
     static constexpr bool active = true;
-    __device__ void operator()(char* stage, int) const {
-        constexpr int NCH = C::A_BYTES / 16;
-        static_assert(NCH % C::THREADS == 0, "whole chunks per thread");
+    static constexpr int NIT = C::A_BYTES / 16 / C::THREADS;
+    static constexpr int NPAIR = NIT * 4;
+    static_assert(C::A_BYTES / 16 % C::THREADS == 0, "whole chunks per thread");
+    struct St { uint32_t a[NPAIR], b[NPAIR]; };   // one bf16 pair per word
+    __device__ void load(const char* stage, int, St& st) const {
 #pragma unroll
-        for (int it = 0; it < NCH / C::THREADS; ++it) {
+        for (int it = 0; it < NIT; ++it) {
             const int q = threadIdx.x + it * C::THREADS;
-            uint4* pa = reinterpret_cast<uint4*>(stage) + q;
-            float a[8], h[8];
-            unpack8(*pa, a);
+            const uint4 va = ld16(stage + q * 16);
+            st.a[4 * it] = va.x; st.a[4 * it + 1] = va.y; st.a[4 * it + 2] = va.z; st.a[4 * it + 3] = va.w;
             if constexpr (ACT == ACT_SWIGLU) {
-                float b[8];
-                unpack8(*(reinterpret_cast<const uint4*>(stage + C::A_BYTES) + q), b);
-#pragma unroll
-                for (int r = 0; r < 8; ++r) h[r] = silu_bf(a[r]) * b[r];
-            } else {
-#pragma unroll
-                for (int r = 0; r < 8; ++r) h[r] = act_f<ACT>(a[r]);
+                const uint4 vb = ld16(stage + C::A_BYTES + q * 16);
+                st.b[4 * it] = vb.x; st.b[4 * it + 1] = vb.y; st.b[4 * it + 2] = vb.z; st.b[4 * it + 3] = vb.w;
             }
-            *pa = pack8(h);
         }
+    }
+    __device__ void pair(St& st, int p) const {
+        const uint32_t w = st.a[p];
+        float h0, h1;
+        if constexpr (ACT == ACT_SWIGLU) {
+            h0 = silu_bf(bf_lo(w)) * bf_lo(st.b[p]);
+            h1 = silu_bf(bf_hi(w)) * bf_hi(st.b[p]);
+        } else {
+            h0 = act_f<ACT>(bf_lo(w));
+            h1 = act_f<ACT>(bf_hi(w));
+        }
+        st.a[p] = pack_bf2(h0, h1);
+    }
+    __device__ void store(char* stage, const St& st) const {
+#pragma unroll
+        for (int it = 0; it < NIT; ++it)
+            st16(stage + (threadIdx.x + it * C::THREADS) * 16,
+                 make_uint4(st.a[4 * it], st.a[4 * it + 1], st.a[4 * it + 2], st.a[4 * it + 3]));
+    }
+    __device__ void operator()(char* stage, int kt) const {
+        St st;
+        load(stage, kt, st);
+#pragma unroll
+        for (int p = 0; p < NPAIR; ++p) pair(st, p);
+        store(stage, st);
     }
 };
 
@@ -462,30 +485,51 @@ constexpr int GS_PAD = 64;   // zero gates past the last slot (a slice reads up 
 template <int ACT, class C>
 struct GPass {
     static constexpr bool active = true;
+    static constexpr int NIT = C::A_BYTES / 16 / C::THREADS;
+    static constexpr int NPAIR = NIT * 4;
+    static constexpr int CPR = C::BM * 2 / 16;      // chunks per slot row
+    static_assert(C::A_BYTES / 16 % C::THREADS == 0, "whole chunks per thread");
     const char* gate_slots;   // NST x 32 floats after the ring
-    __device__ void operator()(char* stage, int kt) const {
-        constexpr int NCH = C::A_BYTES / 16;     // 16-byte chunks of the tile
-        constexpr int CPR = C::BM * 2 / 16;      // chunks per slot row
-        static_assert(NCH % C::THREADS == 0, "whole chunks per thread");
+    struct St { uint32_t a[NPAIR], b[NPAIR]; float g[NIT]; };   // one bf16 pair per word
+    __device__ void load(const char* stage, int kt, St& st) const {
         const float* g = reinterpret_cast<const float*>(gate_slots + (kt % NST) * 128);
 #pragma unroll
-        for (int it = 0; it < NCH / C::THREADS; ++it) {
+        for (int it = 0; it < NIT; ++it) {
             const int q = threadIdx.x + it * C::THREADS;
-            const float gv = g[q / CPR];
-            uint4* pa = reinterpret_cast<uint4*>(stage) + q;
-            float a[8], hg[8];
-            unpack8(*pa, a);
+            st.g[it] = g[q / CPR];
+            const uint4 va = ld16(stage + q * 16);
+            st.a[4 * it] = va.x; st.a[4 * it + 1] = va.y; st.a[4 * it + 2] = va.z; st.a[4 * it + 3] = va.w;
             if constexpr (ACT == ACT_SWIGLU) {
-                float b[8];
-                unpack8(*(reinterpret_cast<const uint4*>(stage + C::A_BYTES) + q), b);
-#pragma unroll
-                for (int r = 0; r < 8; ++r) hg[r] = gv * (silu_bf(a[r]) * b[r]);
-            } else {
-#pragma unroll
-                for (int r = 0; r < 8; ++r) hg[r] = gv * act_f<ACT>(a[r]);
+                const uint4 vb = ld16(stage + C::A_BYTES + q * 16);
+                st.b[4 * it] = vb.x; st.b[4 * it + 1] = vb.y; st.b[4 * it + 2] = vb.z; st.b[4 * it + 3] = vb.w;
             }
-            *pa = pack8(hg);
         }
+    }
+    __device__ void pair(St& st, int p) const {
+        const uint32_t w = st.a[p];
+        const float gv = st.g[p / 4];
+        float h0, h1;
+        if constexpr (ACT == ACT_SWIGLU) {
+            h0 = gv * (silu_bf(bf_lo(w)) * bf_lo(st.b[p]));
+            h1 = gv * (silu_bf(bf_hi(w)) * bf_hi(st.b[p]));
+        } else {
+            h0 = gv * act_f<ACT>(bf_lo(w));
+            h1 = gv * act_f<ACT>(bf_hi(w));
+        }
+        st.a[p] = pack_bf2(h0, h1);
+    }
+    __device__ void store(char* stage, const St& st) const {
+#pragma unroll
+        for (int it = 0; it < NIT; ++it)
+            st16(stage + (threadIdx.x + it * C::THREADS) * 16,
+                 make_uint4(st.a[4 * it], st.a[4 * it + 1], st.a[4 * it + 2], st.a[4 * it + 3]));
+    }
+    __device__ void operator()(char* stage, int kt) const {
+        St st;
+        load(stage, kt, st);
+#pragma unroll
+        for (int p = 0; p < NPAIR; ++p) pair(st, p);
+        store(stage, st);
     }
 };
 

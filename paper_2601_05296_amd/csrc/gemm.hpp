@@ -208,7 +208,10 @@ __device__ __forceinline__ void zero_mc_rows(char* tile, int from) {
 // extra ones included) into the operand the MFMAs consume.
 struct NoPre {
     static constexpr bool active = false;
+    static constexpr int NPAIR = 0;
+    struct St {};
     __device__ void operator()(char*, int) const {}
+    __device__ void pair(St&, int) const {}
 };
 template <class C, class LA, class LB0, class LB1, class PRE = NoPre>
 __device__ __forceinline__ void gemm_mainloop(LA& la, LB0& lb0, LB1& lb1, int nk, int zero_from,
@@ -284,6 +287,50 @@ __device__ __forceinline__ void gemm_mainloop(LA& la, LB0& lb0, LB1& lb1, int nk
             }
         }
     };
+    // The MFMAs of slice kt with the pre-pass of slice kt+1 spread between
+    // them: after each MFMA the thread forms its share of element pairs, fenced
+    // so that the compiler keeps the order. The wave then issues vector work
+    // while the matrix core runs its MFMAs. All fragment reads come first.
+    auto mma_pre = [&](int kt, auto partial, auto& st) {
+        constexpr bool PART = decltype(partial)::value;
+        constexpr int KK = GBK / 16;
+        constexpr int NM = KK * C::NB * C::FM * C::FN;   // MFMAs per slice and wave
+        const char* cur = lds + (kt % NST) * C::STAGE;
+        bf16x8 fa[KK][C::FM], fb[KK][C::NB][C::FN];
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk) {
+#pragma unroll
+            for (int i = 0; i < C::FM; ++i)
+                if (!PART || (i < nfm && nfn > 0))
+                    fa[kk][i] = frag<LA::MC, C::BM>(cur, wm * C::WTM + i * 32, kk, lane);
+#pragma unroll
+            for (int b = 0; b < C::NB; ++b)
+#pragma unroll
+                for (int j = 0; j < C::FN; ++j)
+                    if (!PART || (j < nfn && nfm > 0))
+                        fb[kk][b][j] = frag<LB0::MC, C::BN>(cur + C::AREG + b * C::B_BYTES,
+                                                            wn * C::WTN + j * 32, kk, lane);
+        }
+#pragma unroll
+        for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+            for (int b = 0; b < C::NB; ++b)
+#pragma unroll
+                for (int i = 0; i < C::FM; ++i)
+#pragma unroll
+                    for (int j = 0; j < C::FN; ++j) {
+                        if (!PART || (i < nfm && j < nfn))
+                            acc[b][i][j] = mfma32x32x16(fb[kk][b][j], fa[kk][i], acc[b][i][j]);
+                        const int m = ((kk * C::NB + b) * C::FM + i) * C::FN + j;
+                        const int p0 = m * PRE::NPAIR / NM, p1 = (m + 1) * PRE::NPAIR / NM;
+                        if (p1 > p0) {
+                            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                            for (int q = p0; q < p1; ++q) pre.pair(st, q);
+                            __builtin_amdgcn_sched_barrier(0);
+                        }
+                    }
+    };
     if constexpr (!PRE::active) {
         auto loop = [&](auto partial) {
             for (int kt = 0; kt < nk; ++kt) {
@@ -301,11 +348,9 @@ __device__ __forceinline__ void gemm_mainloop(LA& la, LB0& lb0, LB1& lb1, int nk
         if (nfm == C::FM && nfn == C::FN) loop(std::false_type{});
         else loop(std::true_type{});
     } else {
-        // The pre-pass runs one slice ahead of the MFMAs: slice kt is
-        // multiplied, then slice kt+1 (landed) is transformed in its own stage
-        // while the last MFMAs drain, and slice kt+2 is in flight. (Running the
-        // pre-pass first on every other wave, so that the two waves of a SIMD
-        // overlap vector ALU and MFMA work, measured slower.)
+        // The pre-pass runs one slice ahead of the MFMAs: while slice kt is
+        // multiplied, slice kt+1 (landed) is transformed in its own stage, and
+        // slice kt+2 is in flight.
         static_assert(NST == 3, "stages: multiplied, transformed, in flight");
         pre(lds, 0);
         lds_barrier();
@@ -317,8 +362,13 @@ __device__ __forceinline__ void gemm_mainloop(LA& la, LB0& lb0, LB1& lb1, int nk
                     fix_tail(kt + 1);
                 }
                 if (kt + NST - 1 < nk) issue(kt + NST - 1);   // into the stage slice kt-1 left
-                mma(kt, partial);
-                if (kt + 1 < nk) pre(lds + ((kt + 1) % NST) * C::STAGE, kt + 1);
+                // (after the last slice this transforms a spent stage, which
+                // nothing reads again: one MFMA block in the loop, not two)
+                char* nxt = lds + ((kt + 1) % NST) * C::STAGE;
+                typename PRE::St st;
+                pre.load(nxt, kt + 1, st);
+                mma_pre(kt, partial, st);
+                pre.store(nxt, st);
                 lds_barrier();
             }
         };
