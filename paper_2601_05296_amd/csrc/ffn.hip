@@ -50,8 +50,6 @@ using CS = GemmCfg<256, 256, 2, 4, 1>;  // G2, G3, G6
 // workgroups with 72 KB of LDS, so that two share a CU and one's epilogue
 // overlaps the other's main loop.
 using C4 = GemmCfg<128, 256, 2, 2, 1>;
-// G2 with h formed on load: the stage also holds B's tile (144 KB of LDS)
-using CH = GemmCfg<256, 256, 2, 4, 1, 1>;
 
 // ============================ epilogue helpers ===================================
 
@@ -80,7 +78,11 @@ __device__ __forceinline__ float act_d(float a) {
 // tile configuration of the first-layer and dW1 GEMMs: two right operands
 // when gated (W1|W3, dA|dB), one otherwise
 template <int ACT> using CFirst = std::conditional_t<ACT == ACT_SWIGLU, CD, CS>;
-template <int ACT> using CSecondH = std::conditional_t<ACT == ACT_SWIGLU, CH, CS>;
+// SwiGLU GEMMs with h (or g*h) formed on load: 128 x 512 tiles, so that each
+// h element is formed once per 512 output columns rather than per 256 (the
+// in-LDS pass, two transcendentals per element, outweighs the MFMA work)
+using CHW = GemmCfg<128, 512, 2, 4, 1, 1>;
+template <int ACT> using CSecondH = std::conditional_t<ACT == ACT_SWIGLU, CHW, CS>;
 static_assert(CD::THREADS == CS::THREADS && CD::LDS == CS::LDS, "CD and CS launch alike");
 __device__ __forceinline__ void store8_bf16(bf16_t* p, const float (&v)[8]) { st16(p, pack8(v)); }
 
