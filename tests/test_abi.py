@@ -144,3 +144,40 @@ def test_activation_flags():
     # the non-gated workspaces hold the same buffers (h; partials and g*h)
     assert lib.moe_ffn_fwd_workspace_size(1000, 128, f, 8, 2, B.MOE_ACT_SILU) == \
         lib.moe_ffn_fwd_workspace_size(1000, 128, f, 8, 2, 0) >= S * f * 2
+
+
+
+def test_binding_checks_sizes_and_dtypes_before_the_library():
+    """The C ABI takes bare pointers; the binding checks element counts and
+    dtypes first (here on host tensors, so nothing reaches the library)."""
+    import torch
+    bf, f32, i32 = torch.bfloat16, torch.float32, torch.int32
+    T, d, E, k, f = 10, 128, 8, 2, 256
+
+    def z(n, dt):
+        return torch.zeros(n, dtype=dt)
+
+    with pytest.raises(ValueError, match="w_gate: 1016 elements"):
+        B.moe_route(z(T * d, bf), z(E * d - 8, bf), None, T, d, E, k, 0, z(T * k, i32),
+                    z(T * k, f32), None)
+    with pytest.raises(ValueError, match="topk_ids: dtype torch.int64"):
+        B.moe_route(z(T * d, bf), z(E * d, bf), None, T, d, E, k, 0,
+                    z(T * k, torch.int64), z(T * k, f32), None)
+    with pytest.raises(ValueError, match="x: dtype torch.bfloat16"):   # MOE_F32 wants float32
+        B.moe_route(z(T * d, bf), z(E * d, bf), None, T, d, E, k, B.MOE_F32,
+                    z(T * k, i32), z(T * k, f32), None)
+    with pytest.raises(ValueError, match="src: 2559 elements"):
+        B.moe_combine(z(T * k * d - 1, bf), None, z(T * k, i32), T, d, k, 0, z(T * d, bf))
+    with pytest.raises(ValueError, match="workspace: 16 bytes"):
+        B.moe_build_index(z(T * k, i32), T, E, k, z(E, i32), z(E + 1, i32), z(T * k, i32),
+                          z(T * k, i32), z(T * k, i32), z(16, torch.uint8), 64)
+    with pytest.raises(ValueError, match="B: 0 elements"):   # SwiGLU needs B
+        B.moe_ffn_fwd(z(T * d, bf), z(E * d * f, bf), z(E * d * f, bf), z(E * f * d, bf),
+                      z(E + 1, i32), z(T * k, i32), T, d, f, E, k, 0, z(T * k * f, bf),
+                      z(0, bf), z(T * k * d, bf), None, 0)
+    # non-gated: w3 and B are not needed; every size is right, so the next
+    # check (device placement) is the one that fails
+    with pytest.raises(ValueError, match="must be on the GPU"):
+        B.moe_ffn_fwd(z(T * d, bf), z(E * d * f, bf), None, z(E * f * d, bf), z(E + 1, i32),
+                      z(T * k, i32), T, d, f, E, k, B.MOE_ACT_RELU, z(T * k * f, bf), None,
+                      z(T * k * d, bf), None, 0)

@@ -766,7 +766,10 @@ def test_layer_deterministic_bf16():
 
 
 def test_error_codes_launch_nothing():
-    x = torch.zeros((4, 128), dtype=torch.bfloat16, device="cuda")
+    """The library's own validation, reached with raw device addresses (the
+    binding checks tensor sizes and dtypes, not raw addresses)."""
+    xt = torch.zeros((4, 128), dtype=torch.bfloat16, device="cuda")
+    x = xt.data_ptr()
     with pytest.raises(B.MoEError) as ei:
         B.moe_route(x, x, None, 4, 128, 2, 3, 0, x, x, None)
     assert ei.value.status == B.MOE_ERR_INVALID_ARG
