@@ -25,6 +25,7 @@ SiLU(A), no h and no expert output O is kept.
 """
 from __future__ import annotations
 
+import contextlib
 from dataclasses import dataclass
 
 import torch
@@ -78,12 +79,33 @@ def saved_bytes_per_token(d: int, f: int, E: int, k: int, elem: int, T: int,
     return n_first * k * f * elem + 20.0 * k + 4.0 * E + 4.0 * (2 * E + 1) / T
 
 
+def _on(stream):
+    """Run a layer call on `stream` (a torch.cuda.Stream; None: torch's current
+    stream). The temporaries are allocated under it too, so the caching
+    allocator never hands a freed workspace to other work while the library's
+    kernels on that stream may still use it."""
+    if stream is None:
+        return contextlib.nullcontext()
+    if not isinstance(stream, torch.cuda.Stream):
+        raise TypeError("stream must be a torch.cuda.Stream or None")
+    return torch.cuda.stream(stream)
+
+
 def forward(x, w_gate, bias, w1, w3, w2, k: int, renorm: bool, stream=None, keep_O=False,
             act: str = "swiglu", separate: bool = False, recompute: bool = False,
             h_on_load: bool = False):
     """Returns (y, saved[, O]). ``act`` picks the expert: "swiglu" (gated, w3
     used) or the non-gated "silu" / "relu" (w3 ignored, may be None).
-    ``keep_O`` (returns the expert outputs) implies ``separate``."""
+    ``keep_O`` (returns the expert outputs) implies ``separate``. Everything
+    runs on ``stream`` (torch's current stream if None)."""
+    with _on(stream):
+        return _forward(x, w_gate, bias, w1, w3, w2, k, renorm, keep_O, act, separate,
+                        recompute, h_on_load)
+
+
+def _forward(x, w_gate, bias, w1, w3, w2, k, renorm, keep_O, act, separate, recompute,
+             h_on_load):
+    stream = None   # torch's current stream, set by forward()
     T, d = x.shape
     E, _, f = w1.shape
     dev = x.device
@@ -138,7 +160,14 @@ def backward(saved: Saved, dy, x, w_gate, w1, w3, w2, stream=None, keep=False,
              separate: bool = False):
     """Returns dict(dx, dw_gate, dw1, dw3, dw2, d_gates[, dX_slot]). Overwrites
     saved.A / saved.B with dA / dB. dw3 is None for a non-gated expert.
-    ``keep`` (returns dX_slot and the FFN part of dx) implies ``separate``."""
+    ``keep`` (returns dX_slot and the FFN part of dx) implies ``separate``.
+    Everything runs on ``stream`` (torch's current stream if None)."""
+    with _on(stream):
+        return _backward(saved, dy, x, w_gate, w1, w3, w2, keep, separate)
+
+
+def _backward(saved, dy, x, w_gate, w1, w3, w2, keep, separate):
+    stream = None   # torch's current stream, set by backward()
     s = saved
     T, d, f, E, k = s.T, s.d, s.f, s.E, s.k
     dev = dy.device

@@ -765,6 +765,33 @@ def test_layer_deterministic_bf16():
         assert torch.equal(a, b)
 
 
+def test_layer_on_a_side_stream():
+    """The layer driven on a second stream (default priority) while the
+    current stream is busy with other work: the same bits as on the current
+    stream."""
+    cfg = synth.MoEConfig("st", T=1500, d=256, f=384, E=16, k=4, dtype="bf16", renorm=True)
+    inp = synth.make_inputs(cfg)
+    st = inp.store
+    x, wg, w1, w3, w2, dy = (dev(st[n]) for n in ("x", "w_gate", "w1", "w3", "w2", "dy"))
+    y0, s0 = layer.forward(x, wg, None, w1, w3, w2, cfg.k, cfg.renorm)
+    g0 = layer.backward(s0, dy, x, wg, w1, w3, w2)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    busy = torch.randn(2048, 2048, device="cuda")
+    for _ in range(4):
+        busy = busy @ busy.T / 2048.0     # unrelated work on the current stream
+    y1, s1 = layer.forward(x, wg, None, w1, w3, w2, cfg.k, cfg.renorm, stream=side)
+    g1 = layer.backward(s1, dy, x, wg, w1, w3, w2, stream=side)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    assert torch.equal(y0, y1)
+    for n in ("dx", "dw1", "dw3", "dw2", "dw_gate", "d_gates"):
+        assert torch.equal(g0[n], g1[n]), n
+    with pytest.raises(TypeError):
+        layer.forward(x, wg, None, w1, w3, w2, cfg.k, cfg.renorm, stream=side.cuda_stream)
+
+
 def test_error_codes_launch_nothing():
     """The library's own validation, reached with raw device addresses (the
     binding checks tensor sizes and dtypes, not raw addresses)."""
