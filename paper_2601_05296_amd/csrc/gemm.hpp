@@ -17,6 +17,12 @@
 // publishes them to the other waves. The waits are explicit because a
 // compiler-generated __syncthreads() would drain every outstanding load.
 //
+// A kernel may hand the main loop a pre-pass that rewrites each slice's left
+// operand in LDS before it is multiplied (the h-on-load GEMMs form h =
+// SiLU(A) * B there). It runs one slice ahead: while slice kt is multiplied,
+// slice kt+1 (landed) is transformed, its element pairs spread between the
+// MFMAs of slice kt, and slice kt+2 is in flight.
+//
 // MFMA 32x32x16 operand layout (wave64), verified on gfx950: for D = P * Q,
 // lane L supplies P[L%32][8*(L/32) + 0..7] and Q[8*(L/32) + 0..7][L%32] and
 // receives D[8*(j/4) + 4*(L/32) + j%4][L%32] in accumulator register j. The
