@@ -600,7 +600,7 @@ def cpu_oracle_baseline(inp, cfg, budget_s):
     n_prop = n1 * budget_s / max(t1, 1e-3)
     n = int(min(cfg.T, max(n1, min((budget_s - a) / b, 2.0 * n_prop))))
     t = run(n)
-    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    cores = oracle.threads()
     return {"value": n / t, "unit": "tokens/s", "cores": cores, "kind": "oracle",
             "sample": "first %d of %d tokens of %s, whole-layer fwd+bwd in fp64 "
                       "(%.1f s; calibration runs of %d and %d tokens, %.1f s, not counted)"

@@ -46,6 +46,11 @@
 
 #define ORACLE_API __attribute__((visibility("default")))
 
+#include <omp.h>
+
+/* threads the OpenMP loops of this file run with (for reporting only) */
+ORACLE_API int oracle_threads(void) { return omp_get_max_threads(); }
+
 static double sigmoid(double u) { return 1.0 / (1.0 + exp(-u)); }
 static double silu(double u) { return u * sigmoid(u); }
 

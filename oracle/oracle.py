@@ -48,6 +48,8 @@ def _load():
         _lib.oracle_route_bwd.argtypes = [P, P, P, P, P, I64, I, I, I, I, P, P, P]
         _lib.oracle_ffn_fwd_act.argtypes = [P, P, P, P, P, I64, I, I, I, I, I, P, P]
         _lib.oracle_ffn_bwd_act.argtypes = [P] * 9 + [I64, I, I, I, I, I] + [P] * 5
+        _lib.oracle_threads.argtypes = []
+        _lib.oracle_threads.restype = ctypes.c_int
         for fn in ("oracle_route", "oracle_build_index", "oracle_ffn_fwd",
                    "oracle_combine", "oracle_ffn_bwd", "oracle_route_bwd"):
             getattr(_lib, fn).restype = None
@@ -64,6 +66,11 @@ def _i32(a):
 
 def _p(a):
     return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def threads() -> int:
+    """Number of threads the oracle's OpenMP loops use."""
+    return int(_load().oracle_threads())
 
 
 def route(x, w_gate, bias, k: int, renorm: bool):
