@@ -244,7 +244,8 @@ def test_route_bwd_ignores_invalid_ids(renorm):
     ("bf16", 1000, 256, 8, 2, False, None), ("bf16", 1000, 512, 64, 6, True, None),
     ("bf16", 777, 256, 128, 8, False, "zipf"), ("bf16", 300, 384, 200, 16, False, "dead"),
     ("f32", 1000, 256, 8, 2, False, None), ("f32", 500, 256, 64, 6, True, "dead"),
-    ("bf16", 700, 320, 64, 6, True, None)])
+    ("bf16", 700, 320, 64, 6, True, None),
+    ("bf16", 100, 64, 1, 1, False, None), ("bf16", 100, 64, 3, 3, True, None)])
 def test_route_parity(dtype, T, d, E, k, renorm, bias):
     cfg = synth.MoEConfig("r", T=T, d=d, f=128, E=E, k=k, dtype=dtype, renorm=renorm,
                           zipf_s=1.2 if bias == "zipf" else 0.0,
@@ -323,6 +324,11 @@ FFN_CASES = [
     # d and f odd multiples of 64: partial column tiles in every GEMM
     ("bf16", 300, 320, 192, 8, 2, False, None),
     ("f32", 200, 192, 320, 8, 3, False, None),
+    # the smallest shapes the ABI accepts: d = f = 64 (one or two K slices),
+    # a single expert, top-1
+    ("bf16", 100, 64, 64, 1, 1, False, None),
+    ("bf16", 37, 64, 192, 3, 2, True, None),
+    ("f32", 50, 64, 64, 2, 2, False, None),
 ]
 
 
@@ -398,7 +404,8 @@ def test_ffn_fwd_bwd_parity(dtype, T, d, f, E, k, renorm, pattern):
     ("bf16", 1500, 256, 128, 8, False, True), ("bf16", 777, 384, 200, 16, True, False),
     ("f32", 1000, 256, 8, 2, False, False),
     ("f32", 700, 128, 32, 4, True, True),
-    ("bf16", 900, 192, 64, 6, False, True), ("bf16", 600, 320, 256, 8, True, False)])
+    ("bf16", 900, 192, 64, 6, False, True), ("bf16", 600, 320, 256, 8, True, False),
+    ("bf16", 100, 64, 1, 1, True, False), ("bf16", 300, 64, 4, 3, False, True)])
 def test_route_bwd_parity(dtype, T, d, E, k, renorm, accumulate):
     cfg = synth.MoEConfig("rb", T=T, d=d, f=128, E=E, k=k, dtype=dtype, renorm=renorm)
     inp = synth.make_inputs(cfg)
@@ -535,6 +542,7 @@ COMBINED_CASES = [
     ("bf16", 500, 640, 384, 16, 4, "zipf", "relu"),
     ("f32", 257, 256, 256, 8, 2, None, "swiglu"),
     ("bf16", 500, 576, 448, 16, 4, None, "swiglu"),
+    ("bf16", 100, 64, 64, 2, 2, None, "swiglu"),
     # 393k slots: three strips of 256 columns (bit-exactness only; the
     # full-size tests check multi-strip workloads against the oracle)
     ("bf16", 49152, 768, 256, 16, 8, None, "swiglu"),
