@@ -245,7 +245,8 @@ def test_route_bwd_ignores_invalid_ids(renorm):
     ("bf16", 777, 256, 128, 8, False, "zipf"), ("bf16", 300, 384, 200, 16, False, "dead"),
     ("f32", 1000, 256, 8, 2, False, None), ("f32", 500, 256, 64, 6, True, "dead"),
     ("bf16", 700, 320, 64, 6, True, None),
-    ("bf16", 100, 64, 1, 1, False, None), ("bf16", 100, 64, 3, 3, True, None)])
+    ("bf16", 100, 64, 1, 1, False, None), ("bf16", 100, 64, 3, 3, True, None),
+    ("bf16", 500, 128, 256, 16, False, None), ("bf16", 400, 192, 256, 16, True, "zipf")])
 def test_route_parity(dtype, T, d, E, k, renorm, bias):
     cfg = synth.MoEConfig("r", T=T, d=d, f=128, E=E, k=k, dtype=dtype, renorm=renorm,
                           zipf_s=1.2 if bias == "zipf" else 0.0,
@@ -329,6 +330,8 @@ FFN_CASES = [
     ("bf16", 100, 64, 64, 1, 1, False, None),
     ("bf16", 37, 64, 192, 3, 2, True, None),
     ("f32", 50, 64, 64, 2, 2, False, None),
+    # the largest E and k: 256 experts of about 19 slots each, many empty
+    ("bf16", 300, 128, 128, 256, 16, True, None),
 ]
 
 
@@ -405,7 +408,8 @@ def test_ffn_fwd_bwd_parity(dtype, T, d, f, E, k, renorm, pattern):
     ("f32", 1000, 256, 8, 2, False, False),
     ("f32", 700, 128, 32, 4, True, True),
     ("bf16", 900, 192, 64, 6, False, True), ("bf16", 600, 320, 256, 8, True, False),
-    ("bf16", 100, 64, 1, 1, True, False), ("bf16", 300, 64, 4, 3, False, True)])
+    ("bf16", 100, 64, 1, 1, True, False), ("bf16", 300, 64, 4, 3, False, True),
+    ("bf16", 500, 128, 256, 16, False, True), ("bf16", 400, 192, 256, 16, True, False)])
 def test_route_bwd_parity(dtype, T, d, E, k, renorm, accumulate):
     cfg = synth.MoEConfig("rb", T=T, d=d, f=128, E=E, k=k, dtype=dtype, renorm=renorm)
     inp = synth.make_inputs(cfg)
