@@ -171,7 +171,7 @@ def test_full_size_layer(name):
     assert_close("dx_router", host(dxr), dxr_r, "bf16")
 
 
-@pytest.mark.parametrize("name", ["mid_e64k6", "table1_conf1_relu", "d2880_e128k4"])
+@pytest.mark.parametrize("name", ["mid_e64k6", "table1_conf1_relu", "d2880_e128k4", "few_large_e8k2"])
 def test_full_size_h_on_load_bit_identical(name):
     """MOE_H_ON_LOAD at full size, in the launch configuration bench.py times
     (multi-strip combined calls): outputs and every gradient bit-identical to
