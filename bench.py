@@ -163,7 +163,10 @@ def summarize_stats(stats_csv, out, workload, cmd, profile_cmd):
 def summarize_table1(json_path, out, cmd, profile_cmd):
     """Text summary of a --table1 run (its last output line)."""
     rows = json.loads(open(json_path).read().strip().splitlines()[-1])["table1"]
-    lines = ["# Table 1 shapes (paper Section 6.1): this path vs a materialised PyTorch MoE layer",
+    policy = (", this path with MOE_H_ON_LOAD (no h / g*h buffers)"
+              if rows and rows[0].get("h_on_load") else "")
+    lines = ["# Table 1 shapes (paper Section 6.1): this path vs a materialised PyTorch MoE layer"
+             + policy,
              "# run: %s" % profile_cmd,
              "# summary: python %s" % cmd,
              "# one MI355X, bf16, f = 4d, T = batch x seq_len, plain top-k softmax gates; "
@@ -425,6 +428,7 @@ def table1_sweep(args):
     from paper_2601_05296_amd import layer, synth
     dev = torch.device("cuda:0")
     bf = torch.bfloat16
+    hol = bool(args.h_on_load)   # this path with MOE_H_ON_LOAD
     rows = []
     for act in ("silu", "swiglu"):
         for name in synth.TABLE1:
@@ -440,7 +444,8 @@ def table1_sweep(args):
             w2 = rnd((E, f, d), f ** -0.5)
             x = rnd((T, d), 1.0)
             dy = rnd((T, d), 1.0)
-            row = {"conf": name, "act": act, "T": T, "d": d, "f": f, "E": E, "k": k}
+            row = {"conf": name, "act": act, "T": T, "d": d, "f": f, "E": E, "k": k,
+                   "h_on_load": hol}
 
             def timed(fn, steps, warm):
                 for _ in range(warm):
@@ -455,7 +460,7 @@ def table1_sweep(args):
                 return e0.elapsed_time(e1) / steps
 
             def ours():
-                y, saved = layer.forward(x, wg, None, w1, w3, w2, k, False, act=act)
+                y, saved = layer.forward(x, wg, None, w1, w3, w2, k, False, act=act, h_on_load=hol)
                 return layer.backward(saved, dy, x, wg, w1, w3, w2)
 
             def base():
@@ -470,7 +475,7 @@ def table1_sweep(args):
                 torch.cuda.reset_peak_memory_stats(dev)
                 m0 = torch.cuda.memory_allocated(dev)
                 if which == "ours":
-                    y, saved = layer.forward(x, wg, None, w1, w3, w2, k, False, act=act)
+                    y, saved = layer.forward(x, wg, None, w1, w3, w2, k, False, act=act, h_on_load=hol)
                     del y, saved
                 else:
                     materialised_saved_bytes(x, wg, None, w1, w3, w2, k, False, act)
@@ -486,7 +491,7 @@ def table1_sweep(args):
                 row[which + "_peak_bytes_per_token"] = round(max(fwd_peak, peak - grads) / T, 1)
                 del out
             torch.cuda.empty_cache()
-            y, saved = layer.forward(x, wg, None, w1, w3, w2, k, False, act=act)
+            y, saved = layer.forward(x, wg, None, w1, w3, w2, k, False, act=act, h_on_load=hol)
             row["ours_saved_bytes_per_token"] = round(saved.nbytes() / T, 1)
             del y, saved
             row["base_saved_bytes_per_token"] = round(
