@@ -706,17 +706,29 @@ def main():
     assert abs(saved_bytes - formula) < 1, (saved_bytes, formula)
     del y, saved, g
 
+    # records per step (one event per kernel launch and one per entry point),
+    # counted on one untimed step with room to spare
+    B.moe_probe_enable(4096)
+    step()
+    torch.cuda.synchronize()
+    per_step_records = B.moe_probe_count() + 16
+    assert B.moe_probe_dropped() == 0, "probe pool too small for one step"
+    B.moe_probe_disable()
+
     # timed region: K whole steps, per-kernel events recorded on the stream
-    per_step_records = 32
-    B.moe_probe_enable(per_step_records * args.steps + 64)
+    B.moe_probe_enable(2 * per_step_records * args.steps + 64)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    dropped = B.moe_probe_dropped()
     recs = [B.moe_probe_get(i) for i in range(B.moe_probe_count())]
     B.moe_probe_disable()
+    if dropped:
+        raise RuntimeError("timing probe dropped %d records; per-kernel rates would be wrong"
+                           % dropped)
     ms_step = (t1 - t0) * 1e3 / args.steps
     tokens_per_s = T * args.steps / (t1 - t0)
 
@@ -727,7 +739,10 @@ def main():
     for name, lst in kern.items():
         avg = float(np.mean(lst))
         per_step_ms = float(np.sum(lst)) / args.steps
-        launches = len(lst) / args.steps
+        if len(lst) % args.steps:
+            raise RuntimeError("%s: %d launches over %d steps is not a whole number per step"
+                               % (name, len(lst), args.steps))
+        launches = len(lst) // args.steps
         amount, unit, bound = kernel_model(name, cfg, elem, args.recompute)
         # work of all the step's launches over their total time = the
         # per-launch work over the average launch

@@ -279,19 +279,24 @@ int moe_route_bwd(const float* d_gates, const float* logits, const int32_t* topk
                   hipStream_t stream);
 
 /*
- * Kernel timing probe (diagnostics; not needed for computing anything).
+ * Kernel timing probe (diagnostics; not needed for computing anything, and
+ * the one part of this library that waits on the host: moe_probe_get
+ * synchronises with the event it reads).
  * moe_probe_enable(capacity) creates `capacity` HIP events and starts
  * recording: each entry point then records an event on its stream before its
  * first kernel and one after every kernel it launches. Record i (0-based,
  * counting kernel records only) is the time between the kernel's preceding
- * event and its own, i.e. that kernel's duration on the stream. Recording
- * stops silently when the events run out. moe_probe_get waits for record i
+ * event and its own, i.e. that kernel's duration on the stream. Once the
+ * events run out nothing more is recorded; moe_probe_dropped returns how
+ * many records were lost that way since moe_probe_enable (a caller that
+ * needs every launch must check it is 0). moe_probe_get waits for record i
  * and returns the kernel's name (static storage) and its duration in ms.
  * moe_probe_disable destroys the events. Not thread-safe; single stream.
  */
 int moe_probe_enable(int capacity);
 void moe_probe_disable(void);
 int moe_probe_count(void);
+int moe_probe_dropped(void);
 int moe_probe_get(int index, const char** kernel_name, float* ms);
 
 #ifdef __cplusplus

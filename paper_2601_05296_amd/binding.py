@@ -37,7 +37,7 @@ EXPORTS = ("moe_strerror", "moe_last_error", "moe_route", "moe_build_index_works
            "moe_ffn_fwd_combine",
            "moe_ffn_bwd_combine_workspace_size", "moe_ffn_bwd_combine",
            "moe_route_bwd_workspace_size", "moe_route_bwd", "moe_probe_enable",
-           "moe_probe_disable", "moe_probe_count", "moe_probe_get")
+           "moe_probe_disable", "moe_probe_count", "moe_probe_dropped", "moe_probe_get")
 
 
 class MoEError(RuntimeError):
@@ -85,6 +85,7 @@ def load_library(path: str = LIB):
         "moe_probe_enable": (I, [I]),
         "moe_probe_disable": (None, []),
         "moe_probe_count": (I, []),
+        "moe_probe_dropped": (I, []),
         "moe_probe_get": (I, [I, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_float)]),
     }
     for name, (res, args) in sig.items():
@@ -339,6 +340,10 @@ def moe_probe_disable():
 
 def moe_probe_count() -> int:
     return load_library().moe_probe_count()
+
+
+def moe_probe_dropped() -> int:
+    return load_library().moe_probe_dropped()
 
 
 def moe_probe_get(index: int):

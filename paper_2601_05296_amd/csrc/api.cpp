@@ -195,6 +195,8 @@ void moe_probe_disable(void) { moe::probe::disable(); }
 
 int moe_probe_count(void) { return moe::probe::count(); }
 
+int moe_probe_dropped(void) { return moe::probe::dropped(); }
+
 int moe_probe_get(int index, const char** kernel_name, float* ms) {
     if (!kernel_name || !ms) return fail(MOE_ERR_INVALID_ARG, "moe_probe_get: NULL output");
     if (moe::probe::get(index, kernel_name, ms) != 0)

@@ -21,9 +21,13 @@ struct Rec {
 bool g_on = false;
 std::vector<hipEvent_t> g_pool;
 std::vector<Rec> g_recs;
+int g_dropped = 0;   // records not taken because the events ran out
 
 void record(const char* name, hipStream_t st) {
-    if (g_recs.size() >= g_pool.size()) return;  // capacity reached: stop recording
+    if (g_recs.size() >= g_pool.size()) {   // capacity reached: count, do not record
+        ++g_dropped;
+        return;
+    }
     hipEvent_t ev = g_pool[g_recs.size()];
     if (hipEventRecord(ev, st) != hipSuccess) return;
     g_recs.push_back(Rec{name, ev});
@@ -45,6 +49,7 @@ int enable(int capacity) {
             return -1;
         }
     g_recs.reserve(capacity);
+    g_dropped = 0;
     g_on = true;
     return 0;
 }
@@ -54,7 +59,10 @@ void disable() {
     for (hipEvent_t e : g_pool) (void)hipEventDestroy(e);
     g_pool.clear();
     g_recs.clear();
+    g_dropped = 0;
 }
+
+int dropped() { return g_dropped; }
 
 int count() {
     int n = 0;

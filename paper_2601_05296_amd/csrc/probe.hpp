@@ -11,6 +11,7 @@ void mark(const char* name, hipStream_t st); // after a kernel launch
 int enable(int capacity);
 void disable();
 int count();
+int dropped();                              // records lost to a full pool
 int get(int i, const char** name, float* ms);
 }  // namespace probe
 }  // namespace moe
