@@ -308,7 +308,7 @@ def kernel_model(name, cfg, elem, recompute=False):
              "g4_kernel": g, "g5_kernel": nb * g, "g6_kernel": nb * g}
     if name in flops:
         return flops[name], "TFLOP/s", "mfma"
-    nparts = (f // 128) * 2
+    nparts = -(-f // 256) * 4   # gate-gradient partials per slot (G4: 256-column tiles, 4 waves across)
     byts = {
         "route_bf16": T * d * elem + E * d * elem + T * E * 4 + T * k * 8,
         "tile_hist": S * 4,

@@ -71,8 +71,9 @@ extern "C" {
  * activation). Backward: the dW2 GEMM runs first and forms g*h from A, B and
  * the gates as it loads them, before dA and dB overwrite A and B. Every result
  * is bit-identical to the default path; the forward workspace drops S*f*2
- * bytes (h) and the backward's the same (g*h), at the cost of those two GEMMs
- * reading A and B instead of one buffer. moe_ffn_recompute accepts and ignores
+ * bytes (h; the combined call's strip is rounded to the 512-column tiles of
+ * the GEMM that forms h) and the backward's the same (g*h), at the cost of
+ * those two GEMMs reading A and B instead of one buffer. moe_ffn_recompute accepts and ignores
  * it; route, build, combine and route_bwd reject it (MOE_ERR_INVALID_ARG). */
 #define MOE_H_ON_LOAD   32u
 

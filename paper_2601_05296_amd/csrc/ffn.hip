@@ -34,6 +34,7 @@
 // The float32 debug mode uses plain one-output-per-thread kernels.
 #include "common.hpp"
 #include "gemm.hpp"
+#include "gemm_rs.hpp"
 #include "loaders.hpp"
 #include "launch.hpp"
 #include "probe.hpp"
@@ -44,12 +45,12 @@ namespace {
 // Tile configurations: <BM, BN, WM, WN, NB>. 256-row tiles, 2x4 waves.
 // Single right operand: each wave owns 128 x 64 outputs. Two right operands
 // (G1: W1 and W3; G5: dA and dB): 128 x 32 of each.
-using CD = GemmCfg<256, 128, 2, 4, 2>;  // G1, G5
-using CS = GemmCfg<256, 256, 2, 4, 1>;  // G2, G3, G6
-// G4 has a heavy epilogue (it reads A, B and writes dA, dB, g*h): 4-wave
-// workgroups with 72 KB of LDS, so that two share a CU and one's epilogue
-// overlaps the other's main loop.
-using C4 = GemmCfg<128, 256, 2, 2, 1>;
+using CD = GemmCfg<256, 128, 2, 4, 2>;
+using CS = GemmCfg<256, 256, 2, 4, 1>;  // h-on-load GEMMs of the non-gated experts
+// Register-staged core (gemm_rs.hpp): the same tile shapes and wave layout.
+using RD = rs::Cfg<256, 128, 2, 4, 2>;  // G1, G5
+using RS = rs::Cfg<256, 256, 2, 4, 1>;  // G2, G3, G6
+constexpr int RASTER_GM = 4;            // M tiles per raster group (find_slot_tile)
 
 // ============================ epilogue helpers ===================================
 
@@ -77,13 +78,13 @@ __device__ __forceinline__ float act_d(float a) {
 }
 // tile configuration of the first-layer and dW1 GEMMs: two right operands
 // when gated (W1|W3, dA|dB), one otherwise
-template <int ACT> using CFirst = std::conditional_t<ACT == ACT_SWIGLU, CD, CS>;
-// SwiGLU GEMMs with h (or g*h) formed on load: 128 x 512 tiles, so that each
-// h element is formed once per 512 output columns rather than per 256 (the
-// in-LDS pass, two transcendentals per element, outweighs the MFMA work)
-using CHW = GemmCfg<128, 512, 2, 4, 1, 1>;
-template <int ACT> using CSecondH = std::conditional_t<ACT == ACT_SWIGLU, CHW, CS>;
-static_assert(CD::THREADS == CS::THREADS && CD::LDS == CS::LDS, "CD and CS launch alike");
+template <int ACT> using CFirst = std::conditional_t<ACT == ACT_SWIGLU, RD, RS>;
+// GEMMs with h (or g*h) formed on load: 128 x 512 tiles, so that each h
+// element is formed once per 512 output columns rather than per 256 (forming
+// it costs two transcendentals and some ten other vector operations, about
+// as much vector-ALU time per slice as the slice's MFMAs take).
+using RHW = rs::Cfg<128, 512, 2, 4, 1>;
+static_assert(RD::THREADS == RS::THREADS && RD::LDS == RS::LDS, "RD and RS launch alike");
 __device__ __forceinline__ void store8_bf16(bf16_t* p, const float (&v)[8]) { st16(p, pack8(v)); }
 
 // ============================ kernels ==============================================
@@ -93,7 +94,7 @@ __device__ __forceinline__ void store8_bf16(bf16_t* p, const float (&v)[8]) { st
 // A = x[eti] W1[e] and H = act(A). H == NULL: A and B only (the backward's
 // recompute under the full-recompute policy).
 template <int ACT>
-__global__ void __launch_bounds__(CD::THREADS)
+__global__ void __launch_bounds__(RD::THREADS)
 g1_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w1,
           const bf16_t* __restrict__ w3, const int32_t* __restrict__ offsets,
           const int32_t* __restrict__ eti, int d, int f, int E, bf16_t* __restrict__ A,
@@ -102,20 +103,21 @@ g1_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w1,
     using C = CFirst<ACT>;
     SlotTile t;
     const int NT = (f + C::BN - 1) / C::BN;
-    if (!find_slot_tile<C::THREADS>(offsets, E, C::BM, NT, xcd_remap(blockIdx.x, gridDim.x), C::BN, t))
+    if (!find_slot_tile<C::THREADS>(offsets, E, C::BM, NT, xcd_remap(blockIdx.x, gridDim.x), C::BN,
+                                    t, RASTER_GM))
         return;
-    GatherKC<C, C::BM> la;
+    rs::GatherKC<C, C::BM> la;
     la.init(x, d, eti + t.off + t.m0, t.mrows);
-    DenseMC<C, C::BN> lb0;
+    rs::DenseMC<C, C::BN> lb0;
     lb0.init(w1 + (int64_t)t.e * d * f, f, t.n0, f);
-    Acc<C> acc;
+    rs::Acc<C> acc;
     if constexpr (ACT == ACT_SWIGLU) {
-        DenseMC<C, C::BN> lb1;
+        rs::DenseMC<C, C::BN> lb1;
         lb1.init(w3 + (int64_t)t.e * d * f, f, t.n0, f);
-        gemm_mainloop<C>(la, lb0, lb1, d / GBK, GBK, lds, acc, t.mrows);
+        rs::mainloop<C>(la, lb0, lb1, d / rs::KS, lds, acc);
     } else {
-        NoLoader nl;
-        gemm_mainloop<C>(la, lb0, nl, d / GBK, GBK, lds, acc, t.mrows, f - t.n0);
+        rs::NoLoader nl;
+        rs::mainloop<C>(la, lb0, nl, d / rs::KS, lds, acc);
     }
     WaveCoord<C> wc;
 #pragma unroll
@@ -152,23 +154,24 @@ g1_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w1,
 }
 
 // G2: O = H W2[e], output columns [n_base, n_base + ncols) into rows ldo apart
-__global__ void __launch_bounds__(CS::THREADS)
+__global__ void __launch_bounds__(RS::THREADS)
 g2_kernel(const bf16_t* __restrict__ H, const bf16_t* __restrict__ w2,
           const int32_t* __restrict__ offsets, int d, int f, int E, int n_base, int ncols,
           int64_t ldo, bf16_t* __restrict__ O) {
     extern __shared__ __align__(16) char lds[];
-    using C = CS;
+    using C = RS;
     SlotTile t;
     const int NT = (ncols + C::BN - 1) / C::BN;
-    if (!find_slot_tile<C::THREADS>(offsets, E, C::BM, NT, xcd_remap(blockIdx.x, gridDim.x), C::BN, t))
+    if (!find_slot_tile<C::THREADS>(offsets, E, C::BM, NT, xcd_remap(blockIdx.x, gridDim.x), C::BN,
+                                    t, RASTER_GM))
         return;
-    DenseKC2<C, C::BM> la;
+    rs::DenseKC2<C, C::BM> la;
     la.init(H, H, f, (int64_t)t.off + t.m0, t.mrows, f);
-    DenseMC<C, C::BN> lb;
+    rs::DenseMC<C, C::BN> lb;
     lb.init(w2 + (int64_t)t.e * f * d, d, n_base + t.n0, n_base + ncols);
-    NoLoader nl;
-    Acc<C> acc;
-    gemm_mainloop<C>(la, lb, nl, f / GBK, GBK, lds, acc, t.mrows, ncols - t.n0);
+    rs::NoLoader nl;
+    rs::Acc<C> acc;
+    rs::mainloop<C>(la, lb, nl, f / rs::KS, lds, acc);
     WaveCoord<C> wc;
 #pragma unroll
     for (int i = 0; i < C::FM; ++i) {
@@ -188,85 +191,77 @@ g2_kernel(const bf16_t* __restrict__ H, const bf16_t* __restrict__ w2,
     }
 }
 
-// Pre-pass of the second GEMM with h formed on load: the slice's A tile (and
-// B's, in the extra tile) become h = SiLU(A) * B (act(A) when non-gated) in
-// place, with the arithmetic of G1's epilogue, so h is bit-identical to the
-// buffered one. Layout-oblivious: A and B tiles share one swizzled layout.
-// Each thread owns NIT 16-byte chunks. The work comes in three parts so that
-// the main loop can spread it between the MFMAs of the previous slice: load
-// (LDS reads), pair(p) (elements 2p and 2p+1 of the thread's chunks) and store.
-template <int ACT, class C>
-struct HPass {
-    static constexpr bool active = true;
-    static constexpr int NIT = C::A_BYTES / 16 / C::THREADS;
-    static constexpr int NPAIR = NIT * 4;
-    static_assert(C::A_BYTES / 16 % C::THREADS == 0, "whole chunks per thread");
-    struct St { uint32_t a[NPAIR], b[NPAIR]; };   // one bf16 pair per word
-    __device__ void load(const char* stage, int, St& st) const {
-#pragma unroll
-        for (int it = 0; it < NIT; ++it) {
-            const int q = threadIdx.x + it * C::THREADS;
-            const uint4 va = ld16(stage + q * 16);
-            st.a[4 * it] = va.x; st.a[4 * it + 1] = va.y; st.a[4 * it + 2] = va.z; st.a[4 * it + 3] = va.w;
-            if constexpr (ACT == ACT_SWIGLU) {
-                const uint4 vb = ld16(stage + C::A_BYTES + q * 16);
-                st.b[4 * it] = vb.x; st.b[4 * it + 1] = vb.y; st.b[4 * it + 2] = vb.z; st.b[4 * it + 3] = vb.w;
-            }
-        }
+// h of a pair of elements (one dword of bf16) from the pairs of A and B: the
+// arithmetic of G1's epilogue, on the same bf16 values, so the result is
+// bit-identical to the buffered h. Non-gated: act(A), B unused. With a gate
+// g: g * h, the arithmetic of G4's epilogue for the dW2 GEMM's operand.
+template <int ACT, bool GATE>
+__device__ __forceinline__ uint32_t h_pair(uint32_t a, uint32_t b, float g) {
+    float h0, h1;
+    if constexpr (ACT == ACT_SWIGLU) {
+        h0 = silu_bf(bf_lo(a)) * bf_lo(b);
+        h1 = silu_bf(bf_hi(a)) * bf_hi(b);
+    } else {
+        h0 = act_f<ACT>(bf_lo(a));
+        h1 = act_f<ACT>(bf_hi(a));
     }
-    __device__ void pair(St& st, int p) const {
-        const uint32_t w = st.a[p];
-        float h0, h1;
-        if constexpr (ACT == ACT_SWIGLU) {
-            h0 = silu_bf(bf_lo(w)) * bf_lo(st.b[p]);
-            h1 = silu_bf(bf_hi(w)) * bf_hi(st.b[p]);
-        } else {
-            h0 = act_f<ACT>(bf_lo(w));
-            h1 = act_f<ACT>(bf_hi(w));
-        }
-        st.a[p] = pack_bf2(h0, h1);
+    if constexpr (GATE) { h0 = g * h0; h1 = g * h1; }
+    return pack_bf2(h0, h1);
+}
+
+// Left operand of the second GEMM with h formed on load: KC tile of h rows
+// row0 + r (r < rows, else row0) from the slot-ordered A (and B), h formed in
+// registers between the loads and the LDS write (Section 3.1 keeps only the
+// first MLP's output; Section 5.2 recomputes the activation).
+template <int ACT, class C, int R>
+struct HKC {
+    static constexpr bool MC = false;
+    using G = rs::KCGeom<C, R>;
+    static constexpr int NCH = G::NCH;
+    static constexpr bool GATED = ACT == ACT_SWIGLU;
+    const bf16_t* pa;      // A + row0 * ld + this thread's chunk column
+    int64_t dba;           // B - A, in elements
+    int ld, rows;
+    rs::u32x4 va[NCH], vb[NCH];
+    __device__ void init(const bf16_t* A, const bf16_t* B, int ld_, int64_t row0, int rows_) {
+        ld = ld_;
+        rows = rows_;
+        dba = GATED ? B - A : 0;
+        pa = A + rs::roff(row0, ld) + G::chunk(0) * 8;
     }
-    __device__ void store(char* stage, const St& st) const {
-#pragma unroll
-        for (int it = 0; it < NIT; ++it)
-            st16(stage + (threadIdx.x + it * C::THREADS) * 16,
-                 make_uint4(st.a[4 * it], st.a[4 * it + 1], st.a[4 * it + 2], st.a[4 * it + 3]));
+    template <int i> __device__ void load(int kt) {
+        int r = G::row(i);
+        r = r < rows ? r : 0;
+        const bf16_t* q = pa + rs::roff(r, ld) + kt * rs::KS;
+        va[i] = rs::ldg16(q);
+        if constexpr (GATED) vb[i] = rs::ldg16(q + dba);
     }
-    __device__ void operator()(char* stage, int kt) const {
-        St st;
-        load(stage, kt, st);
-#pragma unroll
-        for (int p = 0; p < NPAIR; ++p) pair(st, p);
-        store(stage, st);
-    }
+    // h of dword p of chunk i, in place of A's
+    static constexpr int NSUB = 4;
+    template <int i, int p> __device__ void sub() { va[i][p] = h_pair<ACT, false>(va[i][p], vb[i][p], 0.f); }
+    template <int i> __device__ void store(char* tile) { rs::sts16(tile + G::lds(i), va[i]); }
 };
 
-// G2 with h formed on load (the paper's recomputation in the second GEMM,
-// Section 3.1): O = h W2[e] from the saved A (and B), no h buffer.
+// G2 with h formed on load: O = h W2[e] from the saved A (and B), no h buffer.
 template <int ACT>
-__global__ void __launch_bounds__(CS::THREADS)
+__global__ void __launch_bounds__(RHW::THREADS)
 g2h_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B,
            const bf16_t* __restrict__ w2, const int32_t* __restrict__ offsets, int d, int f,
            int E, int n_base, int ncols, int64_t ldo, bf16_t* __restrict__ O) {
     extern __shared__ __align__(16) char lds[];
-    using C = CSecondH<ACT>;
+    using C = RHW;
     SlotTile t;
     const int NT = (ncols + C::BN - 1) / C::BN;
-    if (!find_slot_tile<C::THREADS>(offsets, E, C::BM, NT, xcd_remap(blockIdx.x, gridDim.x), C::BN, t))
+    if (!rs::find_slot_tile<C::THREADS>(reinterpret_cast<int*>(lds), offsets, E, C::BM, NT,
+                                        xcd_remap(blockIdx.x, gridDim.x), C::BN, t, RASTER_GM))
         return;
-    DenseMC<C, C::BN> lb;
+    HKC<ACT, C, C::BM> la;
+    la.init(A, B, f, (int64_t)t.off + t.m0, t.mrows);
+    rs::DenseMC<C, C::BN> lb;
     lb.init(w2 + (int64_t)t.e * f * d, d, n_base + t.n0, n_base + ncols);
-    NoLoader nl;
-    Acc<C> acc;
-    if constexpr (ACT == ACT_SWIGLU) {
-        PairKC<C, C::BM> la;
-        la.init(A, B, f, (int64_t)t.off + t.m0, t.mrows);
-        gemm_mainloop<C>(la, lb, nl, f / GBK, GBK, lds, acc, t.mrows, ncols - t.n0, HPass<ACT, C>{});
-    } else {
-        DenseKC2<C, C::BM> la;
-        la.init(A, A, f, (int64_t)t.off + t.m0, t.mrows, f);
-        gemm_mainloop<C>(la, lb, nl, f / GBK, GBK, lds, acc, t.mrows, ncols - t.n0, HPass<ACT, C>{});
-    }
+    rs::NoLoader nl;
+    rs::Acc<C> acc;
+    rs::mainloop<C>(la, lb, nl, f / rs::KS, lds, acc);
     WaveCoord<C> wc;
 #pragma unroll
     for (int i = 0; i < C::FM; ++i) {
@@ -290,26 +285,27 @@ g2h_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B,
 // A/B, and HG = g * h (h recomputed from A, B) for G3. Non-gated: dA = g u
 // act'(A) over A, h = act(A).
 template <int ACT, bool HG_OUT>
-__global__ void __launch_bounds__(C4::THREADS, 2)
+__global__ void __launch_bounds__(RS::THREADS)
 g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
           const float* __restrict__ gates, const int32_t* __restrict__ offsets,
           const int32_t* __restrict__ eti, const int32_t* __restrict__ slot_src, int d, int f,
           int E, bf16_t* __restrict__ A, bf16_t* __restrict__ B, bf16_t* __restrict__ HG,
           float* __restrict__ part) {
     extern __shared__ __align__(16) char lds[];
-    using C = C4;
+    using C = RS;
     SlotTile t;
     const int NT = (f + C::BN - 1) / C::BN;
-    if (!find_slot_tile<C::THREADS>(offsets, E, C::BM, NT, xcd_remap(blockIdx.x, gridDim.x), C::BN, t))
+    if (!find_slot_tile<C::THREADS>(offsets, E, C::BM, NT, xcd_remap(blockIdx.x, gridDim.x), C::BN,
+                                    t, RASTER_GM))
         return;
-    GatherKC<C, C::BM> la;
+    rs::GatherKC<C, C::BM> la;
     la.init(dy, d, eti + t.off + t.m0, t.mrows);
-    DenseKC2<C, C::BN> lb;  // rows c of W2[e] ([f][d]), K = d
+    rs::DenseKC2<C, C::BN> lb;  // rows c of W2[e] ([f][d]), K = d
     const bf16_t* W2e = w2 + (int64_t)t.e * f * d;
     lb.init(W2e, W2e, d, t.n0, min(C::BN, f - t.n0), d);
-    NoLoader nl;
-    Acc<C> acc;
-    gemm_mainloop<C>(la, lb, nl, d / GBK, GBK, lds, acc, t.mrows, f - t.n0);
+    rs::NoLoader nl;
+    rs::Acc<C> acc;
+    rs::mainloop<C>(la, lb, nl, d / rs::KS, lds, acc);
     // ---- epilogue, one round per fragment row-block (64 rows of the tile) ----
     // The A and B rows of the round come into LDS by DMA (1 KB copies, many in
     // flight); every lane reads its values there, writes dA and dB back in
@@ -436,12 +432,12 @@ __device__ __forceinline__ void st_nt(float* p, const f32x4& v) {
 }
 
 // G3: dW2[e] = sum_s HG[s]^T dY[eti[s]]   (M = f, N = d, K = slots of e)
-__global__ void __launch_bounds__(CS::THREADS)
+__global__ void __launch_bounds__(RS::THREADS)
 g3_kernel(const bf16_t* __restrict__ HG, const bf16_t* __restrict__ dy,
           const int32_t* __restrict__ offsets, const int32_t* __restrict__ eti, int d, int f,
           float* __restrict__ dw2) {
     extern __shared__ __align__(16) char lds[];
-    using C = CS;
+    using C = RS;
     const int MT = (f + C::BM - 1) / C::BM, NT = (d + C::BN - 1) / C::BN;
     int e, mt, nt;
     if (!wgrad_tile(blockIdx.x, MT, NT, e, mt, nt)) return;
@@ -449,16 +445,15 @@ g3_kernel(const bf16_t* __restrict__ HG, const bf16_t* __restrict__ dy,
     const int n0 = nt * C::BN;
     const int off = offsets[e];
     const int cnt = offsets[e + 1] - off;
-    SlotMC<C, C::BM> la;
-    GatherMC<C, C::BN> lb;
-    NoLoader nl;
+    rs::SlotMC<C, C::BM> la;
+    rs::GatherMC<C, C::BN> lb;
+    rs::NoLoader nl;
     if (cnt > 0) {
         la.init(HG, f, off, m0, f, cnt);
         lb.init(dy, d, n0, d, eti + off, cnt);
     }
-    Acc<C> acc;
-    gemm_mainloop<C>(la, lb, nl, (cnt + GBK - 1) / GBK, tail_from(cnt), lds, acc, f - m0,
-                     d - n0);
+    rs::Acc<C> acc;
+    rs::mainloop<C>(la, lb, nl, rs::slices(cnt), lds, acc);
     float* out = dw2 + (int64_t)e * f * d;
     RowStage<C, 1>::run(acc, lds, [&](int, int r, int c, const f32x4& v) {
         const int m = m0 + r, n = n0 + c;
@@ -466,87 +461,77 @@ g3_kernel(const bf16_t* __restrict__ HG, const bf16_t* __restrict__ dy,
     });
 }
 
+
+// Left operand of the dW2 GEMM with g*h formed on load: MC tile of g*h slot
+// rows off + kr (K = the expert's slots) from the saved A (and B) and the
+// slot-ordered gates gs. Rows at or past cnt are read from row cnt - 1 and
+// stored as zeros.
+template <int ACT, class C, int R>
+struct GHMC {
+    static constexpr bool MC = true;
+    using G = rs::MCGeom<C, R>;
+    static constexpr int NCH = G::NCH;
+    static constexpr bool GATED = ACT == ACT_SWIGLU;
+    const bf16_t* pa;      // A + off * ld + this thread's column
+    int64_t dba;           // B - A, in elements
+    const float* gsp;      // gates of slots off, off + 1, ...
+    int ld, cnt;
+    uint32_t zmask;
+    rs::u32x4 va[NCH], vb[NCH];
+    float g[NCH];
+    __device__ void init(const bf16_t* A, const bf16_t* B, int ld_, int64_t off, int col0,
+                         int ncols, int cnt_, const float* gs) {
+        ld = ld_;
+        cnt = cnt_;
+        zmask = 0;
+        dba = GATED ? B - A : 0;
+        int c = col0 + G::col(0);
+        c = c < ncols ? c : ncols - 8;
+        pa = A + rs::roff(off, ld) + c;
+        gsp = gs + off;
+    }
+    template <int i> __device__ void load(int kt) {
+        int k = kt * rs::KS + G::krow(i);
+        const bool past = k >= cnt;
+        zmask = past ? (zmask | (1u << i)) : (zmask & ~(1u << i));
+        k = past ? cnt - 1 : k;
+        const bf16_t* q = pa + rs::roff(k, ld);
+        va[i] = rs::ldg16(q);
+        if constexpr (GATED) vb[i] = rs::ldg16(q + dba);
+        g[i] = gsp[k];
+    }
+    // g * h of dword p of chunk i, in place of A's
+    static constexpr int NSUB = 4;
+    template <int i, int p> __device__ void sub() { va[i][p] = h_pair<ACT, true>(va[i][p], vb[i][p], g[i]); }
+    template <int i> __device__ void store(char* tile) {
+        const rs::u32x4 z = {0u, 0u, 0u, 0u};
+        rs::sts16(tile + G::lds(i), (zmask >> i) & 1 ? z : va[i]);
+    }
+};
+
 // gs[s] = gates[slot_src[s]] for the filled slots s < offsets[E], 0 for the
-// rest up to S + pad (the gate of each slot in slot order, for the dW2 GEMM's
-// pre-pass; fewer than S slots are filled only when the index build rejected
-// choices)
+// rest up to S (the gate of each slot in slot order, for the dW2 GEMM's
+// left operand; fewer than S slots are filled only when the index build
+// rejected choices)
 __global__ void slot_gates(const float* __restrict__ gates, const int32_t* __restrict__ slot_src,
-                           const int32_t* __restrict__ offsets, int E, int64_t S, int64_t pad,
+                           const int32_t* __restrict__ offsets, int E, int64_t S,
                            float* __restrict__ gs) {
     const int64_t s = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (s < offsets[E]) gs[s] = gates[slot_src[s]];
-    else if (s < S + pad) gs[s] = 0.0f;
+    else if (s < S) gs[s] = 0.0f;
 }
-constexpr int GS_PAD = 64;   // zero gates past the last slot (a slice reads up to 31 more)
-
-// Pre-pass of the dW2 GEMM with g*h formed on load: the slice's A tile (MC: 32
-// slot rows of 256 columns) and B's, in the extra tile, become g*h = g * SiLU(A)
-// * B in place (g * act(A) when non-gated), with the arithmetic of G4's
-// epilogue, so the result equals the buffered g*h bit for bit. The slot rows'
-// gates sit in the 128-byte gate slot of the stage.
-template <int ACT, class C>
-struct GPass {
-    static constexpr bool active = true;
-    static constexpr int NIT = C::A_BYTES / 16 / C::THREADS;
-    static constexpr int NPAIR = NIT * 4;
-    static constexpr int CPR = C::BM * 2 / 16;      // chunks per slot row
-    static_assert(C::A_BYTES / 16 % C::THREADS == 0, "whole chunks per thread");
-    const char* gate_slots;   // NST x 32 floats after the ring
-    struct St { uint32_t a[NPAIR], b[NPAIR]; float g[NIT]; };   // one bf16 pair per word
-    __device__ void load(const char* stage, int kt, St& st) const {
-        const float* g = reinterpret_cast<const float*>(gate_slots + (kt % NST) * 128);
-#pragma unroll
-        for (int it = 0; it < NIT; ++it) {
-            const int q = threadIdx.x + it * C::THREADS;
-            st.g[it] = g[q / CPR];
-            const uint4 va = ld16(stage + q * 16);
-            st.a[4 * it] = va.x; st.a[4 * it + 1] = va.y; st.a[4 * it + 2] = va.z; st.a[4 * it + 3] = va.w;
-            if constexpr (ACT == ACT_SWIGLU) {
-                const uint4 vb = ld16(stage + C::A_BYTES + q * 16);
-                st.b[4 * it] = vb.x; st.b[4 * it + 1] = vb.y; st.b[4 * it + 2] = vb.z; st.b[4 * it + 3] = vb.w;
-            }
-        }
-    }
-    __device__ void pair(St& st, int p) const {
-        const uint32_t w = st.a[p];
-        const float gv = st.g[p / 4];
-        float h0, h1;
-        if constexpr (ACT == ACT_SWIGLU) {
-            h0 = gv * (silu_bf(bf_lo(w)) * bf_lo(st.b[p]));
-            h1 = gv * (silu_bf(bf_hi(w)) * bf_hi(st.b[p]));
-        } else {
-            h0 = gv * act_f<ACT>(bf_lo(w));
-            h1 = gv * act_f<ACT>(bf_hi(w));
-        }
-        st.a[p] = pack_bf2(h0, h1);
-    }
-    __device__ void store(char* stage, const St& st) const {
-#pragma unroll
-        for (int it = 0; it < NIT; ++it)
-            st16(stage + (threadIdx.x + it * C::THREADS) * 16,
-                 make_uint4(st.a[4 * it], st.a[4 * it + 1], st.a[4 * it + 2], st.a[4 * it + 3]));
-    }
-    __device__ void operator()(char* stage, int kt) const {
-        St st;
-        load(stage, kt, st);
-#pragma unroll
-        for (int p = 0; p < NPAIR; ++p) pair(st, p);
-        store(stage, st);
-    }
-};
 
 // G3 with g*h formed on load from the saved A (and B) and the slot-ordered
 // gates gs: dW2[e] = sum_s (g h)[s]^T dY[eti[s]]. Runs before G4, which then
 // writes dA, dB over A, B and no g*h.
 template <int ACT>
-__global__ void __launch_bounds__(CS::THREADS)
+__global__ void __launch_bounds__(RHW::THREADS)
 g3h_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B,
            const float* __restrict__ gs, const bf16_t* __restrict__ dy,
            const int32_t* __restrict__ offsets, const int32_t* __restrict__ eti, int d, int f,
            float* __restrict__ dw2) {
     extern __shared__ __align__(16) char lds[];
-    using C = CSecondH<ACT>;
-    constexpr int NSRC = ACT == ACT_SWIGLU ? 2 : 1;
+    using C = RHW;
     const int MT = (f + C::BM - 1) / C::BM, NT = (d + C::BN - 1) / C::BN;
     int e, mt, nt;
     if (!wgrad_tile(blockIdx.x, MT, NT, e, mt, nt)) return;
@@ -554,16 +539,15 @@ g3h_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B,
     const int n0 = nt * C::BN;
     const int off = offsets[e];
     const int cnt = offsets[e + 1] - off;
-    SlotMCG<C, C::BM, NSRC> la;
-    GatherMC<C, C::BN> lb;
-    NoLoader nl;
+    GHMC<ACT, C, C::BM> la;
+    rs::GatherMC<C, C::BN> lb;
+    rs::NoLoader nl;
     if (cnt > 0) {
-        la.init(A, NSRC == 2 ? B : A, f, off, m0, f, cnt, gs, lds_offset(lds) + NST * C::STAGE);
+        la.init(A, B, f, off, m0, f, cnt, gs);
         lb.init(dy, d, n0, d, eti + off, cnt);
     }
-    Acc<C> acc;
-    gemm_mainloop<C>(la, lb, nl, (cnt + GBK - 1) / GBK, tail_from(cnt), lds, acc, f - m0,
-                     d - n0, GPass<ACT, C>{lds + NST * C::STAGE});
+    rs::Acc<C> acc;
+    rs::mainloop<C>(la, lb, nl, rs::slices(cnt), lds, acc);
     float* out = dw2 + (int64_t)e * f * d;
     RowStage<C, 1>::run(acc, lds, [&](int, int r, int c, const f32x4& v) {
         const int m = m0 + r, n = n0 + c;
@@ -574,7 +558,7 @@ g3h_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B,
 // G5: dW1[e] = x[eti]^T dA, dW3[e] = x[eti]^T dB   (M = d, N = f, K = slots of e)
 // (non-gated: dW1 alone)
 template <int ACT>
-__global__ void __launch_bounds__(CD::THREADS)
+__global__ void __launch_bounds__(RD::THREADS)
 g5_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ dA,
           const bf16_t* __restrict__ dB, const int32_t* __restrict__ offsets,
           const int32_t* __restrict__ eti, int d, int f, float* __restrict__ dw1,
@@ -588,17 +572,16 @@ g5_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ dA,
     const int n0 = nt * C::BN;
     const int off = offsets[e];
     const int cnt = offsets[e + 1] - off;
-    GatherMC<C, C::BM> la;
-    SlotMC<C, C::BN> lb0;
-    std::conditional_t<ACT == ACT_SWIGLU, SlotMC<C, C::BN>, NoLoader> lb1;
+    rs::GatherMC<C, C::BM> la;
+    rs::SlotMC<C, C::BN> lb0;
+    std::conditional_t<ACT == ACT_SWIGLU, rs::SlotMC<C, C::BN>, rs::NoLoader> lb1;
     if (cnt > 0) {
         la.init(x, d, m0, d, eti + off, cnt);
         lb0.init(dA, f, off, n0, f, cnt);
         if constexpr (ACT == ACT_SWIGLU) lb1.init(dB, f, off, n0, f, cnt);
     }
-    Acc<C> acc;
-    gemm_mainloop<C>(la, lb0, lb1, (cnt + GBK - 1) / GBK, tail_from(cnt), lds, acc, d - m0,
-                     f - n0);
+    rs::Acc<C> acc;
+    rs::mainloop<C>(la, lb0, lb1, rs::slices(cnt), lds, acc);
     float* o1 = dw1 + (int64_t)e * d * f;
     float* o3 = ACT == ACT_SWIGLU ? dw3 + (int64_t)e * d * f : o1;  // dw3 is NULL when non-gated
     RowStage<C, ACT == ACT_SWIGLU ? 2 : 1>::run(acc, lds, [&](int b, int r, int c, const f32x4& v) {
@@ -610,25 +593,26 @@ g5_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ dA,
 // G6: dX_slot = dA W1[e]^T + dB W3[e]^T, output columns [n_base, n_base + ncols)
 // into rows ldo apart   (K = 2f; non-gated: dA W1[e]^T, K = f,
 // called with dB = dA and W3 = W1, whose second halves are then never reached)
-__global__ void __launch_bounds__(CS::THREADS)
+__global__ void __launch_bounds__(RS::THREADS)
 g6_kernel(const bf16_t* __restrict__ dA, const bf16_t* __restrict__ dB,
           const bf16_t* __restrict__ w1, const bf16_t* __restrict__ w3,
           const int32_t* __restrict__ offsets, int d, int f, int E, int kslices, int n_base,
           int ncols, int64_t ldo, bf16_t* __restrict__ dX) {
     extern __shared__ __align__(16) char lds[];
-    using C = CS;
+    using C = RS;
     SlotTile t;
     const int NT = (ncols + C::BN - 1) / C::BN;
-    if (!find_slot_tile<C::THREADS>(offsets, E, C::BM, NT, xcd_remap(blockIdx.x, gridDim.x), C::BN, t))
+    if (!find_slot_tile<C::THREADS>(offsets, E, C::BM, NT, xcd_remap(blockIdx.x, gridDim.x), C::BN,
+                                    t, RASTER_GM))
         return;
-    DenseKC2<C, C::BM> la;
+    rs::DenseKC2<C, C::BM> la;
     la.init(dA, dB, f, (int64_t)t.off + t.m0, t.mrows, f);
-    DenseKC2<C, C::BN> lb;  // rows i of W1[e] / W3[e] ([d][f]), K = f then f
+    rs::DenseKC2<C, C::BN> lb;  // rows i of W1[e] / W3[e] ([d][f]), K = f then f
     lb.init(w1 + (int64_t)t.e * d * f, w3 + (int64_t)t.e * d * f, f, n_base + t.n0,
             min(C::BN, ncols - t.n0), f);
-    NoLoader nl;
-    Acc<C> acc;
-    gemm_mainloop<C>(la, lb, nl, kslices, GBK, lds, acc, t.mrows, ncols - t.n0);
+    rs::NoLoader nl;
+    rs::Acc<C> acc;
+    rs::mainloop<C>(la, lb, nl, kslices, lds, acc);
     WaveCoord<C> wc;
 #pragma unroll
     for (int i = 0; i < C::FM; ++i) {
@@ -832,39 +816,49 @@ hipError_t set_lds_limits() {
         auto per_act = [&](auto act) {
             constexpr int ACT = decltype(act)::value;
             set(reinterpret_cast<const void*>(g1_kernel<ACT>), CFirst<ACT>::LDS);
-            set(reinterpret_cast<const void*>(g4_kernel<ACT, true>), C4::LDS);
-            set(reinterpret_cast<const void*>(g4_kernel<ACT, false>), C4::LDS);
+            set(reinterpret_cast<const void*>(g4_kernel<ACT, true>), RS::LDS);
+            set(reinterpret_cast<const void*>(g4_kernel<ACT, false>), RS::LDS);
             set(reinterpret_cast<const void*>(g5_kernel<ACT>), CFirst<ACT>::LDS);
-            set(reinterpret_cast<const void*>(g2h_kernel<ACT>), CSecondH<ACT>::LDS);
-            set(reinterpret_cast<const void*>(g3h_kernel<ACT>), CSecondH<ACT>::LDS + NST * 128);
+            set(reinterpret_cast<const void*>(g2h_kernel<ACT>), RHW::LDS);
+            set(reinterpret_cast<const void*>(g3h_kernel<ACT>), RHW::LDS);
         };
         per_act(std::integral_constant<int, ACT_SWIGLU>{});
         per_act(std::integral_constant<int, ACT_SILU>{});
         per_act(std::integral_constant<int, ACT_RELU>{});
-        set(reinterpret_cast<const void*>(g2_kernel), CS::LDS);
-        set(reinterpret_cast<const void*>(g3_kernel), CS::LDS);
-        set(reinterpret_cast<const void*>(g6_kernel), CS::LDS);
+        set(reinterpret_cast<const void*>(g2_kernel), RS::LDS);
+        set(reinterpret_cast<const void*>(g3_kernel), RS::LDS);
+        set(reinterpret_cast<const void*>(g6_kernel), RS::LDS);
         return e;
     }();
     return status;
 }
 
 inline size_t align256(size_t b) { return (b + 255) / 256 * 256; }
-inline int g4_nparts(int f) { return cdiv(f, C4::BN) * C4::WN; }
+inline int g4_nparts(int f) { return cdiv(f, RS::BN) * RS::WN; }
 // Column strip of the expert output (or of dX_slot) when the combine follows
 // strip by strip. Narrow strips save memory, but a launch needs enough tiles
 // (here about six waves of 256) or its last partial wave leaves CUs idle, so
-// the strips are as narrow as that allows, in whole 256-column tiles, and of
-// equal width: about 1024 columns for 98k slots and 64 experts, 2048 for 65k
-// slots and 8 experts, 256 for 524k slots.
-inline int strip_width(int64_t S, int E, int d) {
-    const int64_t mtiles = (S + CS::BM - 1) / CS::BM + E / 2;   // tiles per column of tiles
+// the strips are about as narrow as that allows, in whole tiles of the GEMM
+// that produces them (BM x BN): with 256 x 256 tiles about 1024 columns for
+// 98k slots and 64 experts, 2048 for 65k slots and 8 experts, 256 for 524k
+// slots. `narrow`: round the number of strips up rather than down (the last
+// strip may then be narrower), for the memory-lean h-on-load policy.
+inline int strip_width(int64_t S, int E, int d, int BM, int BN, bool narrow) {
+    const int64_t mtiles = (S + BM - 1) / BM + E / 2;   // tiles per column of tiles
     const int64_t want = 6 * 256;
-    const int64_t w = (int64_t)CS::BN * ((want + mtiles - 1) / mtiles);
-    const int n = (int)(d / (w < d ? w : d));                    // strips
-    const int width = ((d + n - 1) / n + CS::BN - 1) / CS::BN * CS::BN;
+    int64_t w = (int64_t)BN * ((want + mtiles - 1) / mtiles);
+    w = w < d ? w : d;
+    const int n = (int)(narrow ? (d + w - 1) / w : d / w);   // strips
+    const int width = ((d + n - 1) / n + BN - 1) / BN * BN;
     return width < d ? width : d;
 }
+// strips of the forward's second GEMM (h on load: its 128 x 512 tiles) and of
+// the backward's dX GEMM
+inline int fwd_strip(int64_t S, int E, int d, bool h_on_load) {
+    return h_on_load ? strip_width(S, E, d, RHW::BM, RHW::BN, true)
+                     : strip_width(S, E, d, RS::BM, RS::BN, false);
+}
+inline int bwd_strip(int64_t S, int E, int d) { return strip_width(S, E, d, RS::BM, RS::BN, false); }
 
 }  // namespace
 
@@ -873,7 +867,7 @@ size_t ffn_fwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool c
     const size_t S = (size_t)T * k;
     if (f32) return combined ? align256(S * d * sizeof(float)) : 0;  // O
     const size_t h = h_on_load ? 0 : align256(S * f * sizeof(bf16_t));   // H
-    return combined ? h + align256(S * strip_width(S, E, d) * sizeof(bf16_t)) : h;
+    return combined ? h + align256(S * fwd_strip(S, E, d, h_on_load) * sizeof(bf16_t)) : h;
 }
 
 namespace {
@@ -896,7 +890,7 @@ hipError_t ffn_fwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
     }
     if (hipError_t e = set_lds_limits(); e != hipSuccess) return e;
     using C1 = CFirst<ACT>;
-    using C2H = CSecondH<ACT>;
+    using C2H = RHW;
     // h buffered between the GEMMs, or (h_on_load) formed again from A, B
     bf16_t* H = a.h_on_load ? nullptr : static_cast<bf16_t*>(a.ws);
     hipLaunchKernelGGL(g1_kernel<ACT>, dim3(slot_grid(S, a.E, C1::BM, cdiv(a.f, C1::BN))),
@@ -912,8 +906,8 @@ hipError_t ffn_fwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
                                c0, nc, ldo, out);
             probe::mark("g2h_kernel", st);
         } else {
-            hipLaunchKernelGGL(g2_kernel, dim3(slot_grid(S, a.E, CS::BM, cdiv(nc, CS::BN))),
-                               dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)H,
+            hipLaunchKernelGGL(g2_kernel, dim3(slot_grid(S, a.E, RS::BM, cdiv(nc, RS::BN))),
+                               dim3(RS::THREADS), RS::LDS, st, (const bf16_t*)H,
                                (const bf16_t*)a.w2, a.offsets, a.d, a.f, a.E, c0, nc, ldo, out);
             probe::mark("g2_kernel", st);
         }
@@ -923,7 +917,7 @@ hipError_t ffn_fwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
         return hipGetLastError();
     }
     // combined: one column strip of O at a time, straight into y
-    const int sw = strip_width(S, a.E, a.d);
+    const int sw = fwd_strip(S, a.E, a.d, a.h_on_load);
     bf16_t* strip = reinterpret_cast<bf16_t*>(
         static_cast<char*>(a.ws) + (a.h_on_load ? 0 : align256((size_t)S * a.f * sizeof(bf16_t))));
     for (int c0 = 0; c0 < a.d; c0 += sw) {
@@ -980,9 +974,9 @@ size_t ffn_bwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool c
     const size_t S = (size_t)T * k;
     if (f32) return combined ? align256(S * d * sizeof(float)) : 0;  // dX_slot
     const size_t part = align256(S * g4_nparts(f) * sizeof(float));  // d_gate partials
-    const size_t strip = combined ? S * strip_width(S, E, d) * sizeof(bf16_t) : 0;
+    const size_t strip = combined ? S * bwd_strip(S, E, d) * sizeof(bf16_t) : 0;
     if (h_on_load) {   // slot-ordered gates for G3, then (same space) the dX strip
-        const size_t gs = (S + GS_PAD) * sizeof(float);
+        const size_t gs = S * sizeof(float);
         return part + align256(gs > strip ? gs : strip);
     }
     const size_t hg = S * f * sizeof(bf16_t);                         // g*h, then dX strips
@@ -1018,7 +1012,7 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
     }
     if (hipError_t e = set_lds_limits(); e != hipSuccess) return e;
     using C5 = CFirst<ACT>;
-    using C3H = CSecondH<ACT>;
+    using C3H = RHW;
     const int nparts = g4_nparts(a.f);
     float* part = static_cast<float*>(a.ws);
     char* const ws2 = static_cast<char*>(a.ws) + align256((size_t)S * nparts * sizeof(float));
@@ -1032,18 +1026,18 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
     const void* Bx = GATED ? a.B : a.A;
     const void* w3x = GATED ? a.w3 : a.w1;
     if (a.h_on_load) {
-        hipLaunchKernelGGL(slot_gates, grid1d(S + GS_PAD, 256), dim3(256), 0, st, a.gates,
-                           a.slot_src, a.offsets, a.E, S, (int64_t)GS_PAD, gs);
+        hipLaunchKernelGGL(slot_gates, grid1d(S, 256), dim3(256), 0, st, a.gates,
+                           a.slot_src, a.offsets, a.E, S, gs);
         probe::mark("slot_gates", st);
         hipLaunchKernelGGL(g3h_kernel<ACT>, dim3(wgrad_grid(a.E, cdiv(a.f, C3H::BM), cdiv(a.d, C3H::BN))),
-                           dim3(C3H::THREADS), C3H::LDS + NST * 128, st, (const bf16_t*)a.A,
+                           dim3(C3H::THREADS), C3H::LDS, st, (const bf16_t*)a.A,
                            (const bf16_t*)Bx, (const float*)gs, (const bf16_t*)a.dy, a.offsets,
                            a.eti, a.d, a.f, a.dw2);
         probe::mark("g3h_kernel", st);
     }
     auto g4 = a.h_on_load ? g4_kernel<ACT, false> : g4_kernel<ACT, true>;
-    hipLaunchKernelGGL(g4, dim3(slot_grid(S, a.E, C4::BM, cdiv(a.f, C4::BN))),
-                       dim3(C4::THREADS), C4::LDS, st, (const bf16_t*)a.dy, (const bf16_t*)a.w2,
+    hipLaunchKernelGGL(g4, dim3(slot_grid(S, a.E, RS::BM, cdiv(a.f, RS::BN))),
+                       dim3(RS::THREADS), RS::LDS, st, (const bf16_t*)a.dy, (const bf16_t*)a.w2,
                        a.gates, a.offsets, a.eti, a.slot_src, a.d, a.f, a.E, (bf16_t*)a.A,
                        (bf16_t*)a.B, HG, part);
     probe::mark("g4_kernel", st);
@@ -1051,8 +1045,8 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
                        a.offsets, a.E, S, a.dgates);
     probe::mark("dgate_reduce", st);
     if (!a.h_on_load) {
-        hipLaunchKernelGGL(g3_kernel, dim3(wgrad_grid(a.E, cdiv(a.f, CS::BM), cdiv(a.d, CS::BN))),
-                           dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)HG, (const bf16_t*)a.dy,
+        hipLaunchKernelGGL(g3_kernel, dim3(wgrad_grid(a.E, cdiv(a.f, RS::BM), cdiv(a.d, RS::BN))),
+                           dim3(RS::THREADS), RS::LDS, st, (const bf16_t*)HG, (const bf16_t*)a.dy,
                            a.offsets, a.eti, a.d, a.f, a.dw2);
         probe::mark("g3_kernel", st);
     }
@@ -1060,10 +1054,10 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
                        dim3(C5::THREADS), C5::LDS, st, (const bf16_t*)a.x, (const bf16_t*)a.A,
                        (const bf16_t*)a.B, a.offsets, a.eti, a.d, a.f, a.dw1, a.dw3);
     probe::mark("g5_kernel", st);
-    const int kslices = (GATED ? 2 : 1) * a.f / GBK;
+    const int kslices = (GATED ? 2 : 1) * a.f / rs::KS;
     if (!a.y) {   // dX_slot [S, d] for the caller's combine
-        hipLaunchKernelGGL(g6_kernel, dim3(slot_grid(S, a.E, CS::BM, cdiv(a.d, CS::BN))),
-                           dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)a.A, (const bf16_t*)Bx,
+        hipLaunchKernelGGL(g6_kernel, dim3(slot_grid(S, a.E, RS::BM, cdiv(a.d, RS::BN))),
+                           dim3(RS::THREADS), RS::LDS, st, (const bf16_t*)a.A, (const bf16_t*)Bx,
                            (const bf16_t*)a.w1, (const bf16_t*)w3x, a.offsets, a.d, a.f, a.E,
                            kslices, 0, a.d, (int64_t)a.d, (bf16_t*)a.dX);
         probe::mark("g6_kernel", st);
@@ -1071,11 +1065,11 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
     }
     // combined: one column strip of dX_slot at a time, summed straight into dx;
     // by default the strip reuses g*h's workspace, which G3 has finished with
-    const int sw = strip_width(S, a.E, a.d);
+    const int sw = bwd_strip(S, a.E, a.d);
     for (int c0 = 0; c0 < a.d; c0 += sw) {
         const int nc = min(sw, a.d - c0);
-        hipLaunchKernelGGL(g6_kernel, dim3(slot_grid(S, a.E, CS::BM, cdiv(nc, CS::BN))),
-                           dim3(CS::THREADS), CS::LDS, st, (const bf16_t*)a.A, (const bf16_t*)Bx,
+        hipLaunchKernelGGL(g6_kernel, dim3(slot_grid(S, a.E, RS::BM, cdiv(nc, RS::BN))),
+                           dim3(RS::THREADS), RS::LDS, st, (const bf16_t*)a.A, (const bf16_t*)Bx,
                            (const bf16_t*)a.w1, (const bf16_t*)w3x, a.offsets, a.d, a.f, a.E,
                            kslices, c0, nc, (int64_t)nc, strip);
         probe::mark("g6_kernel", st);

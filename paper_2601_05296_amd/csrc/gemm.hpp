@@ -507,8 +507,13 @@ __device__ __forceinline__ bool wgrad_tile(int bid, int MT, int NT, int& e, int&
 inline int wgrad_grid(int E, int MT, int NT) { return E * 8 * ((MT * NT + 7) / 8); }
 
 // ---- grouped tile lookup ------------------------------------------------------------
-// Tiles of expert e: ceil(M_e / BM) * NT, laid out expert after expert, with
-// the M tile index running fastest (neighbouring tiles share a weight panel).
+// Tiles of expert e: ceil(M_e / BM) * NT, laid out expert after expert. With
+// GM = 0 the M tile index runs fastest (neighbouring tiles share a weight
+// panel). With GM > 0 the tiles come in groups of GM M tiles, N slower
+// inside a group: the workgroups that run at the same time on one XCD then
+// cover a GM x (32 / GM) block of tiles, which share both their row panels
+// and their weight panels in that XCD's L2 (an expert's last, narrower group
+// holds its remaining M tiles).
 // Every thread of the block must call this. Returns false past the last tile.
 struct SlotTile {
     int e;       // expert
@@ -520,7 +525,7 @@ struct SlotTile {
 
 template <int THREADS>
 __device__ bool find_slot_tile(const int32_t* __restrict__ offsets, int E, int BM, int NT,
-                               int bid, int BN, SlotTile& t) {
+                               int bid, int BN, SlotTile& t, int GM = 0) {
     static_assert(THREADS >= 256, "one thread per expert");
     __shared__ int s_scan[THREADS];
     __shared__ int s_res[2];
@@ -550,11 +555,23 @@ __device__ bool find_slot_tile(const int32_t* __restrict__ offsets, int E, int B
     const int local = s_res[1];
     const int cnt = offsets[e + 1] - offsets[e];
     const int nmt = (cnt + BM - 1) / BM;
+    const int gm = GM > 0 ? GM : nmt;         // M tiles per group
+    const int full = nmt / gm * gm;           // M tiles in whole groups
+    int mt, nt;
+    if (local < full * NT) {
+        const int g = local / (gm * NT), w = local % (gm * NT);
+        mt = g * gm + w % gm;
+        nt = w / gm;
+    } else {
+        const int rem = nmt - full, l2 = local - full * NT;
+        mt = full + l2 % rem;
+        nt = l2 / rem;
+    }
     t.e = e;
     t.off = offsets[e];
-    t.m0 = (local % nmt) * BM;
+    t.m0 = mt * BM;
     t.mrows = min(BM, cnt - t.m0);
-    t.n0 = (local / nmt) * BN;
+    t.n0 = nt * BN;
     return true;
 }
 

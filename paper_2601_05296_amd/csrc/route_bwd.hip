@@ -17,6 +17,7 @@
 // token-chunk partials, float32 FMA throughout.
 #include "common.hpp"
 #include "gemm.hpp"
+#include "gemm_rs.hpp"
 #include "launch.hpp"
 #include "loaders.hpp"
 #include "probe.hpp"
@@ -148,7 +149,7 @@ __global__ void rb_dwg_reduce(const float* __restrict__ part, int nsplit, int E,
     dwg[i] = acc;
 }
 
-using CR = GemmCfg<256, 256, 2, 4, 1>;
+using CR = rs::Cfg<256, 256, 2, 4, 1>;
 constexpr int RB_MCH = 512;  // tokens per split of the MFMA dW_g kernel
 
 inline int epad(int E) { return (E + 31) / 32 * 32; }
@@ -216,13 +217,13 @@ rb_dx_mfma(const bf16_t* __restrict__ hl, const bf16_t* __restrict__ wg, int64_t
     const int64_t m0 = (int64_t)blockIdx.x * C::BM;
     const int n0 = blockIdx.y * C::BN;
     const int rows = (int)min((int64_t)C::BM, T - m0);
-    DenseKC2<C, C::BM> la;
+    rs::DenseKC2<C, C::BM> la;
     la.init(hl, hl, 2 * Ep, m0, rows, 2 * Ep);
-    SplitRowsMC<C, C::BN> lb;
+    rs::SplitRowsMC<C, C::BN> lb;
     lb.init(wg, d, n0, d, Ep, E);
-    NoLoader nl;
-    Acc<C> acc;
-    gemm_mainloop<C>(la, lb, nl, 2 * Ep / GBK, GBK, lds, acc, rows, d - n0);
+    rs::NoLoader nl;
+    rs::Acc<C> acc;
+    rs::mainloop<C>(la, lb, nl, 2 * Ep / rs::KS, lds, acc);
     WaveCoord<C> wc;
     // The lane's dx values are all loaded before the first store: loads placed
     // after a store to the same rows would each wait for the previous one.
@@ -278,14 +279,13 @@ rb_dwg_mfma(const bf16_t* __restrict__ hl, const bf16_t* __restrict__ x, int64_t
     const int64_t t0 = (int64_t)split * RB_MCH;
     const int cnt = (int)min((int64_t)RB_MCH, T - t0);
     const int M = 2 * Ep;
-    SlotMC<C, C::BM> la;
+    rs::SlotMC<C, C::BM> la;
     la.init(hl, M, t0, m0, M, cnt);
-    SlotMC<C, C::BN> lb;
+    rs::SlotMC<C, C::BN> lb;
     lb.init(x, d, t0, n0, d, cnt);
-    NoLoader nl;
-    Acc<C> acc;
-    gemm_mainloop<C>(la, lb, nl, (cnt + GBK - 1) / GBK, tail_from(cnt), lds, acc, M - m0,
-                     d - n0);
+    rs::NoLoader nl;
+    rs::Acc<C> acc;
+    rs::mainloop<C>(la, lb, nl, rs::slices(cnt), lds, acc);
     WaveCoord<C> wc;
     float* out = part + (int64_t)split * M * d;
 #pragma unroll

@@ -704,13 +704,18 @@ def test_ffn_h_on_load_bit_identical(dtype, T, d, f, E, k, pattern, act):
         if gated:
             assert torch.equal(B0, B1)
         assert torch.equal(out0, out1), "combined" if combined else "O"
-        assert ws0 - ws1 == (S * f * 2 + 255) // 256 * 256
+        if combined:
+            # the h buffer is gone; the strip of the h-on-load GEMM is rounded
+            # to its 512-column tiles (at most one 256-column tile wider)
+            assert ws0 - ws1 >= (S * f * 2 + 255) // 256 * 256 - S * 256 * 2 - 256
+        else:
+            assert ws0 - ws1 == (S * f * 2 + 255) // 256 * 256
         dx0 = out0 if combined else None          # combined: accumulate onto y
         r0, wb0 = bwd(base, combined, A0, B0, dx0)
         r1, wb1 = bwd(base | B.MOE_H_ON_LOAD, combined, A1, B1, dx0)
         for n in ("dw1", "dw2", "d_gates", "dx", "dA") + (("dw3", "dB") if gated else ()):
             assert torch.equal(r0[n], r1[n]), (n, combined)
-        assert wb1 <= wb0 if combined else wb0 - wb1 >= S * f * 2 - (S + 64) * 4 - 256
+        assert wb1 <= wb0 if combined else wb0 - wb1 >= S * f * 2 - S * 4 - 256
 
 
 # whole layer (routing included) on the tiny float32 workload
