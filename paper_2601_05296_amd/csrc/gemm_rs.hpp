@@ -547,7 +547,9 @@ struct SplitRowsMC {
 // add nothing.
 
 // MC rows gathered through eti: K row kr -> base[eti[off + kr]] (x or dY). The
-// row index of a chunk is loaded one slice ahead of the row itself.
+// row index of a chunk is loaded one slice ahead of the row itself. When a
+// whole wave covers one K row (R a multiple of 512 columns), the index is the
+// same for the wave and comes in by a scalar load into scalar registers.
 template <class C, int R>
 struct GatherMC {
     static constexpr bool MC = true;
@@ -555,15 +557,27 @@ struct GatherMC {
     static constexpr int NCH = G::NCH;
     static constexpr int NSUB = 0;
     template <int i, int p> __device__ void sub() {}
+    static constexpr bool UNIFORM = G::CPR % WAVE == 0;
     const bf16_t* base;
     const int32_t* idx;   // eti + off
     int ld, cnt;
     int nidx[NCH];        // row of the chunk's next slice
     uint32_t zmask;       // chunks of the loaded slice that lie past cnt
     u32x4 v[NCH];
+    __device__ static int krow(int i) {
+        if constexpr (UNIFORM)   // wave w covers k rows i * (THREADS / CPR) + w * WAVE / CPR
+            return i * (C::THREADS / G::CPR) +
+                   __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6) * (WAVE / G::CPR);
+        else return G::krow(i);
+    }
     __device__ int kr(int i, int kt) const {
-        const int k = kt * KS + G::krow(i);
+        const int k = kt * KS + krow(i);
         return k < cnt ? k : cnt - 1;
+    }
+    __device__ int row_index(int k) const {
+        if constexpr (UNIFORM)   // constant address space: a uniform address is a scalar load
+            return ((const __attribute__((address_space(4))) int32_t*)idx)[k];
+        else return idx[k];
     }
     // cnt_ >= 1
     __device__ void init(const bf16_t* b, int ld_, int col0, int ncols, const int32_t* ix,
@@ -576,13 +590,13 @@ struct GatherMC {
         c = c < ncols ? c : ncols - 8;
         base = b + c;
 #pragma unroll
-        for (int i = 0; i < NCH; ++i) nidx[i] = idx[kr(i, 0)];
+        for (int i = 0; i < NCH; ++i) nidx[i] = row_index(kr(i, 0));
     }
     template <int i> __device__ void load(int kt) {
-        const bool past = kt * KS + G::krow(i) >= cnt;
+        const bool past = kt * KS + krow(i) >= cnt;
         zmask = past ? (zmask | (1u << i)) : (zmask & ~(1u << i));
         v[i] = ldg16(base + roff(nidx[i], ld));
-        nidx[i] = idx[kr(i, kt + 1)];
+        nidx[i] = row_index(kr(i, kt + 1));
     }
     template <int i> __device__ void store(char* tile) {
         const u32x4 z = {0u, 0u, 0u, 0u};
