@@ -11,7 +11,12 @@ dominant kernel, saved and peak activation bytes per token next to a
 materialised-permutation PyTorch baseline, and the CPU oracle timed on a
 bounded token sample of the same workload.
 
-python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload mid_e64k6]
+python bench.py [--gpus 1] [--steps 20] [--warmup 3] [--workload few_large_e8k2]
+
+The default workload is the largest of the layer workloads that fits one GPU
+(T=32768, d=4096, f=14336, E=8, k=2), with the h-on-load policy (no SwiGLU
+intermediate in HBM); --h-buffered times the policy that passes h and g*h
+between the GEMMs through transient buffers.
 """
 from __future__ import annotations
 
@@ -35,12 +40,16 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="mid_e64k6")
+    ap.add_argument("--workload", default=None,
+                    help="layer workload (default: few_large_e8k2; mem_sweep_e64k8 for --sweep)")
     ap.add_argument("--act", choices=("swiglu", "silu", "relu"), default=None,
                     help="expert activation (default: the workload's own)")
-    ap.add_argument("--h-on-load", action="store_true",
-                    help="MOE_H_ON_LOAD: no h buffer between the GEMMs; the second GEMM forms h "
-                         "from A and B as it loads them")
+    ap.add_argument("--h-buffered", dest="h_on_load", action="store_false",
+                    help="buffer h (forward) and g*h (backward) between the GEMMs instead of "
+                         "forming them on load (MOE_H_ON_LOAD, the default)")
+    ap.add_argument("--h-on-load", dest="h_on_load", action="store_true",
+                    help="form h and g*h on load, no SwiGLU intermediate in HBM (the default)")
+    ap.set_defaults(h_on_load=True)
     ap.add_argument("--recompute", action="store_true",
                     help="full-recompute checkpoint policy: save only the routing decision and "
                          "maps, recompute the first layer in the backward")
@@ -77,7 +86,10 @@ def parse():
     ap.add_argument("--table1", action="store_true",
                     help="the seven shapes of the paper's Table 1 (SiLU and SwiGLU experts): "
                          "this path against a materialised PyTorch layer, time and memory")
-    return ap.parse_args()
+    args = ap.parse_args()
+    if args.workload is None:
+        args.workload = "mem_sweep_e64k8" if args.sweep else "few_large_e8k2"
+    return args
 
 
 CSRC = os.path.join(ROOT, "paper_2601_05296_amd", "csrc")
@@ -644,8 +656,7 @@ def main():
         return
     if args.sweep:
         from paper_2601_05296_amd import synth
-        res = memory_sweep(synth.CONFIGS[args.workload if args.workload != "mid_e64k6" else
-                                         "mem_sweep_e64k8"], args.sweep_max_doublings,
+        res = memory_sweep(synth.CONFIGS[args.workload], args.sweep_max_doublings,
                            h_on_load=args.h_on_load)
         print(json.dumps({"sweep": res}), flush=True)
         return
@@ -798,18 +809,20 @@ def main():
         "sparse_to_sparse_tokens_per_s": round(T / ((ms_step - router_ms) * 1e-3), 1),
         "kernels": kernels,
     }
-    if not (args.h_on_load or args.recompute or args.no_baseline_memory):
-        # the other operating point of the same layer: MOE_H_ON_LOAD buffers
-        # neither h nor g*h (bit-identical results, less memory, more time)
+    if not (args.recompute or args.no_baseline_memory):
+        # the other operating point of the same layer: the other h policy
+        # (bit-identical results; buffering h and g*h costs memory, forming
+        # them on load costs vector work)
+        other = not args.h_on_load
         def lean_step():
             y_, s_ = layer.forward(x, wg, bias, w1, w3, w2, k, cfg.renorm, act=cfg.act,
-                                   h_on_load=True)
+                                   h_on_load=other)
             return y_, s_, layer.backward(s_, dy, x, wg, w1, w3, w2)
         lean_step()
         torch.cuda.synchronize()
         torch.cuda.reset_peak_memory_stats(dev)
         b0 = torch.cuda.memory_allocated(dev)
-        y_, s_ = layer.forward(x, wg, bias, w1, w3, w2, k, cfg.renorm, act=cfg.act, h_on_load=True)
+        y_, s_ = layer.forward(x, wg, bias, w1, w3, w2, k, cfg.renorm, act=cfg.act, h_on_load=other)
         torch.cuda.synchronize()
         lf = torch.cuda.max_memory_allocated(dev) - b0
         torch.cuda.reset_peak_memory_stats(dev)
@@ -823,8 +836,9 @@ def main():
             lean_step()
         torch.cuda.synchronize()
         t3 = time.perf_counter()
-        out["h_on_load_policy"] = {
-            "checkpoint": "A,B; h and g*h formed on load (MOE_H_ON_LOAD)",
+        out["h_buffered_policy" if other is False else "h_on_load_policy"] = {
+            "checkpoint": ("A,B; h and g*h formed on load (MOE_H_ON_LOAD)" if other else
+                           "A,B; h and g*h passed through transient buffers"),
             "steps": n_lean, "ms_per_step": round((t3 - t2) * 1e3 / n_lean, 4),
             "tokens_per_s": round(T * n_lean / (t3 - t2), 1),
             "peak_activation_bytes_per_token": round(max(lf, lb) / T, 1),

@@ -13,9 +13,12 @@ Backward (Section 3.2):
 ``recompute=True`` is the full-recompute checkpoint policy: the forward keeps
 only the routing decision and the maps, and the backward first recomputes A
 and B with moe_ffn_recompute (bit-identical to the forward's).
-``h_on_load=True`` (MOE_H_ON_LOAD) buffers neither h in the forward nor g*h in
-the backward: the second GEMM and the dW2 GEMM form them again from A and B as
-they load them (bit-identical results, less memory, more operand traffic).
+``h_on_load=True`` (MOE_H_ON_LOAD, the default) buffers neither h in the
+forward nor g*h in the backward: the second GEMM and the dW2 GEMM form them
+again from A and B as they load them, so no SwiGLU intermediate is ever
+written to HBM. ``h_on_load=False`` is the buffered policy: h passes from the
+first GEMM to the second through a transient buffer, and g*h from the dh GEMM
+to the dW2 GEMM (bit-identical results, more memory, less vector work).
 
 What the forward keeps for the backward (the "saved activations"): the first
 layer outputs A and B [S, f] (A alone for the non-gated SiLU / ReLU experts),
@@ -55,7 +58,7 @@ class Saved:
     slot_src: torch.Tensor
     A: torch.Tensor | None      # None under the full-recompute policy
     B: torch.Tensor | None
-    h_on_load: bool = False
+    h_on_load: bool = True
 
     @property
     def ffn_flags(self) -> int:
@@ -93,7 +96,7 @@ def _on(stream):
 
 def forward(x, w_gate, bias, w1, w3, w2, k: int, renorm: bool, stream=None, keep_O=False,
             act: str = "swiglu", separate: bool = False, recompute: bool = False,
-            h_on_load: bool = False):
+            h_on_load: bool = True):
     """Returns (y, saved[, O]). ``act`` picks the expert: "swiglu" (gated, w3
     used) or the non-gated "silu" / "relu" (w3 ignored, may be None).
     ``keep_O`` (returns the expert outputs) implies ``separate``. Everything

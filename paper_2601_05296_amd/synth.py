@@ -186,6 +186,33 @@ def make_inputs(cfg: MoEConfig, T: int | None = None, with_dy: bool = True) -> L
     return out
 
 
+def device_inputs(cfg: MoEConfig, device, T: int | None = None, with_dy: bool = True) -> dict:
+    """Draw one layer's inputs directly on the GPU (for token counts whose host
+    copies would be too large to draw and upload): a torch generator seeded
+    with ``cfg.seed`` draws, in this fixed order, w_gate, w1, w3 (gated
+    experts only), w2, x and dy with the distributions of the module
+    docstring, each rounded to bfloat16 (round to nearest even). The values
+    differ from ``make_inputs``'s (another generator); the recipe is the same.
+    The Zipf bias of the skewed workload is not drawn here (None)."""
+    import torch
+    assert cfg.dtype == "bf16" and cfg.zipf_s == 0.0 and cfg.n_dead == 0
+    T = cfg.T if T is None else T
+    gen = torch.Generator(device=device)
+    gen.manual_seed(cfg.seed)
+    d, f, E = cfg.d, cfg.f, cfg.E
+
+    def normal(shape, std):
+        return (torch.randn(shape, generator=gen, device=device) * std).to(torch.bfloat16)
+
+    out = {"w_gate": normal((E, d), 0.02), "w1": normal((E, d, f), d ** -0.5)}
+    out["w3"] = normal((E, d, f), d ** -0.5) if cfg.act == "swiglu" else None
+    out["w2"] = normal((E, f, d), f ** -0.5)
+    out["x"] = normal((T, d), 1.0)
+    out["dy"] = normal((T, d), 1.0) if with_dy else None
+    out["bias"] = None
+    return out
+
+
 def random_ids(T: int, E: int, k: int, seed: int = 0, popularity=None) -> np.ndarray:
     """Random top-k expert choices [T, k] int32 with distinct ids per row.
     ``popularity`` (length E, nonnegative) skews the draw (Plackett-Luce)."""

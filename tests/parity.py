@@ -20,9 +20,30 @@ def rel_err(gpu, ref) -> float:
     return float(num / den)
 
 
-def assert_close(name, gpu, ref, dtype):
+# Error statistics of the full-size cases, printed at the end of the session
+# (conftest.pytest_terminal_summary): (case, tensor, max-normalised error,
+# 99.9th percentile and maximum of the element-wise relative error).
+STATS = []
+
+
+def elem_rel(gpu, ref):
+    """Element-wise |gpu - ref| / |ref|, with |ref| floored at 1e-3 max|ref|
+    (elements near zero would otherwise dominate with a meaningless ratio)."""
+    gpu = np.asarray(gpu, dtype=np.float64).ravel()
+    ref = np.asarray(ref, dtype=np.float64).ravel()
+    if ref.size == 0:
+        return np.zeros(0)
+    floor = 1e-3 * max(np.max(np.abs(ref)), 1e-300)
+    return np.abs(gpu - ref) / np.maximum(np.abs(ref), floor)
+
+
+def assert_close(name, gpu, ref, dtype, case=None):
     e = rel_err(gpu, ref)
     assert np.all(np.isfinite(np.asarray(gpu, dtype=np.float64))), "%s has non-finite values" % name
+    if case is not None:
+        r = elem_rel(gpu, ref)
+        STATS.append((case, name, e, float(np.quantile(r, 0.999)) if r.size else 0.0,
+                      float(r.max()) if r.size else 0.0))
     assert e <= TOL[dtype], "%s: max rel err %.3e > %.1e" % (name, e, TOL[dtype])
     return e
 

@@ -5,11 +5,13 @@ The oracle cannot run a whole layer of these sizes, so the checks are:
   * routing for every token (oracle route is cheap): ids equal up to
     near-ties, logits and gates within tolerance;
   * the index build, fed the oracle's ids, bit-exact for every token;
-  * y, dx, d_gates, A, B, dA, dB at sampled tokens, from an oracle run on
-    just those tokens (each of these depends on its own token only);
-  * dw1, dw3, dw2 at sampled hidden columns of one expert, from an oracle run
-    on a sub-problem holding that expert's tokens and those columns of its
-    weights (SwiGLU columns are independent);
+  * y, dx, d_gates, A, B, dA, dB at sampled tokens (half of them those with
+    the highest slots), from an oracle run on just those tokens (each of these
+    depends on its own token only);
+  * dw1, dw3, dw2 at sampled hidden columns (some in the last f-tile) of the
+    most- and the least-loaded expert, from an oracle run on a sub-problem
+    holding that expert's tokens and those columns of its weights (SwiGLU
+    columns are independent);
   * the router backward at full size on the oracle's logits and seeded gate
     gradients, against the oracle's router backward for every token.
 No oracle input is taken from the device.
@@ -27,7 +29,7 @@ pytestmark = pytest.mark.gpu
 
 CASES = ["mid_e64k6", "few_large_e8k2", "many_small_zipf", "mem_sweep_e64k8", "zipf_empty",
          "table1_conf4", "table1_conf1_relu", "d2880_e128k4"]
-NTOK = 12      # sampled tokens
+NTOK = 24      # sampled tokens (half of them holding the highest slots)
 NCOL = 8       # sampled hidden columns
 
 
@@ -71,8 +73,8 @@ def test_full_size_layer(name):
     assert nflip <= max(2, T // 5000), nflip
     same_tok = np.all(ids_g == ids_r, axis=1)
     fin = np.isfinite(logits_r)
-    assert_close("logits", host(saved.logits)[fin], logits_r[fin], "f32")
-    assert_close("gates", host(saved.gates)[same_tok], gates_r[same_tok], "bf16")
+    assert_close("logits", host(saved.logits)[fin], logits_r[fin], "f32", case=name)
+    assert_close("gates", host(saved.gates)[same_tok], gates_r[same_tok], "bf16", case=name)
     if cfg.n_dead:
         dead = np.nonzero(~np.isfinite(v["bias"]))[0]
         assert np.all(saved.counts.cpu().numpy()[dead] == 0)
@@ -93,62 +95,72 @@ def test_full_size_layer(name):
     # ---- sampled tokens: forward and backward rows -------------------------------
     rng = np.random.default_rng(1234)
     cand = np.nonzero(same_tok)[0]
-    toks = np.sort(rng.choice(cand, size=min(NTOK, cand.size), replace=False))
+    tim_all = saved.tim.cpu().numpy()
+    # random tokens, and the tokens holding the highest slots (the tail of the
+    # last experts' segments, where slot-row offsets are largest)
+    top = cand[np.argsort(-tim_all[cand].max(axis=1), kind="stable")[:NTOK // 2]]
+    rest = np.setdiff1d(cand, top)
+    toks = np.sort(np.concatenate([top, rng.choice(rest, size=min(NTOK - top.size, rest.size),
+                                                   replace=False)]))
     sub = lambda a: None if a is None else a[toks]
     fw = oracle.layer_forward(v["x"][toks], v["w_gate"], v["bias"], v["w1"], v["w3"], v["w2"], k,
                               cfg.renorm, act=cfg.act)
     assert np.array_equal(fw["ids"], ids_g[toks])
     bw = oracle.layer_backward(fw, v["dy"][toks], v["x"][toks], v["w_gate"], v["w1"], v["w3"],
                                v["w2"], cfg.renorm)
-    assert_close("y", host(y)[toks], fw["y"], "bf16")
-    assert_close("dx", host(g["dx"])[toks], bw["dx"], "bf16")
-    assert_close("d_gates", host(g["d_gates"])[toks], bw["d_gates"], "bf16")
+    assert_close("y", host(y)[toks], fw["y"], "bf16", case=name)
+    assert_close("dx", host(g["dx"])[toks], bw["dx"], "bf16", case=name)
+    assert_close("d_gates", host(g["d_gates"])[toks], bw["d_gates"], "bf16", case=name)
     tim_g = saved.tim.cpu().numpy()
     slots_g = tim_g[toks].reshape(-1)                 # device slots, (t, j) order
     slots_r = fw["ix"].tim.reshape(-1)                # oracle sub-run slots, same order
     sl = torch.from_numpy(slots_g).long().cuda()
     A_r = fw["A"][slots_r]
-    assert_close("A", host(A_fwd[sl]), A_r, "bf16")
+    assert_close("A", host(A_fwd[sl]), A_r, "bf16", case=name)
     dA_g, dA_r = host(saved.A[sl]), bw["dA"][slots_r]
     if cfg.act == "relu":   # sign decisions within the accumulation error of 0 may differ
         tie = np.abs(A_r) < 1e-4 * np.abs(A_r).max()
         dA_g, dA_r = np.where(tie, 0, dA_g), np.where(tie, 0, dA_r)
-    assert_close("dA", dA_g, dA_r, "bf16")
+    assert_close("dA", dA_g, dA_r, "bf16", case=name)
     if gated:
-        assert_close("B", host(B_fwd[sl]), fw["B"][slots_r], "bf16")
-        assert_close("dB", host(saved.B[sl]), bw["dB"][slots_r], "bf16")
+        assert_close("B", host(B_fwd[sl]), fw["B"][slots_r], "bf16", case=name)
+        assert_close("dB", host(saved.B[sl]), bw["dB"][slots_r], "bf16", case=name)
     del A_fwd, B_fwd
 
-    # ---- weight gradients: sampled columns of one expert ------------------------------
+    # ---- weight gradients: sampled columns of the most- and the least-loaded
+    # expert (whose token sets agree), including columns of the last f-tile ----
     counts_r = ix_r.counts
     off_g = saved.offsets.cpu().numpy()
     eti_g = saved.eti.cpu().numpy()
-    e = None
-    for cand_e in np.argsort(-counts_r):   # most loaded expert whose token set agrees
-        seg_r = ix_r.eti[ix_r.offsets[cand_e]:ix_r.offsets[cand_e + 1]]
-        seg_g = eti_g[off_g[cand_e]:off_g[cand_e + 1]]
-        if counts_r[cand_e] > 0 and np.array_equal(seg_r, seg_g):
-            e = int(cand_e)
-            break
-    assert e is not None
-    cols = np.sort(rng.choice(f, size=NCOL, replace=False))
-    seg = ix_r.eti[ix_r.offsets[e]:ix_r.offsets[e + 1]]
-    jsel = np.argmax(ids_r[seg] == e, axis=1)
-    g_e = gates_r[seg, jsel][:, None]
-    sub_ix = oracle.build_index(np.zeros((seg.size, 1), np.int32), 1)
-    xw = v["x"][seg]
-    W1s = v["w1"][e][:, cols][None]
-    W2s = v["w2"][e][cols, :][None]
-    if gated:
-        W3s = v["w3"][e][:, cols][None]
-        As, Bs, _ = oracle.ffn_fwd(xw, W1s, W3s, W2s, sub_ix, 1)
-        sbw = oracle.ffn_bwd(v["dy"][seg], xw, W1s, W3s, W2s, g_e, sub_ix, As, Bs)
-        assert_close("dw3[e][:,cols]", host(g["dw3"][e])[:, cols], sbw["dw3"][0], "bf16")
-    else:
-        As, _ = oracle.ffn_fwd_act(xw, W1s, W2s, sub_ix, 1, cfg.act)
-        sbw = oracle.ffn_bwd_act(v["dy"][seg], xw, W1s, W2s, g_e, sub_ix, As, cfg.act)
-    assert_close("dw1[e][:,cols]", host(g["dw1"][e])[:, cols], sbw["dw1"][0], "bf16")
-    assert_close("dw2[e][cols,:]", host(g["dw2"][e])[cols, :], sbw["dw2"][0], "bf16")
+
+    def agrees(e):
+        seg_r = ix_r.eti[ix_r.offsets[e]:ix_r.offsets[e + 1]]
+        seg_g = eti_g[off_g[e]:off_g[e + 1]]
+        return counts_r[e] > 0 and np.array_equal(seg_r, seg_g)
+
+    order = np.argsort(-counts_r, kind="stable")
+    heavy = next(int(e) for e in order if agrees(e))
+    light = next(int(e) for e in order[::-1] if agrees(e))
+    cols = np.unique(np.concatenate([rng.choice(f, size=NCOL // 2, replace=False),
+                                     f - 1 - rng.choice(min(f, 256), size=NCOL // 2, replace=False)]))
+    for e, tag in ((heavy, "most-loaded"), (light, "least-loaded")):
+        seg = ix_r.eti[ix_r.offsets[e]:ix_r.offsets[e + 1]]
+        jsel = np.argmax(ids_r[seg] == e, axis=1)
+        g_e = gates_r[seg, jsel][:, None]
+        sub_ix = oracle.build_index(np.zeros((seg.size, 1), np.int32), 1)
+        xw = v["x"][seg]
+        W1s = v["w1"][e][:, cols][None]
+        W2s = v["w2"][e][cols, :][None]
+        if gated:
+            W3s = v["w3"][e][:, cols][None]
+            As, Bs, _ = oracle.ffn_fwd(xw, W1s, W3s, W2s, sub_ix, 1)
+            sbw = oracle.ffn_bwd(v["dy"][seg], xw, W1s, W3s, W2s, g_e, sub_ix, As, Bs)
+            assert_close("dw3 %s" % tag, host(g["dw3"][e])[:, cols], sbw["dw3"][0], "bf16", case=name)
+        else:
+            As, _ = oracle.ffn_fwd_act(xw, W1s, W2s, sub_ix, 1, cfg.act)
+            sbw = oracle.ffn_bwd_act(v["dy"][seg], xw, W1s, W2s, g_e, sub_ix, As, cfg.act)
+        assert_close("dw1 %s" % tag, host(g["dw1"][e])[:, cols], sbw["dw1"][0], "bf16", case=name)
+        assert_close("dw2 %s" % tag, host(g["dw2"][e])[cols, :], sbw["dw2"][0], "bf16", case=name)
     if cfg.n_dead:
         dead = np.nonzero(~np.isfinite(v["bias"]))[0]
         assert np.all(host(g["dw1"][dead[0]]) == 0) and np.all(host(g["dw2"][dead[0]]) == 0)
@@ -167,8 +179,8 @@ def test_full_size_layer(name):
     B.moe_route_bwd(dev(dgates.astype(np.float32)), dev(lg), dev(ids_r),
                     dev(gates_r.astype(np.float32)), x, wg, T, d, E, k, flags, dwg, dxr, ws, wsb)
     torch.cuda.synchronize()
-    assert_close("dw_gate", host(dwg), dwg_r, "bf16")
-    assert_close("dx_router", host(dxr), dxr_r, "bf16")
+    assert_close("dw_gate", host(dwg), dwg_r, "bf16", case=name)
+    assert_close("dx_router", host(dxr), dxr_r, "bf16", case=name)
 
 
 @pytest.mark.parametrize("name", ["mid_e64k6", "table1_conf1_relu", "d2880_e128k4", "few_large_e8k2"])
