@@ -133,6 +133,23 @@ int moe_build_index(const int32_t* topk_ids, int64_t T, int E, int k,
                     void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * moe_build_index_noalloc -- moe_build_index for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation): the same kernels and outputs, with the per-tile
+ * counts in a static 1 MiB device array of the library instead of a caller
+ * workspace. No memory is allocated or freed. Arguments, outputs and errors
+ * as moe_build_index, plus MOE_ERR_UNSUPPORTED if the counts would not fit
+ * the array (never within the limits above: E <= 256 and at most 1024 tiles)
+ * and MOE_ERR_HIP if the array's device address cannot be found. Every call
+ * on one GPU uses that GPU's single array: calls that overlap on one GPU (on
+ * different streams, or from different host threads) race and must not be
+ * made.
+ */
+int moe_build_index_noalloc(const int32_t* topk_ids, int64_t T, int E, int k,
+                            int32_t* counts, int32_t* offsets, int32_t* expert_token_indices,
+                            int32_t* token_index_map, int32_t* slot_src, hipStream_t stream);
+
+/*
  * moe_ffn_fwd -- expert forward without a routed-token buffer (Section 3.1,
  * Algorithm 1 forward). For each slot s of expert e with token
  * t = expert_token_indices[s] (x rows are gathered while loading):

@@ -32,7 +32,7 @@ ACT_FLAG = {"swiglu": 0, "silu": MOE_ACT_SILU, "relu": MOE_ACT_RELU}
 
 # Every symbol declared in include/moeblaze.h.
 EXPORTS = ("moe_strerror", "moe_last_error", "moe_route", "moe_build_index_workspace_size",
-           "moe_build_index", "moe_ffn_fwd_workspace_size", "moe_ffn_fwd", "moe_combine", "moe_ffn_bwd_workspace_size",
+           "moe_build_index", "moe_build_index_noalloc", "moe_ffn_fwd_workspace_size", "moe_ffn_fwd", "moe_combine", "moe_ffn_bwd_workspace_size",
            "moe_ffn_bwd", "moe_ffn_recompute", "moe_ffn_fwd_combine_workspace_size",
            "moe_ffn_fwd_combine",
            "moe_ffn_bwd_combine_workspace_size", "moe_ffn_bwd_combine",
@@ -70,6 +70,7 @@ def load_library(path: str = LIB):
         "moe_route": (I, [P, P, P, I64, I, I, I, U, P, P, P, P]),
         "moe_build_index_workspace_size": (SZ, [I64, I, I]),
         "moe_build_index": (I, [P, I64, I, I, P, P, P, P, P, P, SZ, P]),
+        "moe_build_index_noalloc": (I, [P, I64, I, I, P, P, P, P, P, P]),
         "moe_ffn_fwd_workspace_size": (SZ, [I64, I, I, I, I, U]),
         "moe_ffn_fwd": (I, [P, P, P, P, P, P, I64, I, I, I, I, U, P, P, P, P, SZ, P]),
         "moe_combine": (I, [P, P, P, I64, I, I, U, P, P]),
@@ -214,6 +215,21 @@ def moe_build_index(topk_ids, T, E, k, counts, offsets, expert_token_indices, to
                                           _ptr(expert_token_indices), _ptr(token_index_map),
                                           _ptr(slot_src), _ptr(workspace), workspace_bytes,
                                           _stream(stream)))
+
+
+def moe_build_index_noalloc(topk_ids, T, E, k, counts, offsets, expert_token_indices,
+                            token_index_map, slot_src, stream=None):
+    i32 = torch.int32
+    _need(topk_ids, T * k, "topk_ids", i32)
+    _need(counts, E, "counts", i32)
+    _need(offsets, E + 1, "offsets", i32)
+    _need(expert_token_indices, T * k, "expert_token_indices", i32)
+    _need(token_index_map, T * k, "token_index_map", i32)
+    _need(slot_src, T * k, "slot_src", i32)
+    _check(load_library().moe_build_index_noalloc(_ptr(topk_ids), T, E, k, _ptr(counts),
+                                                  _ptr(offsets), _ptr(expert_token_indices),
+                                                  _ptr(token_index_map), _ptr(slot_src),
+                                                  _stream(stream)))
 
 
 def moe_ffn_fwd_workspace_size(T, d, f, E, k, flags) -> int:

@@ -244,6 +244,27 @@ int moe_build_index(const int32_t* topk_ids, int64_t T, int E, int k, int32_t* c
                                            token_index_map, slot_src, workspace, stream));
 }
 
+int moe_build_index_noalloc(const int32_t* topk_ids, int64_t T, int E, int k, int32_t* counts,
+                            int32_t* offsets, int32_t* expert_token_indices,
+                            int32_t* token_index_map, int32_t* slot_src, hipStream_t stream) {
+    const char* fn = "moe_build_index_noalloc";
+    int r;
+    if ((r = check_common(fn, T, E, k, 0))) return r;
+    if (T == 0) return MOE_OK;
+    REQUIRE_PTR(topk_ids); REQUIRE_PTR(counts); REQUIRE_PTR(offsets);
+    REQUIRE_PTR(expert_token_indices); REQUIRE_PTR(token_index_map); REQUIRE_PTR(slot_src);
+    void* ws = nullptr;
+    size_t have = 0;
+    if (hipError_t e = moe::noalloc_scratch(&ws, &have); e != hipSuccess)
+        return fail(MOE_ERR_HIP, "%s: scratch address lookup failed: %s", fn, hipGetErrorString(e));
+    const size_t need = moe::build_index_workspace(T, E, k);
+    if (need > have)
+        return fail(MOE_ERR_UNSUPPORTED, "%s: needs %zu bytes of scratch, the static scratch holds %zu",
+                    fn, need, have);
+    moe::probe::begin(stream);
+    return hip_status(fn, moe::build_index(topk_ids, T, E, k, counts, offsets, expert_token_indices,
+                                           token_index_map, slot_src, ws, stream));
+}
 
 size_t moe_ffn_fwd_workspace_size(int64_t T, int d, int f, int E, int k, unsigned flags) {
     if (T <= 0 || d < 1 || f < 1 || E < 1 || k < 1) return 0;

@@ -26,9 +26,18 @@
 // (top-k never produces either) is rejected by both passes alike: it gets no
 // slot and its token_index_map entry is -1. Every slot below offsets[E] is
 // then written exactly once, whatever the ids hold.
+#include <mutex>
+
 #include "common.hpp"
 #include "launch.hpp"
 #include "probe.hpp"
+
+// Scratch of the no-allocation index build (moe_build_index_noalloc): the
+// per-tile expert counts of at most 256 experts x 1024 tiles. The workspace of
+// moe_build_index never needs more for any T (the tile count is capped at
+// 1024). Each GPU holds its own copy, at its own address, for the life of the
+// process; calls that overlap on one GPU share it and race.
+static __device__ __align__(256) int32_t scratch[256 * 1024];
 
 namespace moe {
 namespace {
@@ -175,6 +184,31 @@ tile_rank(const int32_t* __restrict__ ids, int64_t T, int E, int k, int64_t tb, 
 }
 
 }  // namespace
+
+// Device address of `scratch` on the current device, looked up once per
+// device (with that device current) and kept. In host code the array's name
+// is only a stand-in for the symbol: kernels must be given this address.
+namespace {
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[MAX_DEVICES];
+}  // namespace
+
+hipError_t noalloc_scratch(void** ptr, size_t* bytes) {
+    int dev = -1;
+    if (hipError_t e = hipGetDevice(&dev); e != hipSuccess) return e;
+    if (dev < 0 || dev >= MAX_DEVICES) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        if (hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)); e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
+    *bytes = sizeof(scratch);
+    return hipSuccess;
+}
 
 size_t build_index_workspace(int64_t T, int E, int k) {
     (void)k;

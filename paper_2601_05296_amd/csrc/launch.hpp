@@ -13,6 +13,9 @@ size_t build_index_workspace(int64_t T, int E, int k);
 hipError_t build_index(const int32_t* ids, int64_t T, int E, int k, int32_t* counts,
                        int32_t* offsets, int32_t* eti, int32_t* tim, int32_t* slot_src,
                        void* ws, hipStream_t st);
+// device address and size of the static scratch of the no-allocation index
+// build on the current device (looked up once per device)
+hipError_t noalloc_scratch(void** ptr, size_t* bytes);
 
 // ---- routing ----
 hipError_t route(const void* x, const void* wg, const float* bias, int64_t T, int d, int E,
