@@ -51,8 +51,9 @@ def parse():
                     help="form h and g*h on load, no SwiGLU intermediate in HBM (the default)")
     ap.set_defaults(h_on_load=True)
     ap.add_argument("--recompute", action="store_true",
-                    help="full-recompute checkpoint policy: save only the routing decision and "
-                         "maps, recompute the first layer in the backward")
+                    help="full-recompute checkpoint policy: save only the routing decision; the "
+                         "dispatch and the expert FFN run over token chunks, and the backward "
+                         "rebuilds each chunk's maps and first layer")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -82,7 +83,7 @@ def parse():
     ap.add_argument("--sweep", action="store_true",
                     help="memory-capacity sweep: double T from the workload's T until out of "
                          "memory, for this path and for the materialised-permutation baseline")
-    ap.add_argument("--sweep-max-doublings", type=int, default=8)
+    ap.add_argument("--sweep-max-doublings", type=int, default=9)
     ap.add_argument("--table1", action="store_true",
                     help="the seven shapes of the paper's Table 1 (SiLU and SwiGLU experts): "
                          "this path against a materialised PyTorch layer, time and memory")
@@ -207,9 +208,12 @@ def summarize_sweep(json_path, out, cmd, profile_cmd):
     from paper_2601_05296_amd import synth
     res = json.loads(open(json_path).read().strip().splitlines()[-1])["sweep"]
     c = synth.CONFIGS[res["workload"]]
-    lines = ["# Memory-capacity sweep, workload %s (d=%d f=%d E=%d k=%d, %s), one MI355X%s"
-             % (c.name, c.d, c.f, c.E, c.k, c.dtype,
-                ", this path with MOE_H_ON_LOAD (no h / g*h buffers)" if res.get("h_on_load") else ""),
+    policy = ("full recompute over token chunks (only the routing decision saved)"
+              if res.get("recompute") else
+              "h and g*h formed on load (MOE_H_ON_LOAD)" if res.get("h_on_load") else
+              "h and g*h buffered between the GEMMs")
+    lines = ["# Memory-capacity sweep, workload %s (d=%d f=%d E=%d k=%d, %s), one MI355X; "
+             "this path: %s" % (c.name, c.d, c.f, c.E, c.k, c.dtype, policy),
              "# run: %s" % profile_cmd,
              "# summary: python %s" % cmd,
              "# ours: one forward + backward through the C ABI (moe_ffn_fwd_combine / "
@@ -321,11 +325,12 @@ def kernel_model(name, cfg, elem, recompute=False):
     if name in flops:
         return flops[name], "TFLOP/s", "mfma"
     nparts = -(-f // 256) * 4   # gate-gradient partials per slot (G4: 256-column tiles, 4 waves across)
+    nbuild = 2 if recompute else 1   # full recompute builds the maps again in the backward
     byts = {
         "route_bf16": T * d * elem + E * d * elem + T * E * 4 + T * k * 8,
-        "tile_hist": S * 4,
+        "tile_hist": nbuild * S * 4,
         "tile_scan": 0,
-        "tile_rank": S * 4 + 3 * S * 4,
+        "tile_rank": nbuild * (S * 4 + 3 * S * 4),
         "combine": 2 * (S * d * elem + T * d * elem + T * k * 8),   # forward and backward
         "dgate_reduce": S * nparts * 4 + S * 8,
         "slot_gates": S * 12,
@@ -519,7 +524,7 @@ def table1_sweep(args):
     return rows
 
 
-def memory_sweep(cfg, max_doublings, h_on_load=False):
+def memory_sweep(cfg, max_doublings, h_on_load=False, recompute=False):
     """Peak activation bytes per token and the largest T that fits, for this
     path (one forward + backward) and for the materialised-permutation
     baseline (forward only: its saved tensors plus forward temporaries, a
@@ -555,7 +560,7 @@ def memory_sweep(cfg, max_doublings, h_on_load=False):
                 base = torch.cuda.memory_allocated(dev)
                 if which == "ours":
                     y, saved = layer.forward(x, wg, None, w1, w3, w2, k, cfg.renorm, act=cfg.act,
-                                             h_on_load=h_on_load)
+                                             h_on_load=h_on_load, recompute=recompute)
                     sb = saved.nbytes()
                     torch.cuda.synchronize()
                     fwd_peak = torch.cuda.max_memory_allocated(dev) - base
@@ -585,7 +590,8 @@ def memory_sweep(cfg, max_doublings, h_on_load=False):
         if not ours_ok and not base_ok:
             break
     fits = lambda key: max([r["T"] for r in rows if key in r], default=0)
-    return {"workload": cfg.name, "h_on_load": bool(h_on_load), "points": rows,
+    return {"workload": cfg.name, "h_on_load": bool(h_on_load), "recompute": bool(recompute),
+            "points": rows,
             "max_T_ours": fits("ours_peak_bytes_per_token"),
             "max_T_baseline_fwd": fits("baseline_fwd_peak_bytes_per_token"),
             "hbm_bytes": torch.cuda.get_device_properties(dev).total_memory}
@@ -657,7 +663,7 @@ def main():
     if args.sweep:
         from paper_2601_05296_amd import synth
         res = memory_sweep(synth.CONFIGS[args.workload], args.sweep_max_doublings,
-                           h_on_load=args.h_on_load)
+                           h_on_load=args.h_on_load, recompute=args.recompute)
         print(json.dumps({"sweep": res}), flush=True)
         return
     if args.gpus != 1:

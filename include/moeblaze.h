@@ -76,6 +76,11 @@ extern "C" {
  * those two GEMMs reading A and B instead of one buffer. moe_ffn_recompute accepts and ignores
  * it; route, build, combine and route_bwd reject it (MOE_ERR_INVALID_ARG). */
 #define MOE_H_ON_LOAD   32u
+/* moe_ffn_bwd / moe_ffn_bwd_combine: add the weight gradients into dw1, dw3
+ * and dw2 instead of overwriting them (the gradient of a layer whose tokens
+ * are processed in several chunks is the sum of the chunks' gradients). Every
+ * other call rejects it (MOE_ERR_INVALID_ARG). */
+#define MOE_ACCUMULATE_DW 64u
 
 /* Human-readable name of a status code (static storage). */
 const char* moe_strerror(int status);
@@ -206,8 +211,8 @@ int moe_combine(const void* src, const float* weights, const int32_t* token_inde
  * Non-gated (MOE_ACT_SILU / MOE_ACT_RELU): h = act(A), dA = g u act'(A)
  *      (written over A), dw1 and dX_slot from dA alone; w3, B, dw3 unused.
  * Out: A, B overwritten with dA, dB; dw1, dw3 [E,d,f], dw2 [E,f,d] float32
- *      (overwritten, zero for experts with no tokens); d_gates [T,k] float32;
- *      dX_slot [T*k, d].
+ *      (overwritten, zero for experts with no tokens; with MOE_ACCUMULATE_DW
+ *      added to); d_gates [T,k] float32; dX_slot [T*k, d].
  * workspace: moe_ffn_bwd_workspace_size(T,d,f,E,k,flags) bytes (gate-gradient
  *      partial sums and g*h for the dw2 GEMM; 0 in MOE_F32 mode).
  */

@@ -32,10 +32,11 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
             return fail(MOE_ERR_INVALID_ARG, "%s: %s is not 16-byte aligned", fn, #p); \
     } while (0)
 
-const unsigned KNOWN_FLAGS =
-    MOE_F32 | MOE_RENORM | MOE_ACCUMULATE | MOE_ACT_SILU | MOE_ACT_RELU | MOE_H_ON_LOAD;
+const unsigned KNOWN_FLAGS = MOE_F32 | MOE_RENORM | MOE_ACCUMULATE | MOE_ACT_SILU |
+                             MOE_ACT_RELU | MOE_H_ON_LOAD | MOE_ACCUMULATE_DW;
 const unsigned ACT_FLAGS = MOE_ACT_SILU | MOE_ACT_RELU;
-const unsigned FFN_ONLY = ACT_FLAGS | MOE_H_ON_LOAD;   // meaningful to the FFN calls only
+// meaningful to the FFN calls only
+const unsigned FFN_ONLY = ACT_FLAGS | MOE_H_ON_LOAD | MOE_ACCUMULATE_DW;
 
 // expert activation code of the FFN calls (0 SwiGLU, 1 SiLU, 2 ReLU), or -1
 int act_of(unsigned flags) {
@@ -83,7 +84,7 @@ int ffn_fwd_impl(const char* fn, bool combined, const void* x, const void* w1, c
     if ((r = check_common(fn, T, E, k, flags)) || (r = check_dim(fn, "d", d)) ||
         (r = check_dim(fn, "f", f)))
         return r;
-    if (flags & (MOE_RENORM | MOE_ACCUMULATE))
+    if (flags & (MOE_RENORM | MOE_ACCUMULATE | MOE_ACCUMULATE_DW))
         return fail(MOE_ERR_INVALID_ARG, "%s: only MOE_F32 / MOE_BF16, an activation flag and MOE_H_ON_LOAD are valid", fn);
     const int act = act_of(flags);
     if (act < 0) return fail(MOE_ERR_INVALID_ARG, "%s: MOE_ACT_SILU and MOE_ACT_RELU both set", fn);
@@ -161,6 +162,7 @@ int ffn_bwd_impl(const char* fn, bool combined, const void* dy, const void* x, c
     a.dw1 = dw1; a.dw3 = dw3; a.dw2 = dw2; a.dgates = d_gates; a.T = T; a.d = d; a.f = f;
     a.E = E; a.k = k; a.ws = workspace; a.act = act;
     a.h_on_load = flags & MOE_H_ON_LOAD;
+    a.accumulate_dw = flags & MOE_ACCUMULATE_DW;
     if (combined) { a.y = out; a.tim = token_index_map; a.accumulate = flags & MOE_ACCUMULATE; }
     else a.dX = out;
     moe::probe::begin(stream);
@@ -210,7 +212,7 @@ int moe_route(const void* x, const void* w_gate, const float* bias, int64_t T, i
     const char* fn = "moe_route";
     int r;
     if ((r = check_common(fn, T, E, k, flags)) || (r = check_dim(fn, "d", d))) return r;
-    if (flags & FFN_ONLY) return fail(MOE_ERR_INVALID_ARG, "%s: activation and h-on-load flags apply to the FFN calls only", fn);
+    if (flags & FFN_ONLY) return fail(MOE_ERR_INVALID_ARG, "%s: activation, h-on-load and weight-gradient accumulation flags apply to the FFN calls only", fn);
     if (flags & MOE_ACCUMULATE) return fail(MOE_ERR_INVALID_ARG, "%s: MOE_ACCUMULATE not valid here", fn);
     if (T == 0) return MOE_OK;
     REQUIRE_PTR(x); REQUIRE_PTR(w_gate); OPT_PTR(bias); REQUIRE_PTR(topk_ids); REQUIRE_PTR(gates);
@@ -289,7 +291,7 @@ int moe_ffn_recompute(const void* x, const void* w1, const void* w3,
     if ((r = check_common(fn, T, E, k, flags)) || (r = check_dim(fn, "d", d)) ||
         (r = check_dim(fn, "f", f)))
         return r;
-    if (flags & (MOE_RENORM | MOE_ACCUMULATE))
+    if (flags & (MOE_RENORM | MOE_ACCUMULATE | MOE_ACCUMULATE_DW))
         return fail(MOE_ERR_INVALID_ARG, "%s: only MOE_F32 / MOE_BF16, an activation flag and MOE_H_ON_LOAD are valid", fn);
     const int act = act_of(flags);
     if (act < 0) return fail(MOE_ERR_INVALID_ARG, "%s: MOE_ACT_SILU and MOE_ACT_RELU both set", fn);
@@ -325,7 +327,7 @@ int moe_combine(const void* src, const float* weights, const int32_t* token_inde
     const char* fn = "moe_combine";
     int r;
     if ((r = check_common(fn, T, k, k, flags)) || (r = check_dim(fn, "d", d))) return r;
-    if (flags & FFN_ONLY) return fail(MOE_ERR_INVALID_ARG, "%s: activation and h-on-load flags apply to the FFN calls only", fn);
+    if (flags & FFN_ONLY) return fail(MOE_ERR_INVALID_ARG, "%s: activation, h-on-load and weight-gradient accumulation flags apply to the FFN calls only", fn);
     if (flags & MOE_RENORM) return fail(MOE_ERR_INVALID_ARG, "%s: MOE_RENORM not valid here", fn);
     if (T == 0) return MOE_OK;
     REQUIRE_PTR(src); OPT_PTR(weights); REQUIRE_PTR(token_index_map); REQUIRE_PTR(out);
@@ -379,7 +381,7 @@ int moe_route_bwd(const float* d_gates, const float* logits, const int32_t* topk
     const char* fn = "moe_route_bwd";
     int r;
     if ((r = check_common(fn, T, E, k, flags)) || (r = check_dim(fn, "d", d))) return r;
-    if (flags & FFN_ONLY) return fail(MOE_ERR_INVALID_ARG, "%s: activation and h-on-load flags apply to the FFN calls only", fn);
+    if (flags & FFN_ONLY) return fail(MOE_ERR_INVALID_ARG, "%s: activation, h-on-load and weight-gradient accumulation flags apply to the FFN calls only", fn);
     if (T == 0) return MOE_OK;
     REQUIRE_PTR(d_gates); REQUIRE_PTR(logits); REQUIRE_PTR(topk_ids); REQUIRE_PTR(gates);
     REQUIRE_PTR(x); REQUIRE_PTR(w_gate); REQUIRE_PTR(dw_gate); REQUIRE_PTR(dx);

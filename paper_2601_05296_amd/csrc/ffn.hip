@@ -426,16 +426,21 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
 }
 
 // Weight gradients are written once and not read again by this layer:
-// nontemporal stores keep them from displacing the operands in L2.
+// nontemporal stores keep them from displacing the operands in L2. With
+// `add`, the tile is added to what the array holds (gradients of several
+// token chunks).
 __device__ __forceinline__ void st_nt(float* p, const f32x4& v) {
     __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(p));
+}
+__device__ __forceinline__ void st_dw(float* p, const f32x4& v, int add) {
+    st_nt(p, add ? v + *reinterpret_cast<const f32x4*>(p) : v);
 }
 
 // G3: dW2[e] = sum_s HG[s]^T dY[eti[s]]   (M = f, N = d, K = slots of e)
 __global__ void __launch_bounds__(RS::THREADS)
 g3_kernel(const bf16_t* __restrict__ HG, const bf16_t* __restrict__ dy,
           const int32_t* __restrict__ offsets, const int32_t* __restrict__ eti, int d, int f,
-          float* __restrict__ dw2) {
+          int add, float* __restrict__ dw2) {
     extern __shared__ __align__(16) char lds[];
     using C = RS;
     const int MT = (f + C::BM - 1) / C::BM, NT = (d + C::BN - 1) / C::BN;
@@ -457,7 +462,7 @@ g3_kernel(const bf16_t* __restrict__ HG, const bf16_t* __restrict__ dy,
     float* out = dw2 + (int64_t)e * f * d;
     RowStage<C, 1>::run(acc, lds, [&](int, int r, int c, const f32x4& v) {
         const int m = m0 + r, n = n0 + c;
-        if (m < f && n < d) st_nt(out + (int64_t)m * d + n, v);
+        if (m < f && n < d) st_dw(out + (int64_t)m * d + n, v, add);
     });
 }
 
@@ -529,7 +534,7 @@ __global__ void __launch_bounds__(RHW::THREADS)
 g3h_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B,
            const float* __restrict__ gs, const bf16_t* __restrict__ dy,
            const int32_t* __restrict__ offsets, const int32_t* __restrict__ eti, int d, int f,
-           float* __restrict__ dw2) {
+           int add, float* __restrict__ dw2) {
     extern __shared__ __align__(16) char lds[];
     using C = RHW;
     const int MT = (f + C::BM - 1) / C::BM, NT = (d + C::BN - 1) / C::BN;
@@ -551,7 +556,7 @@ g3h_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B,
     float* out = dw2 + (int64_t)e * f * d;
     RowStage<C, 1>::run(acc, lds, [&](int, int r, int c, const f32x4& v) {
         const int m = m0 + r, n = n0 + c;
-        if (m < f && n < d) st_nt(out + (int64_t)m * d + n, v);
+        if (m < f && n < d) st_dw(out + (int64_t)m * d + n, v, add);
     });
 }
 
@@ -561,7 +566,7 @@ template <int ACT>
 __global__ void __launch_bounds__(RD::THREADS)
 g5_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ dA,
           const bf16_t* __restrict__ dB, const int32_t* __restrict__ offsets,
-          const int32_t* __restrict__ eti, int d, int f, float* __restrict__ dw1,
+          const int32_t* __restrict__ eti, int d, int f, int add, float* __restrict__ dw1,
           float* __restrict__ dw3) {
     extern __shared__ __align__(16) char lds[];
     using C = CFirst<ACT>;
@@ -586,7 +591,7 @@ g5_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ dA,
     float* o3 = ACT == ACT_SWIGLU ? dw3 + (int64_t)e * d * f : o1;  // dw3 is NULL when non-gated
     RowStage<C, ACT == ACT_SWIGLU ? 2 : 1>::run(acc, lds, [&](int b, int r, int c, const f32x4& v) {
         const int m = m0 + r, n = n0 + c;
-        if (m < d && n < f) st_nt((b ? o3 : o1) + (int64_t)m * f + n, v);
+        if (m < d && n < f) st_dw((b ? o3 : o1) + (int64_t)m * f + n, v, add);
     });
 }
 
@@ -711,7 +716,7 @@ __global__ void f32_g2(const float* A, const float* B, const float* w2, const in
 template <int ACT>
 __global__ void f32_g3(const float* A, const float* B, const float* dy, const float* gates,
                        const int32_t* offsets, const int32_t* eti, const int32_t* slot_src,
-                       int d, int f, int E, float* dw2) {
+                       int d, int f, int E, int add, float* dw2) {
     const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (id >= (int64_t)E * f * d) return;
     const int e = (int)(id / ((int64_t)f * d));
@@ -723,7 +728,7 @@ __global__ void f32_g3(const float* A, const float* B, const float* dy, const fl
                                    ACT == ACT_SWIGLU ? B[(int64_t)s * f + c] : 0.f);
         acc = fmaf(gates[slot_src[s]] * h, dy[(int64_t)eti[s] * d + n], acc);
     }
-    dw2[id] = acc;
+    dw2[id] = add ? dw2[id] + acc : acc;
 }
 
 // one thread per slot: u, d_gate, dA, dB (in place)
@@ -763,7 +768,7 @@ __global__ void f32_g4(const float* dy, const float* w2, const float* gates,
 
 template <int ACT>
 __global__ void f32_g5(const float* x, const float* dA, const float* dB, const int32_t* offsets,
-                       const int32_t* eti, int d, int f, int E, float* dw1, float* dw3) {
+                       const int32_t* eti, int d, int f, int E, int add, float* dw1, float* dw3) {
     const int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (id >= (int64_t)E * d * f) return;
     const int e = (int)(id / ((int64_t)d * f));
@@ -775,8 +780,8 @@ __global__ void f32_g5(const float* x, const float* dA, const float* dB, const i
         a1 = fmaf(xv, dA[(int64_t)s * f + c], a1);
         if constexpr (ACT == ACT_SWIGLU) a3 = fmaf(xv, dB[(int64_t)s * f + c], a3);
     }
-    dw1[id] = a1;
-    if constexpr (ACT == ACT_SWIGLU) dw3[id] = a3;
+    dw1[id] = add ? dw1[id] + a1 : a1;
+    if constexpr (ACT == ACT_SWIGLU) dw3[id] = add ? dw3[id] + a3 : a3;
 }
 
 template <int ACT>
@@ -992,7 +997,7 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
     if (f32) {
         hipLaunchKernelGGL(f32_g3<ACT>, grid1d((int64_t)a.E * a.f * a.d, 256), dim3(256), 0, st,
                            (const float*)a.A, (const float*)a.B, (const float*)a.dy, a.gates,
-                           a.offsets, a.eti, a.slot_src, a.d, a.f, a.E, a.dw2);
+                           a.offsets, a.eti, a.slot_src, a.d, a.f, a.E, (int)a.accumulate_dw, a.dw2);
         probe::mark("f32_g3", st);
         hipLaunchKernelGGL(f32_g4<ACT>, grid1d(S, 64), dim3(64), 0, st, (const float*)a.dy,
                            (const float*)a.w2, a.gates, a.offsets, a.eti, a.slot_src, S, a.d, a.f,
@@ -1000,7 +1005,7 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
         probe::mark("f32_g4", st);
         hipLaunchKernelGGL(f32_g5<ACT>, grid1d((int64_t)a.E * a.d * a.f, 256), dim3(256), 0, st,
                            (const float*)a.x, (const float*)a.A, (const float*)a.B, a.offsets,
-                           a.eti, a.d, a.f, a.E, a.dw1, a.dw3);
+                           a.eti, a.d, a.f, a.E, (int)a.accumulate_dw, a.dw1, a.dw3);
         probe::mark("f32_g5", st);
         float* dX = a.y ? static_cast<float*>(a.ws) : (float*)a.dX;
         hipLaunchKernelGGL(f32_g6<ACT>, grid1d(S * a.d, 256), dim3(256), 0, st, (const float*)a.A,
@@ -1032,7 +1037,7 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
         hipLaunchKernelGGL(g3h_kernel<ACT>, dim3(wgrad_grid(a.E, cdiv(a.f, C3H::BM), cdiv(a.d, C3H::BN))),
                            dim3(C3H::THREADS), C3H::LDS, st, (const bf16_t*)a.A,
                            (const bf16_t*)Bx, (const float*)gs, (const bf16_t*)a.dy, a.offsets,
-                           a.eti, a.d, a.f, a.dw2);
+                           a.eti, a.d, a.f, (int)a.accumulate_dw, a.dw2);
         probe::mark("g3h_kernel", st);
     }
     auto g4 = a.h_on_load ? g4_kernel<ACT, false> : g4_kernel<ACT, true>;
@@ -1047,12 +1052,13 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
     if (!a.h_on_load) {
         hipLaunchKernelGGL(g3_kernel, dim3(wgrad_grid(a.E, cdiv(a.f, RS::BM), cdiv(a.d, RS::BN))),
                            dim3(RS::THREADS), RS::LDS, st, (const bf16_t*)HG, (const bf16_t*)a.dy,
-                           a.offsets, a.eti, a.d, a.f, a.dw2);
+                           a.offsets, a.eti, a.d, a.f, (int)a.accumulate_dw, a.dw2);
         probe::mark("g3_kernel", st);
     }
     hipLaunchKernelGGL(g5_kernel<ACT>, dim3(wgrad_grid(a.E, cdiv(a.d, C5::BM), cdiv(a.f, C5::BN))),
                        dim3(C5::THREADS), C5::LDS, st, (const bf16_t*)a.x, (const bf16_t*)a.A,
-                       (const bf16_t*)a.B, a.offsets, a.eti, a.d, a.f, a.dw1, a.dw3);
+                       (const bf16_t*)a.B, a.offsets, a.eti, a.d, a.f, (int)a.accumulate_dw,
+                       a.dw1, a.dw3);
     probe::mark("g5_kernel", st);
     const int kslices = (GATED ? 2 : 1) * a.f / rs::KS;
     if (!a.y) {   // dX_slot [S, d] for the caller's combine

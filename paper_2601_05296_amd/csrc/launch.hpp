@@ -51,6 +51,8 @@ struct FfnArgs {
     void* y; const int32_t* tim; bool accumulate;
     // h is not buffered: the second GEMM forms it again from A (and B) on load
     bool h_on_load;
+    // backward: add the weight gradients into dw1, dw3, dw2
+    bool accumulate_dw;
 };
 size_t ffn_fwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool combined,
                          bool h_on_load);

@@ -118,6 +118,26 @@ def test_h_on_load_flag():
                          None) == B.MOE_ERR_INVALID_ARG
 
 
+def test_accumulate_dw_flag():
+    lib = B.load_library()
+    T, d, f, E, k = 1000, 256, 384, 8, 2
+    fl = B.MOE_ACCUMULATE_DW
+    # the backward calls accept it (a short workspace stops them before any launch)
+    r = lib.moe_ffn_bwd(*([FAKE] * 11), T, d, f, E, k, fl, *([FAKE] * 6), 16, None)
+    assert r == B.MOE_ERR_WORKSPACE, lib.moe_last_error()
+    r = lib.moe_ffn_bwd_combine(*([FAKE] * 12), T, d, f, E, k, fl, *([FAKE] * 6), 16, None)
+    assert r == B.MOE_ERR_WORKSPACE, lib.moe_last_error()
+    # the forward, the recompute and the other calls reject it
+    r = lib.moe_ffn_fwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, T, d, f, E, k, fl, FAKE, FAKE, FAKE,
+                        FAKE, 1 << 40, None)
+    assert r == B.MOE_ERR_INVALID_ARG
+    assert lib.moe_ffn_recompute(FAKE, FAKE, FAKE, FAKE, FAKE, T, d, f, E, k, fl, FAKE, FAKE,
+                                 None) == B.MOE_ERR_INVALID_ARG
+    assert lib.moe_combine(FAKE, None, FAKE, 10, 128, 2, fl, FAKE, None) == B.MOE_ERR_INVALID_ARG
+    assert lib.moe_route(FAKE, FAKE, None, 10, 128, 8, 2, fl, FAKE, FAKE, None,
+                         None) == B.MOE_ERR_INVALID_ARG
+
+
 def test_activation_flags():
     lib = B.load_library()
     S, f = 1000 * 2, 128

@@ -767,6 +767,45 @@ def test_layer_recompute_policy_bit_identical(act):
             assert torch.equal(a, b)
 
 
+@pytest.mark.parametrize("act,hol", [("swiglu", True), ("swiglu", False), ("relu", True)])
+def test_layer_recompute_chunked_vs_oracle(act, hol):
+    """Full recompute over several token chunks (the last one ragged): every
+    output and gradient against the oracle; y, dx, d_gates and dw_gate
+    bit-identical to the policy that saves A and B (they are per-token
+    results), and the weight gradients equal to float32 summation order (each
+    chunk's are added into the layer's)."""
+    cfg = synth.MoEConfig("rcc", T=1500, d=256, f=384, E=16, k=4, dtype="bf16", renorm=True,
+                          act=act)
+    inp = synth.make_inputs(cfg)
+    v, st = inp.vals, inp.store
+    x, wg, w1, w2, dy = (dev(st[n]) for n in ("x", "w_gate", "w1", "w2", "dy"))
+    gated = act == "swiglu"
+    w3 = dev(st["w3"]) if gated else None
+    y0, s0 = layer.forward(x, wg, None, w1, w3, w2, cfg.k, cfg.renorm, act=act, h_on_load=hol)
+    g0 = layer.backward(s0, dy, x, wg, w1, w3, w2)
+    y1, s1 = layer.forward(x, wg, None, w1, w3, w2, cfg.k, cfg.renorm, act=act, h_on_load=hol,
+                           recompute=True, chunk_tokens=400)
+    assert s1.chunk == 400 and s1.A is None and s1.eti is None
+    assert s1.nbytes() == layer.saved_bytes_per_token(cfg.d, cfg.f, cfg.E, cfg.k, 2, cfg.T, act,
+                                                      recompute=True) * cfg.T
+    g1 = layer.backward(s1, dy, x, wg, w1, w3, w2)
+    torch.cuda.synchronize()
+    assert torch.equal(y0, y1)
+    for n in ("dx", "d_gates", "dw_gate"):
+        assert torch.equal(g0[n], g1[n]), n
+    for n in ("dw1", "dw2") + (("dw3",) if gated else ()):
+        err = float((g0[n] - g1[n]).abs().max() / g0[n].abs().max())
+        assert err <= 1e-5, (n, err)
+    fw = oracle.layer_forward(v["x"], v["w_gate"], None, v["w1"], v["w3"], v["w2"], cfg.k,
+                              cfg.renorm, act=act)
+    assert np.array_equal(fw["ids"], s1.ids.cpu().numpy())
+    bw = oracle.layer_backward(fw, v["dy"], v["x"], v["w_gate"], v["w1"], v["w3"], v["w2"],
+                               cfg.renorm)
+    assert_close("y", host(y1), fw["y"], "bf16")
+    for n in ("dx", "d_gates", "dw_gate", "dw1", "dw2") + (("dw3",) if gated else ()):
+        assert_close(n, host(g1[n]), bw[n], "bf16")
+
+
 def test_layer_deterministic_bf16():
     cfg = synth.MoEConfig("det", T=2000, d=256, f=256, E=16, k=4, dtype="bf16", renorm=True)
     inp = synth.make_inputs(cfg)
