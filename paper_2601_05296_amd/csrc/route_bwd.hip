@@ -25,9 +25,10 @@
 namespace moe {
 namespace {
 
-constexpr int RB_TOK = 32;     // tokens per workgroup in the dx kernel
-constexpr int RB_CHUNK = 1024; // tokens per split in the dW_g kernel
-constexpr int RB_EB = 32;      // experts per workgroup in the dW_g kernel
+constexpr int RB_TOK = 32;        // tokens per workgroup in the dx kernel
+constexpr int RB_CHUNK = 1024;    // least tokens per split in the dW_g kernels
+constexpr int RB_MAXSPLIT = 128;  // most splits: the partials stay O(E d), not O(T)
+constexpr int RB_EB = 32;         // experts per workgroup in the dW_g kernel
 
 __global__ void __launch_bounds__(256)
 rb_dlogits(const float* __restrict__ dg, const float* __restrict__ logits,
@@ -104,14 +105,14 @@ rb_dx(const float* __restrict__ dl, const void* __restrict__ wg_, int64_t T, int
 template <bool F32>
 __global__ void __launch_bounds__(256)
 rb_dwg_partial(const float* __restrict__ dl, const void* __restrict__ x_, int64_t T, int d,
-               int E, float* __restrict__ part) {
+               int E, int64_t chunk, float* __restrict__ part) {
     __shared__ float s_dl[64][RB_EB];
     const int tid = threadIdx.x;
     const int c = blockIdx.x * 256 + tid;
     const int e0 = blockIdx.y * RB_EB;
     const int split = blockIdx.z;
-    const int64_t tlo = (int64_t)split * RB_CHUNK;
-    const int64_t thi = min(T, tlo + RB_CHUNK);
+    const int64_t tlo = (int64_t)split * chunk;
+    const int64_t thi = min(T, tlo + chunk);
     float acc[RB_EB];
 #pragma unroll
     for (int i = 0; i < RB_EB; ++i) acc[i] = 0.f;
@@ -150,7 +151,7 @@ __global__ void rb_dwg_reduce(const float* __restrict__ part, int nsplit, int E,
 }
 
 using CR = rs::Cfg<256, 256, 2, 4, 1>;
-constexpr int RB_MCH = 512;  // tokens per split of the MFMA dW_g kernel
+constexpr int RB_MCH = 512;  // least tokens per split of the MFMA dW_g kernel
 
 inline int epad(int E) { return (E + 31) / 32 * 32; }
 
@@ -270,14 +271,14 @@ rb_dx_mfma(const bf16_t* __restrict__ hl, const bf16_t* __restrict__ wg, int64_t
 // part[split][m][n] = sum over the split's tokens of hl[t][m] * x[t][n], m < 2Ep
 __global__ void __launch_bounds__(CR::THREADS)
 rb_dwg_mfma(const bf16_t* __restrict__ hl, const bf16_t* __restrict__ x, int64_t T, int d,
-            int Ep, float* __restrict__ part) {
+            int Ep, int64_t chunk, float* __restrict__ part) {
     extern __shared__ __align__(16) char lds[];
     using C = CR;
     const int n0 = blockIdx.x * C::BN;
     const int m0 = blockIdx.y * C::BM;
     const int split = blockIdx.z;
-    const int64_t t0 = (int64_t)split * RB_MCH;
-    const int cnt = (int)min((int64_t)RB_MCH, T - t0);
+    const int64_t t0 = (int64_t)split * chunk;
+    const int cnt = (int)min(chunk, T - t0);
     const int M = 2 * Ep;
     rs::SlotMC<C, C::BM> la;
     la.init(hl, M, t0, m0, M, cnt);
@@ -320,8 +321,14 @@ __global__ void rb_dwg_reduce_hilo(const float* __restrict__ part, int nsplit, i
     dwg[i] = acc;
 }
 
-inline int nsplits(int64_t T) { return (int)((T + RB_CHUNK - 1) / RB_CHUNK); }
-inline int msplits(int64_t T) { return (int)((T + RB_MCH - 1) / RB_MCH); }
+// tokens per split: at least `least`, and at most RB_MAXSPLIT splits
+inline int64_t split_tokens(int64_t T, int64_t least) {
+    int64_t c = (T + RB_MAXSPLIT - 1) / RB_MAXSPLIT;
+    c = (c + 63) / 64 * 64;
+    return c > least ? c : least;
+}
+inline int nsplits(int64_t T) { const int64_t c = split_tokens(T, RB_CHUNK); return (int)((T + c - 1) / c); }
+inline int msplits(int64_t T) { const int64_t c = split_tokens(T, RB_MCH); return (int)((T + c - 1) / c); }
 inline size_t al256(size_t b) { return (b + 255) / 256 * 256; }
 
 hipError_t set_rb_lds_limits() {
@@ -365,7 +372,7 @@ hipError_t route_bwd(const float* dgates, const float* logits, const int32_t* id
         const int ns = nsplits(T);
         hipLaunchKernelGGL(rb_dwg_partial<true>,
                            dim3((unsigned)((d + 255) / 256), (unsigned)((E + RB_EB - 1) / RB_EB), (unsigned)ns),
-                           dim3(256), 0, st, dl, x, T, d, E, part);
+                           dim3(256), 0, st, dl, x, T, d, E, split_tokens(T, RB_CHUNK), part);
         probe::mark("rb_dwg_partial", st);
         hipLaunchKernelGGL(rb_dwg_reduce, dim3((unsigned)(((int64_t)E * d + 255) / 256)), dim3(256), 0,
                            st, part, ns, E, d, dwg);
@@ -387,7 +394,7 @@ hipError_t route_bwd(const float* dgates, const float* logits, const int32_t* id
     const int ms = msplits(T);
     hipLaunchKernelGGL(rb_dwg_mfma, dim3((unsigned)((d + CR::BN - 1) / CR::BN), (unsigned)((2 * Ep + CR::BM - 1) / CR::BM), (unsigned)ms),
                        dim3(CR::THREADS), CR::LDS, st, (const bf16_t*)hl, (const bf16_t*)x, T, d, Ep,
-                       part);
+                       split_tokens(T, RB_MCH), part);
     probe::mark("rb_dwg_partial", st);
     hipLaunchKernelGGL(rb_dwg_reduce_hilo, dim3((unsigned)(((int64_t)E * d + 255) / 256)), dim3(256), 0,
                        st, part, ms, E, Ep, d, dwg);

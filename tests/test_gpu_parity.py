@@ -409,7 +409,9 @@ def test_ffn_fwd_bwd_parity(dtype, T, d, f, E, k, renorm, pattern):
     ("f32", 700, 128, 32, 4, True, True),
     ("bf16", 900, 192, 64, 6, False, True), ("bf16", 600, 320, 256, 8, True, False),
     ("bf16", 100, 64, 1, 1, True, False), ("bf16", 300, 64, 4, 3, False, True),
-    ("bf16", 500, 128, 256, 16, False, True), ("bf16", 400, 192, 256, 16, True, False)])
+    ("bf16", 500, 128, 256, 16, False, True), ("bf16", 400, 192, 256, 16, True, False),
+    # more tokens than 128 splits of 512 (bf16) / 1024 (f32): longer, capped splits
+    ("bf16", 150001, 128, 16, 2, False, True), ("f32", 140001, 64, 8, 2, True, False)])
 def test_route_bwd_parity(dtype, T, d, E, k, renorm, accumulate):
     cfg = synth.MoEConfig("rb", T=T, d=d, f=128, E=E, k=k, dtype=dtype, renorm=renorm)
     inp = synth.make_inputs(cfg)
