@@ -489,10 +489,14 @@ struct RowStage {
 // The weight-gradient GEMMs have P = MT*NT output tiles per expert, each looping
 // over the expert's tokens. Workgroup ids are dealt round-robin to the 8 XCDs
 // (each with its own L2). Every XCD takes, for every expert, one band of
-// ceil(P/8) consecutive tiles in row-major (m, n) order: the tiles of a band
-// share the left operand's token stream in that XCD's L2, and every XCD gets
-// the same share of every expert, whatever the experts' token counts.
+// ceil(P/8) consecutive tiles, so that every XCD gets the same share of every
+// expert whatever the experts' token counts. Inside an expert the tiles come in
+// groups of WG_GM row tiles with the column tile slower: the ~32 workgroups
+// an XCD runs at once then cover a WG_GM x 8 block of tiles, which read
+// WG_GM + 8 operand panels per K slice from L2 instead of the 1 + 32 of a
+// row-major band (an expert's last, narrower group holds its remaining rows).
 // Returns false for the padding tiles of the last band.
+constexpr int WG_GM = 4;
 __device__ __forceinline__ bool wgrad_tile(int bid, int MT, int NT, int& e, int& mt, int& nt) {
     const int P = MT * NT;
     const int G = (P + 7) >> 3;
@@ -500,8 +504,12 @@ __device__ __forceinline__ bool wgrad_tile(int bid, int MT, int NT, int& e, int&
     e = j / G;
     const int lt = x * G + j % G;
     if (lt >= P) return false;
-    mt = lt / NT;
-    nt = lt % NT;
+    const int grp = lt / (WG_GM * NT);
+    const int m_base = grp * WG_GM;
+    const int gm = min(WG_GM, MT - m_base);
+    const int in = lt - grp * WG_GM * NT;
+    mt = m_base + in % gm;
+    nt = in / gm;
     return true;
 }
 inline int wgrad_grid(int E, int MT, int NT) { return E * 8 * ((MT * NT + 7) / 8); }
