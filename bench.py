@@ -58,6 +58,8 @@ def parse():
                     help="approximate CPU time budget of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-baseline-memory", action="store_true")
+    ap.add_argument("--no-reference-rates", action="store_true",
+                    help="skip the two measured ceilings (device copy, hipBLASLt dense GEMM)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (reference for HBM byte counters)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -250,26 +252,32 @@ def summarize_counters(tcp_csv, sq_csv, out, workload, cmd, profile_cmd):
     """Per-kernel means per launch of the L1-to-L2 request counters and of
     the MFMA busy cycles. GRBM_GUI_ACTIVE is summed over the XCDs, so one
     XCD's cycles are GUI/8; the mean number of read requests in flight per CU
-    is the latency sum (request-cycles) over CU-cycles."""
+    is the latency sum (request-cycles) over CU-cycles. The clock is one XCD's
+    cycles over the dispatch's duration (meaningful for launches of a
+    millisecond or more; short ones count the dispatch overhead's cycles)."""
     import csv
-    acc, launches = {}, {}
+    acc, launches, dur = {}, {}, {}
     for path in (tcp_csv, sq_csv):
         seen = {}
         for r in csv.DictReader(open(path)):
             name = kernel_short_name(r["Kernel_Name"])
             a = acc.setdefault(name, {})
             a[r["Counter_Name"]] = a.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
-            seen.setdefault(name, set()).add(r["Dispatch_Id"])
+            ids = seen.setdefault(name, set())
+            if path == sq_csv and r["Dispatch_Id"] not in ids:
+                dur[name] = dur.get(name, 0.0) + (int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+            ids.add(r["Dispatch_Id"])
         for name, ids in seen.items():
             launches[name] = max(launches.get(name, 0), len(ids))
-    lines = ["# L1-to-L2 requests and MFMA busy time per launch, workload %s" % workload,
+    lines = ["# L1-to-L2 requests, MFMA busy time and clock per launch, workload %s" % workload,
              "# profile: %s" % profile_cmd,
              "# summary: python %s" % cmd,
              "# cycles = GRBM_GUI_ACTIVE / %d (one XCD); %d CUs, %d SIMDs per CU" % (N_XCD, N_CU, SIMD_PER_CU),
              "# rd_req: TCP_TCC_READ_REQ; lat: mean read latency in cycles; inflight: mean read "
              "requests in flight per CU; pend: share of CU-cycles the L1 stalls on pending "
-             "requests; wr_req: TCP_TCC_WRITE_REQ; mfma: MFMA busy share of SIMD-cycles",
-             "# kernel launches cycles rd_req lat inflight pend wr_req mfma"]
+             "requests; wr_req: TCP_TCC_WRITE_REQ; mfma: MFMA busy share of SIMD-cycles; "
+             "us: mean duration; clk: cycles / duration (GHz)",
+             "# kernel launches cycles rd_req lat inflight pend wr_req mfma us clk"]
     def per(a, key, n):
         return a.get(key, 0.0) / n
     order = sorted(acc, key=lambda k: -acc[k].get("GRBM_GUI_ACTIVE", 0.0))
@@ -280,11 +288,13 @@ def summarize_counters(tcp_csv, sq_csv, out, workload, cmd, profile_cmd):
             continue
         rq = per(a, "TCP_TCC_READ_REQ_sum", n)
         lat_sum = per(a, "TCP_TCC_READ_REQ_LATENCY_sum", n)
-        lines.append("%-20s %4d %9.0f %10.3g %6.0f %8.1f %6.2f %10.3g %6.2f" % (
-            name, n, cyc, rq, lat_sum / rq if rq else float("nan"), lat_sum / (N_CU * cyc),
+        us = dur.get(name, 0.0) / n / 1e3
+        lines.append("%-20s %4d %9.0f %10.3g %6.0f %8.1f %6.2f %10.3g %6.2f %9.1f %5.2f" % (
+            name[:40], n, cyc, rq, lat_sum / rq if rq else float("nan"), lat_sum / (N_CU * cyc),
             per(a, "TCP_PENDING_STALL_CYCLES_sum", n) / (N_CU * cyc),
             per(a, "TCP_TCC_WRITE_REQ_sum", n),
-            per(a, "SQ_VALU_MFMA_BUSY_CYCLES", n) / (N_CU * SIMD_PER_CU * cyc)))
+            per(a, "SQ_VALU_MFMA_BUSY_CYCLES", n) / (N_CU * SIMD_PER_CU * cyc),
+            us, cyc / (us * 1e3) if us > 0 else float("nan")))
     with open(out, "w") as fh:
         fh.write("\n".join(lines) + "\n")
     print("wrote", out)
@@ -630,6 +640,45 @@ def cpu_oracle_baseline(inp, cfg, budget_s):
                       % (n, cfg.T, cfg.name, t, n0, n1, t0 + t1)}
 
 
+def reference_rates(cfg, dev):
+    """Two ceilings measured on this GPU beside the kernels, with events on the
+    current stream, 5 timed calls after 2 untimed: a device-to-device copy of
+    1 GiB (1 GiB read + 1 GiB written, the rate an HBM-bound gather-reduce can
+    hope for), and hipBLASLt's dense bf16 GEMM (torch.matmul, contiguous
+    operands) at one expert's even share of the first FFN product,
+    [S/E x d] x [d x f], the rate a dense library GEMM of the same shape
+    reaches. Neither is on the layer's path."""
+    import torch
+
+    def timed(fn, n=5):
+        for _ in range(2):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+    out = {}
+    src = torch.empty(COPY_BYTES // 2, dtype=torch.bfloat16, device=dev)
+    dst = torch.empty_like(src)
+    ms = timed(lambda: dst.copy_(src))
+    out["device_copy"] = {"bytes_read_plus_written": 2 * COPY_BYTES, "ms": round(ms, 4),
+                          "GB_per_s": round(2 * COPY_BYTES / ms / 1e6, 1)}
+    del src, dst
+    m = max(256, (cfg.T * cfg.k // cfg.E) // 256 * 256)
+    g = torch.Generator(device=dev).manual_seed(1)
+    a = torch.randn((m, cfg.d), device=dev, generator=g).to(torch.bfloat16)
+    b = torch.randn((cfg.d, cfg.f), device=dev, generator=g).to(torch.bfloat16)
+    ms = timed(lambda: torch.matmul(a, b))
+    out["hipblaslt_dense_bf16"] = {"M": m, "N": cfg.f, "K": cfg.d, "ms": round(ms, 4),
+                                   "TFLOP_per_s": round(2.0 * m * cfg.d * cfg.f / ms / 1e9, 1)}
+    del a, b
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     args = parse()
     if args.summarize_pmc:
@@ -849,6 +898,8 @@ def main():
             "tokens_per_s": round(T * n_lean / (t3 - t2), 1),
             "peak_activation_bytes_per_token": round(max(lf, lb) / T, 1),
             "peak_activation_bytes_per_token_fwd_bwd": [round(lf / T, 1), round(lb / T, 1)]}
+    if not args.no_reference_rates:
+        out["reference_rates"] = reference_rates(cfg, dev)
     if args.copy_calibration:
         src = torch.empty(COPY_BYTES // 2, dtype=torch.bfloat16, device=dev)
         dst = torch.empty_like(src)

@@ -119,16 +119,21 @@ void launch_combine(const void* src, int64_t src_ld, const float* w, const int32
                     int64_t out_ld, hipStream_t st) {
     const int nchunk = ncols / (f32 ? 4 : 8);
     // lanes per token: the smallest power of two covering the row's chunks
-    // (at most the whole workgroup; wider rows loop)
+    // (at most the whole workgroup; wider rows loop). A row whose chunk count
+    // is not a power of two, or a token with more than four sources, takes at
+    // most one wave per token instead, so that no lane idles and each lane
+    // keeps more source loads in flight (measured faster on both).
+    const bool pow2 = (nchunk & (nchunk - 1)) == 0;
+    const int cap = (!pow2 || k > 4) ? WAVE : CMB_THREADS;
     int lpt_log2 = 0;
-    while ((1 << lpt_log2) < nchunk && (1 << lpt_log2) < CMB_THREADS) ++lpt_log2;
+    while ((1 << lpt_log2) < nchunk && (1 << lpt_log2) < cap) ++lpt_log2;
     const int64_t tpb = CMB_THREADS >> lpt_log2;
     const dim3 grid((unsigned)((T + tpb - 1) / tpb));
     if (f32) {
         hipLaunchKernelGGL((combine_kernel<true, 2, KMAX>), grid, dim3(CMB_THREADS), 0, st, src,
                            src_ld, w, tim, T, ncols, k, (int)accumulate, out, out_ld, lpt_log2);
         probe::mark("combine_f32", st);
-    } else if (nchunk <= CMB_THREADS) {
+    } else if (nchunk <= (1 << lpt_log2) || k > 4) {
         hipLaunchKernelGGL((combine_kernel<false, 1, KMAX>), grid, dim3(CMB_THREADS), 0, st, src,
                            src_ld, w, tim, T, ncols, k, (int)accumulate, out, out_ld, lpt_log2);
         probe::mark("combine", st);

@@ -11,9 +11,10 @@
 //                   [T, E] map is materialised: the per-tile counts carry the
 //                   same information.
 //   2. tile_scan:   one workgroup takes the exclusive prefix sum of cnt in
-//                   expert-major order. Entry (e, tile) then holds
-//                   offsets[e] + (tokens of e in earlier tiles), i.e. the first
-//                   slot of that tile's run inside expert e's segment.
+//                   expert-major order (wave-level scans over batches of
+//                   16K entries). Entry (e, tile) then holds offsets[e] + (tokens
+//                   of e in earlier tiles), i.e. the first slot of that
+//                   tile's run inside expert e's segment.
 //   3. tile_rank:   each workgroup revisits its tile in chunks of 64 tokens per
 //                   wave. A lane sets its bit in an LDS 64-bit mask per chosen
 //                   expert; the token's rank among the expert's tokens is the
@@ -84,43 +85,77 @@ tile_hist(const int32_t* __restrict__ ids, int64_t T, int E, int k, int64_t tb, 
 
 constexpr int SCAN_THREADS = 1024;
 
+// inclusive prefix sum over the 64 lanes of a wave
+__device__ __forceinline__ int wave_incl_scan(int v, int lane) {
+#pragma unroll
+    for (int o = 1; o < WAVE; o <<= 1) {
+        const int u = __shfl_up(v, o, WAVE);
+        if (lane >= o) v += u;
+    }
+    return v;
+}
+
+// One workgroup scans cnt (expert-major) in batches of SCAN_RB rounds of 1024
+// consecutive entries. All loads of a batch are issued together; each wave
+// scans its 64 entries of every round (wave-level scans), the batch's
+// SCAN_RB x 16 wave totals, which lie in entry order, are scanned by the
+// first four waves, and a carry runs from batch to batch.
+constexpr int SCAN_RB = 16;
+
 __global__ void __launch_bounds__(SCAN_THREADS)
 tile_scan(int32_t* __restrict__ cnt, int E, int ntiles, int32_t* __restrict__ counts,
           int32_t* __restrict__ offsets) {
-    __shared__ int32_t part[SCAN_THREADS];
+    constexpr int NW = SCAN_THREADS / WAVE;
+    constexpr int NT = SCAN_RB * NW;            // wave totals per batch (256)
+    static_assert(NT <= SCAN_THREADS && NT % WAVE == 0, "one thread per wave total");
+    __shared__ int32_t wt[NT];                  // wave totals, then their exclusive prefix
+    __shared__ int32_t wt_ex[NT];
+    __shared__ int32_t part[NT / WAVE];         // totals of the four scanning waves
     const int tid = threadIdx.x;
+    const int lane = tid & (WAVE - 1);
+    const int wv = tid / WAVE;
     const int n = E * ntiles;
-    const int per = (n + SCAN_THREADS - 1) / SCAN_THREADS;
-    const int lo = tid * per;
-    const int hi = min(lo + per, n);
-    int s = 0;
-    for (int i = lo; i < hi; ++i) s += cnt[i];
-    part[tid] = s;
-    __syncthreads();
-    // Hillis-Steele inclusive scan of the per-thread sums
-    for (int o = 1; o < SCAN_THREADS; o <<= 1) {
-        int v = tid >= o ? part[tid - o] : 0;
+    int carry = 0;
+    for (int b0 = 0; b0 < n; b0 += SCAN_RB * SCAN_THREADS) {
+        int v[SCAN_RB], inc[SCAN_RB];
+#pragma unroll
+        for (int r = 0; r < SCAN_RB; ++r) {
+            const int i = b0 + r * SCAN_THREADS + tid;
+            v[r] = i < n ? cnt[i] : 0;
+        }
+#pragma unroll
+        for (int r = 0; r < SCAN_RB; ++r) {
+            inc[r] = wave_incl_scan(v[r], lane);
+            if (lane == WAVE - 1) wt[r * NW + wv] = inc[r];
+        }
         __syncthreads();
-        part[tid] += v;
+        int x = 0, xi = 0;
+        if (tid < NT) {                         // whole waves 0..3
+            x = wt[tid];
+            xi = wave_incl_scan(x, lane);
+            if (lane == WAVE - 1) part[wv] = xi;
+        }
         __syncthreads();
+        int total = 0, before = 0;
+#pragma unroll
+        for (int w = 0; w < NT / WAVE; ++w) {
+            total += part[w];
+            before += w < wv ? part[w] : 0;
+        }
+        if (tid < NT) wt_ex[tid] = before + xi - x;
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < SCAN_RB; ++r) {
+            const int i = b0 + r * SCAN_THREADS + tid;
+            if (i < n) cnt[i] = carry + wt_ex[r * NW + wv] + inc[r] - v[r];
+        }
+        carry += total;
+        __syncthreads();                        // wt, wt_ex and part are reused
     }
-    int run = tid ? part[tid - 1] : 0;
-    for (int i = lo; i < hi; ++i) {
-        const int c = cnt[i];
-        cnt[i] = run;
-        run += c;
-    }
-    __syncthreads();
-    const int total = part[SCAN_THREADS - 1];
-    for (int e = tid; e <= E; e += SCAN_THREADS) {
-        const int oe = e < E ? cnt[e * ntiles] : total;
-        offsets[e] = oe;
-    }
-    __syncthreads();
-    for (int e = tid; e < E; e += SCAN_THREADS) {
-        const int nxt = e + 1 < E ? cnt[(e + 1) * ntiles] : total;
-        counts[e] = nxt - cnt[e * ntiles];
-    }
+    // carry is now the number of choices that take a slot
+    for (int e = tid; e <= E; e += SCAN_THREADS) offsets[e] = e < E ? cnt[e * ntiles] : carry;
+    for (int e = tid; e < E; e += SCAN_THREADS)
+        counts[e] = (e + 1 < E ? cnt[(e + 1) * ntiles] : carry) - cnt[e * ntiles];
 }
 
 __global__ void __launch_bounds__(IDX_THREADS)
