@@ -35,19 +35,15 @@
 #include "common.hpp"
 #include "gemm.hpp"
 #include "gemm_rs.hpp"
-#include "loaders.hpp"
 #include "launch.hpp"
 #include "probe.hpp"
 
 namespace moe {
 namespace {
 
-// Tile configurations: <BM, BN, WM, WN, NB>. 256-row tiles, 2x4 waves.
-// Single right operand: each wave owns 128 x 64 outputs. Two right operands
-// (G1: W1 and W3; G5: dA and dB): 128 x 32 of each.
-using CD = GemmCfg<256, 128, 2, 4, 2>;
-using CS = GemmCfg<256, 256, 2, 4, 1>;  // h-on-load GEMMs of the non-gated experts
-// Register-staged core (gemm_rs.hpp): the same tile shapes and wave layout.
+// Tile configurations (gemm_rs.hpp): <BM, BN, WM, WN, NB>. 256-row tiles,
+// 2x4 waves. Single right operand: each wave owns 128 x 64 outputs. Two right
+// operands (G1: W1 and W3; G5: dA and dB): 128 x 32 of each.
 using RD = rs::Cfg<256, 128, 2, 4, 2>;  // G1, G5
 using RS = rs::Cfg<256, 256, 2, 4, 1>;  // G2, G3, G6
 constexpr int RASTER_GM = 4;            // M tiles per raster group (find_slot_tile)

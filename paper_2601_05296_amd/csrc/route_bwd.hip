@@ -19,7 +19,6 @@
 #include "gemm.hpp"
 #include "gemm_rs.hpp"
 #include "launch.hpp"
-#include "loaders.hpp"
 #include "probe.hpp"
 
 namespace moe {
