@@ -85,13 +85,18 @@ tile_hist(const int32_t* __restrict__ ids, int64_t T, int E, int k, int64_t tb, 
 
 constexpr int SCAN_THREADS = 1024;
 
-// inclusive prefix sum over the 64 lanes of a wave
-__device__ __forceinline__ int wave_incl_scan(int v, int lane) {
-#pragma unroll
-    for (int o = 1; o < WAVE; o <<= 1) {
-        const int u = __shfl_up(v, o, WAVE);
-        if (lane >= o) v += u;
-    }
+// Inclusive prefix sum over the 64 lanes of a wave, by DPP lane moves: a
+// Hillis-Steele scan inside each row of 16 lanes (row_shr 1, 2, 4, 8; a lane
+// whose source lies before its row's start adds 0), then the last lane of row
+// 0 and of row 2 added into rows 1 and 3 (row_bcast:15, row mask 0b1010) and
+// the last lane of row 1 into rows 2 and 3 (row_bcast:31, row mask 0b1100).
+__device__ __forceinline__ int wave_incl_scan(int v) {
+    v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);   // row_shr:1
+    v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);   // row_shr:2
+    v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);   // row_shr:4
+    v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);   // row_shr:8
+    v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);   // row_bcast:15
+    v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);   // row_bcast:31
     return v;
 }
 
@@ -123,16 +128,17 @@ tile_scan(int32_t* __restrict__ cnt, int E, int ntiles, int32_t* __restrict__ co
             const int i = b0 + r * SCAN_THREADS + tid;
             v[r] = i < n ? cnt[i] : 0;
         }
+        // rounds past the end hold zeros (the test is uniform over the workgroup)
 #pragma unroll
         for (int r = 0; r < SCAN_RB; ++r) {
-            inc[r] = wave_incl_scan(v[r], lane);
+            inc[r] = b0 + r * SCAN_THREADS < n ? wave_incl_scan(v[r]) : 0;
             if (lane == WAVE - 1) wt[r * NW + wv] = inc[r];
         }
         __syncthreads();
         int x = 0, xi = 0;
         if (tid < NT) {                         // whole waves 0..3
             x = wt[tid];
-            xi = wave_incl_scan(x, lane);
+            xi = wave_incl_scan(x);
             if (lane == WAVE - 1) part[wv] = xi;
         }
         __syncthreads();

@@ -246,7 +246,9 @@ def test_route_bwd_ignores_invalid_ids(renorm):
     ("f32", 1000, 256, 8, 2, False, None), ("f32", 500, 256, 64, 6, True, "dead"),
     ("bf16", 700, 320, 64, 6, True, None),
     ("bf16", 100, 64, 1, 1, False, None), ("bf16", 100, 64, 3, 3, True, None),
-    ("bf16", 500, 128, 256, 16, False, None), ("bf16", 400, 192, 256, 16, True, "zipf")])
+    ("bf16", 500, 128, 256, 16, False, None), ("bf16", 400, 192, 256, 16, True, "zipf"),
+    # 128-token workgroups (E > 64, T >= 65536), ragged last workgroup
+    ("bf16", 70000, 256, 128, 8, False, "zipf"), ("bf16", 65601, 128, 256, 16, True, None)])
 def test_route_parity(dtype, T, d, E, k, renorm, bias):
     cfg = synth.MoEConfig("r", T=T, d=d, f=128, E=E, k=k, dtype=dtype, renorm=renorm,
                           zipf_s=1.2 if bias == "zipf" else 0.0,
