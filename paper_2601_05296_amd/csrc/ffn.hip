@@ -235,7 +235,7 @@ struct HKC {
     // h of dword p of chunk i, in place of A's
     static constexpr int NSUB = 4;
     template <int i, int p> __device__ void sub() { va[i][p] = h_pair<ACT, false>(va[i][p], vb[i][p], 0.f); }
-    template <int i> __device__ void store(char* tile) { rs::sts16(tile + G::lds(i), va[i]); }
+    template <int i, bool TAIL> __device__ void store(char* tile) { rs::sts16(tile + G::lds(i), va[i]); }
 };
 
 // G2 with h formed on load: O = h W2[e] from the saved A (and B), no h buffer.
@@ -504,9 +504,10 @@ struct GHMC {
     // g * h of dword p of chunk i, in place of A's
     static constexpr int NSUB = 4;
     template <int i, int p> __device__ void sub() { va[i][p] = h_pair<ACT, true>(va[i][p], vb[i][p], g[i]); }
-    template <int i> __device__ void store(char* tile) {
+    template <int i, bool TAIL> __device__ void store(char* tile) {
         const rs::u32x4 z = {0u, 0u, 0u, 0u};
-        rs::sts16(tile + G::lds(i), (zmask >> i) & 1 ? z : va[i]);
+        if constexpr (TAIL) rs::sts16(tile + G::lds(i), (zmask >> i) & 1 ? z : va[i]);
+        else rs::sts16(tile + G::lds(i), va[i]);
     }
 };
 

@@ -163,7 +163,7 @@ struct MCGeom {
 // load<i>(kt) (issue the global load(s) of chunk i of slice kt into its
 // registers), static int NSUB and sub<i, p>() for p < NSUB (the pieces of a
 // transform of chunk i in registers, run in order after its data has arrived;
-// NSUB = 0 for a plain copy) and store<i>(tile) (write chunk i at its place in
+// NSUB = 0 for a plain copy) and store<i, TAIL>(tile) (write chunk i at its place in
 // the LDS tile). On return acc[b][i][j] holds sum_k A[m][k] B_b[k][n] for the
 // fragment at rows wm*WTM + 32i, columns wn*WTN + 32j.
 // Every wave computes all its fragments, also those that lie beyond the
@@ -179,7 +179,7 @@ struct NoLoader {
     static constexpr int NSUB = 0;
     template <int i> __device__ void load(int) {}
     template <int i, int p> __device__ void sub() {}
-    template <int i> __device__ void store(char*) {}
+    template <int i, bool TAIL> __device__ void store(char*) {}
 };
 
 // ---- side operations of one slice -------------------------------------------------------
@@ -276,11 +276,14 @@ __device__ __forceinline__ void mainloop(LA& la, LB0& lb0, LB1& lb1, int nk, cha
         else if constexpr (g < NA + N0) lb0.template load<g - NA>(kt);
         else lb1.template load<g - NA - N0>(kt);
     };
-    auto store_chunk = [&](auto g_c, char* stage) __attribute__((always_inline)) {
+    // TAIL: the chunk belongs to the last slice, whose K rows may run past the
+    // operand's extent (loaders that zero such rows do so only then)
+    auto store_chunk = [&](auto g_c, char* stage, auto tail_c) __attribute__((always_inline)) {
         constexpr int g = decltype(g_c)::value;
-        if constexpr (g < NA) la.template store<g>(stage);
-        else if constexpr (g < NA + N0) lb0.template store<g - NA>(stage + C::A_BYTES);
-        else lb1.template store<g - NA - N0>(stage + C::A_BYTES + C::B_BYTES);
+        constexpr bool TAIL = decltype(tail_c)::value;
+        if constexpr (g < NA) la.template store<g, TAIL>(stage);
+        else if constexpr (g < NA + N0) lb0.template store<g - NA, TAIL>(stage + C::A_BYTES);
+        else lb1.template store<g - NA - N0, TAIL>(stage + C::A_BYTES + C::B_BYTES);
     };
     auto sub_chunk = [&](auto g_c, auto p_c) __attribute__((always_inline)) {
         constexpr int g = decltype(g_c)::value, p = decltype(p_c)::value;
@@ -295,7 +298,7 @@ __device__ __forceinline__ void mainloop(LA& la, LB0& lb0, LB1& lb1, int nk, cha
     // the chunk's transform and LDS write, all at once (prologue)
     auto commit_chunk = [&](auto g_c, char* stage) __attribute__((always_inline)) {
         sfor<decltype(nsub_of(g_c))::value>([&](auto p) { sub_chunk(g_c, p); });
-        store_chunk(g_c, stage);
+        store_chunk(g_c, stage, std::true_type{});   // slice 0 may be the last
     };
 
     bf16x8 fr[2][NR];
@@ -398,7 +401,8 @@ __device__ __forceinline__ void mainloop(LA& la, LB0& lb0, LB1& lb1, int nk, cha
                             sub_chunk(std::integral_constant<int, g>{},
                                       std::integral_constant<int, SCH::ops.piece[o]>{});
                         else if constexpr (SCH::ops.kind[o] == 1)
-                            store_chunk(std::integral_constant<int, g>{}, nxt);
+                            store_chunk(std::integral_constant<int, g>{}, nxt,
+                                        std::integral_constant<bool, MODE == 1>{});
                         else
                             load_chunk(std::integral_constant<int, g>{}, kt + 2);
                     });
@@ -455,7 +459,7 @@ struct GatherKC {
         }
     }
     template <int i> __device__ void load(int kt) { v[i] = ldg16(p + roff(row[i], ld) + kt * KS); }
-    template <int i> __device__ void store(char* tile) { sts16(tile + G::lds(i), v[i]); }
+    template <int i, bool TAIL> __device__ void store(char* tile) { sts16(tile + G::lds(i), v[i]); }
 };
 
 // KC rows row0 + r (r < rows, else row0) of a dense row-major matrix, K split
@@ -485,7 +489,7 @@ struct DenseKC2 {
         r = r < rows ? r : 0;
         v[i] = ldg16(p0 + roff(r, ld) + kt * KS + (kt < kst ? 0 : d01));
     }
-    template <int i> __device__ void store(char* tile) { sts16(tile + G::lds(i), v[i]); }
+    template <int i, bool TAIL> __device__ void store(char* tile) { sts16(tile + G::lds(i), v[i]); }
 };
 
 // MC tile of a dense row-major [K][ncols] matrix, columns col0.. (clamped)
@@ -508,7 +512,7 @@ struct DenseMC {
     template <int i> __device__ void load(int kt) {
         v[i] = ldg16(p + roff(kt * KS + (G::krow(i) - G::krow(0)), ld));
     }
-    template <int i> __device__ void store(char* tile) { sts16(tile + G::lds(i), v[i]); }
+    template <int i, bool TAIL> __device__ void store(char* tile) { sts16(tile + G::lds(i), v[i]); }
 };
 
 // MC tile of a [K][ncols] matrix whose K rows come from two row ranges of one
@@ -538,7 +542,7 @@ struct SplitRowsMC {
         k = k < nrows ? k : nrows - 1;
         v[i] = ldg16(base + roff(k, ld));
     }
-    template <int i> __device__ void store(char* tile) { sts16(tile + G::lds(i), v[i]); }
+    template <int i, bool TAIL> __device__ void store(char* tile) { sts16(tile + G::lds(i), v[i]); }
 };
 
 // ---- loaders whose K is the slot dimension of one expert (weight gradients) ----
@@ -598,9 +602,10 @@ struct GatherMC {
         v[i] = ldg16(base + roff(nidx[i], ld));
         nidx[i] = row_index(kr(i, kt + 1));
     }
-    template <int i> __device__ void store(char* tile) {
+    template <int i, bool TAIL> __device__ void store(char* tile) {
         const u32x4 z = {0u, 0u, 0u, 0u};
-        sts16(tile + G::lds(i), (zmask >> i) & 1 ? z : v[i]);
+        if constexpr (TAIL) sts16(tile + G::lds(i), (zmask >> i) & 1 ? z : v[i]);
+        else sts16(tile + G::lds(i), v[i]);
     }
 };
 
@@ -632,9 +637,10 @@ struct SlotMC {
         k = past ? cnt - 1 : k;
         v[i] = ldg16(base + roff(k, ld));
     }
-    template <int i> __device__ void store(char* tile) {
+    template <int i, bool TAIL> __device__ void store(char* tile) {
         const u32x4 z = {0u, 0u, 0u, 0u};
-        sts16(tile + G::lds(i), (zmask >> i) & 1 ? z : v[i]);
+        if constexpr (TAIL) sts16(tile + G::lds(i), (zmask >> i) & 1 ? z : v[i]);
+        else sts16(tile + G::lds(i), v[i]);
     }
 };
 
