@@ -303,28 +303,31 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
     rs::Acc<C> acc;
     rs::mainloop<C>(la, lb, nl, d / rs::KS, lds, acc);
     // ---- epilogue, one round per fragment row-block (64 rows of the tile) ----
-    // The A and B rows of the round come into LDS by DMA (1 KB copies, many in
-    // flight); every lane reads its values there, writes dA and dB back in
-    // place, and the rows then leave LDS as whole 512-byte runs. g*h goes out
-    // straight from registers, 16 bytes per lane (staging it through LDS as
-    // well took two more barriers per round and spilled registers: 4% slower).
-    // 16-byte chunks are XOR-swizzled by row, so the fragment-ordered LDS
-    // accesses (32 rows, one column) are conflict-free.
+    // The A and B rows of a round come into LDS by DMA (1 KB copies, many in
+    // flight), two LDS buffers deep: the copies of round i+1 are issued as
+    // round i starts and land while round i is computed and stored. Every
+    // lane reads its values in LDS, writes dA and dB back in place, and the
+    // rows then leave LDS as whole 512-byte runs. g*h goes out straight from
+    // registers, 16 bytes per lane (staging it through LDS as well took two
+    // more barriers per round and spilled registers: 4% slower). 16-byte
+    // chunks are XOR-swizzled by row, so the fragment-ordered LDS accesses
+    // (32 rows, one column) are conflict-free.
     constexpr int RR = C::WM * 32;       // rows per round
     constexpr int RB = C::BN * 2;        // bytes per row
     constexpr int CPR = RB / 16;         // 16-byte chunks per row (32)
     constexpr int ARR = RR * RB;         // bytes of one array in LDS
     constexpr int NARR = ACT == ACT_SWIGLU ? 2 : 1;   // A, B or A alone
-    static_assert(CPR == 32 && 2 * ARR <= C::LDS, "G4 staging layout");
+    constexpr int BUF = 2 * ARR;         // one round's buffer (A and B)
+    static_assert(CPR == 32 && 2 * BUF <= C::LDS, "G4 staging layout");
     const WaveCoord<C> wc;
     const int nparts = NT * C::WN;
     const int pidx = (t.n0 / C::BN) * C::WN + wc.wn;
     const uint32_t lds_base = lds_offset(lds);
     const int wv = wave_id();
     auto tile_row = [&](int rr, int i) { return (rr / 32) * C::WTM + i * 32 + (rr & 31); };
-#pragma unroll
-    for (int i = 0; i < C::FM; ++i) {
-        // DMA the round's A and B rows: copy q covers rows 2q', 2q'+1 of array q / (ARR/1024)
+    // DMA round i's A and B rows into buffer i & 1: copy q covers rows 2q',
+    // 2q'+1 of array q / (ARR/1024)
+    auto issue_round = [&](int i) {
 #pragma unroll
         for (int c = 0; c < NARR * ARR / 1024 / C::NW; ++c) {
             const int q = wv + c * C::NW;
@@ -336,18 +339,27 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
             int n = t.n0 + lc * 8;
             n = n < f ? n : f - 8;
             const bf16_t* src = (arr ? B : A) + ((int64_t)t.off + t.m0 + m) * f + n;
-            dma16(src, lds_base + arr * ARR + qq * 1024);
+            dma16(src, lds_base + (i & 1) * BUF + arr * ARR + qq * 1024);
         }
+    };
+    issue_round(0);
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i) {
+        // round i's rows have landed (and round i-1's stores have completed);
+        // buffer (i+1) & 1 was last read by round i-1's stores, before its
+        // closing barrier
         wait_vmcnt<0>();
         barrier_only();
+        if (i + 1 < C::FM) issue_round(i + 1);
+        char* const buf = lds + (i & 1) * BUF;
         // this lane's row of the round and its gate
         const int rr = wc.wm * 32 + (wc.lane & 31);
         const int m = wc.row(i);
         const bool valid = m < t.mrows;
         const int64_t s = (int64_t)t.off + t.m0 + (valid ? m : 0);
         const float g = gates[slot_src[s]];
-        char* rowA = lds + rr * RB;
-        char* rowB = lds + ARR + rr * RB;
+        char* rowA = buf + rr * RB;
+        char* rowB = buf + ARR + rr * RB;
         float dg = 0.f;
         uint4 hgv[C::FN][2];
 #pragma unroll
@@ -397,7 +409,7 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
                 const int r2 = (cid / CPR) % RR, pc = cid % CPR;
                 const int mm = tile_row(r2, i);
                 const int n = t.n0 + ((pc ^ (r2 & 31)) << 3);
-                const uint4 v = *reinterpret_cast<const uint4*>(lds + arr * ARR + r2 * RB + pc * 16);
+                const uint4 v = *reinterpret_cast<const uint4*>(buf + arr * ARR + r2 * RB + pc * 16);
                 if (mm < t.mrows && n < f) st16_nt(dst[arr] + ((int64_t)t.off + t.m0 + mm) * f + n, v);
             }
         };
