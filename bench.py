@@ -344,6 +344,7 @@ def kernel_model(name, cfg, elem, recompute=False):
         "combine": 2 * (S * d * elem + T * d * elem + T * k * 8),   # forward and backward
         "dgate_reduce": S * nparts * 4 + S * 8,
         "slot_gates": S * 12,
+        "expert_ranks": E * 4 + E * 16,
         "rb_dlogits": T * E * 4 * 2 + T * k * 12,
         "rb_dx": T * E * 4 + E * d * elem + 2 * T * d * elem,
         "rb_dwg_partial": T * E * 4 + T * d * elem,
@@ -831,7 +832,7 @@ def main():
     # per-stage kernel time (ms per step); the router's two stages are the part
     # a sparse-to-sparse timing leaves out
     stage_of = {"route": ("route_",), "build": ("tile_",), "ffn_fwd": ("g1_", "g2_", "g2h_", "f32_g1", "f32_g2"),
-                "combine": ("combine",), "ffn_bwd": ("g3_", "g3h_", "g4_", "g5_", "g6_", "dgate", "slot_gates", "f32_g3",
+                "combine": ("combine",), "ffn_bwd": ("g3_", "g3h_", "g4_", "g5_", "g6_", "dgate", "slot_gates", "expert_ranks", "f32_g3",
                                                       "f32_g4", "f32_g5", "f32_g6"),
                 "route_bwd": ("rb_",)}
     stages = {st: round(sum(v["ms_per_step"] for n, v in kernels.items()

@@ -214,7 +214,9 @@ int moe_combine(const void* src, const float* weights, const int32_t* token_inde
  *      (overwritten, zero for experts with no tokens; with MOE_ACCUMULATE_DW
  *      added to); d_gates [T,k] float32; dX_slot [T*k, d].
  * workspace: moe_ffn_bwd_workspace_size(T,d,f,E,k,flags) bytes (gate-gradient
- *      partial sums and g*h for the dw2 GEMM; 0 in MOE_F32 mode).
+ *      partial sums, g*h for the dw2 GEMM, and the experts ordered by token
+ *      count, which the weight-gradient GEMMs take longest first; 0 in
+ *      MOE_F32 mode).
  */
 size_t moe_ffn_bwd_workspace_size(int64_t T, int d, int f, int E, int k, unsigned flags);
 int moe_ffn_bwd(const void* dy, const void* x, const void* w1, const void* w3, const void* w2,

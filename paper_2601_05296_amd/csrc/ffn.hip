@@ -447,17 +447,17 @@ __device__ __forceinline__ void st_dw(float* p, const f32x4& v, int add) {
 // G3: dW2[e] = sum_s HG[s]^T dY[eti[s]]   (M = f, N = d, K = slots of e)
 __global__ void __launch_bounds__(RS::THREADS)
 g3_kernel(const bf16_t* __restrict__ HG, const bf16_t* __restrict__ dy,
-          const int32_t* __restrict__ offsets, const int32_t* __restrict__ eti, int d, int f,
+          const ExpertRank* __restrict__ rank, const int32_t* __restrict__ eti, int d, int f,
           int add, float* __restrict__ dw2) {
     extern __shared__ __align__(16) char lds[];
     using C = RS;
     const int MT = (f + C::BM - 1) / C::BM, NT = (d + C::BN - 1) / C::BN;
-    int e, mt, nt;
-    if (!wgrad_tile(blockIdx.x, MT, NT, e, mt, nt)) return;
+    ExpertRank er;
+    int mt, nt;
+    if (!wgrad_tile(rank, blockIdx.x, MT, NT, er, mt, nt)) return;
+    const int e = er.e, off = er.off, cnt = er.cnt;
     const int m0 = mt * C::BM;
     const int n0 = nt * C::BN;
-    const int off = offsets[e];
-    const int cnt = offsets[e + 1] - off;
     rs::SlotMC<C, C::BM> la;
     rs::GatherMC<C, C::BN> lb;
     rs::NoLoader nl;
@@ -542,17 +542,17 @@ template <int ACT>
 __global__ void __launch_bounds__(RHW::THREADS)
 g3h_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B,
            const float* __restrict__ gs, const bf16_t* __restrict__ dy,
-           const int32_t* __restrict__ offsets, const int32_t* __restrict__ eti, int d, int f,
+           const ExpertRank* __restrict__ rank, const int32_t* __restrict__ eti, int d, int f,
            int add, float* __restrict__ dw2) {
     extern __shared__ __align__(16) char lds[];
     using C = RHW;
     const int MT = (f + C::BM - 1) / C::BM, NT = (d + C::BN - 1) / C::BN;
-    int e, mt, nt;
-    if (!wgrad_tile(blockIdx.x, MT, NT, e, mt, nt)) return;
+    ExpertRank er;
+    int mt, nt;
+    if (!wgrad_tile(rank, blockIdx.x, MT, NT, er, mt, nt)) return;
+    const int e = er.e, off = er.off, cnt = er.cnt;
     const int m0 = mt * C::BM;
     const int n0 = nt * C::BN;
-    const int off = offsets[e];
-    const int cnt = offsets[e + 1] - off;
     GHMC<ACT, C, C::BM> la;
     rs::GatherMC<C, C::BN> lb;
     rs::NoLoader nl;
@@ -574,18 +574,18 @@ g3h_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B,
 template <int ACT>
 __global__ void __launch_bounds__(RD::THREADS)
 g5_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ dA,
-          const bf16_t* __restrict__ dB, const int32_t* __restrict__ offsets,
+          const bf16_t* __restrict__ dB, const ExpertRank* __restrict__ rank,
           const int32_t* __restrict__ eti, int d, int f, int add, float* __restrict__ dw1,
           float* __restrict__ dw3) {
     extern __shared__ __align__(16) char lds[];
     using C = CFirst<ACT>;
     const int MT = (d + C::BM - 1) / C::BM, NT = (f + C::BN - 1) / C::BN;
-    int e, mt, nt;
-    if (!wgrad_tile(blockIdx.x, MT, NT, e, mt, nt)) return;
+    ExpertRank er;
+    int mt, nt;
+    if (!wgrad_tile(rank, blockIdx.x, MT, NT, er, mt, nt)) return;
+    const int e = er.e, off = er.off, cnt = er.cnt;
     const int m0 = mt * C::BM;
     const int n0 = nt * C::BN;
-    const int off = offsets[e];
-    const int cnt = offsets[e + 1] - off;
     rs::GatherMC<C, C::BM> la;
     rs::SlotMC<C, C::BN> lb0;
     std::conditional_t<ACT == ACT_SWIGLU, rs::SlotMC<C, C::BN>, rs::NoLoader> lb1;
@@ -644,6 +644,26 @@ g6_kernel(const bf16_t* __restrict__ dA, const bf16_t* __restrict__ dB,
             }
         }
     }
+}
+
+// rank[r] = (expert, first slot, slot count) of the expert of rank r by slot
+// count, descending, ties to the lower index: the order in which the
+// weight-gradient GEMMs take the experts (wgrad_tile). One workgroup, one
+// thread per expert.
+__global__ void __launch_bounds__(256)
+expert_ranks(const int32_t* __restrict__ offsets, int E, ExpertRank* __restrict__ rank) {
+    __shared__ int cnt[256];
+    const int t = threadIdx.x;
+    if (t < E) cnt[t] = offsets[t + 1] - offsets[t];
+    __syncthreads();
+    if (t >= E) return;
+    const int c = cnt[t];
+    int r = 0;
+    for (int u = 0; u < E; ++u) {
+        const int cu = cnt[u];
+        r += (cu > c) | ((cu == c) & (u < t));
+    }
+    rank[r] = ExpertRank{t, offsets[t], c, 0};
 }
 
 // d_gates[slot_src[s]] = sum of the G4 partials of slot s (fixed order)
@@ -983,10 +1003,8 @@ hipError_t ffn_fwd(const FfnArgs& a, bool f32, hipStream_t st) {
     }
 }
 
-size_t ffn_bwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool combined,
-                         bool h_on_load) {
-    const size_t S = (size_t)T * k;
-    if (f32) return combined ? align256(S * d * sizeof(float)) : 0;  // dX_slot
+// bytes of the backward workspace before the expert rank table
+inline size_t bwd_main_bytes(size_t S, int d, int f, int E, bool combined, bool h_on_load) {
     const size_t part = align256(S * g4_nparts(f) * sizeof(float));  // d_gate partials
     const size_t strip = combined ? S * bwd_strip(S, E, d) * sizeof(bf16_t) : 0;
     if (h_on_load) {   // slot-ordered gates for G3, then (same space) the dX strip
@@ -995,6 +1013,13 @@ size_t ffn_bwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool c
     }
     const size_t hg = S * f * sizeof(bf16_t);                         // g*h, then dX strips
     return part + align256(hg > strip ? hg : strip);
+}
+
+size_t ffn_bwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool combined,
+                         bool h_on_load) {
+    const size_t S = (size_t)T * k;
+    if (f32) return combined ? align256(S * d * sizeof(float)) : 0;  // dX_slot
+    return bwd_main_bytes(S, d, f, E, combined, h_on_load) + align256(E * sizeof(ExpertRank));
 }
 
 namespace {
@@ -1036,6 +1061,10 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
     float* gs = a.h_on_load ? reinterpret_cast<float*>(ws2) : nullptr;
     bf16_t* HG = a.h_on_load ? nullptr : reinterpret_cast<bf16_t*>(ws2);
     bf16_t* strip = reinterpret_cast<bf16_t*>(ws2);
+    ExpertRank* rank = reinterpret_cast<ExpertRank*>(
+        static_cast<char*>(a.ws) + bwd_main_bytes(S, a.d, a.f, a.E, a.y != nullptr, a.h_on_load));
+    hipLaunchKernelGGL(expert_ranks, dim3(1), dim3(256), 0, st, a.offsets, a.E, rank);
+    probe::mark("expert_ranks", st);
     // non-gated: the second operand of the two-branch kernels is the first again
     const void* Bx = GATED ? a.B : a.A;
     const void* w3x = GATED ? a.w3 : a.w1;
@@ -1045,7 +1074,7 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
         probe::mark("slot_gates", st);
         hipLaunchKernelGGL(g3h_kernel<ACT>, dim3(wgrad_grid(a.E, cdiv(a.f, C3H::BM), cdiv(a.d, C3H::BN))),
                            dim3(C3H::THREADS), C3H::LDS, st, (const bf16_t*)a.A,
-                           (const bf16_t*)Bx, (const float*)gs, (const bf16_t*)a.dy, a.offsets,
+                           (const bf16_t*)Bx, (const float*)gs, (const bf16_t*)a.dy, rank,
                            a.eti, a.d, a.f, (int)a.accumulate_dw, a.dw2);
         probe::mark("g3h_kernel", st);
     }
@@ -1061,12 +1090,12 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
     if (!a.h_on_load) {
         hipLaunchKernelGGL(g3_kernel, dim3(wgrad_grid(a.E, cdiv(a.f, RS::BM), cdiv(a.d, RS::BN))),
                            dim3(RS::THREADS), RS::LDS, st, (const bf16_t*)HG, (const bf16_t*)a.dy,
-                           a.offsets, a.eti, a.d, a.f, (int)a.accumulate_dw, a.dw2);
+                           rank, a.eti, a.d, a.f, (int)a.accumulate_dw, a.dw2);
         probe::mark("g3_kernel", st);
     }
     hipLaunchKernelGGL(g5_kernel<ACT>, dim3(wgrad_grid(a.E, cdiv(a.d, C5::BM), cdiv(a.f, C5::BN))),
                        dim3(C5::THREADS), C5::LDS, st, (const bf16_t*)a.x, (const bf16_t*)a.A,
-                       (const bf16_t*)a.B, a.offsets, a.eti, a.d, a.f, (int)a.accumulate_dw,
+                       (const bf16_t*)a.B, rank, a.eti, a.d, a.f, (int)a.accumulate_dw,
                        a.dw1, a.dw3);
     probe::mark("g5_kernel", st);
     const int kslices = (GATED ? 2 : 1) * a.f / rs::KS;

@@ -173,23 +173,32 @@ struct RowStage {
 
 // ---- weight-gradient tile order ---------------------------------------------------------
 // The weight-gradient GEMMs have P = MT*NT output tiles per expert, each looping
-// over the expert's tokens. Workgroup ids are dealt round-robin to the 8 XCDs
-// (each with its own L2). Every XCD takes, for every expert, one band of
-// ceil(P/8) consecutive tiles, so that every XCD gets the same share of every
-// expert whatever the experts' token counts. Inside an expert the tiles come in
-// groups of WG_GM row tiles with the column tile slower: the ~32 workgroups
-// an XCD runs at once then cover a WG_GM x 8 block of tiles, which read
-// WG_GM + 8 operand panels per K slice from L2 instead of the 1 + 32 of a
-// row-major band (an expert's last, narrower group holds its remaining rows).
-// Returns false for the padding tiles of the last band.
+// over the expert's tokens, so a tile's length is its expert's token count.
+// Workgroup ids are dealt round-robin to the 8 XCDs (each with its own L2).
+// Every XCD takes, for every expert, one band of ceil(P/8) consecutive tiles,
+// so that every XCD gets the same share of every expert whatever the experts'
+// token counts. The experts are taken longest first: rank[r] holds the expert
+// of rank r by token count (descending, ties to the lower index), its first
+// slot and its count (expert_ranks). Under a skewed routing the longest tiles
+// then start first and the many short ones fill in around them, instead of a
+// late start of the longest tiles setting the kernel's end. Inside an expert
+// the tiles are grouped WG_GM row tiles at a time with the column tile slower:
+// the ~32 workgroups an XCD runs at once then cover a WG_GM x 8 block of
+// tiles, which read WG_GM + 8 operand panels per K slice from L2 instead of
+// the 1 + 32 of a row-major band (an expert's last, narrower group holds its
+// remaining rows). Returns false for the padding tiles of the last band.
 constexpr int WG_GM = 4;
-__device__ __forceinline__ bool wgrad_tile(int bid, int MT, int NT, int& e, int& mt, int& nt) {
+struct ExpertRank {
+    int32_t e, off, cnt, pad;
+};
+__device__ __forceinline__ bool wgrad_tile(const ExpertRank* __restrict__ rank, int bid, int MT,
+                                           int NT, ExpertRank& er, int& mt, int& nt) {
     const int P = MT * NT;
     const int G = (P + 7) >> 3;
     const int x = bid & 7, j = bid >> 3;
-    e = j / G;
     const int lt = x * G + j % G;
     if (lt >= P) return false;
+    er = rank[j / G];
     const int grp = lt / (WG_GM * NT);
     const int m_base = grp * WG_GM;
     const int gm = min(WG_GM, MT - m_base);
