@@ -54,6 +54,21 @@ __device__ __forceinline__ uint4 pack8(const float (&o)[8]) {
     return v;
 }
 
+// Inclusive prefix sum over the 64 lanes of a wave, by DPP lane moves: a
+// Hillis-Steele scan inside each row of 16 lanes (row_shr 1, 2, 4, 8; a lane
+// whose source lies before its row's start adds 0), then the last lane of row
+// 0 and of row 2 added into rows 1 and 3 (row_bcast:15, row mask 0b1010) and
+// the last lane of row 1 into rows 2 and 3 (row_bcast:31, row mask 0b1100).
+__device__ __forceinline__ int wave_incl_scan(int v) {
+    v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);   // row_shr:1
+    v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);   // row_shr:2
+    v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);   // row_shr:4
+    v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);   // row_shr:8
+    v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);   // row_bcast:15
+    v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);   // row_bcast:31
+    return v;
+}
+
 // ---- activation -------------------------------------------------------------
 // logistic function with the hardware reciprocal (v_rcp_f32, about 1 ulp)
 // instead of a correctly rounded divide, which takes some ten instructions

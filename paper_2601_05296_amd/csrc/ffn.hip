@@ -99,7 +99,8 @@ g1_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w1,
     using C = CFirst<ACT>;
     SlotTile t;
     const int NT = (f + C::BN - 1) / C::BN;
-    if (!find_slot_tile<C::THREADS>(offsets, E, C::BM, NT, xcd_remap(blockIdx.x, gridDim.x), C::BN,
+    if (!find_slot_tile<C::THREADS>(reinterpret_cast<int*>(lds), offsets, E, C::BM, NT,
+                                    xcd_remap(blockIdx.x, gridDim.x), C::BN,
                                     t, RASTER_GM))
         return;
     rs::GatherKC<C, C::BM> la;
@@ -158,7 +159,8 @@ g2_kernel(const bf16_t* __restrict__ H, const bf16_t* __restrict__ w2,
     using C = RS;
     SlotTile t;
     const int NT = (ncols + C::BN - 1) / C::BN;
-    if (!find_slot_tile<C::THREADS>(offsets, E, C::BM, NT, xcd_remap(blockIdx.x, gridDim.x), C::BN,
+    if (!find_slot_tile<C::THREADS>(reinterpret_cast<int*>(lds), offsets, E, C::BM, NT,
+                                    xcd_remap(blockIdx.x, gridDim.x), C::BN,
                                     t, RASTER_GM))
         return;
     rs::DenseKC2<C, C::BM> la;
@@ -248,7 +250,7 @@ g2h_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B,
     using C = RHW;
     SlotTile t;
     const int NT = (ncols + C::BN - 1) / C::BN;
-    if (!rs::find_slot_tile<C::THREADS>(reinterpret_cast<int*>(lds), offsets, E, C::BM, NT,
+    if (!find_slot_tile<C::THREADS>(reinterpret_cast<int*>(lds), offsets, E, C::BM, NT,
                                         xcd_remap(blockIdx.x, gridDim.x), C::BN, t, RASTER_GM))
         return;
     HKC<ACT, C, C::BM> la;
@@ -291,7 +293,8 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
     using C = RS;
     SlotTile t;
     const int NT = (f + C::BN - 1) / C::BN;
-    if (!find_slot_tile<C::THREADS>(offsets, E, C::BM, NT, xcd_remap(blockIdx.x, gridDim.x), C::BN,
+    if (!find_slot_tile<C::THREADS>(reinterpret_cast<int*>(lds), offsets, E, C::BM, NT,
+                                    xcd_remap(blockIdx.x, gridDim.x), C::BN,
                                     t, RASTER_GM))
         return;
     rs::GatherKC<C, C::BM> la;
@@ -616,7 +619,8 @@ g6_kernel(const bf16_t* __restrict__ dA, const bf16_t* __restrict__ dB,
     using C = RS;
     SlotTile t;
     const int NT = (ncols + C::BN - 1) / C::BN;
-    if (!find_slot_tile<C::THREADS>(offsets, E, C::BM, NT, xcd_remap(blockIdx.x, gridDim.x), C::BN,
+    if (!find_slot_tile<C::THREADS>(reinterpret_cast<int*>(lds), offsets, E, C::BM, NT,
+                                    xcd_remap(blockIdx.x, gridDim.x), C::BN,
                                     t, RASTER_GM))
         return;
     rs::DenseKC2<C, C::BM> la;

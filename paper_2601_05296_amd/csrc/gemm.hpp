@@ -216,8 +216,9 @@ inline int wgrad_grid(int E, int MT, int NT) { return E * 8 * ((MT * NT + 7) / 8
 // inside a group: the workgroups that run at the same time on one XCD then
 // cover a GM x (32 / GM) block of tiles, which share both their row panels
 // and their weight panels in that XCD's L2 (an expert's last, narrower group
-// holds its remaining M tiles).
-// Every thread of the block must call this. Returns false past the last tile.
+// holds its remaining M tiles). Every thread of the block must call this;
+// `sh` is 8 ints of LDS, free on entry and again on return. Returns false past
+// the last tile.
 struct SlotTile {
     int e;       // expert
     int m0;      // first row inside the expert's slot segment
@@ -227,36 +228,34 @@ struct SlotTile {
 };
 
 template <int THREADS>
-__device__ bool find_slot_tile(const int32_t* __restrict__ offsets, int E, int BM, int NT,
+__device__ bool find_slot_tile(int* sh, const int32_t* __restrict__ offsets, int E, int BM, int NT,
                                int bid, int BN, SlotTile& t, int GM = 0) {
     static_assert(THREADS >= 256, "one thread per expert");
-    __shared__ int s_scan[THREADS];
-    __shared__ int s_res[2];
-    const int tid = threadIdx.x;
-    int tiles = 0;
+    const int tid = threadIdx.x, lane = tid & (WAVE - 1), wv = tid / WAVE;
+    int tiles = 0, cnt = 0, off = 0;
     if (tid < E) {
-        const int cnt = offsets[tid + 1] - offsets[tid];
+        off = offsets[tid];
+        cnt = offsets[tid + 1] - off;
         tiles = ((cnt + BM - 1) / BM) * NT;
     }
-    s_scan[tid] = tiles;
-    if (tid == 0) { s_res[0] = -1; s_res[1] = 0; }
+    // expert e's tiles are [start, end): a wave-level scan, plus the totals of
+    // the waves before (E <= 256: four waves)
+    const int inc = wave_incl_scan(tiles);
+    if (wv < 4 && lane == WAVE - 1) sh[wv] = inc;
+    if (tid == 0) sh[4] = -1;
     __syncthreads();
-    for (int o = 1; o < THREADS; o <<= 1) {
-        const int v = tid >= o ? s_scan[tid - o] : 0;
-        __syncthreads();
-        s_scan[tid] += v;
-        __syncthreads();
-    }
     if (tid < E) {
-        const int end = s_scan[tid];
+        int end = inc;
+        for (int w = 0; w < wv; ++w) end += sh[w];
         const int start = end - tiles;
-        if (bid >= start && bid < end) { s_res[0] = tid; s_res[1] = bid - start; }
+        if (bid >= start && bid < end) { sh[4] = tid; sh[5] = bid - start; sh[6] = off; sh[7] = cnt; }
     }
     __syncthreads();
-    const int e = s_res[0];
+    const int e = sh[4], local = sh[5];
+    off = sh[6];
+    cnt = sh[7];
+    __syncthreads();
     if (e < 0) return false;
-    const int local = s_res[1];
-    const int cnt = offsets[e + 1] - offsets[e];
     const int nmt = (cnt + BM - 1) / BM;
     const int gm = GM > 0 ? GM : nmt;         // M tiles per group
     const int full = nmt / gm * gm;           // M tiles in whole groups
@@ -271,7 +270,7 @@ __device__ bool find_slot_tile(const int32_t* __restrict__ offsets, int E, int B
         nt = l2 / rem;
     }
     t.e = e;
-    t.off = offsets[e];
+    t.off = off;
     t.m0 = mt * BM;
     t.mrows = min(BM, cnt - t.m0);
     t.n0 = nt * BN;

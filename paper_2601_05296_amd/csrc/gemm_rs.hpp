@@ -644,62 +644,6 @@ struct SlotMC {
     }
 };
 
-// ---- grouped tile lookup (row-wise GEMMs) ------------------------------------------
-// As moe::find_slot_tile (gemm.hpp), with its scan in `scan` (THREADS + 2 ints
-// of the dynamic LDS) instead of static LDS, so that a kernel can give the
-// main loop all 160 KB. Ends with a barrier: the LDS is free again on return.
-template <int THREADS>
-__device__ bool find_slot_tile(int* scan, const int32_t* __restrict__ offsets, int E, int BM,
-                               int NT, int bid, int BN, SlotTile& t, int GM) {
-    static_assert(THREADS >= 256, "one thread per expert");
-    int* s_res = scan + THREADS;
-    const int tid = threadIdx.x;
-    int tiles = 0;
-    if (tid < E) {
-        const int cnt = offsets[tid + 1] - offsets[tid];
-        tiles = ((cnt + BM - 1) / BM) * NT;
-    }
-    scan[tid] = tiles;
-    if (tid == 0) { s_res[0] = -1; s_res[1] = 0; }
-    __syncthreads();
-    for (int o = 1; o < THREADS; o <<= 1) {
-        const int v = tid >= o ? scan[tid - o] : 0;
-        __syncthreads();
-        scan[tid] += v;
-        __syncthreads();
-    }
-    if (tid < E) {
-        const int end = scan[tid];
-        const int start = end - tiles;
-        if (bid >= start && bid < end) { s_res[0] = tid; s_res[1] = bid - start; }
-    }
-    __syncthreads();
-    const int e = s_res[0];
-    const int local = s_res[1];
-    __syncthreads();
-    if (e < 0) return false;
-    const int cnt = offsets[e + 1] - offsets[e];
-    const int nmt = (cnt + BM - 1) / BM;
-    const int gm = GM > 0 ? GM : nmt;
-    const int full = nmt / gm * gm;
-    int mt, nt;
-    if (local < full * NT) {
-        const int g = local / (gm * NT), w = local % (gm * NT);
-        mt = g * gm + w % gm;
-        nt = w / gm;
-    } else {
-        const int rem = nmt - full, l2 = local - full * NT;
-        mt = full + l2 % rem;
-        nt = l2 / rem;
-    }
-    t.e = e;
-    t.off = offsets[e];
-    t.m0 = mt * BM;
-    t.mrows = min(BM, cnt - t.m0);
-    t.n0 = nt * BN;
-    return true;
-}
-
 // slices of a K extent of cnt rows
 __device__ __forceinline__ int slices(int cnt) { return (cnt + KS - 1) / KS; }
 
