@@ -784,12 +784,16 @@ def main():
 
     # timed region: K whole steps, per-kernel events recorded on the stream
     B.moe_probe_enable(2 * per_step_records * args.steps + 64)
+    bounds = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    bounds[0].record()
+    for i in range(args.steps):
         step()
+        bounds[i + 1].record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    step_ms = [bounds[i].elapsed_time(bounds[i + 1]) for i in range(args.steps)]
     dropped = B.moe_probe_dropped()
     recs = [B.moe_probe_get(i) for i in range(B.moe_probe_count())]
     B.moe_probe_disable()
@@ -846,6 +850,10 @@ def main():
         "metric": "MoE layer fwd+bwd tokens/sec + peak activation bytes/token, 1 MI355X",
         "value": round(tokens_per_s, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
+        # per-step device times from events between the steps (the mean above is
+        # the host clock over the whole timed region)
+        "ms_per_step_median": round(float(np.median(step_ms)), 4),
+        "ms_per_step_min_max": [round(min(step_ms), 4), round(max(step_ms), 4)],
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": cfg.name, "T": T, "d": d, "f": f, "E": E, "k": k,
                    "renorm": cfg.renorm, "zipf_s": cfg.zipf_s, "act": cfg.act,
