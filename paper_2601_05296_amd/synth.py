@@ -21,21 +21,28 @@ bias, perm, so that changing one tensor's size never changes another's values.
 
 For the skewed many-small-experts workload a per-expert bias is added to the
 router logits before the softmax. Expert ``e`` has popularity rank ``r(e)``
-(a seeded permutation) and bias ``-s * c * log(r(e))`` with ``s = 1.2`` and
-``c = sigma * sqrt(6) / pi``, where ``sigma = 0.02 * sqrt(d)`` is the standard
-deviation of one router logit. With Gumbel noise of that scale, top-k selection
-would be Plackett-Luce sampling with weights ``r**-s`` (Zipf(s)); the Gaussian
-router noise makes the shares Zipf-like rather than exact. The popular head is
-capped at T tokens per expert by top-k itself.
+(a seeded permutation). The target loads are Zipf(1.2) shares of the T*k
+choices water-filled at 1/k (``zipf_targets``: an expert takes every token at
+most once, so the two most popular experts saturate at T and the excess goes
+down the ranks). The bias that produces them is read from
+``tests/golden/zipf_bias_<workload>.txt``, written once by
+``tests/golden/make_zipf_bias.py`` (fixed-point steps on a calibration draw of
+x with its own seed). Any other shape with ``zipf_s > 0`` takes the analytic
+bias ``-s * c * log(r(e))`` with ``c = sigma * sqrt(6) / pi``, where ``sigma =
+0.02 * sqrt(d)`` is the standard deviation of one router logit: with Gumbel
+noise of that scale top-k selection would be Plackett-Luce sampling with
+weights ``r**-s``; the Gaussian router noise makes the shares Zipf-like.
 """
 from __future__ import annotations
 
 import math
+import os
 from dataclasses import dataclass, field
 
 import numpy as np
 
 DTYPES = ("f32", "bf16")
+_ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
 @dataclass(frozen=True)
@@ -132,27 +139,87 @@ def _normal(rng: np.random.Generator, shape, std: float) -> np.ndarray:
     return out
 
 
+def zipf_targets(E: int, k: int, s: float) -> np.ndarray:
+    """Zipf(s) shares of the T*k expert choices by popularity rank (rank 1
+    first), water-filled at 1/k: an expert can take at most every token once,
+    so shares above 1/k are capped there and the excess is spread over the
+    other ranks in proportion to their Zipf weights, until none exceeds the
+    cap. Returns float64 [E] summing to 1."""
+    w = np.arange(1, E + 1, dtype=np.float64) ** -s
+    cap = 1.0 / k
+    capped = np.zeros(E, dtype=bool)
+    while True:
+        free = 1.0 - cap * capped.sum()
+        share = np.where(capped, cap, free * w / w[~capped].sum())
+        over = (share > cap) & ~capped
+        if not over.any():
+            return share
+        capped |= over
+
+
+def zipf_ranks(cfg: MoEConfig) -> np.ndarray:
+    """Popularity rank (1 = most popular) of every expert: a permutation drawn
+    from the workload's own stream."""
+    ss = np.random.SeedSequence(cfg.seed)
+    s_perm = ss.spawn(8)[7]
+    return np.random.Generator(np.random.PCG64(s_perm)).permutation(cfg.E) + 1
+
+
+def calibrated_bias_path(cfg: MoEConfig) -> str:
+    return os.path.join(_ROOT, "tests", "golden", "zipf_bias_%s.txt" % cfg.name)
+
+
+def load_calibrated_bias(cfg: MoEConfig):
+    """The calibrated router bias of a named workload (float32 [E]), or None
+    when no table exists for it or the table was made for other sizes."""
+    p = calibrated_bias_path(cfg)
+    if not os.path.exists(p):
+        return None
+    head, vals = {}, []
+    for line in open(p):
+        parts = line.split()
+        if not parts:
+            continue
+        if parts[0] == "#":
+            continue
+        if parts[0] == "bias":
+            vals.append(float(parts[2]))
+        else:
+            head[parts[0]] = parts[1]
+    if (int(head.get("d", -1)), int(head.get("E", -1)), int(head.get("k", -1)),
+            float(head.get("zipf_s", -1))) != (cfg.d, cfg.E, cfg.k, cfg.zipf_s):
+        return None
+    assert len(vals) == cfg.E
+    return np.array(vals, dtype=np.float32)
+
+
 def zipf_bias(cfg: MoEConfig, rng_bias: np.random.Generator, rng_perm: np.random.Generator):
     """Per-expert router bias (float32 [E]) or None; see the module docstring."""
     if cfg.zipf_s <= 0.0 and cfg.n_dead == 0:
         return None
     E = cfg.E
     bias = np.zeros(E, dtype=np.float64)
+    rank = rng_perm.permutation(E) + 1          # rank 1 = most popular
     if cfg.zipf_s > 0.0:
-        sigma = 0.02 * math.sqrt(cfg.d)
-        c = sigma * math.sqrt(6.0) / math.pi
-        rank = rng_perm.permutation(E) + 1          # rank 1 = most popular
-        bias = -cfg.zipf_s * c * np.log(rank.astype(np.float64))
+        table = load_calibrated_bias(cfg)
+        if table is not None:
+            bias = table.astype(np.float64)
+        else:
+            sigma = 0.02 * math.sqrt(cfg.d)
+            c = sigma * math.sqrt(6.0) / math.pi
+            bias = -cfg.zipf_s * c * np.log(rank.astype(np.float64))
     if cfg.n_dead > 0:
         dead = rng_bias.choice(E, size=cfg.n_dead, replace=False)
         bias[dead] = -np.inf
     return bias.astype(np.float32)
 
 
-def make_inputs(cfg: MoEConfig, T: int | None = None, with_dy: bool = True) -> LayerInputs:
+def make_inputs(cfg: MoEConfig, T: int | None = None, with_dy: bool = True,
+                experts: bool = True) -> LayerInputs:
     """Draw one layer's inputs. ``T`` overrides the token count (the first T
     rows of x and dy are the same for every T, because each row is drawn from
-    the same stream in order)."""
+    the same stream in order). ``experts=False`` leaves out w1, w3 and w2
+    (None); the other tensors keep their values, each having its own stream."""
     T = cfg.T if T is None else T
     ss = np.random.SeedSequence(cfg.seed)
     s_x, s_g, s_w1, s_w3, s_w2, s_dy, s_bias, s_perm = ss.spawn(8)
@@ -161,11 +228,12 @@ def make_inputs(cfg: MoEConfig, T: int | None = None, with_dy: bool = True) -> L
     raw = {
         "x": _normal(rng(s_x), (T, d), 1.0),
         "w_gate": _normal(rng(s_g), (E, d), 0.02),
-        "w1": _normal(rng(s_w1), (E, d, f), 1.0 / math.sqrt(d)),
+        "w1": _normal(rng(s_w1), (E, d, f), 1.0 / math.sqrt(d)) if experts else None,
         # (the W3 stream is spawned for every expert type, so the other
         # draws do not depend on it)
-        "w3": _normal(rng(s_w3), (E, d, f), 1.0 / math.sqrt(d)) if cfg.act == "swiglu" else None,
-        "w2": _normal(rng(s_w2), (E, f, d), 1.0 / math.sqrt(f)),
+        "w3": (_normal(rng(s_w3), (E, d, f), 1.0 / math.sqrt(d))
+               if experts and cfg.act == "swiglu" else None),
+        "w2": _normal(rng(s_w2), (E, f, d), 1.0 / math.sqrt(f)) if experts else None,
     }
     if with_dy:
         raw["dy"] = _normal(rng(s_dy), (T, d), 1.0)
