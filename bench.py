@@ -635,7 +635,16 @@ def cpu_oracle_baseline(inp, cfg, budget_s):
     n = int(min(cfg.T, max(n1, min((budget_s - a) / b, 2.0 * n_prop))))
     t = run(n)
     cores = oracle.threads()
-    return {"value": n / t, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+    cpu = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    cpu = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"value": n / t, "unit": "tokens/s", "cores": cores, "kind": "oracle", "cpu": cpu,
             "sample": "first %d of %d tokens of %s, whole-layer fwd+bwd in fp64 "
                       "(%.1f s; calibration runs of %d and %d tokens, %.1f s, not counted)"
                       % (n, cfg.T, cfg.name, t, n0, n1, t0 + t1)}
