@@ -50,6 +50,13 @@ def parse():
     ap.add_argument("--h-on-load", dest="h_on_load", action="store_true",
                     help="form h and g*h on load, no SwiGLU intermediate in HBM (the default)")
     ap.set_defaults(h_on_load=True)
+    ap.add_argument("--atomic-combine", dest="atomic_combine", action="store_true",
+                    help="fold the combine into the epilogues of the second GEMM and the dX GEMM "
+                         "(MOE_ATOMIC_COMBINE: packed-bf16 atomic adds into y and dx, no strips); "
+                         "default: only where that is deterministic (k <= 2)")
+    ap.add_argument("--strip-combine", dest="atomic_combine", action="store_false",
+                    help="combine strip by strip with the ordered gather-reduce")
+    ap.set_defaults(atomic_combine=None)
     ap.add_argument("--recompute", action="store_true",
                     help="full-recompute checkpoint policy: save only the routing decision; the "
                          "dispatch and the expert FFN run over token chunks, and the backward "
@@ -214,6 +221,8 @@ def summarize_sweep(json_path, out, cmd, profile_cmd):
               if res.get("recompute") else
               "h and g*h formed on load (MOE_H_ON_LOAD)" if res.get("h_on_load") else
               "h and g*h buffered between the GEMMs")
+    if res.get("atomic_combine"):
+        policy += "; combine folded into the GEMM epilogues (MOE_ATOMIC_COMBINE)"
     lines = ["# Memory-capacity sweep, workload %s (d=%d f=%d E=%d k=%d, %s), one MI355X; "
              "this path: %s" % (c.name, c.d, c.f, c.E, c.k, c.dtype, policy),
              "# run: %s" % profile_cmd,
@@ -344,6 +353,8 @@ def kernel_model(name, cfg, elem, recompute=False):
         "combine": 2 * (S * d * elem + T * d * elem + T * k * 8),   # forward and backward
         "dgate_reduce": S * nparts * 4 + S * 8,
         "slot_gates": S * 12,
+        "fwd_slot_gates": S * 12,
+        "zero_bf16": 2 * T * d * elem,   # y in the forward, dx in the backward
         "expert_ranks": E * 4 + E * 16,
         "rb_dlogits": T * E * 4 * 2 + T * k * 12,
         "rb_dx": T * E * 4 + E * d * elem + 2 * T * d * elem,
@@ -535,7 +546,7 @@ def table1_sweep(args):
     return rows
 
 
-def memory_sweep(cfg, max_doublings, h_on_load=False, recompute=False):
+def memory_sweep(cfg, max_doublings, h_on_load=False, recompute=False, atomic_combine=None):
     """Peak activation bytes per token and the largest T that fits, for this
     path (one forward + backward) and for the materialised-permutation
     baseline (forward only: its saved tensors plus forward temporaries, a
@@ -547,6 +558,8 @@ def memory_sweep(cfg, max_doublings, h_on_load=False, recompute=False):
     gen = torch.Generator(device=dev)
     gen.manual_seed(cfg.seed)
     d, f, E, k = cfg.d, cfg.f, cfg.E, cfg.k
+    if atomic_combine is None:   # the layer's default
+        atomic_combine = k <= 2
     bf = torch.bfloat16
     wg = (torch.randn((E, d), generator=gen, device=dev) * 0.02).to(bf)
     w1 = (torch.randn((E, d, f), generator=gen, device=dev) * d ** -0.5).to(bf)
@@ -571,7 +584,8 @@ def memory_sweep(cfg, max_doublings, h_on_load=False, recompute=False):
                 base = torch.cuda.memory_allocated(dev)
                 if which == "ours":
                     y, saved = layer.forward(x, wg, None, w1, w3, w2, k, cfg.renorm, act=cfg.act,
-                                             h_on_load=h_on_load, recompute=recompute)
+                                             h_on_load=h_on_load, recompute=recompute,
+                                             atomic_combine=atomic_combine)
                     sb = saved.nbytes()
                     torch.cuda.synchronize()
                     fwd_peak = torch.cuda.max_memory_allocated(dev) - base
@@ -602,7 +616,7 @@ def memory_sweep(cfg, max_doublings, h_on_load=False, recompute=False):
             break
     fits = lambda key: max([r["T"] for r in rows if key in r], default=0)
     return {"workload": cfg.name, "h_on_load": bool(h_on_load), "recompute": bool(recompute),
-            "points": rows,
+            "atomic_combine": bool(atomic_combine), "points": rows,
             "max_T_ours": fits("ours_peak_bytes_per_token"),
             "max_T_baseline_fwd": fits("baseline_fwd_peak_bytes_per_token"),
             "hbm_bytes": torch.cuda.get_device_properties(dev).total_memory}
@@ -722,7 +736,8 @@ def main():
     if args.sweep:
         from paper_2601_05296_amd import synth
         res = memory_sweep(synth.CONFIGS[args.workload], args.sweep_max_doublings,
-                           h_on_load=args.h_on_load, recompute=args.recompute)
+                           h_on_load=args.h_on_load, recompute=args.recompute,
+                           atomic_combine=args.atomic_combine)
         print(json.dumps({"sweep": res}), flush=True)
         return
     if args.gpus != 1:
@@ -753,9 +768,12 @@ def main():
     bias = up(inp.store["bias"])
     T, d, f, E, k = cfg.T, cfg.d, cfg.f, cfg.E, cfg.k
 
+    atomic = args.atomic_combine if args.atomic_combine is not None else k <= 2
+
     def step():
         y, saved = layer.forward(x, wg, bias, w1, w3, w2, k, cfg.renorm, act=cfg.act,
-                                 recompute=args.recompute, h_on_load=args.h_on_load)
+                                 recompute=args.recompute, h_on_load=args.h_on_load,
+                                 atomic_combine=atomic)
         g = layer.backward(saved, dy, x, wg, w1, w3, w2)
         return y, saved, g
 
@@ -768,7 +786,8 @@ def main():
     torch.cuda.reset_peak_memory_stats(dev)
     base = torch.cuda.memory_allocated(dev)
     y, saved = layer.forward(x, wg, bias, w1, w3, w2, k, cfg.renorm, act=cfg.act,
-                             recompute=args.recompute, h_on_load=args.h_on_load)
+                             recompute=args.recompute, h_on_load=args.h_on_load,
+                             atomic_combine=atomic)
     torch.cuda.synchronize()
     fwd_peak = torch.cuda.max_memory_allocated(dev) - base
     saved_bytes = saved.nbytes()   # before the backward (which may recompute A, B into it)
@@ -845,7 +864,7 @@ def main():
     # per-stage kernel time (ms per step); the router's two stages are the part
     # a sparse-to-sparse timing leaves out
     stage_of = {"route": ("route_",), "build": ("tile_",), "ffn_fwd": ("g1_", "g2_", "g2h_", "f32_g1", "f32_g2"),
-                "combine": ("combine",), "ffn_bwd": ("g3_", "g3h_", "g4_", "g5_", "g6_", "dgate", "slot_gates", "expert_ranks", "f32_g3",
+                "combine": ("combine", "zero_", "fwd_slot_gates"), "ffn_bwd": ("g3_", "g3h_", "g4_", "g5_", "g6_", "dgate", "slot_gates", "expert_ranks", "f32_g3",
                                                       "f32_g4", "f32_g5", "f32_g6"),
                 "route_bwd": ("rb_",)}
     stages = {st: round(sum(v["ms_per_step"] for n, v in kernels.items()
@@ -868,6 +887,7 @@ def main():
                    "renorm": cfg.renorm, "zipf_s": cfg.zipf_s, "act": cfg.act,
                    "checkpoint": "recompute" if args.recompute else "A,B",
                    "h_on_load": bool(args.h_on_load),
+                   "combine": "atomic" if atomic else "strips",
                    "parallelism": "none"},
         "peak_activation_bytes_per_token": round(peak / T, 1),
         "peak_activation_bytes_per_token_fwd_bwd": [round(fwd_peak / T, 1), round(bwd_peak / T, 1)],
@@ -889,13 +909,14 @@ def main():
         other = not args.h_on_load
         def lean_step():
             y_, s_ = layer.forward(x, wg, bias, w1, w3, w2, k, cfg.renorm, act=cfg.act,
-                                   h_on_load=other)
+                                   h_on_load=other, atomic_combine=atomic)
             return y_, s_, layer.backward(s_, dy, x, wg, w1, w3, w2)
         lean_step()
         torch.cuda.synchronize()
         torch.cuda.reset_peak_memory_stats(dev)
         b0 = torch.cuda.memory_allocated(dev)
-        y_, s_ = layer.forward(x, wg, bias, w1, w3, w2, k, cfg.renorm, act=cfg.act, h_on_load=other)
+        y_, s_ = layer.forward(x, wg, bias, w1, w3, w2, k, cfg.renorm, act=cfg.act, h_on_load=other,
+                               atomic_combine=atomic)
         torch.cuda.synchronize()
         lf = torch.cuda.max_memory_allocated(dev) - b0
         torch.cuda.reset_peak_memory_stats(dev)

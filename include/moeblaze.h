@@ -81,6 +81,21 @@ extern "C" {
  * are processed in several chunks is the sum of the chunks' gradients). Every
  * other call rejects it (MOE_ERR_INVALID_ARG). */
 #define MOE_ACCUMULATE_DW 64u
+/* moe_ffn_fwd_combine / moe_ffn_bwd_combine and their workspace queries: the
+ * combine is folded into the epilogue of the GEMM that produces the slot rows
+ * (Section 3.1: the expert outputs are reduced as they are produced). Each
+ * slot row, times its gate in the forward, is rounded to bfloat16 and added
+ * into its token's row of y (dx) by packed-bf16 atomic adds, so no [T*k, d]
+ * output nor any strip of it is held: the forward workspace drops the strip
+ * and holds T*k float32 slot gates instead, the backward's drops the strip.
+ * y (dx, unless MOE_ACCUMULATE) is cleared first. Each atomic add rounds to
+ * bfloat16, so a token's k terms are rounded k times, not once, and for k > 2
+ * (or with MOE_ACCUMULATE) the result depends on the order in which tiles
+ * finish: it is not deterministic bit for bit. With k <= 2 and no
+ * MOE_ACCUMULATE it is (bfloat16 addition of two terms onto zero does not
+ * depend on their order). bfloat16 only: with MOE_F32, MOE_ERR_UNSUPPORTED.
+ * Every other call rejects it (MOE_ERR_INVALID_ARG). */
+#define MOE_ATOMIC_COMBINE 128u
 
 /* Human-readable name of a status code (static storage). */
 const char* moe_strerror(int status);

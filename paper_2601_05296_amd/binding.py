@@ -29,6 +29,7 @@ MOE_ACT_SILU = 8
 MOE_ACT_RELU = 16
 MOE_H_ON_LOAD = 32
 MOE_ACCUMULATE_DW = 64
+MOE_ATOMIC_COMBINE = 128
 ACT_FLAG = {"swiglu": 0, "silu": MOE_ACT_SILU, "relu": MOE_ACT_RELU}
 
 # Every symbol declared in include/moeblaze.h.

@@ -33,10 +33,21 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
     } while (0)
 
 const unsigned KNOWN_FLAGS = MOE_F32 | MOE_RENORM | MOE_ACCUMULATE | MOE_ACT_SILU |
-                             MOE_ACT_RELU | MOE_H_ON_LOAD | MOE_ACCUMULATE_DW;
+                             MOE_ACT_RELU | MOE_H_ON_LOAD | MOE_ACCUMULATE_DW |
+                             MOE_ATOMIC_COMBINE;
 const unsigned ACT_FLAGS = MOE_ACT_SILU | MOE_ACT_RELU;
 // meaningful to the FFN calls only
-const unsigned FFN_ONLY = ACT_FLAGS | MOE_H_ON_LOAD | MOE_ACCUMULATE_DW;
+const unsigned FFN_ONLY = ACT_FLAGS | MOE_H_ON_LOAD | MOE_ACCUMULATE_DW | MOE_ATOMIC_COMBINE;
+
+// MOE_ATOMIC_COMBINE: combined bf16 calls only
+int check_scatter(const char* fn, bool combined, unsigned flags) {
+    if (!(flags & MOE_ATOMIC_COMBINE)) return MOE_OK;
+    if (!combined)
+        return fail(MOE_ERR_INVALID_ARG, "%s: MOE_ATOMIC_COMBINE applies to the combined calls only", fn);
+    if (flags & MOE_F32)
+        return fail(MOE_ERR_UNSUPPORTED, "%s: MOE_ATOMIC_COMBINE is bfloat16 only", fn);
+    return MOE_OK;
+}
 
 // expert activation code of the FFN calls (0 SwiGLU, 1 SiLU, 2 ReLU), or -1
 int act_of(unsigned flags) {
@@ -85,7 +96,8 @@ int ffn_fwd_impl(const char* fn, bool combined, const void* x, const void* w1, c
         (r = check_dim(fn, "f", f)))
         return r;
     if (flags & (MOE_RENORM | MOE_ACCUMULATE | MOE_ACCUMULATE_DW))
-        return fail(MOE_ERR_INVALID_ARG, "%s: only MOE_F32 / MOE_BF16, an activation flag and MOE_H_ON_LOAD are valid", fn);
+        return fail(MOE_ERR_INVALID_ARG, "%s: only MOE_F32 / MOE_BF16, an activation flag, MOE_H_ON_LOAD and (combined) MOE_ATOMIC_COMBINE are valid", fn);
+    if ((r = check_scatter(fn, combined, flags))) return r;
     const int act = act_of(flags);
     if (act < 0) return fail(MOE_ERR_INVALID_ARG, "%s: MOE_ACT_SILU and MOE_ACT_RELU both set", fn);
     if (T == 0) return MOE_OK;
@@ -101,7 +113,8 @@ int ffn_fwd_impl(const char* fn, bool combined, const void* x, const void* w1, c
     if (act == 0) { REQUIRE_PTR(w3); REQUIRE_PTR(B); }
     else { OPT_PTR(w3); OPT_PTR(B); }
     const size_t need =
-        moe::ffn_fwd_workspace(T, d, f, E, k, flags & MOE_F32, combined, flags & MOE_H_ON_LOAD);
+        moe::ffn_fwd_workspace(T, d, f, E, k, flags & MOE_F32, combined, flags & MOE_H_ON_LOAD,
+                               flags & MOE_ATOMIC_COMBINE);
     if (need && (!workspace || workspace_bytes < need))
         return fail(MOE_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, workspace_bytes, need);
     OPT_PTR(workspace);
@@ -110,6 +123,7 @@ int ffn_fwd_impl(const char* fn, bool combined, const void* x, const void* w1, c
     a.A = A; a.B = B; a.T = T; a.d = d; a.f = f; a.E = E; a.k = k; a.ws = workspace;
     a.act = act;
     a.h_on_load = flags & MOE_H_ON_LOAD;
+    a.scatter = flags & MOE_ATOMIC_COMBINE;
     if (combined) { a.y = out; a.gates = gates; a.tim = token_index_map; }
     else a.O = out;
     moe::probe::begin(stream);
@@ -135,6 +149,7 @@ int ffn_bwd_impl(const char* fn, bool combined, const void* dy, const void* x, c
         return r;
     if ((flags & MOE_RENORM) || (!combined && (flags & MOE_ACCUMULATE)))
         return fail(MOE_ERR_INVALID_ARG, "%s: flag not valid here", fn);
+    if ((r = check_scatter(fn, combined, flags))) return r;
     const int act = act_of(flags);
     if (act < 0) return fail(MOE_ERR_INVALID_ARG, "%s: MOE_ACT_SILU and MOE_ACT_RELU both set", fn);
     if (T == 0) return MOE_OK;
@@ -152,7 +167,8 @@ int ffn_bwd_impl(const char* fn, bool combined, const void* dy, const void* x, c
     if (act == 0) { REQUIRE_PTR(w3); REQUIRE_PTR(B); REQUIRE_PTR(dw3); }
     else { OPT_PTR(w3); OPT_PTR(B); OPT_PTR(dw3); }
     const size_t need =
-        moe::ffn_bwd_workspace(T, d, f, E, k, flags & MOE_F32, combined, flags & MOE_H_ON_LOAD);
+        moe::ffn_bwd_workspace(T, d, f, E, k, flags & MOE_F32, combined, flags & MOE_H_ON_LOAD,
+                               flags & MOE_ATOMIC_COMBINE);
     if (need && (!workspace || workspace_bytes < need))
         return fail(MOE_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", fn, workspace_bytes, need);
     OPT_PTR(workspace);
@@ -163,6 +179,7 @@ int ffn_bwd_impl(const char* fn, bool combined, const void* dy, const void* x, c
     a.E = E; a.k = k; a.ws = workspace; a.act = act;
     a.h_on_load = flags & MOE_H_ON_LOAD;
     a.accumulate_dw = flags & MOE_ACCUMULATE_DW;
+    a.scatter = flags & MOE_ATOMIC_COMBINE;
     if (combined) { a.y = out; a.tim = token_index_map; a.accumulate = flags & MOE_ACCUMULATE; }
     else a.dX = out;
     moe::probe::begin(stream);
@@ -270,7 +287,8 @@ int moe_build_index_noalloc(const int32_t* topk_ids, int64_t T, int E, int k, in
 
 size_t moe_ffn_fwd_workspace_size(int64_t T, int d, int f, int E, int k, unsigned flags) {
     if (T <= 0 || d < 1 || f < 1 || E < 1 || k < 1) return 0;
-    return moe::ffn_fwd_workspace(T, d, f, E, k, flags & MOE_F32, false, flags & MOE_H_ON_LOAD);
+    return moe::ffn_fwd_workspace(T, d, f, E, k, flags & MOE_F32, false, flags & MOE_H_ON_LOAD,
+                                  false);
 }
 
 int moe_ffn_fwd(const void* x, const void* w1, const void* w3, const void* w2,
@@ -291,7 +309,7 @@ int moe_ffn_recompute(const void* x, const void* w1, const void* w3,
     if ((r = check_common(fn, T, E, k, flags)) || (r = check_dim(fn, "d", d)) ||
         (r = check_dim(fn, "f", f)))
         return r;
-    if (flags & (MOE_RENORM | MOE_ACCUMULATE | MOE_ACCUMULATE_DW))
+    if (flags & (MOE_RENORM | MOE_ACCUMULATE | MOE_ACCUMULATE_DW | MOE_ATOMIC_COMBINE))
         return fail(MOE_ERR_INVALID_ARG, "%s: only MOE_F32 / MOE_BF16, an activation flag and MOE_H_ON_LOAD are valid", fn);
     const int act = act_of(flags);
     if (act < 0) return fail(MOE_ERR_INVALID_ARG, "%s: MOE_ACT_SILU and MOE_ACT_RELU both set", fn);
@@ -309,7 +327,8 @@ int moe_ffn_recompute(const void* x, const void* w1, const void* w3,
 
 size_t moe_ffn_fwd_combine_workspace_size(int64_t T, int d, int f, int E, int k, unsigned flags) {
     if (T <= 0 || d < 1 || f < 1 || E < 1 || k < 1) return 0;
-    return moe::ffn_fwd_workspace(T, d, f, E, k, flags & MOE_F32, true, flags & MOE_H_ON_LOAD);
+    return moe::ffn_fwd_workspace(T, d, f, E, k, flags & MOE_F32, true, flags & MOE_H_ON_LOAD,
+                                  flags & MOE_ATOMIC_COMBINE);
 }
 
 int moe_ffn_fwd_combine(const void* x, const void* w1, const void* w3, const void* w2,
@@ -339,7 +358,8 @@ int moe_combine(const void* src, const float* weights, const int32_t* token_inde
 
 size_t moe_ffn_bwd_workspace_size(int64_t T, int d, int f, int E, int k, unsigned flags) {
     if (T <= 0 || d < 1 || f < 1 || E < 1 || k < 1) return 0;
-    return moe::ffn_bwd_workspace(T, d, f, E, k, flags & MOE_F32, false, flags & MOE_H_ON_LOAD);
+    return moe::ffn_bwd_workspace(T, d, f, E, k, flags & MOE_F32, false, flags & MOE_H_ON_LOAD,
+                                  false);
 }
 
 int moe_ffn_bwd(const void* dy, const void* x, const void* w1, const void* w3, const void* w2,
@@ -354,7 +374,8 @@ int moe_ffn_bwd(const void* dy, const void* x, const void* w1, const void* w3, c
 
 size_t moe_ffn_bwd_combine_workspace_size(int64_t T, int d, int f, int E, int k, unsigned flags) {
     if (T <= 0 || d < 1 || f < 1 || E < 1 || k < 1) return 0;
-    return moe::ffn_bwd_workspace(T, d, f, E, k, flags & MOE_F32, true, flags & MOE_H_ON_LOAD);
+    return moe::ffn_bwd_workspace(T, d, f, E, k, flags & MOE_F32, true, flags & MOE_H_ON_LOAD,
+                                  flags & MOE_ATOMIC_COMBINE);
 }
 
 int moe_ffn_bwd_combine(const void* dy, const void* x, const void* w1, const void* w3,

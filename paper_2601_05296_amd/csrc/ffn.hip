@@ -150,26 +150,11 @@ g1_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ w1,
     }
 }
 
-// G2: O = H W2[e], output columns [n_base, n_base + ncols) into rows ldo apart
-__global__ void __launch_bounds__(RS::THREADS)
-g2_kernel(const bf16_t* __restrict__ H, const bf16_t* __restrict__ w2,
-          const int32_t* __restrict__ offsets, int d, int f, int E, int n_base, int ncols,
-          int64_t ldo, bf16_t* __restrict__ O) {
-    extern __shared__ __align__(16) char lds[];
-    using C = RS;
-    SlotTile t;
-    const int NT = (ncols + C::BN - 1) / C::BN;
-    if (!find_slot_tile<C::THREADS>(reinterpret_cast<int*>(lds), offsets, E, C::BM, NT,
-                                    xcd_remap(blockIdx.x, gridDim.x), C::BN,
-                                    t, RASTER_GM))
-        return;
-    rs::DenseKC2<C, C::BM> la;
-    la.init(H, H, f, (int64_t)t.off + t.m0, t.mrows, f);
-    rs::DenseMC<C, C::BN> lb;
-    lb.init(w2 + (int64_t)t.e * f * d, d, n_base + t.n0, n_base + ncols);
-    rs::NoLoader nl;
-    rs::Acc<C> acc;
-    rs::mainloop<C>(la, lb, nl, f / rs::KS, lds, acc);
+// Output rows of a slot tile (G2, G6), columns n < ncols of the tile's strip:
+// slot row s goes to row s of O, rows ldo apart.
+template <class C>
+__device__ __forceinline__ void slot_rows_out(const rs::Acc<C>& acc, const SlotTile& t,
+                                              int ncols, int64_t ldo, bf16_t* __restrict__ O) {
     WaveCoord<C> wc;
 #pragma unroll
     for (int i = 0; i < C::FM; ++i) {
@@ -187,6 +172,97 @@ g2_kernel(const bf16_t* __restrict__ H, const bf16_t* __restrict__ w2,
             }
         }
     }
+}
+
+// The combine folded into the epilogue (Section 3.1): slot row s of the tile,
+// times gs[s] (1 when gs is null), rounded to bf16, is added into row tok[s]
+// of O (rows ldo apart) by packed-bf16 atomics, so that O receives the sum
+// over a token's slots in whatever order the tiles finish. The tile goes
+// through LDS first (free once the main loop is done), so that each atomic
+// instruction of a wave covers 256 contiguous bytes of one row: 64 lanes, two
+// columns each (straight from the fragments, a wave's atomics would touch 32
+// rows 16 bytes apiece). 16-byte chunks are XOR-swizzled by row, so that both
+// the fragment-ordered writes and the row-ordered reads are free of bank
+// conflicts.
+template <class C>
+__device__ __forceinline__ void slot_rows_scatter(const rs::Acc<C>& acc, const SlotTile& t,
+                                                  int ncols, int64_t ldo,
+                                                  bf16_t* __restrict__ O,
+                                                  const int32_t* __restrict__ tok,
+                                                  const float* __restrict__ gs, char* lds) {
+    constexpr int RB = C::BN * 2;      // bytes per tile row in LDS
+    constexpr int CPR = C::BN / 8;     // 16-byte chunks per row
+    static_assert(C::BM * RB <= C::LDS && CPR >= 32 && C::BN % 128 == 0, "scatter staging");
+    const WaveCoord<C> wc;
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i) {
+        const int m = wc.row(i);
+        const float g = (gs && m < t.mrows) ? gs[(int64_t)t.off + t.m0 + m] : 1.0f;
+#pragma unroll
+        for (int j = 0; j < C::FN; ++j) {
+            float v[2][8];
+            frag_cols8(acc[0][i][j], v);
+#pragma unroll
+            for (int p = 0; p < 2; ++p) {
+#pragma unroll
+                for (int r = 0; r < 8; ++r) v[p][r] *= g;
+                const int chunk = (wc.col8(j, p) >> 3) ^ (m & 31);
+                *reinterpret_cast<uint4*>(lds + m * RB + chunk * 16) = pack8(v[p]);
+            }
+        }
+    }
+    __syncthreads();
+    const int wv = wave_id();
+    const int rows = min(C::BM, t.mrows);
+    for (int r = wv; r < rows; r += C::NW) {
+        bf16_t* dst = O + (int64_t)tok[(int64_t)t.off + t.m0 + r] * ldo + t.n0;
+#pragma unroll
+        for (int c = 0; c < C::BN / 128; ++c) {
+            const int col = c * 128 + 2 * wc.lane;
+            if (t.n0 + col >= ncols) continue;
+            const int chunk = (col >> 3) ^ (r & 31);
+            const uint32_t v =
+                *reinterpret_cast<const uint32_t*>(lds + r * RB + chunk * 16 + (col & 7) * 2);
+            __builtin_amdgcn_global_atomic_fadd_v2bf16(reinterpret_cast<bf16x2_t*>(dst + col),
+                                                       __builtin_bit_cast(bf16x2_t, v));
+        }
+    }
+}
+
+// slot rows out, plain or (SCATTER) added into the token rows
+template <bool SCATTER, class C>
+__device__ __forceinline__ void slot_rows(const rs::Acc<C>& acc, const SlotTile& t, int ncols,
+                                          int64_t ldo, bf16_t* __restrict__ O,
+                                          const int32_t* __restrict__ tok,
+                                          const float* __restrict__ gs, char* lds) {
+    if constexpr (SCATTER) slot_rows_scatter<C>(acc, t, ncols, ldo, O, tok, gs, lds);
+    else slot_rows_out<C>(acc, t, ncols, ldo, O);
+}
+
+// G2: O = H W2[e], output columns [n_base, n_base + ncols) into rows ldo apart
+// (SCATTER: added into the token rows, see slot_rows_out)
+template <bool SCATTER>
+__global__ void __launch_bounds__(RS::THREADS)
+g2_kernel(const bf16_t* __restrict__ H, const bf16_t* __restrict__ w2,
+          const int32_t* __restrict__ offsets, int d, int f, int E, int n_base, int ncols,
+          int64_t ldo, bf16_t* __restrict__ O, const int32_t* __restrict__ tok,
+          const float* __restrict__ gs) {
+    extern __shared__ __align__(16) char lds[];
+    using C = RS;
+    SlotTile t;
+    const int NT = (ncols + C::BN - 1) / C::BN;
+    if (!find_slot_tile<C::THREADS>(reinterpret_cast<int*>(lds), offsets, E, C::BM, NT,
+                                    xcd_remap(blockIdx.x, gridDim.x), C::BN,
+                                    t, RASTER_GM))
+        return;
+    rs::DenseKC2<C, C::BM> la;
+    la.init(H, H, f, (int64_t)t.off + t.m0, t.mrows, f);
+    rs::DenseMC<C, C::BN> lb;
+    lb.init(w2 + (int64_t)t.e * f * d, d, n_base + t.n0, n_base + ncols);
+    rs::NoLoader nl;
+    rs::Acc<C> acc;
+    rs::mainloop<C>(la, lb, nl, f / rs::KS, lds, acc);
+    slot_rows<SCATTER, C>(acc, t, ncols, ldo, O, tok, gs, lds);
 }
 
 // h of a pair of elements (one dword of bf16) from the pairs of A and B: the
@@ -241,11 +317,12 @@ struct HKC {
 };
 
 // G2 with h formed on load: O = h W2[e] from the saved A (and B), no h buffer.
-template <int ACT>
+template <int ACT, bool SCATTER>
 __global__ void __launch_bounds__(RHW::THREADS)
 g2h_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B,
            const bf16_t* __restrict__ w2, const int32_t* __restrict__ offsets, int d, int f,
-           int E, int n_base, int ncols, int64_t ldo, bf16_t* __restrict__ O) {
+           int E, int n_base, int ncols, int64_t ldo, bf16_t* __restrict__ O,
+           const int32_t* __restrict__ tok, const float* __restrict__ gs) {
     extern __shared__ __align__(16) char lds[];
     using C = RHW;
     SlotTile t;
@@ -260,23 +337,7 @@ g2h_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B,
     rs::NoLoader nl;
     rs::Acc<C> acc;
     rs::mainloop<C>(la, lb, nl, f / rs::KS, lds, acc);
-    WaveCoord<C> wc;
-#pragma unroll
-    for (int i = 0; i < C::FM; ++i) {
-        const int m = wc.row(i);
-        if (m >= t.mrows) continue;
-        const int64_t s = (int64_t)t.off + t.m0 + m;
-#pragma unroll
-        for (int j = 0; j < C::FN; ++j) {
-            float v[2][8];
-            frag_cols8(acc[0][i][j], v);
-#pragma unroll
-            for (int p = 0; p < 2; ++p) {
-                const int n = t.n0 + wc.col8(j, p);
-                if (n < ncols) store8_bf16(O + s * ldo + n, v[p]);
-            }
-        }
-    }
+    slot_rows<SCATTER, C>(acc, t, ncols, ldo, O, tok, gs, lds);
 }
 
 // G4: u = dY[eti] W2[e]^T; epilogue: d_gate partials sum(u*h), dA/dB over
@@ -538,6 +599,26 @@ __global__ void slot_gates(const float* __restrict__ gates, const int32_t* __res
     else if (s < S) gs[s] = 0.0f;
 }
 
+// gs[token_index_map[i]] = gates[i] for the accepted choices i < T*k: the
+// gate of each filled slot in slot order, from the token-side map (the
+// forward has no slot_src)
+__global__ void fwd_slot_gates(const float* __restrict__ gates,
+                                    const int32_t* __restrict__ tim, int64_t n,
+                                    float* __restrict__ gs) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) {
+        const int32_t s = tim[i];
+        if (s >= 0) gs[s] = gates[i];
+    }
+}
+
+// p[0..n) = 0 for n bf16 values, n a multiple of 8, p 16-byte aligned (a
+// kernel rather than a memset, so that it can be captured in a graph)
+__global__ void zero_bf16(bf16_t* __restrict__ p, int64_t n) {
+    const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 8;
+    if (i < n) st16(p + i, uint4{0u, 0u, 0u, 0u});
+}
+
 // G3 with g*h formed on load from the saved A (and B) and the slot-ordered
 // gates gs: dW2[e] = sum_s (g h)[s]^T dY[eti[s]]. Runs before G4, which then
 // writes dA, dB over A, B and no g*h.
@@ -610,11 +691,12 @@ g5_kernel(const bf16_t* __restrict__ x, const bf16_t* __restrict__ dA,
 // G6: dX_slot = dA W1[e]^T + dB W3[e]^T, output columns [n_base, n_base + ncols)
 // into rows ldo apart   (K = 2f; non-gated: dA W1[e]^T, K = f,
 // called with dB = dA and W3 = W1, whose second halves are then never reached)
+template <bool SCATTER>
 __global__ void __launch_bounds__(RS::THREADS)
 g6_kernel(const bf16_t* __restrict__ dA, const bf16_t* __restrict__ dB,
           const bf16_t* __restrict__ w1, const bf16_t* __restrict__ w3,
           const int32_t* __restrict__ offsets, int d, int f, int E, int kslices, int n_base,
-          int ncols, int64_t ldo, bf16_t* __restrict__ dX) {
+          int ncols, int64_t ldo, bf16_t* __restrict__ dX, const int32_t* __restrict__ tok) {
     extern __shared__ __align__(16) char lds[];
     using C = RS;
     SlotTile t;
@@ -631,23 +713,7 @@ g6_kernel(const bf16_t* __restrict__ dA, const bf16_t* __restrict__ dB,
     rs::NoLoader nl;
     rs::Acc<C> acc;
     rs::mainloop<C>(la, lb, nl, kslices, lds, acc);
-    WaveCoord<C> wc;
-#pragma unroll
-    for (int i = 0; i < C::FM; ++i) {
-        const int m = wc.row(i);
-        if (m >= t.mrows) continue;
-        const int64_t s = (int64_t)t.off + t.m0 + m;
-#pragma unroll
-        for (int j = 0; j < C::FN; ++j) {
-            float v[2][8];
-            frag_cols8(acc[0][i][j], v);
-#pragma unroll
-            for (int p = 0; p < 2; ++p) {
-                const int n = t.n0 + wc.col8(j, p);
-                if (n < ncols) store8_bf16(dX + s * ldo + n, v[p]);
-            }
-        }
-    }
+    slot_rows<SCATTER, C>(acc, t, ncols, ldo, dX, tok, nullptr, lds);
 }
 
 // rank[r] = (expert, first slot, slot count) of the expert of rank r by slot
@@ -857,15 +923,18 @@ hipError_t set_lds_limits() {
             set(reinterpret_cast<const void*>(g4_kernel<ACT, true>), RS::LDS);
             set(reinterpret_cast<const void*>(g4_kernel<ACT, false>), RS::LDS);
             set(reinterpret_cast<const void*>(g5_kernel<ACT>), CFirst<ACT>::LDS);
-            set(reinterpret_cast<const void*>(g2h_kernel<ACT>), RHW::LDS);
+            set(reinterpret_cast<const void*>(g2h_kernel<ACT, false>), RHW::LDS);
+            set(reinterpret_cast<const void*>(g2h_kernel<ACT, true>), RHW::LDS);
             set(reinterpret_cast<const void*>(g3h_kernel<ACT>), RHW::LDS);
         };
         per_act(std::integral_constant<int, ACT_SWIGLU>{});
         per_act(std::integral_constant<int, ACT_SILU>{});
         per_act(std::integral_constant<int, ACT_RELU>{});
-        set(reinterpret_cast<const void*>(g2_kernel), RS::LDS);
+        set(reinterpret_cast<const void*>(g2_kernel<false>), RS::LDS);
+        set(reinterpret_cast<const void*>(g2_kernel<true>), RS::LDS);
         set(reinterpret_cast<const void*>(g3_kernel), RS::LDS);
-        set(reinterpret_cast<const void*>(g6_kernel), RS::LDS);
+        set(reinterpret_cast<const void*>(g6_kernel<false>), RS::LDS);
+        set(reinterpret_cast<const void*>(g6_kernel<true>), RS::LDS);
         return e;
     }();
     return status;
@@ -901,11 +970,13 @@ inline int bwd_strip(int64_t S, int E, int d) { return strip_width(S, E, d, RS::
 }  // namespace
 
 size_t ffn_fwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool combined,
-                         bool h_on_load) {
+                         bool h_on_load, bool scatter) {
     const size_t S = (size_t)T * k;
     if (f32) return combined ? align256(S * d * sizeof(float)) : 0;  // O
     const size_t h = h_on_load ? 0 : align256(S * f * sizeof(bf16_t));   // H
-    return combined ? h + align256(S * fwd_strip(S, E, d, h_on_load) * sizeof(bf16_t)) : h;
+    if (!combined) return h;
+    if (scatter) return h + align256(S * sizeof(float));                  // slot gates
+    return h + align256(S * fwd_strip(S, E, d, h_on_load) * sizeof(bf16_t));
 }
 
 namespace {
@@ -936,22 +1007,39 @@ hipError_t ffn_fwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
                        (const bf16_t*)a.w3, a.offsets, a.eti, a.d, a.f, a.E, (bf16_t*)a.A,
                        (bf16_t*)a.B, H);
     probe::mark("g1_kernel", st);
-    auto second = [&](int c0, int nc, int64_t ldo, bf16_t* out) {
+    // the second GEMM over columns [c0, c0 + nc): slot rows into out (ldo
+    // apart), or with gs (scatter) added into the token rows of out
+    auto second = [&](int c0, int nc, int64_t ldo, bf16_t* out, const float* gs) {
         if (a.h_on_load) {
-            hipLaunchKernelGGL(g2h_kernel<ACT>, dim3(slot_grid(S, a.E, C2H::BM, cdiv(nc, C2H::BN))),
+            auto g2h = gs ? g2h_kernel<ACT, true> : g2h_kernel<ACT, false>;
+            hipLaunchKernelGGL(g2h, dim3(slot_grid(S, a.E, C2H::BM, cdiv(nc, C2H::BN))),
                                dim3(C2H::THREADS), C2H::LDS, st, (const bf16_t*)a.A,
                                (const bf16_t*)a.B, (const bf16_t*)a.w2, a.offsets, a.d, a.f, a.E,
-                               c0, nc, ldo, out);
+                               c0, nc, ldo, out, a.eti, gs);
             probe::mark("g2h_kernel", st);
         } else {
-            hipLaunchKernelGGL(g2_kernel, dim3(slot_grid(S, a.E, RS::BM, cdiv(nc, RS::BN))),
+            auto g2 = gs ? g2_kernel<true> : g2_kernel<false>;
+            hipLaunchKernelGGL(g2, dim3(slot_grid(S, a.E, RS::BM, cdiv(nc, RS::BN))),
                                dim3(RS::THREADS), RS::LDS, st, (const bf16_t*)H,
-                               (const bf16_t*)a.w2, a.offsets, a.d, a.f, a.E, c0, nc, ldo, out);
+                               (const bf16_t*)a.w2, a.offsets, a.d, a.f, a.E, c0, nc, ldo, out,
+                               a.eti, gs);
             probe::mark("g2_kernel", st);
         }
     };
     if (!a.y) {   // O [S, d] for the caller's combine
-        second(0, a.d, (int64_t)a.d, (bf16_t*)a.O);
+        second(0, a.d, (int64_t)a.d, (bf16_t*)a.O, nullptr);
+        return hipGetLastError();
+    }
+    if (a.scatter) {   // y = 0, then every slot row times its gate added into y
+        float* gs = reinterpret_cast<float*>(
+            static_cast<char*>(a.ws) + (a.h_on_load ? 0 : align256((size_t)S * a.f * sizeof(bf16_t))));
+        hipLaunchKernelGGL(fwd_slot_gates, grid1d(S, 256), dim3(256), 0, st, a.gates, a.tim,
+                           S, gs);
+        probe::mark("fwd_slot_gates", st);
+        hipLaunchKernelGGL(zero_bf16, grid1d(a.T * a.d / 8, 256), dim3(256), 0, st,
+                           static_cast<bf16_t*>(a.y), a.T * a.d);
+        probe::mark("zero_bf16", st);
+        second(0, a.d, (int64_t)a.d, static_cast<bf16_t*>(a.y), gs);
         return hipGetLastError();
     }
     // combined: one column strip of O at a time, straight into y
@@ -960,7 +1048,7 @@ hipError_t ffn_fwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
         static_cast<char*>(a.ws) + (a.h_on_load ? 0 : align256((size_t)S * a.f * sizeof(bf16_t))));
     for (int c0 = 0; c0 < a.d; c0 += sw) {
         const int nc = min(sw, a.d - c0);
-        second(c0, nc, (int64_t)nc, strip);
+        second(c0, nc, (int64_t)nc, strip, nullptr);
         if (hipError_t e = combine_cols(strip, nc, a.gates, a.tim, a.T, nc, a.k, false, false,
                                         static_cast<bf16_t*>(a.y) + c0, a.d, st);
             e != hipSuccess)
@@ -1009,6 +1097,7 @@ hipError_t ffn_fwd(const FfnArgs& a, bool f32, hipStream_t st) {
 
 // bytes of the backward workspace before the expert rank table
 inline size_t bwd_main_bytes(size_t S, int d, int f, int E, bool combined, bool h_on_load) {
+    // combined: the dX strips (none when they are scattered into dx)
     const size_t part = align256(S * g4_nparts(f) * sizeof(float));  // d_gate partials
     const size_t strip = combined ? S * bwd_strip(S, E, d) * sizeof(bf16_t) : 0;
     if (h_on_load) {   // slot-ordered gates for G3, then (same space) the dX strip
@@ -1020,10 +1109,11 @@ inline size_t bwd_main_bytes(size_t S, int d, int f, int E, bool combined, bool 
 }
 
 size_t ffn_bwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool combined,
-                         bool h_on_load) {
+                         bool h_on_load, bool scatter) {
     const size_t S = (size_t)T * k;
     if (f32) return combined ? align256(S * d * sizeof(float)) : 0;  // dX_slot
-    return bwd_main_bytes(S, d, f, E, combined, h_on_load) + align256(E * sizeof(ExpertRank));
+    return bwd_main_bytes(S, d, f, E, combined && !scatter, h_on_load) +
+           align256(E * sizeof(ExpertRank));
 }
 
 namespace {
@@ -1066,7 +1156,8 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
     bf16_t* HG = a.h_on_load ? nullptr : reinterpret_cast<bf16_t*>(ws2);
     bf16_t* strip = reinterpret_cast<bf16_t*>(ws2);
     ExpertRank* rank = reinterpret_cast<ExpertRank*>(
-        static_cast<char*>(a.ws) + bwd_main_bytes(S, a.d, a.f, a.E, a.y != nullptr, a.h_on_load));
+        static_cast<char*>(a.ws) +
+        bwd_main_bytes(S, a.d, a.f, a.E, a.y != nullptr && !a.scatter, a.h_on_load));
     hipLaunchKernelGGL(expert_ranks, dim3(1), dim3(256), 0, st, a.offsets, a.E, rank);
     probe::mark("expert_ranks", st);
     // non-gated: the second operand of the two-branch kernels is the first again
@@ -1104,10 +1195,23 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
     probe::mark("g5_kernel", st);
     const int kslices = (GATED ? 2 : 1) * a.f / rs::KS;
     if (!a.y) {   // dX_slot [S, d] for the caller's combine
-        hipLaunchKernelGGL(g6_kernel, dim3(slot_grid(S, a.E, RS::BM, cdiv(a.d, RS::BN))),
+        hipLaunchKernelGGL(g6_kernel<false>, dim3(slot_grid(S, a.E, RS::BM, cdiv(a.d, RS::BN))),
                            dim3(RS::THREADS), RS::LDS, st, (const bf16_t*)a.A, (const bf16_t*)Bx,
                            (const bf16_t*)a.w1, (const bf16_t*)w3x, a.offsets, a.d, a.f, a.E,
-                           kslices, 0, a.d, (int64_t)a.d, (bf16_t*)a.dX);
+                           kslices, 0, a.d, (int64_t)a.d, (bf16_t*)a.dX, a.eti);
+        probe::mark("g6_kernel", st);
+        return hipGetLastError();
+    }
+    if (a.scatter) {   // every dX_slot row added into dx (cleared first unless accumulating)
+        if (!a.accumulate) {
+            hipLaunchKernelGGL(zero_bf16, grid1d(a.T * a.d / 8, 256), dim3(256), 0, st,
+                               static_cast<bf16_t*>(a.y), a.T * a.d);
+            probe::mark("zero_bf16", st);
+        }
+        hipLaunchKernelGGL(g6_kernel<true>, dim3(slot_grid(S, a.E, RS::BM, cdiv(a.d, RS::BN))),
+                           dim3(RS::THREADS), RS::LDS, st, (const bf16_t*)a.A, (const bf16_t*)Bx,
+                           (const bf16_t*)a.w1, (const bf16_t*)w3x, a.offsets, a.d, a.f, a.E,
+                           kslices, 0, a.d, (int64_t)a.d, static_cast<bf16_t*>(a.y), a.eti);
         probe::mark("g6_kernel", st);
         return hipGetLastError();
     }
@@ -1116,10 +1220,10 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
     const int sw = bwd_strip(S, a.E, a.d);
     for (int c0 = 0; c0 < a.d; c0 += sw) {
         const int nc = min(sw, a.d - c0);
-        hipLaunchKernelGGL(g6_kernel, dim3(slot_grid(S, a.E, RS::BM, cdiv(nc, RS::BN))),
+        hipLaunchKernelGGL(g6_kernel<false>, dim3(slot_grid(S, a.E, RS::BM, cdiv(nc, RS::BN))),
                            dim3(RS::THREADS), RS::LDS, st, (const bf16_t*)a.A, (const bf16_t*)Bx,
                            (const bf16_t*)a.w1, (const bf16_t*)w3x, a.offsets, a.d, a.f, a.E,
-                           kslices, c0, nc, (int64_t)nc, strip);
+                           kslices, c0, nc, (int64_t)nc, strip, a.eti);
         probe::mark("g6_kernel", st);
         if (hipError_t e = combine_cols(strip, nc, nullptr, a.tim, a.T, nc, a.k, false,
                                         a.accumulate, static_cast<bf16_t*>(a.y) + c0, a.d, st);

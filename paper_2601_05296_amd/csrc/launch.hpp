@@ -53,14 +53,17 @@ struct FfnArgs {
     bool h_on_load;
     // backward: add the weight gradients into dw1, dw3, dw2
     bool accumulate_dw;
+    // combined calls: the second GEMM (forward) or the dX GEMM (backward) adds
+    // its rows into y / dx with atomics instead of strips and a gather-reduce
+    bool scatter;
 };
 size_t ffn_fwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool combined,
-                         bool h_on_load);
+                         bool h_on_load, bool scatter);
 hipError_t ffn_fwd(const FfnArgs& a, bool f32, hipStream_t st);
 // first layer only: A (and B) from x, nothing else
 hipError_t ffn_first(const FfnArgs& a, bool f32, hipStream_t st);
 size_t ffn_bwd_workspace(int64_t T, int d, int f, int E, int k, bool f32, bool combined,
-                         bool h_on_load);
+                         bool h_on_load, bool scatter);
 hipError_t ffn_bwd(const FfnArgs& a, bool f32, hipStream_t st);
 
 }  // namespace moe

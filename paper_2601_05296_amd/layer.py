@@ -26,6 +26,13 @@ again from A and B as they load them, so no SwiGLU intermediate is ever
 written to HBM. ``h_on_load=False`` is the buffered policy: h passes from the
 first GEMM to the second through a transient buffer, and g*h from the dh GEMM
 to the dW2 GEMM (bit-identical results, more memory, less vector work).
+``atomic_combine`` (MOE_ATOMIC_COMBINE, combined calls only) folds the
+combine into the epilogues of the second GEMM and of the dX GEMM: their slot
+rows are added into y and dx by packed-bf16 atomics, so no strip of the expert
+output or of dX_slot is held, and no separate combine pass runs. Each add
+rounds to bf16, and for k > 2 the result depends on the order in which the
+tiles finish. The default (None) uses it where it is deterministic: bf16 and
+k <= 2; otherwise the strips and the ordered gather-reduce.
 
 What the forward keeps for the backward (the "saved activations"): the first
 layer outputs A and B [S, f] (A alone for the non-gated SiLU / ReLU experts),
@@ -67,10 +74,16 @@ class Saved:
     B: torch.Tensor | None
     h_on_load: bool = True
     chunk: int = 0                  # full recompute: tokens per chunk
+    atomic_combine: bool = False
 
     @property
     def ffn_flags(self) -> int:
         return self.flags | B.ACT_FLAG[self.act] | (B.MOE_H_ON_LOAD if self.h_on_load else 0)
+
+    @property
+    def combine_flags(self) -> int:
+        """Flags of the combined FFN calls."""
+        return self.ffn_flags | (B.MOE_ATOMIC_COMBINE if self.atomic_combine else 0)
 
     def tensors(self):
         return [t for t in (self.ids, self.gates, self.logits, self.counts, self.offsets,
@@ -113,19 +126,25 @@ def _on(stream):
 
 def forward(x, w_gate, bias, w1, w3, w2, k: int, renorm: bool, stream=None, keep_O=False,
             act: str = "swiglu", separate: bool = False, recompute: bool = False,
-            h_on_load: bool = True, chunk_tokens: int | None = None):
+            h_on_load: bool = True, chunk_tokens: int | None = None,
+            atomic_combine: bool | None = None):
     """Returns (y, saved[, O]). ``act`` picks the expert: "swiglu" (gated, w3
     used) or the non-gated "silu" / "relu" (w3 ignored, may be None).
     ``keep_O`` (returns the expert outputs) implies ``separate``. Everything
     runs on ``stream`` (torch's current stream if None)."""
+    if atomic_combine and (keep_O or separate):
+        raise ValueError("atomic_combine applies to the combined calls only")
+    if atomic_combine is None:   # where the atomic sum is deterministic
+        atomic_combine = (not (keep_O or separate) and k <= 2 and
+                          x.dtype == torch.bfloat16)
     with _on(stream):
         if recompute:
             if keep_O or separate:
                 raise ValueError("the full-recompute policy runs the combined calls only")
             return _forward_recompute(x, w_gate, bias, w1, w3, w2, k, renorm, act, h_on_load,
-                                      chunk_tokens)
+                                      chunk_tokens, atomic_combine)
         return _forward(x, w_gate, bias, w1, w3, w2, k, renorm, keep_O, act, separate,
-                        h_on_load)
+                        h_on_load, atomic_combine)
 
 
 def _route(x, w_gate, bias, E, k, renorm, flags):
@@ -158,14 +177,16 @@ def _chunks(T, chunk):
         yield t0, min(T, t0 + chunk)
 
 
-def _forward_recompute(x, w_gate, bias, w1, w3, w2, k, renorm, act, h_on_load, chunk_tokens):
+def _forward_recompute(x, w_gate, bias, w1, w3, w2, k, renorm, act, h_on_load, chunk_tokens,
+                       atomic_combine):
     T, d = x.shape
     E, _, f = w1.shape
     flags = B.dtype_flag(x)
     gated = act == "swiglu"
     ids, gates, logits = _route(x, w_gate, bias, E, k, renorm, flags)
     chunk = chunk_tokens or default_chunk(T, k, f, gated, x.element_size())
-    fflags = flags | B.ACT_FLAG[act] | (B.MOE_H_ON_LOAD if h_on_load else 0)
+    fflags = (flags | B.ACT_FLAG[act] | (B.MOE_H_ON_LOAD if h_on_load else 0)
+              | (B.MOE_ATOMIC_COMBINE if atomic_combine else 0))
     y = torch.empty((T, d), dtype=x.dtype, device=x.device)
     for t0, t1 in _chunks(T, chunk):
         Tc = t1 - t0
@@ -178,11 +199,12 @@ def _forward_recompute(x, w_gate, bias, w1, w3, w2, k, renorm, act, h_on_load, c
                               tim, Tc, d, f, E, k, fflags, A, Bm, y[t0:t1], ws, wsb, None)
         del counts, offsets, eti, tim, slot_src, A, Bm, ws
     saved = Saved(T, d, f, E, k, flags, act, renorm, ids, gates, logits, None, None, None, None,
-                  None, None, None, h_on_load, chunk)
+                  None, None, None, h_on_load, chunk, atomic_combine)
     return y, saved
 
 
-def _forward(x, w_gate, bias, w1, w3, w2, k, renorm, keep_O, act, separate, h_on_load):
+def _forward(x, w_gate, bias, w1, w3, w2, k, renorm, keep_O, act, separate, h_on_load,
+             atomic_combine):
     stream = None   # torch's current stream, set by forward()
     T, d = x.shape
     E, _, f = w1.shape
@@ -211,12 +233,13 @@ def _forward(x, w_gate, bias, w1, w3, w2, k, renorm, keep_O, act, separate, h_on
     Bm = torch.empty((S, f), dtype=x.dtype, device=dev) if gated else None
     y = torch.empty((T, d), dtype=x.dtype, device=dev)
     saved = Saved(T, d, f, E, k, flags, act, renorm, ids, gates, logits, counts, offsets, eti,
-                  tim, slot_src, A, Bm, h_on_load)
+                  tim, slot_src, A, Bm, h_on_load, 0, atomic_combine)
     w3g = w3 if gated else None
     if not (separate or keep_O):
-        wsb = B.moe_ffn_fwd_combine_workspace_size(T, d, f, E, k, fflags)
+        cflags = saved.combine_flags
+        wsb = B.moe_ffn_fwd_combine_workspace_size(T, d, f, E, k, cflags)
         ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
-        B.moe_ffn_fwd_combine(x, w1, w3g, w2, offsets, eti, gates, tim, T, d, f, E, k, fflags, A,
+        B.moe_ffn_fwd_combine(x, w1, w3g, w2, offsets, eti, gates, tim, T, d, f, E, k, cflags, A,
                               Bm, y, ws, wsb, stream)
         del ws
         return y, saved
@@ -262,7 +285,7 @@ def _backward_recompute(s, dy, x, w_gate, w1, w3, w2):
         Bm = torch.empty((Tc * k, f), dtype=dy.dtype, device=dev) if gated else None
         B.moe_ffn_recompute(x[t0:t1], w1, w3g, offsets, eti, Tc, d, f, E, k, s.ffn_flags, A, Bm,
                             None)
-        fl = s.ffn_flags | (B.MOE_ACCUMULATE_DW if i else 0)
+        fl = s.combine_flags | (B.MOE_ACCUMULATE_DW if i else 0)
         wsb = B.moe_ffn_bwd_combine_workspace_size(Tc, d, f, E, k, fl)
         ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
         B.moe_ffn_bwd_combine(dy[t0:t1], x[t0:t1], w1, w3g, w2, s.gates[t0:t1], offsets, eti,
@@ -292,10 +315,10 @@ def _backward(saved, dy, x, w_gate, w1, w3, w2, keep, separate):
     w3g = w3 if gated else None
     out = dict(dw1=dw1, dw3=dw3, dw2=dw2, d_gates=d_gates)
     if not (separate or keep):
-        wsb = B.moe_ffn_bwd_combine_workspace_size(T, d, f, E, k, s.ffn_flags)
+        wsb = B.moe_ffn_bwd_combine_workspace_size(T, d, f, E, k, s.combine_flags)
         ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
         B.moe_ffn_bwd_combine(dy, x, w1, w3g, w2, s.gates, s.offsets, s.eti, s.slot_src, s.tim,
-                              s.A, s.B, T, d, f, E, k, s.ffn_flags, dw1, dw3, dw2, d_gates, dx,
+                              s.A, s.B, T, d, f, E, k, s.combine_flags, dw1, dw3, dw2, d_gates, dx,
                               ws, wsb, stream)
         del ws
     else:

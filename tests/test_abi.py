@@ -62,7 +62,8 @@ def test_null_and_misaligned_pointers():
     assert lib.moe_route(FAKE + 2, FAKE, None, 10, 128, 8, 2, 0, FAKE, FAKE, None, None) == B.MOE_ERR_INVALID_ARG
     assert b"aligned" in lib.moe_last_error()
     assert lib.moe_combine(FAKE, None, FAKE, 10, 128, 2, B.MOE_RENORM, FAKE, None) == B.MOE_ERR_INVALID_ARG
-    assert lib.moe_route(FAKE, FAKE, None, 10, 128, 8, 2, 0x80, FAKE, FAKE, None, None) == B.MOE_ERR_INVALID_ARG
+    assert lib.moe_route(FAKE, FAKE, None, 10, 128, 8, 2, 0x100, FAKE, FAKE, None, None) == B.MOE_ERR_INVALID_ARG
+    assert b"unknown flag" in lib.moe_last_error()
 
 
 def test_workspace_checks_and_zero_tokens():
@@ -201,3 +202,43 @@ def test_binding_checks_sizes_and_dtypes_before_the_library():
         B.moe_ffn_fwd(z(T * d, bf), z(E * d * f, bf), None, z(E * f * d, bf), z(E + 1, i32),
                       z(T * k, i32), T, d, f, E, k, B.MOE_ACT_RELU, z(T * k * f, bf), None,
                       z(T * k * d, bf), None, 0)
+
+
+def test_atomic_combine_flag():
+    lib = B.load_library()
+    T, d, f, E, k = 1000, 256, 384, 8, 2
+    S = T * k
+    gs = (S * 4 + 255) // 256 * 256
+    for fl in (0, B.MOE_H_ON_LOAD, B.MOE_ACT_SILU | B.MOE_H_ON_LOAD):
+        # the forward holds the slot gates instead of a strip of the expert output
+        plain = lib.moe_ffn_fwd_combine_workspace_size(T, d, f, E, k, fl)
+        atomic = lib.moe_ffn_fwd_combine_workspace_size(T, d, f, E, k, fl | B.MOE_ATOMIC_COMBINE)
+        assert plain - atomic > 0
+        assert atomic == lib.moe_ffn_fwd_workspace_size(T, d, f, E, k, fl) + gs
+        # the backward drops its dX strip: what is left is the separate call's workspace
+        assert lib.moe_ffn_bwd_combine_workspace_size(T, d, f, E, k, fl | B.MOE_ATOMIC_COMBINE) == \
+            lib.moe_ffn_bwd_workspace_size(T, d, f, E, k, fl)
+    fl = B.MOE_ATOMIC_COMBINE
+    # the combined calls accept it (a short workspace stops them before any launch)
+    r = lib.moe_ffn_fwd_combine(*([FAKE] * 8), T, d, f, E, k, fl, *([FAKE] * 4), 16, None)
+    assert r == B.MOE_ERR_WORKSPACE, lib.moe_last_error()
+    r = lib.moe_ffn_bwd_combine(*([FAKE] * 12), T, d, f, E, k, fl, *([FAKE] * 6), 16, None)
+    assert r == B.MOE_ERR_WORKSPACE, lib.moe_last_error()
+    # bf16 only
+    r = lib.moe_ffn_fwd_combine(*([FAKE] * 8), T, d, f, E, k, fl | B.MOE_F32, *([FAKE] * 4),
+                                1 << 40, None)
+    assert r == B.MOE_ERR_UNSUPPORTED, lib.moe_last_error()
+    r = lib.moe_ffn_bwd_combine(*([FAKE] * 12), T, d, f, E, k, fl | B.MOE_F32, *([FAKE] * 6),
+                                1 << 40, None)
+    assert r == B.MOE_ERR_UNSUPPORTED, lib.moe_last_error()
+    # the separate FFN calls, the recompute and the other calls reject it
+    r = lib.moe_ffn_fwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, T, d, f, E, k, fl, FAKE, FAKE, FAKE,
+                        FAKE, 1 << 40, None)
+    assert r == B.MOE_ERR_INVALID_ARG
+    r = lib.moe_ffn_bwd(*([FAKE] * 11), T, d, f, E, k, fl, *([FAKE] * 6), 1 << 40, None)
+    assert r == B.MOE_ERR_INVALID_ARG
+    assert lib.moe_ffn_recompute(FAKE, FAKE, FAKE, FAKE, FAKE, T, d, f, E, k, fl, FAKE, FAKE,
+                                 None) == B.MOE_ERR_INVALID_ARG
+    assert lib.moe_combine(FAKE, None, FAKE, 10, 128, 2, fl, FAKE, None) == B.MOE_ERR_INVALID_ARG
+    assert lib.moe_route(FAKE, FAKE, None, 10, 128, 8, 2, fl, FAKE, FAKE, None,
+                         None) == B.MOE_ERR_INVALID_ARG

@@ -129,7 +129,8 @@ def test_build_index_rejects_invalid_ids(T, E, k, frac):
 
 @pytest.mark.parametrize("dtype,act,h_on_load,combined", [
     ("bf16", "swiglu", False, True), ("bf16", "swiglu", True, True), ("bf16", "swiglu", False, False),
-    ("bf16", "relu", False, True), ("f32", "swiglu", False, False)])
+    ("bf16", "relu", False, True), ("f32", "swiglu", False, False),
+    ("bf16", "swiglu", True, "atomic"), ("bf16", "silu", False, "atomic")])
 def test_ffn_with_rejected_choices(dtype, act, h_on_load, combined):
     T, d, f, E, k = 300, 256, 384, 8, 3
     inp, _, g = _layer_case(dtype, T, d, f, E, k, False, None)
@@ -172,6 +173,10 @@ def test_ffn_with_rejected_choices(dtype, act, h_on_load, combined):
     dg = torch.full((T, k), nan, **f32)
     dx = torch.empty((T, d), dtype=tdt, device="cuda")
     if combined:
+        if combined == "atomic":   # y and dx start as NaN: the call clears them
+            flags |= B.MOE_ATOMIC_COMBINE
+            y.fill_(nan)
+            dx.fill_(nan)
         wsb = B.moe_ffn_fwd_combine_workspace_size(T, d, f, E, k, flags)
         ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
         B.moe_ffn_fwd_combine(x, w1, w3, w2, offsets, eti, gates, tim, T, d, f, E, k, flags,
@@ -643,6 +648,88 @@ def test_ffn_combined_equals_separate(dtype, T, d, f, E, k, pattern, act):
     assert_close("dw1", host(r_c["dw1"]), bw["dw1"], dtype)
 
 
+ATOMIC_CASES = [
+    # T, d, f, E, k, ids pattern, activation, h on load
+    (400, 1280, 256, 8, 2, None, "swiglu", True),
+    (333, 384, 256, 12, 3, "dead", "silu", True),
+    (500, 640, 384, 16, 4, "zipf", "relu", False),
+    (500, 576, 448, 16, 4, None, "swiglu", False),
+    (100, 64, 64, 2, 2, None, "swiglu", True),
+    (1000, 512, 320, 64, 8, None, "swiglu", True),
+    (3000, 256, 128, 32, 6, "zipf", "swiglu", True),
+]
+
+
+@pytest.mark.parametrize("T,d,f,E,k,pattern,act,hol", ATOMIC_CASES)
+def test_ffn_atomic_combine(T, d, f, E, k, pattern, act, hol):
+    """MOE_ATOMIC_COMBINE: the second GEMM and the dX GEMM add their slot rows
+    into y and dx by atomics. A, B and every weight and gate gradient are those
+    of the strip path bit for bit (the same kernels); y and dx match the
+    oracle (each term rounded to bf16 before it is added, each add rounded
+    again), with and without MOE_ACCUMULATE; with k <= 2 the atomic result is
+    deterministic, which a second run checks."""
+    inp, ids, g = _layer_case("bf16", T, d, f, E, k, False, pattern)
+    v, st = inp.vals, inp.store
+    gated = act == "swiglu"
+    S = T * k
+    gi = _gpu_index(ids, E)
+    x, w1, w2, dy = (dev(st[n]) for n in ("x", "w1", "w2", "dy"))
+    w3 = dev(st["w3"]) if gated else None
+    offsets, eti, tim, ss = (dev(gi[n]) for n in ("offsets", "eti", "tim", "slot_src"))
+    gates = dev(g)
+    base = B.dtype_flag(x) | B.ACT_FLAG[act] | (B.MOE_H_ON_LOAD if hol else 0)
+    f32 = dict(dtype=torch.float32, device="cuda")
+    bf = dict(dtype=torch.bfloat16, device="cuda")
+
+    def run(atomic, dx0=None):
+        flags = base | (B.MOE_ATOMIC_COMBINE if atomic else 0)
+        A = torch.empty((S, f), **bf)
+        Bm = torch.empty((S, f), **bf) if gated else None
+        y = torch.full((T, d), float("nan"), **bf)
+        wsb = B.moe_ffn_fwd_combine_workspace_size(T, d, f, E, k, flags)
+        ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+        B.moe_ffn_fwd_combine(x, w1, w3, w2, offsets, eti, gates, tim, T, d, f, E, k, flags,
+                              A, Bm, y, ws, wsb)
+        A0 = A.clone()
+        Bm0 = Bm.clone() if gated else None
+        out = dict(A=A0, B=Bm0, y=y)
+        dw1 = torch.empty((E, d, f), **f32)
+        dw3 = torch.empty((E, d, f), **f32) if gated else None
+        dw2 = torch.empty((E, f, d), **f32)
+        dg = torch.empty((T, k), **f32)
+        dx = torch.full((T, d), float("nan"), **bf) if dx0 is None else dx0.clone()
+        fl = flags | (B.MOE_ACCUMULATE if dx0 is not None else 0)
+        wsb = B.moe_ffn_bwd_combine_workspace_size(T, d, f, E, k, flags)
+        ws = torch.empty(max(wsb, 16), dtype=torch.uint8, device="cuda")
+        B.moe_ffn_bwd_combine(dy, x, w1, w3, w2, gates, offsets, eti, ss, tim, A, Bm, T, d, f, E,
+                              k, fl, dw1, dw3, dw2, dg, dx, ws, wsb)
+        torch.cuda.synchronize()
+        out.update(dw1=dw1, dw3=dw3, dw2=dw2, d_gates=dg, dx=dx)
+        return out
+
+    ref = run(False)
+    at = run(True)
+    dx1 = dev(synth.bf16_round(np.random.default_rng(9).standard_normal((T, d),
+                                                                        dtype=np.float32)))
+    at_acc = run(True, dx0=dx1)
+    for n in ("A", "dw1", "dw2", "d_gates") + (("B", "dw3") if gated else ()):
+        assert torch.equal(at[n], ref[n]), n
+    if k <= 2:
+        again = run(True)
+        assert torch.equal(again["y"], at["y"]) and torch.equal(again["dx"], at["dx"])
+    ix = oracle.build_index(ids, E)
+    if gated:
+        A_r, B_r, O_r = oracle.ffn_fwd(v["x"], v["w1"], v["w3"], v["w2"], ix, k)
+        bw = oracle.ffn_bwd(v["dy"], v["x"], v["w1"], v["w3"], v["w2"], g, ix, A_r, B_r)
+    else:
+        A_r, O_r = oracle.ffn_fwd_act(v["x"], v["w1"], v["w2"], ix, k, act)
+        bw = oracle.ffn_bwd_act(v["dy"], v["x"], v["w1"], v["w2"], g, ix, A_r, act)
+    dx_r = oracle.combine(bw["dX_slot"], None, ix.tim)
+    assert_close("y", host(at["y"]), oracle.combine(O_r, g, ix.tim), "bf16")
+    assert_close("dx", host(at["dx"]), dx_r, "bf16")
+    assert_close("dx accumulated", host(at_acc["dx"]), host(dx1) + dx_r, "bf16")
+
+
 @pytest.mark.parametrize("dtype,T,d,f,E,k,pattern,act", [c for c in COMBINED_CASES if c[0] == "bf16"])
 def test_ffn_h_on_load_bit_identical(dtype, T, d, f, E, k, pattern, act):
     """MOE_H_ON_LOAD: the second GEMM forms h from A (and B) as it loads them,
@@ -808,6 +895,39 @@ def test_layer_recompute_chunked_vs_oracle(act, hol):
     assert_close("y", host(y1), fw["y"], "bf16")
     for n in ("dx", "d_gates", "dw_gate", "dw1", "dw2") + (("dw3",) if gated else ()):
         assert_close(n, host(g1[n]), bw[n], "bf16")
+
+
+@pytest.mark.parametrize("recompute", [False, True])
+def test_layer_atomic_combine_vs_oracle(recompute):
+    """The layer with the combine folded into the GEMM epilogues
+    (atomic_combine), saving A and B or fully recomputing them: y and every
+    gradient against the oracle; the routing and the weight and gate gradients
+    equal to the strip path's (per-token dx and y differ by bf16 rounding)."""
+    cfg = synth.MoEConfig("atc", T=1500, d=256, f=384, E=16, k=4, dtype="bf16", renorm=True)
+    inp = synth.make_inputs(cfg)
+    v, st = inp.vals, inp.store
+    x, wg, w1, w3, w2, dy = (dev(st[n]) for n in ("x", "w_gate", "w1", "w3", "w2", "dy"))
+    kw = dict(recompute=True, chunk_tokens=400) if recompute else {}
+    y0, s0 = layer.forward(x, wg, None, w1, w3, w2, cfg.k, cfg.renorm, **kw)
+    g0 = layer.backward(s0, dy, x, wg, w1, w3, w2)
+    y1, s1 = layer.forward(x, wg, None, w1, w3, w2, cfg.k, cfg.renorm, atomic_combine=True, **kw)
+    assert s1.atomic_combine
+    g1 = layer.backward(s1, dy, x, wg, w1, w3, w2)
+    torch.cuda.synchronize()
+    assert torch.equal(s0.ids, s1.ids)
+    for n in ("d_gates", "dw1", "dw3", "dw2"):
+        assert torch.equal(g0[n], g1[n]), n
+    fw = oracle.layer_forward(v["x"], v["w_gate"], None, v["w1"], v["w3"], v["w2"], cfg.k,
+                              cfg.renorm)
+    assert np.array_equal(fw["ids"], s1.ids.cpu().numpy())
+    bw = oracle.layer_backward(fw, v["dy"], v["x"], v["w_gate"], v["w1"], v["w3"], v["w2"],
+                               cfg.renorm)
+    assert_close("y", host(y1), fw["y"], "bf16")
+    for n in ("dx", "d_gates", "dw_gate", "dw1", "dw3", "dw2"):
+        assert_close(n, host(g1[n]), bw[n], "bf16")
+    with pytest.raises(ValueError):
+        layer.forward(x, wg, None, w1, w3, w2, cfg.k, cfg.renorm, atomic_combine=True,
+                      separate=True)
 
 
 def test_layer_deterministic_bf16():
