@@ -27,13 +27,18 @@ from tests.parity import assert_close, dev, host, near_tie_ok
 
 pytestmark = pytest.mark.gpu
 
+# "_atomic": the combine folded into the GEMM epilogues where the layer would
+# otherwise use the ordered strips (k > 2)
 CASES = ["mid_e64k6", "few_large_e8k2", "many_small_zipf", "mem_sweep_e64k8", "zipf_empty",
-         "table1_conf4", "table1_conf1_relu", "d2880_e128k4"]
+         "table1_conf4", "table1_conf1_relu", "d2880_e128k4", "mid_e64k6_atomic",
+         "many_small_zipf_atomic"]
 NTOK = 24      # sampled tokens (half of them holding the highest slots)
 NCOL = 8       # sampled hidden columns
 
 
 def _cfg(name):
+    if name.endswith("_atomic"):   # the same workload and inputs
+        return _cfg(name[:-len("_atomic")])
     if name == "zipf_empty":
         return synth.CONFIGS["many_small_zipf"].with_(name="zipf_empty", n_dead=16)
     if name == "table1_conf1_relu":
@@ -60,7 +65,10 @@ def test_full_size_layer(name):
     bias = dev(st["bias"]) if st["bias"] is not None else None
 
     # ---- device: the benchmarked forward + backward --------------------------
-    y, saved = layer.forward(x, wg, bias, w1, w3, w2, k, cfg.renorm, act=cfg.act)
+    atomic = True if name.endswith("_atomic") else None
+    y, saved = layer.forward(x, wg, bias, w1, w3, w2, k, cfg.renorm, act=cfg.act,
+                             atomic_combine=atomic)
+    assert saved.atomic_combine == (k <= 2 or atomic is True)
     A_fwd = saved.A.clone()
     B_fwd = saved.B.clone() if gated else None
     g = layer.backward(saved, dy, x, wg, w1, w3, w2)
