@@ -106,13 +106,42 @@ CSRC = os.path.join(ROOT, "paper_2601_05296_amd", "csrc")
 COPY_BYTES = 1 << 30
 
 
-def source_digest() -> str:
-    """sha256 over the HIP sources: a traffic summary is valid only for them."""
+def code_tokens(src: str) -> str:
+    """C/C++ source without its comments, whitespace runs collapsed to one
+    space (string and character literals kept as they are)."""
+    out, i, n = [], 0, len(src)
+    while i < n:
+        c = src[i]
+        if c in "\"'":                                  # literal
+            j = i + 1
+            while j < n and src[j] != c:
+                j += 2 if src[j] == "\\" else 1
+            out.append(src[i:j + 1])
+            i = j + 1
+        elif src.startswith("//", i):
+            j = src.find("\n", i)
+            i = n if j < 0 else j
+            out.append(" ")
+        elif src.startswith("/*", i):
+            j = src.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        else:
+            out.append(c)
+            i += 1
+    return " ".join("".join(out).split())
+
+
+def source_digest(csrc: str = CSRC) -> str:
+    """sha256 over the code of the HIP sources (comments and layout left out):
+    a traffic summary is valid only for that code."""
     import hashlib
     h = hashlib.sha256()
-    for name in sorted(os.listdir(CSRC)):
-        with open(os.path.join(CSRC, name), "rb") as fh:
-            h.update(name.encode() + b"\0" + fh.read())
+    for name in sorted(os.listdir(csrc)):
+        if not name.endswith((".hip", ".hpp", ".cpp", ".h")):
+            continue
+        with open(os.path.join(csrc, name), encoding="utf-8") as fh:
+            h.update(name.encode() + b"\0" + code_tokens(fh.read()).encode())
     return h.hexdigest()
 
 

@@ -263,6 +263,8 @@ int moe_ffn_recompute(const void* x, const void* w1, const void* w3,
  * each strip is combined into y before the next one is computed (Section 2.3
  * aggregation, Section 3.1). Same arithmetic and summation order as the two
  * separate calls, so the result is identical and deterministic.
+ * MOE_ATOMIC_COMBINE instead folds the combine into the second GEMM's
+ * epilogue (no strip; see the flag).
  * In:  as moe_ffn_fwd, plus gates [T,k] float32 and token_index_map [T,k].
  * Out: A, B as moe_ffn_fwd; y [T,d] (element type per flags).
  * workspace: moe_ffn_fwd_combine_workspace_size(T,d,f,E,k,flags) bytes (h and
@@ -282,7 +284,8 @@ int moe_ffn_fwd_combine(const void* x, const void* w1, const void* w3, const voi
  * step 3, without the [T*k, d] dX_slot buffer: dX_slot is produced one column
  * strip at a time in the workspace (reusing the space of g*h, which the dw2
  * GEMM has consumed by then) and each strip is summed into dx. Identical to
- * the two separate calls.
+ * the two separate calls. MOE_ATOMIC_COMBINE instead adds the dX_slot rows
+ * into dx from the dX GEMM's epilogue (no strip; see the flag).
  * In:  as moe_ffn_bwd, plus token_index_map [T,k].
  * Out: as moe_ffn_bwd, with dx [T,d] in place of dX_slot; MOE_ACCUMULATE adds
  *      into dx instead of overwriting it.

@@ -24,6 +24,11 @@
 // The token gradient is then a unit-weight combine (combine.hip). Forming h
 // on load costs the second GEMMs a second operand stream and an in-LDS pass
 // per K slice; it returns the same bits.
+// The combined calls (moe_ffn_fwd_combine / moe_ffn_bwd_combine) run G2 and
+// G6 over column strips, each followed by the ordered combine; with
+// MOE_ATOMIC_COMBINE they run once, and the epilogue adds each slot row
+// (times its gate in the forward) into the token's row of y or dx by
+// packed-bf16 atomics (Section 3.1's reduction as the outputs are produced).
 //
 // Row-wise GEMMs (G1, G2, G4, G6) tile each expert's slot segment; their grid
 // is sized for the worst case (S/BM + E tiles per column block) and each
