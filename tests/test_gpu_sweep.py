@@ -1,5 +1,6 @@
 """GPU parity at the memory-sweep sizes (d=4096, f=2048, E=64, k=8): T = 2^20
-tokens with the buffered h policy and T = 2^21 with h formed on load, the
+tokens with the buffered h policy and T = 2^21 with h formed on load (with the
+ordered strip combine, and with the combine folded into the GEMM epilogues), the
 largest T each policy fits in one GPU's memory (paper Sections 3.1-3.2: the
 method exists to run larger T in the same memory). Here S = T*k reaches 2^24
 slots, and slot-row element offsets (slot * f) pass 2^31.
@@ -34,7 +35,10 @@ from tests.parity import assert_close, host, near_tie_ok
 
 pytestmark = pytest.mark.gpu
 
-CASES = [("sweep_T2^20_buffered", 1 << 20, False), ("sweep_T2^21_h_on_load", 1 << 21, True)]
+# name, T, h on load, combine folded into the GEMM epilogues (atomics)
+CASES = [("sweep_T2^20_buffered", 1 << 20, False, False),
+         ("sweep_T2^21_h_on_load", 1 << 21, True, False),
+         ("sweep_T2^21_h_on_load_atomic", 1 << 21, True, True)]
 NTOK = 16
 NCOL = 8
 CHUNK = 1 << 17      # tokens per host chunk of the oracle's routing
@@ -70,13 +74,13 @@ def check_maps(ids, counts, offsets, eti, tim, slot_src, E):
     assert np.all(step_up[inner] > 0)                                   # ascending tokens
 
 
-@pytest.mark.parametrize("name,T,hol", CASES)
-def test_memory_sweep_size(name, T, hol):
+@pytest.mark.parametrize("name,T,hol,atomic", CASES)
+def test_memory_sweep_size(name, T, hol, atomic):
     cfg = synth.CONFIGS["mem_sweep_e64k8"].with_(T=T)
     d, f, E, k = cfg.d, cfg.f, cfg.E, cfg.k
     S = T * k
-    step("sweep case %s: T=%d d=%d f=%d E=%d k=%d h_on_load=%s (S*f = %d elements)"
-         % (name, T, d, f, E, k, hol, S * f))
+    step("sweep case %s: T=%d d=%d f=%d E=%d k=%d h_on_load=%s atomic combine=%s "
+         "(S*f = %d elements)" % (name, T, d, f, E, k, hol, atomic, S * f))
     inp = synth.device_inputs(cfg, "cuda")
     x, wg, w1, w3, w2, dy = (inp[n] for n in ("x", "w_gate", "w1", "w3", "w2", "dy"))
 
@@ -106,8 +110,10 @@ def test_memory_sweep_size(name, T, hol):
 
     # ---- the layer, forward -------------------------------------------------------
     step("  layer forward")
-    y, saved = layer.forward(x, wg, None, w1, w3, w2, k, cfg.renorm, h_on_load=hol)
+    y, saved = layer.forward(x, wg, None, w1, w3, w2, k, cfg.renorm, h_on_load=hol,
+                             atomic_combine=atomic)
     torch.cuda.synchronize()
+    assert saved.atomic_combine == atomic
     ids_g = saved.ids.cpu().numpy()
     nflip = near_tie_ok(ids_g, ids_r, logits_r)
     assert nflip <= max(2, T // 5000), nflip
@@ -184,7 +190,8 @@ def test_memory_sweep_size(name, T, hol):
     torch.cuda.empty_cache()
     acc = None
     for h0, h1 in ((0, T // 2), (T // 2, T)):
-        yh, sh = layer.forward(x[h0:h1], wg, None, w1, w3, w2, k, cfg.renorm, h_on_load=hol)
+        yh, sh = layer.forward(x[h0:h1], wg, None, w1, w3, w2, k, cfg.renorm, h_on_load=hol,
+                               atomic_combine=atomic)
         gh = layer.backward(sh, dy[h0:h1], x[h0:h1], wg, w1, w3, w2)
         del yh, sh
         part = {n: gh[n] for n in full}
