@@ -244,8 +244,9 @@ __device__ __forceinline__ void slot_rows(const rs::Acc<C>& acc, const SlotTile&
     else slot_rows_out<C>(acc, t, ncols, ldo, O);
 }
 
-// G2: O = H W2[e], output columns [n_base, n_base + ncols) into rows ldo apart
-// (SCATTER: added into the token rows, see slot_rows_out)
+// G2: O = H W2[e], output columns [n_base, n_base + ncols) of W2 into columns
+// [0, ncols) of O, rows ldo apart (SCATTER: added into the token rows, see
+// slot_rows_scatter)
 template <bool SCATTER>
 __global__ void __launch_bounds__(RS::THREADS)
 g2_kernel(const bf16_t* __restrict__ H, const bf16_t* __restrict__ w2,
