@@ -972,6 +972,47 @@ def test_layer_on_a_side_stream():
         layer.forward(x, wg, None, w1, w3, w2, cfg.k, cfg.renorm, stream=side.cuda_stream)
 
 
+@pytest.mark.parametrize("k", [2, 4])
+def test_layer_graph_replay(k):
+    """The whole layer step, forward and backward through every entry point,
+    captured in a HIP graph (the library allocates nothing, clears memory with
+    kernels rather than memsets, and never synchronises): every replay, with
+    eager steps between the replays, gives the eager step's bits. k = 2 runs
+    the combine folded into the GEMM epilogues, k = 4 the strips."""
+    cfg = synth.MoEConfig("gr", T=1500, d=256, f=384, E=16, k=k, dtype="bf16", renorm=True)
+    inp = synth.make_inputs(cfg)
+    st = inp.store
+    x, wg, w1, w3, w2, dy = (dev(st[n]) for n in ("x", "w_gate", "w1", "w3", "w2", "dy"))
+    names = ("dx", "dw1", "dw3", "dw2", "dw_gate", "d_gates")
+
+    def step():
+        y, s = layer.forward(x, wg, None, w1, w3, w2, cfg.k, cfg.renorm)
+        return y, s, layer.backward(s, dy, x, wg, w1, w3, w2)
+
+    y0, s0, g0 = step()
+    torch.cuda.synchronize()
+    assert s0.atomic_combine == (k <= 2)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):        # warm-up on a side stream before the capture
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        y1, _, g1 = step()
+    for r in range(3):
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y1, y0), r
+        for n in names:
+            assert torch.equal(g1[n], g0[n]), (r, n)
+        y2, _, g2 = step()               # eager work between the replays
+        torch.cuda.synchronize()
+        assert torch.equal(y2, y0) and torch.equal(g2["dx"], g0["dx"]), r
+    del graph
+
+
 def test_error_codes_launch_nothing():
     """The library's own validation, reached with raw device addresses (the
     binding checks tensor sizes and dtypes, not raw addresses)."""
