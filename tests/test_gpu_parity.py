@@ -657,6 +657,9 @@ ATOMIC_CASES = [
     (100, 64, 64, 2, 2, None, "swiglu", True),
     (1000, 512, 320, 64, 8, None, "swiglu", True),
     (3000, 256, 128, 32, 6, "zipf", "swiglu", True),
+    # a single expert with top-1; 256 experts with top-16 (16 adds into each row)
+    (100, 64, 64, 1, 1, None, "swiglu", True),
+    (300, 128, 128, 256, 16, None, "swiglu", False),
 ]
 
 
