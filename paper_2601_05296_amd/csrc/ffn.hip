@@ -271,22 +271,27 @@ g2_kernel(const bf16_t* __restrict__ H, const bf16_t* __restrict__ w2,
     slot_rows<SCATTER, C>(acc, t, ncols, ldo, O, tok, gs, lds);
 }
 
-// h of a pair of elements (one dword of bf16) from the pairs of A and B: the
-// arithmetic of G1's epilogue, on the same bf16 values, so the result is
-// bit-identical to the buffered h. Non-gated: act(A), B unused. With a gate
-// g: g * h, the arithmetic of G4's epilogue for the dW2 GEMM's operand.
+// h of one element from its (bf16-valued) A and B: the arithmetic of G1's
+// epilogue, on the same values, so the result is bit-identical to the
+// buffered h. Non-gated: act(A), B unused. With a gate g: g * h, the
+// arithmetic of G4's epilogue for the dW2 GEMM's operand.
 template <int ACT, bool GATE>
-__device__ __forceinline__ uint32_t h_pair(uint32_t a, uint32_t b, float g) {
-    float h0, h1;
-    if constexpr (ACT == ACT_SWIGLU) {
-        h0 = silu_bf(bf_lo(a)) * bf_lo(b);
-        h1 = silu_bf(bf_hi(a)) * bf_hi(b);
-    } else {
-        h0 = act_f<ACT>(bf_lo(a));
-        h1 = act_f<ACT>(bf_hi(a));
-    }
-    if constexpr (GATE) { h0 = g * h0; h1 = g * h1; }
-    return pack_bf2(h0, h1);
+__device__ __forceinline__ float h_one(float a, float b, float g) {
+    float h;
+    if constexpr (ACT == ACT_SWIGLU) h = silu_bf(a) * b;
+    else h = act_f<ACT>(a);
+    if constexpr (GATE) h = g * h;
+    return h;
+}
+// h of element pair dword p of (va, vb) as two transform pieces of one element
+// each: piece 2p forms the low element into hl, piece 2p+1 the high one and
+// packs the pair in place of va's dword (pieces of one element keep the
+// vector work between two MFMAs short)
+template <int ACT, bool GATE, int P>
+__device__ __forceinline__ void h_piece(rs::u32x4& va, const rs::u32x4& vb, float g, float& hl) {
+    constexpr int q = P >> 1;
+    if constexpr ((P & 1) == 0) hl = h_one<ACT, GATE>(bf_lo(va[q]), bf_lo(vb[q]), g);
+    else va[q] = pack_bf2(hl, h_one<ACT, GATE>(bf_hi(va[q]), bf_hi(vb[q]), g));
 }
 
 // Left operand of the second GEMM with h formed on load: KC tile of h rows
@@ -316,9 +321,10 @@ struct HKC {
         va[i] = rs::ldg16(q);
         if constexpr (GATED) vb[i] = rs::ldg16(q + dba);
     }
-    // h of dword p of chunk i, in place of A's
-    static constexpr int NSUB = 4;
-    template <int i, int p> __device__ void sub() { va[i][p] = h_pair<ACT, false>(va[i][p], vb[i][p], 0.f); }
+    // h of chunk i in place of A's, one element per piece
+    static constexpr int NSUB = 8;
+    float hl;
+    template <int i, int p> __device__ void sub() { h_piece<ACT, false, p>(va[i], vb[i], 0.f, hl); }
     template <int i, bool TAIL> __device__ void store(char* tile) { rs::sts16(tile + G::lds(i), va[i]); }
 };
 
@@ -583,9 +589,10 @@ struct GHMC {
         if constexpr (GATED) vb[i] = rs::ldg16(q + dba);
         g[i] = gsp[k];
     }
-    // g * h of dword p of chunk i, in place of A's
-    static constexpr int NSUB = 4;
-    template <int i, int p> __device__ void sub() { va[i][p] = h_pair<ACT, true>(va[i][p], vb[i][p], g[i]); }
+    // g * h of chunk i in place of A's, one element per piece
+    static constexpr int NSUB = 8;
+    float hl;
+    template <int i, int p> __device__ void sub() { h_piece<ACT, true, p>(va[i], vb[i], g[i], hl); }
     template <int i, bool TAIL> __device__ void store(char* tile) {
         const rs::u32x4 z = {0u, 0u, 0u, 0u};
         if constexpr (TAIL) rs::sts16(tile + G::lds(i), (zmask >> i) & 1 ? z : va[i]);

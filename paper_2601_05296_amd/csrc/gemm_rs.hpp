@@ -187,10 +187,10 @@ struct NoLoader {
 // pieces, its LDS write (slice kt+1) and its load (slice kt+2). The chunks of
 // the loaders are interleaved in proportion to their numbers, and every
 // operation is placed after one of the slice's NPOS MFMAs before the barrier,
-// by its cumulative weight: a transform piece (h of one dword pair: some 13
-// vector instructions and 4 transcendentals) weighs W_PIECE, a memory
+// by its cumulative weight: a transform piece (h of one element: some 6
+// vector instructions and 2 transcendentals) weighs W_PIECE, a memory
 // instruction 1, so that the vector work is spread evenly between the MFMAs.
-constexpr int W_PIECE = 8;
+constexpr int W_PIECE = 4;
 template <int MAXN>
 struct SliceOps {
     int n = 0;
