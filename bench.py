@@ -57,6 +57,9 @@ def parse():
     ap.add_argument("--strip-combine", dest="atomic_combine", action="store_false",
                     help="combine strip by strip with the ordered gather-reduce")
     ap.set_defaults(atomic_combine=None)
+    ap.add_argument("--graph", action="store_true",
+                    help="also time the step captured once in a HIP graph and replayed "
+                         "(graph_replay in the JSON line; the main figures stay eager)")
     ap.add_argument("--recompute", action="store_true",
                     help="full-recompute checkpoint policy: save only the routing decision; the "
                          "dispatch and the expert FFN run over token chunks, and the backward "
@@ -931,6 +934,30 @@ def main():
         "sparse_to_sparse_tokens_per_s": round(T / ((ms_step - router_ms) * 1e-3), 1),
         "kernels": kernels,
     }
+    if args.graph:
+        # the same step captured once in a HIP graph (every entry point is
+        # capturable: no allocation, memset or synchronisation inside), then
+        # replayed: the launch overhead the eager step pays is the difference
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        graph.replay()
+        torch.cuda.synchronize()
+        g0 = time.perf_counter()
+        for _ in range(args.steps):
+            graph.replay()
+        torch.cuda.synchronize()
+        g1 = time.perf_counter()
+        del graph
+        out["graph_replay"] = {"steps": args.steps,
+                               "ms_per_step": round((g1 - g0) * 1e3 / args.steps, 4),
+                               "tokens_per_s": round(T * args.steps / (g1 - g0), 1)}
     if not (args.recompute or args.no_baseline_memory):
         # the other operating point of the same layer: the other h policy
         # (bit-identical results; buffering h and g*h costs memory, forming
