@@ -934,6 +934,23 @@ def main():
         "sparse_to_sparse_tokens_per_s": round(T / ((ms_step - router_ms) * 1e-3), 1),
         "kernels": kernels,
     }
+    # the same steps with the 256 MB MALL evicted before each one (a 1 GiB
+    # scratch fill between steps, outside the events that time the step)
+    scratch = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    fl = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for i in range(args.steps):
+        scratch.fill_(i & 0x7F)
+        fl[i][0].record()
+        step()
+        fl[i][1].record()
+    torch.cuda.synchronize()
+    del scratch
+    flushed = [a.elapsed_time(b) for a, b in fl]
+    out["mall_flushed"] = {"steps": args.steps,
+                           "ms_per_step_median": round(float(np.median(flushed)), 4),
+                           "ms_per_step_min_max": [round(min(flushed), 4), round(max(flushed), 4)]}
     if args.graph:
         # the same step captured once in a HIP graph (every entry point is
         # capturable: no allocation, memset or synchronisation inside), then
