@@ -89,7 +89,8 @@ extern "C" {
  * output nor any strip of it is held: the forward workspace drops the strip
  * and holds T*k float32 slot gates instead, the backward's drops the strip.
  * y (dx, unless MOE_ACCUMULATE) is cleared first. Each atomic add rounds to
- * bfloat16, so a token's k terms are rounded k times, not once, and for k > 2
+ * bfloat16, so a token's k terms are rounded k times, not once (the error
+ * grows with k: about 3x the ordered combine's at k = 15), and for k > 2
  * (or with MOE_ACCUMULATE) the result depends on the order in which tiles
  * finish: it is not deterministic bit for bit. With k <= 2 and no
  * MOE_ACCUMULATE it is (bfloat16 addition of two terms onto zero does not

@@ -933,6 +933,72 @@ def test_layer_atomic_combine_vs_oracle(recompute):
                       separate=True)
 
 
+def _random_layer_cases(n=16, seed=2601, tmax=700, wmax=8, emax=32, kmax=8, i0=0):
+    """Seeded random shapes over the whole option space: T, d, f (multiples
+    of 64 up to 64 wmax), E, k, activation, h policy, combine mode, renorm."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(i0, i0 + n):
+        E = int(rng.integers(1, emax + 1))
+        k = int(rng.integers(1, min(E, kmax) + 1))
+        cases.append(dict(i=i, T=int(rng.integers(1, tmax)), d=64 * int(rng.integers(1, wmax + 1)),
+                          f=64 * int(rng.integers(1, wmax + 1)), E=E, k=k,
+                          act=("swiglu", "silu", "relu")[int(rng.integers(3))],
+                          hol=bool(rng.integers(2)), atomic=bool(rng.integers(2)),
+                          renorm=bool(rng.integers(2))))
+    return cases
+
+
+@pytest.mark.parametrize("c", _random_layer_cases() +
+                         _random_layer_cases(n=16, seed=2602, tmax=2500, wmax=16, emax=256,
+                                             kmax=16, i0=16),
+                         ids=lambda c: "r%d" % c["i"])
+def test_layer_random_shapes_vs_oracle(c):
+    """The layer on seeded random small shapes against the oracle: y and every
+    gradient within the bf16 tolerance, the routing equal up to near-ties
+    (the oracle is then run on the device's choices)."""
+    cfg = synth.MoEConfig("rnd%d" % c["i"], T=c["T"], d=c["d"], f=c["f"], E=c["E"], k=c["k"],
+                          dtype="bf16", renorm=c["renorm"], act=c["act"], seed=300 + c["i"])
+    inp = synth.make_inputs(cfg)
+    v, st = inp.vals, inp.store
+    gated = c["act"] == "swiglu"
+    x, wg, w1, w2, dy = (dev(st[n]) for n in ("x", "w_gate", "w1", "w2", "dy"))
+    w3 = dev(st["w3"]) if gated else None
+    y, s = layer.forward(x, wg, None, w1, w3, w2, cfg.k, cfg.renorm, act=cfg.act,
+                         h_on_load=c["hol"], atomic_combine=c["atomic"])
+    g = layer.backward(s, dy, x, wg, w1, w3, w2)
+    torch.cuda.synchronize()
+    ids_g = s.ids.cpu().numpy()
+    ids_r, _, logits_r, _ = oracle.route(v["x"], v["w_gate"], None, cfg.k, cfg.renorm)
+    near_tie_ok(ids_g, ids_r, logits_r)
+    fw = oracle.layer_forward(v["x"], v["w_gate"], None, v["w1"], v["w3"], v["w2"], cfg.k,
+                              cfg.renorm, ids=ids_g, act=cfg.act)
+    bw = oracle.layer_backward(fw, v["dy"], v["x"], v["w_gate"], v["w1"], v["w3"], v["w2"],
+                               cfg.renorm)
+    assert_close("y", host(y), fw["y"], "bf16")
+    keep_dx = np.ones(cfg.T, dtype=bool)
+    keep_dw1 = np.ones(bw["dw1"].shape, dtype=bool)
+    if cfg.act == "relu":
+        # ReLU'(A) is decided on the device's bf16 A: where the oracle's A is
+        # within 1e-4 max|A| of zero either decision is valid (as in the other
+        # ReLU tests), and a flipped one moves a whole term of the token's dx
+        # and of its expert's dW1 column; those are left out, found from the
+        # oracle's A alone
+        A_r, ix = fw["A"], fw["ix"]
+        tie = np.abs(A_r) < 1e-4 * np.abs(A_r).max()
+        assert tie.mean() < 1e-3
+        tok_of_slot = ix.eti[: A_r.shape[0]]
+        keep_dx[np.unique(tok_of_slot[tie.any(axis=1)])] = False
+        for e in range(cfg.E):
+            lo, hi = ix.offsets[e], ix.offsets[e + 1]
+            keep_dw1[e][:, tie[lo:hi].any(axis=0)] = False
+    assert_close("dx", host(g["dx"])[keep_dx], bw["dx"][keep_dx], "bf16")
+    assert_close("dw1", np.where(keep_dw1, host(g["dw1"]), 0), np.where(keep_dw1, bw["dw1"], 0),
+                 "bf16")
+    for n in ("d_gates", "dw_gate", "dw2") + (("dw3",) if gated else ()):
+        assert_close(n, host(g[n]), bw[n], "bf16")
+
+
 def test_layer_deterministic_bf16():
     cfg = synth.MoEConfig("det", T=2000, d=256, f=256, E=16, k=4, dtype="bf16", renorm=True)
     inp = synth.make_inputs(cfg)
