@@ -13,8 +13,9 @@ Backward (Section 3.2):
 ``recompute=True`` is the full-recompute checkpoint policy (Section 5.2's
 checkpoint carried one step further): the forward keeps only the routing
 decision (ids, gates, logits). It runs the dispatch and the expert FFN over
-chunks of tokens (``chunk_tokens``; by default as many tokens as keep a
-chunk's A and B within 4 GiB), so that A, B and the maps of no more than one
+chunks of tokens (``chunk_tokens``, rounded down to a multiple of 4 tokens;
+by default as many tokens as keep a chunk's A and B within 4 GiB), so that
+A, B and the maps of no more than one
 chunk exist at a time. The backward rebuilds each chunk's maps, recomputes its
 A and B with moe_ffn_recompute (bit-identical to the forward's), and adds the
 chunk's weight gradients into the layer's (MOE_ACCUMULATE_DW). Per token, y,
@@ -112,6 +113,16 @@ def default_chunk(T: int, k: int, f: int, gated: bool, elem: int) -> int:
     return int(max(1, min(T, max(4096, (4 << 30) // per_token))))
 
 
+def aligned_chunk(chunk: int, T: int) -> int:
+    """A chunk of T tokens as the chunked calls take it: all of T, or a
+    multiple of 4 tokens (at least 4), so that every chunk's rows of the
+    [T, k] routing arrays (4-byte elements) start 16-byte aligned, as the C
+    ABI requires of its pointers."""
+    if chunk >= T:
+        return T
+    return max(4, chunk - chunk % 4)
+
+
 def _on(stream):
     """Run a layer call on `stream` (a torch.cuda.Stream; None: torch's current
     stream). The temporaries are allocated under it too, so the caching
@@ -184,7 +195,7 @@ def _forward_recompute(x, w_gate, bias, w1, w3, w2, k, renorm, act, h_on_load, c
     flags = B.dtype_flag(x)
     gated = act == "swiglu"
     ids, gates, logits = _route(x, w_gate, bias, E, k, renorm, flags)
-    chunk = chunk_tokens or default_chunk(T, k, f, gated, x.element_size())
+    chunk = aligned_chunk(chunk_tokens or default_chunk(T, k, f, gated, x.element_size()), T)
     fflags = (flags | B.ACT_FLAG[act] | (B.MOE_H_ON_LOAD if h_on_load else 0)
               | (B.MOE_ATOMIC_COMBINE if atomic_combine else 0))
     y = torch.empty((T, d), dtype=x.dtype, device=x.device)

@@ -933,7 +933,7 @@ def test_layer_atomic_combine_vs_oracle(recompute):
                       separate=True)
 
 
-def _random_layer_cases(n=16, seed=2601, tmax=700, wmax=8, emax=32, kmax=8, i0=0):
+def _random_layer_cases(n=16, seed=2601, tmax=700, wmax=8, emax=32, kmax=8, i0=0, modes=False):
     """Seeded random shapes over the whole option space: T, d, f (multiples
     of 64 up to 64 wmax), E, k, activation, h policy, combine mode, renorm."""
     rng = np.random.default_rng(seed)
@@ -946,27 +946,39 @@ def _random_layer_cases(n=16, seed=2601, tmax=700, wmax=8, emax=32, kmax=8, i0=0
                           act=("swiglu", "silu", "relu")[int(rng.integers(3))],
                           hol=bool(rng.integers(2)), atomic=bool(rng.integers(2)),
                           renorm=bool(rng.integers(2))))
+        if modes:   # also the calling mode, the chunking and the element type
+            mode = ("combined", "separate", "recompute")[int(rng.integers(3))]
+            dtype = "f32" if rng.random() < 0.25 else "bf16"
+            cases[-1].update(mode=mode, dtype=dtype,
+                             chunk=int(rng.integers(1, cases[-1]["T"] + 1)))
+            if mode == "separate" or dtype == "f32":
+                cases[-1]["atomic"] = False
     return cases
 
 
 @pytest.mark.parametrize("c", _random_layer_cases() +
                          _random_layer_cases(n=16, seed=2602, tmax=2500, wmax=16, emax=256,
-                                             kmax=16, i0=16),
+                                             kmax=16, i0=16) +
+                         _random_layer_cases(n=16, seed=2603, tmax=1500, wmax=8, emax=64,
+                                             kmax=8, i0=32, modes=True),
                          ids=lambda c: "r%d" % c["i"])
 def test_layer_random_shapes_vs_oracle(c):
     """The layer on seeded random small shapes against the oracle: y and every
     gradient within the bf16 tolerance, the routing equal up to near-ties
     (the oracle is then run on the device's choices)."""
+    dtype, mode = c.get("dtype", "bf16"), c.get("mode", "combined")
     cfg = synth.MoEConfig("rnd%d" % c["i"], T=c["T"], d=c["d"], f=c["f"], E=c["E"], k=c["k"],
-                          dtype="bf16", renorm=c["renorm"], act=c["act"], seed=300 + c["i"])
+                          dtype=dtype, renorm=c["renorm"], act=c["act"], seed=300 + c["i"])
     inp = synth.make_inputs(cfg)
     v, st = inp.vals, inp.store
     gated = c["act"] == "swiglu"
     x, wg, w1, w2, dy = (dev(st[n]) for n in ("x", "w_gate", "w1", "w2", "dy"))
     w3 = dev(st["w3"]) if gated else None
+    extra = dict(separate=True) if mode == "separate" else \
+        dict(recompute=True, chunk_tokens=c["chunk"]) if mode == "recompute" else {}
     y, s = layer.forward(x, wg, None, w1, w3, w2, cfg.k, cfg.renorm, act=cfg.act,
-                         h_on_load=c["hol"], atomic_combine=c["atomic"])
-    g = layer.backward(s, dy, x, wg, w1, w3, w2)
+                         h_on_load=c["hol"], atomic_combine=c["atomic"], **extra)
+    g = layer.backward(s, dy, x, wg, w1, w3, w2, separate=mode == "separate")
     torch.cuda.synchronize()
     ids_g = s.ids.cpu().numpy()
     ids_r, _, logits_r, _ = oracle.route(v["x"], v["w_gate"], None, cfg.k, cfg.renorm)
@@ -975,7 +987,7 @@ def test_layer_random_shapes_vs_oracle(c):
                               cfg.renorm, ids=ids_g, act=cfg.act)
     bw = oracle.layer_backward(fw, v["dy"], v["x"], v["w_gate"], v["w1"], v["w3"], v["w2"],
                                cfg.renorm)
-    assert_close("y", host(y), fw["y"], "bf16")
+    assert_close("y", host(y), fw["y"], dtype)
     keep_dx = np.ones(cfg.T, dtype=bool)
     keep_dw1 = np.ones(bw["dw1"].shape, dtype=bool)
     if cfg.act == "relu":
@@ -992,11 +1004,11 @@ def test_layer_random_shapes_vs_oracle(c):
         for e in range(cfg.E):
             lo, hi = ix.offsets[e], ix.offsets[e + 1]
             keep_dw1[e][:, tie[lo:hi].any(axis=0)] = False
-    assert_close("dx", host(g["dx"])[keep_dx], bw["dx"][keep_dx], "bf16")
+    assert_close("dx", host(g["dx"])[keep_dx], bw["dx"][keep_dx], dtype)
     assert_close("dw1", np.where(keep_dw1, host(g["dw1"]), 0), np.where(keep_dw1, bw["dw1"], 0),
-                 "bf16")
+                 dtype)
     for n in ("d_gates", "dw_gate", "dw2") + (("dw3",) if gated else ()):
-        assert_close(n, host(g[n]), bw[n], "bf16")
+        assert_close(n, host(g[n]), bw[n], dtype)
 
 
 def test_layer_deterministic_bf16():
