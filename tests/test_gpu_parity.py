@@ -950,7 +950,9 @@ def _random_layer_cases(n=16, seed=2601, tmax=700, wmax=8, emax=32, kmax=8, i0=0
             mode = ("combined", "separate", "recompute")[int(rng.integers(3))]
             dtype = "f32" if rng.random() < 0.25 else "bf16"
             cases[-1].update(mode=mode, dtype=dtype,
-                             chunk=int(rng.integers(1, cases[-1]["T"] + 1)))
+                             chunk=int(rng.integers(1, cases[-1]["T"] + 1)),
+                             zipf=float(rng.choice([0.0, 1.2])),
+                             dead=int(rng.integers(0, (E - k) // 2 + 1)))
             if mode == "separate" or dtype == "f32":
                 cases[-1]["atomic"] = False
     return cases
@@ -968,22 +970,24 @@ def test_layer_random_shapes_vs_oracle(c):
     (the oracle is then run on the device's choices)."""
     dtype, mode = c.get("dtype", "bf16"), c.get("mode", "combined")
     cfg = synth.MoEConfig("rnd%d" % c["i"], T=c["T"], d=c["d"], f=c["f"], E=c["E"], k=c["k"],
-                          dtype=dtype, renorm=c["renorm"], act=c["act"], seed=300 + c["i"])
+                          dtype=dtype, renorm=c["renorm"], act=c["act"], seed=300 + c["i"],
+                          zipf_s=c.get("zipf", 0.0), n_dead=c.get("dead", 0))
     inp = synth.make_inputs(cfg)
     v, st = inp.vals, inp.store
+    bias = dev(st["bias"]) if st["bias"] is not None else None
     gated = c["act"] == "swiglu"
     x, wg, w1, w2, dy = (dev(st[n]) for n in ("x", "w_gate", "w1", "w2", "dy"))
     w3 = dev(st["w3"]) if gated else None
     extra = dict(separate=True) if mode == "separate" else \
         dict(recompute=True, chunk_tokens=c["chunk"]) if mode == "recompute" else {}
-    y, s = layer.forward(x, wg, None, w1, w3, w2, cfg.k, cfg.renorm, act=cfg.act,
+    y, s = layer.forward(x, wg, bias, w1, w3, w2, cfg.k, cfg.renorm, act=cfg.act,
                          h_on_load=c["hol"], atomic_combine=c["atomic"], **extra)
     g = layer.backward(s, dy, x, wg, w1, w3, w2, separate=mode == "separate")
     torch.cuda.synchronize()
     ids_g = s.ids.cpu().numpy()
-    ids_r, _, logits_r, _ = oracle.route(v["x"], v["w_gate"], None, cfg.k, cfg.renorm)
+    ids_r, _, logits_r, _ = oracle.route(v["x"], v["w_gate"], v["bias"], cfg.k, cfg.renorm)
     near_tie_ok(ids_g, ids_r, logits_r)
-    fw = oracle.layer_forward(v["x"], v["w_gate"], None, v["w1"], v["w3"], v["w2"], cfg.k,
+    fw = oracle.layer_forward(v["x"], v["w_gate"], v["bias"], v["w1"], v["w3"], v["w2"], cfg.k,
                               cfg.renorm, ids=ids_g, act=cfg.act)
     bw = oracle.layer_backward(fw, v["dy"], v["x"], v["w_gate"], v["w1"], v["w3"], v["w2"],
                                cfg.renorm)
