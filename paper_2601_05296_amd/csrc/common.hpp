@@ -79,11 +79,15 @@ __device__ __forceinline__ float sigmoidf_(float u) {
 // ---- memory helpers -----------------------------------------------------------
 __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
 __device__ __forceinline__ void st16(void* p, const uint4& v) { *reinterpret_cast<uint4*>(p) = v; }
-// streaming store of 16 bytes; only for stores that cover whole 128-byte lines
-// (partial-line nontemporal stores measured slower than plain ones)
+// streaming store of 16 bytes to global memory; only for stores that cover
+// whole 128-byte lines (partial-line nontemporal stores measured slower than
+// plain ones). The pointer is cast to the global address space: where the
+// compiler cannot infer it, it would otherwise emit a flat store, which also
+// counts as an LDS access for the wait counters.
 __device__ __forceinline__ void st16_nt(void* p, const uint4& v) {
     typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
-    __builtin_nontemporal_store(u32x4_t{v.x, v.y, v.z, v.w}, reinterpret_cast<u32x4_t*>(p));
+    typedef __attribute__((address_space(1))) u32x4_t* gptr_t;
+    __builtin_nontemporal_store(u32x4_t{v.x, v.y, v.z, v.w}, (gptr_t)p);
 }
 __device__ __forceinline__ uint4 zero16() { return make_uint4(0u, 0u, 0u, 0u); }
 

@@ -418,13 +418,35 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
             dma16(src, lds_base + (i & 1) * BUF + arr * ARR + qq * 1024);
         }
     };
+    // The gates of this lane's rows in every round, loaded (and waited for,
+    // by a wait the compiler sees) before the first copy is issued. The
+    // compiler does not see the copies: a load of its own issued after them
+    // would end in a wait for all outstanding loads, copies included, and
+    // each round's copies would then no longer overlap the round before.
+    float gr[C::FM];
+#pragma unroll
+    for (int i = 0; i < C::FM; ++i) {
+        const int m = wc.row(i);
+        gr[i] = gates[slot_src[(int64_t)t.off + t.m0 + (m < t.mrows ? m : 0)]];
+    }
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+    // Stores a round issues after the copies of the next round: the d_gate
+    // partial, the dA (dB) row chunks, the g*h chunks.
+    constexpr int NSTORE = 1 + NARR * RR * CPR / C::THREADS + (HG_OUT ? 2 * C::FN : 0);
+    // In a full tile every one of them is issued by every wave (no lane
+    // condition empties a wave's execution mask).
+    const bool full = t.mrows >= C::BM && t.n0 + C::BN <= f;
     issue_round(0);
 #pragma unroll
     for (int i = 0; i < C::FM; ++i) {
-        // round i's rows have landed (and round i-1's stores have completed);
-        // buffer (i+1) & 1 was last read by round i-1's stores, before its
-        // closing barrier
-        wait_vmcnt<0>();
+        // Round i's rows have landed. The wait counter counts vector-memory
+        // operations down in issue order, so in a full tile, once at most
+        // NSTORE remain, round i's copies (issued before round i-1's stores)
+        // are done and the stores may still be in flight. Otherwise wait for
+        // everything. Buffer (i+1) & 1 was last read by round i-1's stores,
+        // before its closing barrier.
+        if (i > 0 && full) wait_vmcnt<NSTORE>();
+        else wait_vmcnt<0>();
         barrier_only();
         if (i + 1 < C::FM) issue_round(i + 1);
         char* const buf = lds + (i & 1) * BUF;
@@ -433,7 +455,7 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
         const int m = wc.row(i);
         const bool valid = m < t.mrows;
         const int64_t s = (int64_t)t.off + t.m0 + (valid ? m : 0);
-        const float g = gates[slot_src[s]];
+        const float g = gr[i];
         char* rowA = buf + rr * RB;
         char* rowB = buf + ARR + rr * RB;
         float dg = 0.f;
