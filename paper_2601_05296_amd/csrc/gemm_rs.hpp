@@ -39,7 +39,12 @@
 //    groups of the 64 banks, and a chunk write of two whole rows does too.
 //  * MC ("rows contiguous"): [64 k][R] bf16, for operands whose K is the
 //    outer dimension. The 32-byte chunk index inside a k row is XOR-ed with
-//    (k & 3). Fragments are read with gfx950's transposing LDS load
+//    2 * (k & 3). A fragment read's 32 lanes of one pass take k rows k0..k0+3
+//    at two neighbouring chunks (one even, one odd), so these eight
+//    (row, chunk) pairs land on eight distinct 32-byte bank groups of the
+//    256 bytes a k row spans in the banks (with (k & 3) alone, the odd and
+//    the even chunk fell on the same four groups: a two-way bank conflict).
+//    Fragments are read with gfx950's transposing LDS load
 //    ds_read_b64_tr_b16: within each 16-lane group, lane l receives element
 //    l%4 of the 4-element pieces supplied by lanes 4q + l/4 (q = 0..3), so
 //    when lane 4q + c points at columns 4c..4c+3 of k row q, lane l receives
@@ -93,7 +98,8 @@ struct Cfg {
 __device__ __forceinline__ int kc_off(int r, int c) { return r * 128 + ((c ^ ((r >> 1) & 7)) << 4); }
 template <int R>
 __device__ __forceinline__ int mc_off(int k, int p) {   // p: logical 16-byte chunk of k row
-    return k * (R * 2) + ((((p >> 1) ^ (k & 3)) << 5) | ((p & 1) << 4));
+    static_assert(R >= 128, "the MC swizzle permutes 32-byte chunks 0..7 of a k row");
+    return k * (R * 2) + ((((p >> 1) ^ ((k & 3) << 1)) << 5) | ((p & 1) << 4));
 }
 
 // ---- fragment reads (32 rows x 16 k of MFMA step kk of the slice) ------------------
@@ -110,8 +116,8 @@ __device__ __forceinline__ bf16x8 frag_mc(const char* tile, int rbase, int kk, i
     const int cc = (rbase >> 4) + (g & 1);
     const int cb = (p & 3) * 8;
     typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-    const char* a0 = tile + k * (R * 2) + (((cc ^ (k & 3)) << 5) | cb);
-    const char* a1 = tile + (k + 4) * (R * 2) + (((cc ^ ((k + 4) & 3)) << 5) | cb);
+    const char* a0 = tile + k * (R * 2) + (((cc ^ ((k & 3) << 1)) << 5) | cb);
+    const char* a1 = tile + (k + 4) * (R * 2) + (((cc ^ (((k + 4) & 3) << 1)) << 5) | cb);
     const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(a0));
     const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(a1));
     typedef short i16x8 __attribute__((ext_vector_type(8)));
