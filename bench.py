@@ -85,6 +85,10 @@ def parse():
                          "TCP_TCC_READ_REQ_LATENCY_sum TCP_TCC_WRITE_REQ_sum "
                          "TCP_PENDING_STALL_CYCLES_sum, then SQ_VALU_MFMA_BUSY_CYCLES "
                          "SQ_BUSY_CYCLES GRBM_GUI_ACTIVE)")
+    ap.add_argument("--summarize-lds", metavar="LDS_CSV",
+                    help="write the per-kernel LDS bank-conflict summary from a rocprofv3 "
+                         "--pmc run of this script (SQ_LDS_BANK_CONFLICT SQ_LDS_IDX_ACTIVE "
+                         "SQ_INSTS_LDS GRBM_GUI_ACTIVE)")
     ap.add_argument("--summarize-table1", metavar="JSON",
                     help="write profiles/table1_sweep.txt from the last line of a --table1 run")
     ap.add_argument("--summarize-sweep", metavar="JSON",
@@ -336,6 +340,37 @@ def summarize_counters(tcp_csv, sq_csv, out, workload, cmd, profile_cmd):
             per(a, "TCP_TCC_WRITE_REQ_sum", n),
             per(a, "SQ_VALU_MFMA_BUSY_CYCLES", n) / (N_CU * SIMD_PER_CU * cyc),
             us, cyc / (us * 1e3) if us > 0 else float("nan")))
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("wrote", out)
+
+
+def summarize_lds(lds_csv, out, workload, cmd, profile_cmd):
+    """Per-kernel means per launch of the LDS counters: cycles the LDS was
+    busy with indexed accesses, the part of them lost to bank conflicts, and
+    LDS instructions (summed over all CUs)."""
+    import csv
+    acc, ids = {}, {}
+    for r in csv.DictReader(open(lds_csv)):
+        name = kernel_short_name(r["Kernel_Name"])
+        a = acc.setdefault(name, {})
+        a[r["Counter_Name"]] = a.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+        ids.setdefault(name, set()).add(r["Dispatch_Id"])
+    lines = ["# LDS bank conflicts per launch, workload %s" % workload,
+             "# profile: %s" % profile_cmd,
+             "# summary: python %s" % cmd,
+             "# active: SQ_LDS_IDX_ACTIVE; conflict: SQ_LDS_BANK_CONFLICT (cycles, all CUs); "
+             "share: conflict / active; insts: SQ_INSTS_LDS",
+             "# kernel launches active conflict share insts"]
+    order = sorted(acc, key=lambda k: -acc[k].get("SQ_LDS_IDX_ACTIVE", 0.0) / len(ids[k]))
+    for name in order:
+        a, n = acc[name], len(ids[name])
+        act = a.get("SQ_LDS_IDX_ACTIVE", 0.0) / n
+        if act <= 0:
+            continue
+        bc = a.get("SQ_LDS_BANK_CONFLICT", 0.0) / n
+        lines.append("%-20s %4d %10.3g %10.3g %6.3f %10.3g" % (
+            name[:40], n, act, bc, bc / act, a.get("SQ_INSTS_LDS", 0.0) / n))
     with open(out, "w") as fh:
         fh.write("\n".join(lines) + "\n")
     print("wrote", out)
@@ -756,6 +791,11 @@ def main():
         summarize_sweep(args.summarize_sweep,
                         args.summary_out or os.path.join(ROOT, "profiles", "memory_sweep_mem_sweep_e64k8.txt"),
                         " ".join(sys.argv), args.profile_command)
+        return
+    if args.summarize_lds:
+        summarize_lds(args.summarize_lds,
+                      args.summary_out or os.path.join(ROOT, "profiles", "lds_bank_conflicts_%s.txt" % args.workload),
+                      args.workload, " ".join(sys.argv), args.profile_command)
         return
     if args.summarize_counters:
         summarize_counters(args.summarize_counters[0], args.summarize_counters[1],
