@@ -557,9 +557,14 @@ struct SplitRowsMC {
 // add nothing.
 
 // MC rows gathered through eti: K row kr -> base[eti[off + kr]] (x or dY). The
-// row index of a chunk is loaded one slice ahead of the row itself. When a
-// whole wave covers one K row (R a multiple of 512 columns), the index is the
-// same for the wave and comes in by a scalar load into scalar registers.
+// row index of a chunk is loaded one slice ahead of the row itself.
+// When a whole wave covers one K row (R a multiple of 512 columns), the index
+// is the same for the whole wave. All NCH indices of a wave's slice then come
+// in by one vector load, lane j holding chunk j's, issued with the first chunk
+// of the slice before (so that the wait for it is a counted one), and each
+// chunk takes its index with a lane read. With scalar loads instead (one per
+// chunk) the compiler cannot count LDS reads while one is outstanding, and the
+// LDS waits of the loop became waits for everything.
 template <class C, int R>
 struct GatherMC {
     static constexpr bool MC = true;
@@ -568,26 +573,31 @@ struct GatherMC {
     static constexpr int NSUB = 0;
     template <int i, int p> __device__ void sub() {}
     static constexpr bool UNIFORM = G::CPR % WAVE == 0;
+    static_assert(!UNIFORM || NCH <= WAVE, "one lane per chunk index");
     const bf16_t* base;
     const int32_t* idx;   // eti + off
     int ld, cnt;
-    int nidx[NCH];        // row of the chunk's next slice
+    // row of the chunk's next slice; UNIFORM: [0] this slice's rows, [1] the
+    // next slice's (lane j: chunk j)
+    int nidx[UNIFORM ? 2 : NCH];
     uint32_t zmask;       // chunks of the loaded slice that lie past cnt
     u32x4 v[NCH];
     __device__ static int krow(int i) {
         if constexpr (UNIFORM)   // wave w covers k rows i * (THREADS / CPR) + w * WAVE / CPR
             return i * (C::THREADS / G::CPR) +
-                   __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6) * (WAVE / G::CPR);
+                   __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6) * WAVE / G::CPR;
         else return G::krow(i);
     }
     __device__ int kr(int i, int kt) const {
         const int k = kt * KS + krow(i);
         return k < cnt ? k : cnt - 1;
     }
-    __device__ int row_index(int k) const {
-        if constexpr (UNIFORM)   // constant address space: a uniform address is a scalar load
-            return ((const __attribute__((address_space(4))) int32_t*)idx)[k];
-        else return idx[k];
+    // UNIFORM: the indices of all of this wave's chunks at slice kt, lane j
+    // loading chunk j's (lanes past NCH repeat the last)
+    __device__ int lane_rows(int kt) const {
+        const int j = min((int)(threadIdx.x & (WAVE - 1)), NCH - 1);
+        const int k = kt * KS + j * (C::THREADS / G::CPR) + ((int)threadIdx.x >> 6) * WAVE / G::CPR;
+        return idx[k < cnt ? k : cnt - 1];
     }
     // cnt_ >= 1
     __device__ void init(const bf16_t* b, int ld_, int col0, int ncols, const int32_t* ix,
@@ -599,14 +609,29 @@ struct GatherMC {
         int c = col0 + G::col(0);
         c = c < ncols ? c : ncols - 8;
         base = b + c;
+        if constexpr (UNIFORM) nidx[1] = lane_rows(0);
+        else {
 #pragma unroll
-        for (int i = 0; i < NCH; ++i) nidx[i] = row_index(kr(i, 0));
+            for (int i = 0; i < NCH; ++i) nidx[i] = idx[kr(i, 0)];
+        }
     }
+    // chunks are loaded in the order i = 0 .. NCH-1 within a slice
     template <int i> __device__ void load(int kt) {
         const bool past = kt * KS + krow(i) >= cnt;
         zmask = past ? (zmask | (1u << i)) : (zmask & ~(1u << i));
-        v[i] = ldg16(base + roff(nidx[i], ld));
-        nidx[i] = row_index(kr(i, kt + 1));
+        if constexpr (UNIFORM) {
+            if constexpr (i == 0) {
+                // a real move (identity DPP), never merged with the load: at the
+                // loop head no index register may still wait for its load, or
+                // the compiler waits there for every load in flight
+                nidx[0] = __builtin_amdgcn_update_dpp(0, nidx[1], 0xE4, 0xF, 0xF, false);
+                nidx[1] = lane_rows(kt + 1);
+            }
+            v[i] = ldg16(base + roff(__builtin_amdgcn_readlane(nidx[0], i), ld));
+        } else {
+            v[i] = ldg16(base + roff(nidx[i], ld));
+            nidx[i] = idx[kr(i, kt + 1)];
+        }
     }
     template <int i, bool TAIL> __device__ void store(char* tile) {
         const u32x4 z = {0u, 0u, 0u, 0u};
