@@ -359,7 +359,8 @@ template <int ACT, bool HG_OUT>
 __global__ void __launch_bounds__(RS::THREADS)
 g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
           const float* __restrict__ gates, const int32_t* __restrict__ offsets,
-          const int32_t* __restrict__ eti, const int32_t* __restrict__ slot_src, int d, int f,
+          const int32_t* __restrict__ eti, const int32_t* __restrict__ slot_src,
+          const float* __restrict__ gs, int d, int f,
           int E, bf16_t* __restrict__ A, bf16_t* __restrict__ B, bf16_t* __restrict__ HG,
           float* __restrict__ part) {
     extern __shared__ __align__(16) char lds[];
@@ -376,8 +377,30 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
     const bf16_t* W2e = w2 + (int64_t)t.e * f * d;
     lb.init(W2e, W2e, d, t.n0, min(C::BN, f - t.n0), d);
     rs::NoLoader nl;
+    const WaveCoord<C> wc;
+    // The gate of this lane's row in every epilogue round. With h on load
+    // (no HG output) they stand in slot order already (gs, for G3) and are
+    // loaded before the main loop, whose waits cover them. Otherwise they
+    // are gathered through slot_src after it. Either way they are waited for
+    // (by a wait the compiler sees) before the epilogue's first copy: the
+    // compiler does not see the copies, and a load of its own issued after
+    // them would end in a wait for everything outstanding, copies included.
+    float gr[C::FM];
+    auto gate_row = [&](int i) {
+        const int m = wc.row(i);
+        return (int64_t)t.off + t.m0 + (m < t.mrows ? m : 0);
+    };
+    if constexpr (!HG_OUT) {
+#pragma unroll
+        for (int i = 0; i < C::FM; ++i) gr[i] = gs[gate_row(i)];
+    }
     rs::Acc<C> acc;
     rs::mainloop<C>(la, lb, nl, d / rs::KS, lds, acc);
+    if constexpr (HG_OUT) {
+#pragma unroll
+        for (int i = 0; i < C::FM; ++i) gr[i] = gates[slot_src[gate_row(i)]];
+    }
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
     // ---- epilogue, one round per fragment row-block (64 rows of the tile) ----
     // The A and B rows of a round come into LDS by DMA (1 KB copies, many in
     // flight), two LDS buffers deep: the copies of round i+1 are issued as
@@ -395,7 +418,6 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
     constexpr int NARR = ACT == ACT_SWIGLU ? 2 : 1;   // A, B or A alone
     constexpr int BUF = 2 * ARR;         // one round's buffer (A and B)
     static_assert(CPR == 32 && 2 * BUF <= C::LDS, "G4 staging layout");
-    const WaveCoord<C> wc;
     const int nparts = NT * C::WN;
     const int pidx = (t.n0 / C::BN) * C::WN + wc.wn;
     const uint32_t lds_base = lds_offset(lds);
@@ -418,18 +440,6 @@ g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
             dma16(src, lds_base + (i & 1) * BUF + arr * ARR + qq * 1024);
         }
     };
-    // The gates of this lane's rows in every round, loaded (and waited for,
-    // by a wait the compiler sees) before the first copy is issued. The
-    // compiler does not see the copies: a load of its own issued after them
-    // would end in a wait for all outstanding loads, copies included, and
-    // each round's copies would then no longer overlap the round before.
-    float gr[C::FM];
-#pragma unroll
-    for (int i = 0; i < C::FM; ++i) {
-        const int m = wc.row(i);
-        gr[i] = gates[slot_src[(int64_t)t.off + t.m0 + (m < t.mrows ? m : 0)]];
-    }
-    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
     // Stores a round issues after the copies of the next round: the d_gate
     // partial, the dA (dB) row chunks, the g*h chunks.
     constexpr int NSTORE = 1 + NARR * RR * CPR / C::THREADS + (HG_OUT ? 2 * C::FN : 0);
@@ -1211,8 +1221,8 @@ hipError_t ffn_bwd_act(const FfnArgs& a, bool f32, hipStream_t st) {
     auto g4 = a.h_on_load ? g4_kernel<ACT, false> : g4_kernel<ACT, true>;
     hipLaunchKernelGGL(g4, dim3(slot_grid(S, a.E, RS::BM, cdiv(a.f, RS::BN))),
                        dim3(RS::THREADS), RS::LDS, st, (const bf16_t*)a.dy, (const bf16_t*)a.w2,
-                       a.gates, a.offsets, a.eti, a.slot_src, a.d, a.f, a.E, (bf16_t*)a.A,
-                       (bf16_t*)a.B, HG, part);
+                       a.gates, a.offsets, a.eti, a.slot_src, (const float*)gs, a.d, a.f, a.E,
+                       (bf16_t*)a.A, (bf16_t*)a.B, HG, part);
     probe::mark("g4_kernel", st);
     hipLaunchKernelGGL(dgate_reduce, grid1d(S, 256), dim3(256), 0, st, part, nparts, a.slot_src,
                        a.offsets, a.E, S, a.dgates);
