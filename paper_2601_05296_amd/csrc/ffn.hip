@@ -354,7 +354,8 @@ g2h_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B,
 
 // G4: u = dY[eti] W2[e]^T; epilogue: d_gate partials sum(u*h), dA/dB over
 // A/B, and HG = g * h (h recomputed from A, B) for G3. Non-gated: dA = g u
-// act'(A) over A, h = act(A).
+// act'(A) over A, h = act(A). gs: the gates in slot order (read when HG_OUT is
+// false, i.e. with h on load, where G3 has built them already).
 template <int ACT, bool HG_OUT>
 __global__ void __launch_bounds__(RS::THREADS)
 g4_kernel(const bf16_t* __restrict__ dy, const bf16_t* __restrict__ w2,
